@@ -1,0 +1,186 @@
+"""Benchmark of the grid-octree hot path on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config c4] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one batch of the workload:
+octree build from the resident occupancy grid (with leaf counts and prefix
+scan), input features, and the layer stack (conv3x3x3 with fused ReLU,
+max-pooling, unpooling).  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  `value` is leaf-cells per second of whole steps
+(leaves of the convolution's input octree x steps / wall time of the steps);
+the convolution alone is reported as conv_leaf_cells_per_s and
+dense_voxels_per_s, and its roofline fraction (fp32 MFMA peak) in
+`roofline`, timed with HIP events on the stream the kernel runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_TFLOPS = 157.3   # MI355X dense fp32 (vector and MFMA)
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--impl", default="auto", choices=["auto", "generic", "mfma"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=6000,
+                    help="leaves in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def conv_flops_bytes(n_leaves, n_trees, cin, cout):
+    """Algorithmic work of one conv layer: one (27 cin) x cout contraction per
+    leaf; every input and output row read/written once, plus bit strings,
+    prefix and weights."""
+    flops = 2.0 * 27 * cin * cout * n_leaves
+    nbytes = 4.0 * n_leaves * (cin + cout) + 24.0 * n_trees + 4.0 * (27 * cin * cout + cout)
+    return flops, nbytes
+
+
+def cpu_baseline(W, rows_wanted):
+    """The oracle (never tuned) on a random sample of the workload's leaves,
+    for the first conv layer: leaf-cells per second on the host cores."""
+    sys.path.insert(0, os.path.join(ROOT, "oracle"))
+    import octref as O
+    import torch
+    from paper_1611_05009_amd import pipeline
+
+    recs = []
+    pipeline.run_step(W, recs)
+    torch.cuda.synchronize()
+    conv = next(r for r in recs if r.op == "conv")
+    g = conv.g_in
+    ref = O.make_grid(g.trees.cpu().numpy().view(np.uint32).reshape(-1, 4), *g.dims())
+    x = conv.x_in.cpu().numpy()
+    info = O.leaf_info(ref)
+    rng = np.random.default_rng(7)
+    rows = np.sort(rng.choice(ref.n_leaves, size=min(rows_wanted, ref.n_leaves), replace=False))
+    w = conv.params["w"].cpu().numpy()
+    b = conv.params["b"].cpu().numpy()
+    t0 = time.perf_counter()
+    O.conv3_sampled(ref, x, w, b, conv.params["relu"], rows, info=info)
+    dt = time.perf_counter() - t0
+    return {
+        "value": rows.size / dt,
+        "unit": "leaf-cells/s",
+        "cores": O.num_threads(),
+        "kind": "oracle",
+        "sample": "conv layer 0 on %d uniformly drawn leaves of %d (%.1f s, fp64, rowmaps built per sample)"
+                  % (rows.size, ref.n_leaves, dt),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md for how the work would shard)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_1611_05009_amd import octnet as oc
+    from paper_1611_05009_amd import pipeline
+
+    oc.lib()
+    torch.cuda.set_device(0)
+    t_gen = time.perf_counter()
+    W = pipeline.Workload(args.config)
+    t_gen = time.perf_counter() - t_gen
+    print("inputs ready (%.1f s): %s, %d leaves" % (t_gen, args.config, W.n_leaves), file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    events = []
+
+    def timer():
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        events.append((s, e))
+        return s, e
+
+    for _ in range(args.warmup):
+        pipeline.run_step(W, impl=args.impl)
+    torch.cuda.synchronize()
+    print("warmup done", file=sys.stderr, flush=True)
+
+    events.clear()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        pipeline.run_step(W, conv_timer=timer, impl=args.impl)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = 1e3 * dt / args.steps
+
+    convs = [L for L in W.layers if L[0] == "conv"]
+    n_conv = len(convs)
+    per_layer_ms = [0.0] * n_conv
+    for k, (s, e) in enumerate(events):
+        per_layer_ms[k % n_conv] += s.elapsed_time(e) / args.steps
+    # Dominant kernel: the first conv layer (the only one in the 256^3 workload).
+    p0 = convs[0][1]
+    gd = W.occ_np.shape[1] // 8
+    n_trees = W.batch * gd ** 3
+    flops, nbytes = conv_flops_bytes(W.n_leaves, n_trees, p0["cin"], p0["cout"])
+    t_conv = per_layer_ms[0] * 1e-3
+    achieved = flops / t_conv / 1e12
+    out = {
+        "metric": "octree conv3x3x3 leaf-cells/s + effective dense voxels/s at 256^3; % roofline",
+        "value": W.n_leaves * args.steps / dt,
+        "unit": "leaf-cells/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": W.wl.description,
+            "key": args.config,
+            "batch": W.batch,
+            "grid": list(W.occ_np.shape[1:]),
+            "n_leaves": W.n_leaves,
+            "n_trees": n_trees,
+            "layers": [L.op if L.op != "conv" else "conv%dx%d" % (L.cin, L.cout) for L in W.wl.layers],
+            "impl": args.impl,
+        },
+        "conv_ms": per_layer_ms,
+        "conv_leaf_cells_per_s": W.n_leaves / t_conv,
+        "dense_voxels_per_s": W.dense_voxels / t_conv,
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_FP32_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_FP32_TFLOPS,
+            "traffic": None,
+            "kernel": "conv3x3x3 execute, layer 0 (%dx%d)" % (p0["cin"], p0["cout"]),
+            "alg_flops": flops,
+            "alg_bytes": nbytes,
+            "hbm_frac": nbytes / t_conv / 1e9 / PEAK_HBM_GBS,
+        },
+    }
+    if not args.no_cpu_baseline:
+        print("timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(W, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+/*
+ * octnet_hip.h -- C ABI of the MI355X (gfx950) grid-octree library.
+ *
+ * Implements the hot path of OctNet (Riegler, Ulusoy, Geiger, "OctNet:
+ * Learning Deep 3D Representations at High Resolutions", CVPR 2017):
+ * the hybrid grid-octree of Sec. 3.1 and the convolution, pooling and
+ * unpooling of Sec. 3.2, all run by hand-written HIP kernels.
+ *
+ * Data layout (shared by every call):
+ *   - A batch of n grids, each of gd x gh x gw shallow octrees of depth 3,
+ *     covers a voxel grid of 8gd x 8gh x 8gw (Sec. 3.1).
+ *   - trees: uint32 [n_trees][4], n_trees = n*gd*gh*gw, trees ordered
+ *     (n, d, h, w) with w fastest.  Split bit j (0 <= j < 73, Sec. 3.1) is
+ *     (trees[4t + (j>>5)] >> (j&31)) & 1; bits 73..127 are 0.  Bit 0 is the
+ *     root, bits 1..8 depth 1, bits 9..72 depth 2; bit indices 73..584 name
+ *     the implicit depth-3 voxels.  parent(i) = (i-1)/8 and child(i) = 8i+1
+ *     (Eq. 1-2).  The child with octant o covers the sub-cube offset by
+ *     ((o>>2)&1, (o>>1)&1, o&1) times the child size along (d, h, w).
+ *   - A tree is canonical when no bit is set below an unsplit node.  Every
+ *     call below assumes canonical trees (oc_validate checks it).
+ *   - prefix: int64 [n_trees + 1], prefix[t] = leaves in trees 0..t-1.  The
+ *     leaves of tree t occupy rows prefix[t] .. prefix[t+1]-1 in ascending
+ *     bit-index order, i.e. row = prefix[t] + data_idx(i) with data_idx from
+ *     Eq. 3.
+ *   - Leaf features: float [n_leaves][c], row-major.
+ *   - Dense tensors: float [n][8gd][8gh][8gw][c] (NDHWC).
+ *
+ * Conventions: every pointer is a device pointer unless marked [host].
+ * `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ * asynchronous on that stream except where marked "synchronizes".  The caller
+ * owns every buffer; no call allocates or frees device memory.  Outputs must
+ * not alias inputs (except oc_relu).  Argument errors are detected on the host
+ * before any launch and leave every buffer untouched.
+ */
+#ifndef OCTNET_HIP_H
+#define OCTNET_HIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes. */
+#define OC_OK 0
+#define OC_EINVAL (-1)      /* null pointer, non-positive size, odd dims for pooling, ... */
+#define OC_ESTRUCT (-2)     /* non-canonical tree, or a guide that does not pool to the input */
+#define OC_EWORKSPACE (-3)  /* workspace smaller than the matching *_workspace query */
+#define OC_EHIP (-4)        /* HIP runtime or launch failure; see oc_last_error() */
+#define OC_EOVERFLOW (-5)   /* a count exceeds what the layout supports */
+
+/* Split rules of oc_build. */
+#define OC_SPLIT_MIXED 0 /* split a node iff its occupancy is mixed */
+#define OC_SPLIT_ANY 1   /* split a node iff any voxel in it is occupied */
+
+/* Pooling functions of oc_ten2oc (Eq. 5). */
+#define OC_POOL_AVG 0
+#define OC_POOL_MAX 1
+
+/* Convolution implementations (oc_conv3x3x3_ex). */
+#define OC_CONV_AUTO 0    /* fastest available for the channel counts */
+#define OC_CONV_GENERIC 1 /* any channel counts: window sums + VALU contraction */
+#define OC_CONV_MFMA 2    /* fp32 MFMA contraction; OC_EINVAL if unsupported */
+
+/* Static text for a return code. */
+const char* oc_error_string(int code);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* oc_last_error(void);
+
+/* Library version (major*10000 + minor*100 + patch). */
+int oc_version(void);
+
+/* Bytes of workspace needed by oc_build, oc_prefix, oc_validate and the
+ * structure calls of pooling/unpooling for n_trees trees. */
+size_t oc_structure_workspace(int64_t n_trees);
+
+/*
+ * Octree creation from an occupancy grid (Sec. 1: cells that contain data are
+ * split recursively down to the finest level).  occ: uint8
+ * [n][8gd][8gh][8gw], non-zero = occupied.  Each node at depth 0, 1, 2 whose
+ * parent is split is split according to `rule`.  Writes trees and prefix;
+ * *n_leaves [host] receives prefix[n_trees].  Synchronizes.
+ */
+int oc_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32_t* trees,
+             int64_t* prefix, int64_t* n_leaves, void* ws, size_t ws_bytes, void* stream);
+
+/* prefix from trees: leaves per tree = 1 + 7 * (set bits) (Eq. 3 counted to
+ * the end of the tree), exclusive scan over trees.  *n_leaves [host] receives
+ * the total.  Synchronizes. */
+int oc_prefix(const uint32_t* trees, int64_t n_trees, int64_t* prefix, int64_t* n_leaves,
+              void* ws, size_t ws_bytes, void* stream);
+
+/* Counts non-canonical trees into *n_bad [host].  Synchronizes. */
+int oc_validate(const uint32_t* trees, int64_t n_trees, int64_t* n_bad, void* ws,
+                size_t ws_bytes, void* stream);
+
+/* leaf_info[row] = tree << 10 | bit index of the leaf stored at that row
+ * (Eq. 3 inverted).  leaf_info: uint64 [prefix[n_trees]]. */
+int oc_leaf_index(const uint32_t* trees, const int64_t* prefix, int64_t n_trees,
+                  uint64_t* leaf_info, void* stream);
+
+/* rowmap[n][8gd][8gh][8gw] = row of the leaf holding each voxel (the voxel
+ * addressing of Sec. 3.2: tree = voxel/8, local = voxel mod 8, then the
+ * smallest cell containing it and Eq. 3).  rowmap: int64. */
+int oc_rowmap(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              int64_t* rowmap, void* stream);
+
+/* Eq. 4: dense[v][k] = data[row of the leaf holding voxel v][k]. */
+int oc_oc2ten(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              const float* data, int c, float* dense, void* stream);
+
+/* Eq. 5: data[leaf][k] = pool over the leaf's voxels of dense[v][k]; pool is
+ * OC_POOL_AVG (sum accumulated in double) or OC_POOL_MAX. */
+int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              const float* dense, int c, int pool, float* data, void* stream);
+
+/* Bytes of workspace for oc_conv3x3x3 on a structure with n_trees trees and
+ * n_leaves leaves.  *bytes [host]. */
+int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes);
+
+/*
+ * Grid-octree 3x3x3 convolution, Eq. 8 with average pooling: for every leaf,
+ * the mean over its cell of the dense convolution of Eq. 7 (zero padding 1,
+ * zero outside the grid) applied to oc2ten(in), plus bias, optionally
+ * followed by max(0, .).  The output has the input's structure.
+ *   in:     float [n_leaves][cin]
+ *   weight: float [cout][cin][3][3][3] in Eq. 7's orientation: tap (l,m,n)
+ *           multiplies input voxel (i-l+1, j-m+1, k-n+1) for output (i,j,k).
+ *   bias:   float [cout] or NULL.
+ *   out:    float [n_leaves][cout].
+ * Requires n_leaves < 2^31.  ws: at least oc_conv3x3x3_workspace bytes.
+ */
+int oc_conv3x3x3(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                 int64_t n_leaves, const float* in, int cin, const float* weight,
+                 const float* bias, int cout, int relu, float* out, void* ws, size_t ws_bytes,
+                 void* stream);
+
+/* As oc_conv3x3x3 with an explicit implementation (OC_CONV_*). */
+int oc_conv3x3x3_ex(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                    int64_t n_leaves, const float* in, int cin, const float* weight,
+                    const float* bias, int cout, int relu, float* out, void* ws,
+                    size_t ws_bytes, int impl, void* stream);
+
+/* The two halves of oc_conv3x3x3_ex, for callers that reuse a structure or
+ * time the convolution proper.  prepare writes everything that depends on
+ * the structure and the weights into ws (it reads weight, not the features);
+ * execute runs the convolution from that workspace and must get the same
+ * structure, channel counts and ws as the prepare call before it. */
+int oc_conv3x3x3_prepare(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                         int64_t n_leaves, const float* weight, int cin, int cout, void* ws,
+                         size_t ws_bytes, void* stream);
+int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                         int64_t n_leaves, const float* in, int cin, const float* bias, int cout,
+                         int relu, float* out, const void* ws, size_t ws_bytes, int impl,
+                         void* stream);
+
+/* Does OC_CONV_MFMA support (cin, cout)?  1 yes, 0 no. */
+int oc_conv3x3x3_mfma_supported(int cin, int cout);
+
+/*
+ * 2x2x2 pooling structure (Eq. 10): input grid 2D x 2H x 2W trees (gd, gh, gw
+ * even) -> output D x H x W.  Input trees (2d+a, 2h+b, 2w+c) become octant
+ * o = 4a+2b+c of output tree (d,h,w); every input node moves one level down;
+ * the output root is always split.  Writes out_trees, out_prefix and
+ * *out_n_leaves [host].  Synchronizes.
+ */
+int oc_pool2_structure(const uint32_t* in_trees, int n, int gd, int gh, int gw,
+                       uint32_t* out_trees, int64_t* out_prefix, int64_t* out_n_leaves,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Eq. 10 data: an output leaf that comes from an input cell of size >= 2
+ * copies it; an output unit voxel that comes from a split depth-2 input node
+ * takes the maximum of its 8 unit-voxel children.  gd, gh, gw are the input
+ * dims; the output structure comes from oc_pool2_structure. */
+int oc_pool2_max(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                 int gw, const float* in, int c, const uint32_t* out_trees,
+                 const int64_t* out_prefix, float* out, void* stream);
+
+/*
+ * 2x2x2 unpooling structure.  guide_trees == NULL: plain unpooling (Eq. 12):
+ * input tree (d,h,w) spawns output trees (2d+a, 2h+b, 2w+c); input node 1+o
+ * becomes the root of output tree o = 4a+2b+c and every node below it moves
+ * one level up; an unsplit input root spawns 8 unsplit trees.
+ * guide_trees != NULL: guided unpooling (the remark after Eq. 12): the output
+ * structure is the guide (2gd x 2gh x 2gw trees), which must pool to the
+ * input structure (else OC_ESTRUCT).  gd, gh, gw are the input dims.  Writes
+ * out_trees, out_prefix and *out_n_leaves [host].  Synchronizes.
+ */
+int oc_unpool2_structure(const uint32_t* in_trees, int n, int gd, int gh, int gw,
+                         const uint32_t* guide_trees, uint32_t* out_trees, int64_t* out_prefix,
+                         int64_t* out_n_leaves, void* ws, size_t ws_bytes, void* stream);
+
+/* Eq. 12 data: every output leaf copies the input leaf that holds its voxels
+ * at half resolution (plain or guided structure alike).  gd, gh, gw are the
+ * input dims; out_trees/out_prefix come from oc_unpool2_structure. */
+int oc_unpool2(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh, int gw,
+               const float* in, int c, const uint32_t* out_trees, const int64_t* out_prefix,
+               float* out, void* stream);
+
+/* Pointwise max(0, x) on leaf data (pointwise ops act on leaf data alone,
+ * Sec. 3.2).  In place allowed. */
+int oc_relu(float* data, int64_t count, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OCTNET_HIP_H */

@@ -333,17 +333,20 @@ def pool2_structure(g: Grid) -> Grid:
     return make_grid(out, g.n, g.gd // 2, g.gh // 2, g.gw // 2)
 
 
-def pool2_max(g: Grid, data: np.ndarray, out_g: Grid | None = None) -> tuple[Grid, np.ndarray]:
-    """Eq. 10: returns (output structure, output data)."""
+def pool2_max(g: Grid, data: np.ndarray, out_g: Grid | None = None, rows=None) -> tuple[Grid, np.ndarray]:
+    """Eq. 10: returns (output structure, output data); ``rows`` restricts the
+    data to a subset of output rows."""
     data = _c(data, np.float64)
     c = data.shape[1]
     out_g = pool2_structure(g) if out_g is None else out_g
     info_in = leaf_info(g)
     info_out = leaf_info(out_g)
+    if rows is not None:
+        info_out = _c(info_out[np.asarray(rows, dtype=np.int64)], np.uint64)
     rm = rowmap(g)
-    out = np.zeros((out_g.n_leaves, c), dtype=np.float64)
+    out = np.zeros((info_out.size, c), dtype=np.float64)
     lib().ocref_pool2_max(_p(info_in), _p(rm), g.n, g.gd, g.gh, g.gw, _p(data), c,
-                          _p(info_out), out_g.n_leaves, _p(out))
+                          _p(info_out), info_out.size, _p(out))
     return out_g, out
 
 
@@ -353,8 +356,9 @@ def unpool2_structure(g: Grid) -> Grid:
     return make_grid(out, g.n, 2 * g.gd, 2 * g.gh, 2 * g.gw)
 
 
-def unpool2(g: Grid, data: np.ndarray, guide: Grid | None = None) -> tuple[Grid, np.ndarray]:
-    """Eq. 12 (guide None) or the guided variant: returns (structure, data)."""
+def unpool2(g: Grid, data: np.ndarray, guide: Grid | None = None, rows=None) -> tuple[Grid, np.ndarray]:
+    """Eq. 12 (guide None) or the guided variant: returns (structure, data);
+    ``rows`` restricts the data to a subset of output rows."""
     data = _c(data, np.float64)
     c = data.shape[1]
     if guide is None:
@@ -363,9 +367,11 @@ def unpool2(g: Grid, data: np.ndarray, guide: Grid | None = None) -> tuple[Grid,
         assert (guide.n, guide.gd, guide.gh, guide.gw) == (g.n, 2 * g.gd, 2 * g.gh, 2 * g.gw)
         out_g = guide
     info_out = leaf_info(out_g)
+    if rows is not None:
+        info_out = _c(info_out[np.asarray(rows, dtype=np.int64)], np.uint64)
     rm = rowmap(g)
-    out = np.zeros((out_g.n_leaves, c), dtype=np.float64)
-    lib().ocref_unpool2(_p(rm), g.gd, g.gh, g.gw, _p(data), c, _p(info_out), out_g.n_leaves, _p(out))
+    out = np.zeros((info_out.size, c), dtype=np.float64)
+    lib().ocref_unpool2(_p(rm), g.gd, g.gh, g.gw, _p(data), c, _p(info_out), info_out.size, _p(out))
     return out_g, out
 
 

@@ -1,0 +1,362 @@
+// C ABI entry points: host-side argument checks, workspace carving, launches.
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/octnet_hip.h"
+#include "oc_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(OC_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+#define OC_CHECK_HIP(expr, where)                 \
+  do {                                            \
+    hipError_t _e = (expr);                       \
+    if (_e != hipSuccess) return hip_fail(_e, where); \
+  } while (0)
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+bool dims_ok(int n, int gd, int gh, int gw) { return n > 0 && gd > 0 && gh > 0 && gw > 0; }
+
+// Voxel and tree counts must fit the int64 index arithmetic of the kernels,
+// and a launch grid (blocks of 256 threads over voxels) must fit 2^31 blocks.
+bool sizes_ok(int n, int gd, int gh, int gw) {
+  const double vox = 512.0 * n * gd * gh * gw;
+  return vox < 4.0e12;
+}
+
+int64_t n_trees_of(int n, int gd, int gh, int gw) { return (int64_t)n * gd * gh * gw; }
+
+// Scan counts (already in ws) into prefix and read the total back.
+int finish_prefix(int64_t nt, int64_t* prefix, int64_t* n_leaves, void* ws, hipStream_t s,
+                  const char* where) {
+  OC_CHECK_HIP(oci::scan_counts(oci::scan_counts_buffer(ws), nt, prefix, ws, s), where);
+  int64_t total = 0;
+  OC_CHECK_HIP(hipMemcpyAsync(&total, prefix + nt, sizeof(int64_t), hipMemcpyDeviceToHost, s), where);
+  OC_CHECK_HIP(hipStreamSynchronize(s), where);
+  *n_leaves = total;
+  return OC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* oc_error_string(int code) {
+  switch (code) {
+    case OC_OK: return "ok";
+    case OC_EINVAL: return "invalid argument";
+    case OC_ESTRUCT: return "invalid octree structure";
+    case OC_EWORKSPACE: return "workspace too small";
+    case OC_EHIP: return "HIP runtime error";
+    case OC_EOVERFLOW: return "size overflow";
+    default: return "unknown error";
+  }
+}
+
+const char* oc_last_error(void) { return g_last_error.c_str(); }
+
+int oc_version(void) { return 100; }
+
+size_t oc_structure_workspace(int64_t n_trees) {
+  if (n_trees < 0) return 0;
+  return oci::scan_workspace(n_trees) + 256;
+}
+
+int oc_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32_t* trees,
+             int64_t* prefix, int64_t* n_leaves, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!occ || !trees || !prefix || !n_leaves || !ws) return fail(OC_EINVAL, "oc_build: null pointer");
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_build: non-positive dims");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_build: grid too large");
+  if (rule != OC_SPLIT_MIXED && rule != OC_SPLIT_ANY) return fail(OC_EINVAL, "oc_build: bad rule %d", rule);
+  const int64_t nt = n_trees_of(n, gd, gh, gw);
+  if (ws_bytes < oc_structure_workspace(nt)) return fail(OC_EWORKSPACE, "oc_build: workspace too small");
+  hipStream_t s = as_stream(stream);
+  OC_CHECK_HIP(oci::launch_build(occ, n, gd, gh, gw, rule, trees, oci::scan_counts_buffer(ws), s),
+               "oc_build");
+  return finish_prefix(nt, prefix, n_leaves, ws, s, "oc_build");
+}
+
+int oc_prefix(const uint32_t* trees, int64_t n_trees, int64_t* prefix, int64_t* n_leaves, void* ws,
+              size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!trees || !prefix || !n_leaves || !ws) return fail(OC_EINVAL, "oc_prefix: null pointer");
+  if (n_trees <= 0) return fail(OC_EINVAL, "oc_prefix: n_trees <= 0");
+  if (ws_bytes < oc_structure_workspace(n_trees)) return fail(OC_EWORKSPACE, "oc_prefix: workspace too small");
+  hipStream_t s = as_stream(stream);
+  OC_CHECK_HIP(oci::launch_count(trees, n_trees, oci::scan_counts_buffer(ws), s), "oc_prefix");
+  return finish_prefix(n_trees, prefix, n_leaves, ws, s, "oc_prefix");
+}
+
+int oc_validate(const uint32_t* trees, int64_t n_trees, int64_t* n_bad, void* ws, size_t ws_bytes,
+                void* stream) {
+  g_last_error.clear();
+  if (!trees || !n_bad || !ws) return fail(OC_EINVAL, "oc_validate: null pointer");
+  if (n_trees <= 0) return fail(OC_EINVAL, "oc_validate: n_trees <= 0");
+  if (ws_bytes < oc_structure_workspace(n_trees)) return fail(OC_EWORKSPACE, "oc_validate: workspace too small");
+  hipStream_t s = as_stream(stream);
+  int32_t* counter = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + oc_structure_workspace(n_trees) - 256);
+  OC_CHECK_HIP(hipMemsetAsync(counter, 0, sizeof(int32_t), s), "oc_validate");
+  OC_CHECK_HIP(oci::launch_validate(trees, n_trees, counter, s), "oc_validate");
+  int32_t total = 0;
+  OC_CHECK_HIP(hipMemcpyAsync(&total, counter, sizeof(int32_t), hipMemcpyDeviceToHost, s), "oc_validate");
+  OC_CHECK_HIP(hipStreamSynchronize(s), "oc_validate");
+  *n_bad = total;
+  return OC_OK;
+}
+
+int oc_leaf_index(const uint32_t* trees, const int64_t* prefix, int64_t n_trees, uint64_t* leaf_info,
+                  void* stream) {
+  g_last_error.clear();
+  if (!trees || !prefix || !leaf_info) return fail(OC_EINVAL, "oc_leaf_index: null pointer");
+  if (n_trees <= 0) return fail(OC_EINVAL, "oc_leaf_index: n_trees <= 0");
+  if (n_trees >= (1LL << 54)) return fail(OC_EOVERFLOW, "oc_leaf_index: too many trees");
+  OC_CHECK_HIP(oci::launch_leaf_index(trees, prefix, n_trees, leaf_info, as_stream(stream)),
+               "oc_leaf_index");
+  return OC_OK;
+}
+
+int oc_rowmap(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              int64_t* rowmap, void* stream) {
+  g_last_error.clear();
+  if (!trees || !prefix || !rowmap) return fail(OC_EINVAL, "oc_rowmap: null pointer");
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_rowmap: non-positive dims");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_rowmap: grid too large");
+  OC_CHECK_HIP(oci::launch_rowmap(trees, prefix, n, gd, gh, gw, rowmap, as_stream(stream)),
+               "oc_rowmap");
+  return OC_OK;
+}
+
+int oc_oc2ten(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              const float* data, int c, float* dense, void* stream) {
+  g_last_error.clear();
+  if (!trees || !prefix || !data || !dense) return fail(OC_EINVAL, "oc_oc2ten: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0) return fail(OC_EINVAL, "oc_oc2ten: non-positive dims");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_oc2ten: grid too large");
+  OC_CHECK_HIP(oci::launch_oc2ten(trees, prefix, n, gd, gh, gw, data, c, dense, as_stream(stream)),
+               "oc_oc2ten");
+  return OC_OK;
+}
+
+int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+              const float* dense, int c, int pool, float* data, void* stream) {
+  g_last_error.clear();
+  if (!trees || !prefix || !data || !dense) return fail(OC_EINVAL, "oc_ten2oc: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0) return fail(OC_EINVAL, "oc_ten2oc: non-positive dims");
+  if (pool != OC_POOL_AVG && pool != OC_POOL_MAX) return fail(OC_EINVAL, "oc_ten2oc: bad pool %d", pool);
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_ten2oc: grid too large");
+  OC_CHECK_HIP(oci::launch_ten2oc(trees, prefix, n, gd, gh, gw, dense, c, pool, data,
+                                  as_stream(stream)),
+               "oc_ten2oc");
+  return OC_OK;
+}
+
+int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(OC_EINVAL, "oc_conv3x3x3_workspace: null pointer");
+  if (n_trees <= 0 || n_leaves <= 0 || cin <= 0 || cout <= 0)
+    return fail(OC_EINVAL, "oc_conv3x3x3_workspace: non-positive size");
+  *bytes = oci::conv_workspace(n_trees, n_leaves, cin, cout);
+  return OC_OK;
+}
+
+int oc_conv3x3x3_mfma_supported(int cin, int cout) { return oci::conv_mfma_supported(cin, cout) ? 1 : 0; }
+
+namespace {
+
+// Shared argument checks of the convolution entry points; fills `a`.
+int conv_args(const char* who, const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+              int gw, int64_t n_leaves, int cin, int cout, size_t ws_bytes, const void* ws,
+              oci::ConvArgs* a) {
+  if (!trees || !prefix || !ws) return fail(OC_EINVAL, "%s: null pointer", who);
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "%s: non-positive dims", who);
+  if (cin <= 0 || cout <= 0 || cin > 256 || cout > 4096)
+    return fail(OC_EINVAL, "%s: channels (%d, %d) outside [1,256] x [1,4096]", who, cin, cout);
+  if (n_leaves <= 0) return fail(OC_EINVAL, "%s: n_leaves <= 0", who);
+  if (n_leaves >= (1LL << 31)) return fail(OC_EOVERFLOW, "%s: n_leaves >= 2^31", who);
+  const int64_t nt = n_trees_of(n, gd, gh, gw);
+  if (n_leaves > 512 * nt) return fail(OC_EINVAL, "%s: n_leaves > 512 * n_trees", who);
+  const size_t need = oci::conv_workspace(nt, n_leaves, cin, cout);
+  if (ws_bytes < need) return fail(OC_EWORKSPACE, "%s: workspace %zu < %zu", who, ws_bytes, need);
+  *a = oci::ConvArgs();
+  a->trees = trees; a->prefix = prefix;
+  a->n = n; a->gd = gd; a->gh = gh; a->gw = gw;
+  a->n_trees = nt; a->n_leaves = n_leaves;
+  a->cin = cin; a->cout = cout;
+  return OC_OK;
+}
+
+int conv_impl(const char* who, int impl, int cin, int cout, int* use) {
+  if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA)
+    return fail(OC_EINVAL, "%s: bad impl %d", who, impl);
+  const bool mfma_ok = oci::conv_mfma_supported(cin, cout);
+  if (impl == OC_CONV_MFMA && !mfma_ok)
+    return fail(OC_EINVAL, "%s: no MFMA kernel for (%d, %d)", who, cin, cout);
+  *use = impl == OC_CONV_AUTO ? (mfma_ok ? OC_CONV_MFMA : OC_CONV_GENERIC) : impl;
+  return OC_OK;
+}
+
+}  // namespace
+
+int oc_conv3x3x3_prepare(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                         int64_t n_leaves, const float* weight, int cin, int cout, void* ws,
+                         size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  oci::ConvArgs a;
+  int rc = conv_args("oc_conv3x3x3_prepare", trees, prefix, n, gd, gh, gw, n_leaves, cin, cout,
+                     ws_bytes, ws, &a);
+  if (rc != OC_OK) return rc;
+  if (!weight) return fail(OC_EINVAL, "oc_conv3x3x3_prepare: null weight");
+  a.weight = weight;
+  OC_CHECK_HIP(oci::launch_conv_prepare(a, ws, as_stream(stream)), "oc_conv3x3x3_prepare");
+  return OC_OK;
+}
+
+int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                         int64_t n_leaves, const float* in, int cin, const float* bias, int cout,
+                         int relu, float* out, const void* ws, size_t ws_bytes, int impl,
+                         void* stream) {
+  g_last_error.clear();
+  oci::ConvArgs a;
+  int rc = conv_args("oc_conv3x3x3_execute", trees, prefix, n, gd, gh, gw, n_leaves, cin, cout,
+                     ws_bytes, ws, &a);
+  if (rc != OC_OK) return rc;
+  if (!in || !out) return fail(OC_EINVAL, "oc_conv3x3x3_execute: null pointer");
+  int use = 0;
+  rc = conv_impl("oc_conv3x3x3_execute", impl, cin, cout, &use);
+  if (rc != OC_OK) return rc;
+  a.in = in; a.bias = bias; a.relu = relu ? 1 : 0; a.out = out;
+  OC_CHECK_HIP(oci::launch_conv_execute(a, ws, use, as_stream(stream)), "oc_conv3x3x3_execute");
+  return OC_OK;
+}
+
+int oc_conv3x3x3_ex(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                    int64_t n_leaves, const float* in, int cin, const float* weight,
+                    const float* bias, int cout, int relu, float* out, void* ws, size_t ws_bytes,
+                    int impl, void* stream) {
+  g_last_error.clear();
+  oci::ConvArgs a;
+  int rc = conv_args("oc_conv3x3x3", trees, prefix, n, gd, gh, gw, n_leaves, cin, cout, ws_bytes, ws,
+                     &a);
+  if (rc != OC_OK) return rc;
+  if (!in || !weight || !out) return fail(OC_EINVAL, "oc_conv3x3x3: null pointer");
+  int use = 0;
+  rc = conv_impl("oc_conv3x3x3", impl, cin, cout, &use);
+  if (rc != OC_OK) return rc;
+  a.in = in; a.weight = weight; a.bias = bias; a.relu = relu ? 1 : 0; a.out = out;
+  hipStream_t s = as_stream(stream);
+  OC_CHECK_HIP(oci::launch_conv_prepare(a, ws, s), "oc_conv3x3x3");
+  OC_CHECK_HIP(oci::launch_conv_execute(a, ws, use, s), "oc_conv3x3x3");
+  return OC_OK;
+}
+
+int oc_conv3x3x3(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                 int64_t n_leaves, const float* in, int cin, const float* weight, const float* bias,
+                 int cout, int relu, float* out, void* ws, size_t ws_bytes, void* stream) {
+  return oc_conv3x3x3_ex(trees, prefix, n, gd, gh, gw, n_leaves, in, cin, weight, bias, cout, relu,
+                         out, ws, ws_bytes, OC_CONV_AUTO, stream);
+}
+
+int oc_pool2_structure(const uint32_t* in_trees, int n, int gd, int gh, int gw, uint32_t* out_trees,
+                       int64_t* out_prefix, int64_t* out_n_leaves, void* ws, size_t ws_bytes,
+                       void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !out_trees || !out_prefix || !out_n_leaves || !ws)
+    return fail(OC_EINVAL, "oc_pool2_structure: null pointer");
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_pool2_structure: non-positive dims");
+  if ((gd | gh | gw) & 1) return fail(OC_EINVAL, "oc_pool2_structure: odd tree grid %dx%dx%d", gd, gh, gw);
+  const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
+  if (ws_bytes < oc_structure_workspace(no)) return fail(OC_EWORKSPACE, "oc_pool2_structure: workspace too small");
+  hipStream_t s = as_stream(stream);
+  OC_CHECK_HIP(oci::launch_pool_structure(in_trees, n, gd, gh, gw, out_trees,
+                                          oci::scan_counts_buffer(ws), s),
+               "oc_pool2_structure");
+  return finish_prefix(no, out_prefix, out_n_leaves, ws, s, "oc_pool2_structure");
+}
+
+int oc_pool2_max(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh, int gw,
+                 const float* in, int c, const uint32_t* out_trees, const int64_t* out_prefix,
+                 float* out, void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !in_prefix || !in || !out_trees || !out_prefix || !out)
+    return fail(OC_EINVAL, "oc_pool2_max: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0) return fail(OC_EINVAL, "oc_pool2_max: non-positive dims");
+  if ((gd | gh | gw) & 1) return fail(OC_EINVAL, "oc_pool2_max: odd tree grid");
+  OC_CHECK_HIP(oci::launch_pool_max(in_trees, in_prefix, n, gd, gh, gw, in, c, out_trees, out_prefix,
+                                    out, as_stream(stream)),
+               "oc_pool2_max");
+  return OC_OK;
+}
+
+int oc_unpool2_structure(const uint32_t* in_trees, int n, int gd, int gh, int gw,
+                         const uint32_t* guide_trees, uint32_t* out_trees, int64_t* out_prefix,
+                         int64_t* out_n_leaves, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !out_trees || !out_prefix || !out_n_leaves || !ws)
+    return fail(OC_EINVAL, "oc_unpool2_structure: null pointer");
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_unpool2_structure: non-positive dims");
+  if (!sizes_ok(n, 2 * gd, 2 * gh, 2 * gw)) return fail(OC_EOVERFLOW, "oc_unpool2_structure: grid too large");
+  const int64_t no = 8LL * n * gd * gh * gw;
+  if (ws_bytes < oc_structure_workspace(no)) return fail(OC_EWORKSPACE, "oc_unpool2_structure: workspace too small");
+  hipStream_t s = as_stream(stream);
+  // The mismatch flag of the guided check sits in the last 256 bytes.
+  int32_t* mismatch = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + oc_structure_workspace(no) - 256);
+  if (guide_trees) OC_CHECK_HIP(hipMemsetAsync(mismatch, 0, sizeof(int32_t), s), "oc_unpool2_structure");
+  OC_CHECK_HIP(oci::launch_unpool_structure(in_trees, guide_trees, n, gd, gh, gw, out_trees,
+                                            oci::scan_counts_buffer(ws), mismatch, s),
+               "oc_unpool2_structure");
+  int rc = finish_prefix(no, out_prefix, out_n_leaves, ws, s, "oc_unpool2_structure");
+  if (rc != OC_OK) return rc;
+  if (guide_trees) {
+    int32_t bad = 0;
+    OC_CHECK_HIP(hipMemcpyAsync(&bad, mismatch, sizeof(int32_t), hipMemcpyDeviceToHost, s),
+                 "oc_unpool2_structure");
+    OC_CHECK_HIP(hipStreamSynchronize(s), "oc_unpool2_structure");
+    if (bad) return fail(OC_ESTRUCT, "oc_unpool2_structure: guide does not pool to the input (%d trees)", bad);
+  }
+  return OC_OK;
+}
+
+int oc_unpool2(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh, int gw,
+               const float* in, int c, const uint32_t* out_trees, const int64_t* out_prefix,
+               float* out, void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !in_prefix || !in || !out_trees || !out_prefix || !out)
+    return fail(OC_EINVAL, "oc_unpool2: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0) return fail(OC_EINVAL, "oc_unpool2: non-positive dims");
+  OC_CHECK_HIP(oci::launch_unpool(in_trees, in_prefix, n, gd, gh, gw, in, c, out_trees, out_prefix,
+                                  out, as_stream(stream)),
+               "oc_unpool2");
+  return OC_OK;
+}
+
+int oc_relu(float* data, int64_t count, void* stream) {
+  g_last_error.clear();
+  if (!data) return fail(OC_EINVAL, "oc_relu: null pointer");
+  if (count < 0) return fail(OC_EINVAL, "oc_relu: negative count");
+  OC_CHECK_HIP(oci::launch_relu(data, count, as_stream(stream)), "oc_relu");
+  return OC_OK;
+}
+
+}  // extern "C"

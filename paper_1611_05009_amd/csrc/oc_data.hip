@@ -1,0 +1,242 @@
+// Feature kernels: oc2ten / ten2oc (Eq. 4-5), 2x2x2 max-pooling data
+// (Eq. 10), 2x2x2 unpooling data (Eq. 12 and its guided variant), ReLU.
+#include "oc_internal.h"
+
+using namespace ocd;
+
+namespace {
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+// Eq. 4: one thread per voxel copies the c features of the leaf holding it.
+__global__ void k_oc2ten(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                         int64_t n_vox, int gd, int gh, int gw, const float* __restrict__ data,
+                         int c, float* __restrict__ dense) {
+  const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= n_vox) return;
+  const int64_t W = 8LL * gw, H = 8LL * gh, D = 8LL * gd;
+  int64_t r = v;
+  const int vw = (int)(r % W); r /= W;
+  const int vh = (int)(r % H); r /= H;
+  const int vd = (int)(r % D); r /= D;
+  const int64_t t = ((r * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
+  const Bits b = load_bits(trees, t);
+  const int64_t row = prefix[t] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7));
+  const float* src = data + row * c;
+  float* dst = dense + v * c;
+  for (int k = 0; k < c; ++k) dst[k] = src[k];
+}
+
+// Eq. 5: one wave per tree, one lane per leaf; sums in double.
+__global__ void __launch_bounds__(256) k_ten2oc(const uint32_t* __restrict__ trees,
+                                                const int64_t* __restrict__ prefix, int64_t n_trees,
+                                                int gd, int gh, int gw,
+                                                const float* __restrict__ dense, int c, int pool,
+                                                float* __restrict__ data) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_trees) return;
+  const Bits b = load_bits(trees, t);
+  const TreePos p = tree_pos(t, gd, gh, gw);
+  const int64_t W = 8LL * gw, H = 8LL * gh, D = 8LL * gd;
+  const int64_t row0 = prefix[t];
+  int base = 0;
+  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+    const int i = c0 + lane_id();
+    const bool leaf = i < kNodes && is_leaf(b, i);
+    const uint64_t m = __ballot(leaf);
+    if (leaf) {
+      const int64_t row = row0 + base + __popcll(m & lanemask_lt());
+      const Cell cl = cell_of(i);
+      const int64_t vd0 = 8LL * p.d + cl.d, vh0 = 8LL * p.h + cl.h, vw0 = 8LL * p.w + cl.w;
+      for (int k = 0; k < c; ++k) {
+        double acc = 0.0;
+        float mx = -INFINITY;
+        for (int a = 0; a < cl.size; ++a)
+          for (int bb = 0; bb < cl.size; ++bb) {
+            const float* src = dense + (((p.n * D + vd0 + a) * H + vh0 + bb) * W + vw0) * c + k;
+            for (int e = 0; e < cl.size; ++e) {
+              const float x = src[(int64_t)e * c];
+              acc += (double)x;
+              mx = fmaxf(mx, x);
+            }
+          }
+        data[row * c + k] =
+            pool == 0 ? (float)(acc / (double)(cl.size * cl.size * cl.size)) : mx;
+      }
+    }
+    base += __popcll(m);
+  }
+}
+
+// Copy (or max over 8 consecutive rows) of leaf rows, lanes over channels.
+// Each lane first resolves one output leaf of the current 64-position chunk;
+// the wave then walks those leaves one by one.
+__device__ __forceinline__ void copy_rows(uint64_t m, int64_t out_row, int64_t src_row, int nmax,
+                                          const float* __restrict__ in, int c,
+                                          float* __restrict__ out) {
+  while (m) {
+    const int j = __ffsll((unsigned long long)m) - 1;
+    m &= m - 1;
+    const int64_t orow = __shfl(out_row, j, 64);
+    const int64_t srow = __shfl(src_row, j, 64);
+    const int nm = __shfl(nmax, j, 64);
+    for (int k = lane_id(); k < c; k += 64) {
+      const float* s = in + srow * c + k;
+      float v = s[0];
+      for (int r = 1; r < nm; ++r) v = fmaxf(v, s[(int64_t)r * c]);
+      out[orow * c + k] = v;
+    }
+  }
+}
+
+// Eq. 10 data: one wave per output tree.
+__global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ in_trees,
+                                                  const int64_t* __restrict__ in_prefix, int64_t n_out,
+                                                  int gd, int gh, int gw, const float* __restrict__ in,
+                                                  int c, const uint32_t* __restrict__ out_trees,
+                                                  const int64_t* __restrict__ out_prefix,
+                                                  float* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_out) return;
+  const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
+  const Bits ob = load_bits(out_trees, t);
+  const int64_t row0 = out_prefix[t];
+  int base = 0;
+  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+    const int i = c0 + lane_id();
+    const bool leaf = i < kNodes && is_leaf(ob, i);
+    const uint64_t m = __ballot(leaf);
+    int64_t orow = 0, srow = 0;
+    int nmax = 1;
+    if (leaf) {
+      orow = row0 + base + __popcll(m & lanemask_lt());
+      int o, node;
+      if (i < 9) {          // output depth 1 <- input root
+        o = i - 1; node = 0;
+      } else if (i < 73) {  // output depth 2 <- input depth 1
+        o = (i - 9) >> 3; node = 1 + ((i - 9) & 7);
+      } else {              // output depth 3 <- input depth 2 node
+        o = (i - 73) >> 6; node = 9 + ((i - 73) & 63);
+      }
+      const int64_t ti = ((p.n * gd + 2 * p.d + ((o >> 2) & 1)) * gh + 2 * p.h + ((o >> 1) & 1)) * gw +
+                         2 * p.w + (o & 1);
+      const Bits ib = load_bits(in_trees, ti);
+      if (node >= 9 && bit(ib, node)) {  // split depth-2 node: max of its 8 voxels
+        node = 8 * node + 1;
+        nmax = 8;
+      }
+      srow = in_prefix[ti] + data_idx(ib, node);
+    }
+    copy_rows(m, orow, srow, nmax, in, c, out);
+    base += __popcll(m);
+  }
+}
+
+// Eq. 12 data (plain or guided): one wave per output tree.
+__global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_trees,
+                                                const int64_t* __restrict__ in_prefix, int64_t n_out,
+                                                int gd, int gh, int gw, const float* __restrict__ in,
+                                                int c, const uint32_t* __restrict__ out_trees,
+                                                const int64_t* __restrict__ out_prefix,
+                                                float* __restrict__ out) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_out) return;
+  const TreePos p = tree_pos(t, 2 * gd, 2 * gh, 2 * gw);
+  const int o = ((p.d & 1) << 2) | ((p.h & 1) << 1) | (p.w & 1);
+  const int64_t ti = ((p.n * gd + (p.d >> 1)) * gh + (p.h >> 1)) * gw + (p.w >> 1);
+  const Bits ib = load_bits(in_trees, ti);
+  const int64_t in_row0 = in_prefix[ti];
+  const Bits ob = load_bits(out_trees, t);
+  const int64_t row0 = out_prefix[t];
+  int base = 0;
+  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+    const int i = c0 + lane_id();
+    const bool leaf = i < kNodes && is_leaf(ob, i);
+    const uint64_t m = __ballot(leaf);
+    int64_t orow = 0, srow = 0;
+    if (leaf) {
+      orow = row0 + base + __popcll(m & lanemask_lt());
+      int node;
+      if (!(ib.lo & 1ull)) node = 0;                      // unsplit input tree
+      else if (i == 0) node = 1 + o;                      // output root <- input depth 1
+      else if (i < 9) node = 9 + 8 * o + (i - 1);         // depth 1 <- depth 2
+      else if (i < 73) node = 73 + 64 * o + (i - 9);      // depth 2 <- depth-3 voxel
+      else node = 73 + 64 * o + ((i - 73) >> 3);          // guided depth 3 <- same voxel
+      srow = in_row0 + data_idx(ib, node);
+    }
+    copy_rows(m, orow, srow, 1, in, c, out);
+    base += __popcll(m);
+  }
+}
+
+__global__ void k_relu(float* __restrict__ x, int64_t count) {
+  const int64_t n4 = count >> 2;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  float4* x4 = reinterpret_cast<float4*>(x);
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+    float4 v = x4[i];
+    v.x = fmaxf(v.x, 0.f); v.y = fmaxf(v.y, 0.f); v.z = fmaxf(v.z, 0.f); v.w = fmaxf(v.w, 0.f);
+    x4[i] = v;
+  }
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    x[i] = fmaxf(x[i], 0.f);
+}
+
+__global__ void k_relu_scalar(float* __restrict__ x, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    x[i] = fmaxf(x[i], 0.f);
+}
+
+}  // namespace
+
+namespace oci {
+
+hipError_t launch_oc2ten(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, const float* data, int c, float* dense, hipStream_t s) {
+  const int64_t nv = 512LL * n * gd * gh * gw;
+  hipLaunchKernelGGL(k_oc2ten, dim3(blocks_for(nv, 256)), dim3(256), 0, s, trees, prefix, nv, gd,
+                     gh, gw, data, c, dense);
+  return hipGetLastError();
+}
+
+hipError_t launch_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, const float* dense, int c, int pool, float* data, hipStream_t s) {
+  const int64_t nt = (int64_t)n * gd * gh * gw;
+  hipLaunchKernelGGL(k_ten2oc, dim3(blocks_for(nt, 4)), dim3(256), 0, s, trees, prefix, nt, gd, gh,
+                     gw, dense, c, pool, data);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_max(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                           int gh, int gw, const float* in, int c, const uint32_t* out_trees,
+                           const int64_t* out_prefix, float* out, hipStream_t s) {
+  const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
+  hipLaunchKernelGGL(k_pool_max, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
+                     gd, gh, gw, in, c, out_trees, out_prefix, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpool(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                         int gw, const float* in, int c, const uint32_t* out_trees,
+                         const int64_t* out_prefix, float* out, hipStream_t s) {
+  const int64_t no = 8LL * n * gd * gh * gw;
+  hipLaunchKernelGGL(k_unpool, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
+                     gd, gh, gw, in, c, out_trees, out_prefix, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_relu(float* x, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count / 4 + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  if (blocks < 1) blocks = 1;
+  if ((reinterpret_cast<uintptr_t>(x) & 15) != 0) {  // float4 path needs 16-byte alignment
+    hipLaunchKernelGGL(k_relu_scalar, dim3((unsigned)blocks), dim3(256), 0, s, x, count);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_relu, dim3((unsigned)blocks), dim3(256), 0, s, x, count);
+  return hipGetLastError();
+}
+
+}  // namespace oci

@@ -1,0 +1,67 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "oc_device.h"
+
+namespace oci {
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Prefix scan of int32 counts (n entries) into int64 prefix (n + 1 entries).
+// The workspace starts with the counts buffer (scan_counts_buffer).
+size_t scan_workspace(int64_t n);
+int32_t* scan_counts_buffer(void* ws);
+hipError_t scan_counts(const int32_t* counts, int64_t n, int64_t* prefix, void* ws, hipStream_t s);
+
+hipError_t launch_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule,
+                        uint32_t* trees, int32_t* counts, hipStream_t s);
+hipError_t launch_count(const uint32_t* trees, int64_t nt, int32_t* counts, hipStream_t s);
+hipError_t launch_validate(const uint32_t* trees, int64_t nt, int32_t* bad, hipStream_t s);
+hipError_t launch_leaf_index(const uint32_t* trees, const int64_t* prefix, int64_t nt,
+                             uint64_t* info, hipStream_t s);
+hipError_t launch_rowmap(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, int64_t* rowmap, hipStream_t s);
+hipError_t launch_pool_structure(const uint32_t* in, int n, int gd, int gh, int gw, uint32_t* out,
+                                 int32_t* counts, hipStream_t s);
+hipError_t launch_unpool_structure(const uint32_t* in, const uint32_t* guide, int n, int gd, int gh,
+                                   int gw, uint32_t* out, int32_t* counts, int32_t* mismatch,
+                                   hipStream_t s);
+
+hipError_t launch_oc2ten(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, const float* data, int c, float* dense, hipStream_t s);
+hipError_t launch_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, const float* dense, int c, int pool, float* data, hipStream_t s);
+hipError_t launch_pool_max(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                           int gh, int gw, const float* in, int c, const uint32_t* out_trees,
+                           const int64_t* out_prefix, float* out, hipStream_t s);
+hipError_t launch_unpool(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                         int gw, const float* in, int c, const uint32_t* out_trees,
+                         const int64_t* out_prefix, float* out, hipStream_t s);
+hipError_t launch_relu(float* x, int64_t count, hipStream_t s);
+
+// Convolution.
+struct ConvArgs {
+  const uint32_t* trees;
+  const int64_t* prefix;
+  int n, gd, gh, gw;
+  int64_t n_trees, n_leaves;
+  const float* in;
+  int cin;
+  const float* weight;
+  const float* bias;
+  int cout;
+  int relu;
+  float* out;
+};
+size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout);
+bool conv_mfma_supported(int cin, int cout);
+// Structure- and weight-dependent preparation into the workspace (the
+// weight pointer of `a` is read, the features are not).
+hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
+// The convolution proper; impl: 1 generic, 2 mfma (caller checked support).
+hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s);
+
+}  // namespace oci

@@ -1,0 +1,389 @@
+// Structure kernels: octree build, leaf counts and prefix scan, leaf index,
+// voxel->row map, canonical-form check, and the structure side of 2x2x2
+// pooling / unpooling (OctNet Sec. 3.1, Eq. 1-3, Eq. 10, Eq. 12).
+#include "oc_internal.h"
+
+using namespace ocd;
+
+namespace {
+
+constexpr int kScanThreads = 256;
+constexpr int kScanItems = 16;
+constexpr int kScanChunk = kScanThreads * kScanItems;
+
+// ---------------------------------------------------------------------------
+// Build: one wave per tree.  Lane q = 8*o1 + o2 owns the 2x2x2 block of the
+// depth-2 node (o1, o2) (bit 9 + q).  Two ballots (any occupied / all
+// occupied per block) give every split decision of the tree.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_build(const uint8_t* __restrict__ occ, int64_t n_trees,
+                                               int gd, int gh, int gw, int rule,
+                                               uint32_t* __restrict__ trees,
+                                               int32_t* __restrict__ counts) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_trees) return;  // whole wave exits together
+  const int q = lane_id();
+  const TreePos p = tree_pos(t, gd, gh, gw);
+  const int o1 = q >> 3, o2 = q & 7;
+  const int d0 = 4 * ((o1 >> 2) & 1) + 2 * ((o2 >> 2) & 1);
+  const int h0 = 4 * ((o1 >> 1) & 1) + 2 * ((o2 >> 1) & 1);
+  const int w0 = 4 * (o1 & 1) + 2 * (o2 & 1);
+  const int64_t H = 8LL * gh, W = 8LL * gw, D = 8LL * gd;
+  const int64_t vd = 8LL * p.d + d0, vh = 8LL * p.h + h0, vw = 8LL * p.w + w0;
+  const uint8_t* base = occ + ((p.n * D + vd) * H + vh) * W + vw;
+  int any = 0, all = 1;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const uint16_t v = *reinterpret_cast<const uint16_t*>(base + (a * H + b) * W);
+      const int v0 = (v & 0xFF) != 0, v1 = (v >> 8) != 0;
+      any |= v0 | v1;
+      all &= v0 & v1;
+    }
+  const uint64_t A = __ballot(any);
+  const uint64_t L = __ballot(all);
+  const uint64_t split2_ok = rule == 0 ? (A & ~L) : A;
+  int split0 = rule == 0 ? (A != 0ull && L != ~0ull) : (A != 0ull);
+  uint32_t s1 = 0;
+  uint64_t s2 = 0;
+  if (split0) {
+#pragma unroll
+    for (int o = 0; o < 8; ++o) {
+      const uint32_t ga = (uint32_t)((A >> (8 * o)) & 0xFFull);
+      const uint32_t gl = (uint32_t)((L >> (8 * o)) & 0xFFull);
+      const int sp = rule == 0 ? (ga != 0u && gl != 0xFFu) : (ga != 0u);
+      if (sp) {
+        s1 |= 1u << o;
+        s2 |= split2_ok & (0xFFull << (8 * o));
+      }
+    }
+  }
+  if (q == 0) {
+    const uint64_t lo = (uint64_t)split0 | ((uint64_t)s1 << 1) | (s2 << 9);
+    const uint32_t hi = (uint32_t)(s2 >> 55);
+    uint4 w;
+    w.x = (uint32_t)lo;
+    w.y = (uint32_t)(lo >> 32);
+    w.z = hi;
+    w.w = 0u;
+    reinterpret_cast<uint4*>(trees)[t] = w;
+    counts[t] = 1 + 7 * (split0 + __popc(s1) + __popcll(s2));
+  }
+}
+
+__global__ void k_count(const uint32_t* __restrict__ trees, int64_t n_trees,
+                        int32_t* __restrict__ counts) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_trees) return;
+  counts[t] = n_leaves_of(load_bits(trees, t));
+}
+
+__global__ void k_validate(const uint32_t* __restrict__ trees, int64_t n_trees,
+                           int32_t* __restrict__ n_bad) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_trees) return;
+  const uint4 w = reinterpret_cast<const uint4*>(trees)[t];
+  int ok = (w.z >> 9) == 0u && w.w == 0u;
+  const Bits b = load_bits(trees, t);
+  // every set bit i >= 1 needs its parent set
+  for (int i = 1; i < kBits && ok; ++i)
+    if (bit(b, i) && !bit(b, (i - 1) >> 3)) ok = 0;
+  if (!ok) atomicAdd(n_bad, 1);
+}
+
+// ---------------------------------------------------------------------------
+// Exclusive scan of int32 counts into int64 prefix (three passes).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t u = __shfl_up(v, off, 64);
+    if (l >= off) v += u;
+  }
+  return v;
+}
+
+// Exclusive scan of one value per thread over a 256-thread block.
+__device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t* sh_waves, int64_t* total) {
+  const int wv = threadIdx.x >> 6;
+  const int64_t incl = wave_incl_scan(v);
+  if (lane_id() == 63) sh_waves[wv] = incl;
+  __syncthreads();
+  int64_t off = 0, tot = 0;
+  for (int k = 0; k < (int)(blockDim.x >> 6); ++k) {
+    if (k < wv) off += sh_waves[k];
+    tot += sh_waves[k];
+  }
+  __syncthreads();
+  *total = tot;
+  return off + incl - v;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const int32_t* __restrict__ counts,
+                                                              int64_t n, int64_t* __restrict__ sums) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k)
+    if (base + k < n) s += counts[base + k];
+  int64_t tot;
+  block_excl_scan(s, sh, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+// Single block: exclusive scan of the per-chunk sums in place; total -> *total.
+__global__ void __launch_bounds__(kScanThreads) k_scan_sums(int64_t* __restrict__ sums, int64_t nb,
+                                                            int64_t* __restrict__ total) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  int64_t carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
+    const int64_t i = b0 + threadIdx.x;
+    const int64_t v = i < nb ? sums[i] : 0;
+    int64_t tot;
+    const int64_t ex = block_excl_scan(v, sh, &tot);
+    if (i < nb) sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_apply(const int32_t* __restrict__ counts,
+                                                             int64_t n, const int64_t* __restrict__ sums,
+                                                             int64_t* __restrict__ prefix) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    v[k] = base + k < n ? counts[base + k] : 0;
+    s += v[k];
+  }
+  int64_t tot;
+  int64_t run = block_excl_scan(s, sh, &tot) + sums[blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    if (base + k < n) prefix[base + k] = run;
+    run += v[k];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Leaf index: one wave per tree enumerates its leaves in ascending bit index
+// (breadth-first, the order Eq. 3 counts) with ballots over 64 positions.
+// ---------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_leaf_index(const uint32_t* __restrict__ trees,
+                                                    const int64_t* __restrict__ prefix,
+                                                    int64_t n_trees, uint64_t* __restrict__ info) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_trees) return;
+  const Bits b = load_bits(trees, t);
+  const int64_t row0 = prefix[t];
+  const uint64_t tag = (uint64_t)t << 10;
+  if (!(b.lo & 1ull)) {
+    if (lane_id() == 0) info[row0] = tag;
+    return;
+  }
+  int base = 0;
+  for (int c0 = 1; c0 < kNodes; c0 += 64) {
+    const int i = c0 + lane_id();
+    const bool leaf = i < kNodes && is_leaf(b, i);
+    const uint64_t m = __ballot(leaf);
+    if (leaf) info[row0 + base + __popcll(m & lanemask_lt())] = tag | (uint64_t)i;
+    base += __popcll(m);
+  }
+}
+
+// rowmap: one thread per voxel.
+__global__ void k_rowmap(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                         int64_t n_vox, int gd, int gh, int gw, int64_t* __restrict__ rowmap) {
+  const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= n_vox) return;
+  const int64_t W = 8LL * gw, H = 8LL * gh, D = 8LL * gd;
+  int64_t r = v;
+  const int vw = (int)(r % W); r /= W;
+  const int vh = (int)(r % H); r /= H;
+  const int vd = (int)(r % D); r /= D;
+  const int64_t t = ((r * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
+  const Bits b = load_bits(trees, t);
+  rowmap[v] = prefix[t] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7));
+}
+
+// ---------------------------------------------------------------------------
+// Pool structure: thread per output tree (Eq. 10).  Input tree of octant o
+// contributes its root bit as output bit 1+o and its depth-1 bits as output
+// bits 9+8o+q; the output root is always split.
+// ---------------------------------------------------------------------------
+__global__ void k_pool_structure(const uint32_t* __restrict__ in, int64_t n_out, int gd, int gh,
+                                 int gw, uint32_t* __restrict__ out, int32_t* __restrict__ counts) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_out) return;
+  const int od = gd / 2, oh = gh / 2, ow = gw / 2;
+  const TreePos p = tree_pos(t, od, oh, ow);
+  uint64_t lo = 1ull;
+  uint32_t hi = 0;
+#pragma unroll
+  for (int o = 0; o < 8; ++o) {
+    const int a = (o >> 2) & 1, bb = (o >> 1) & 1, c = o & 1;
+    const int64_t ti = ((p.n * gd + 2 * p.d + a) * gh + 2 * p.h + bb) * gw + 2 * p.w + c;
+    const Bits ib = load_bits(in, ti);
+    lo |= (ib.lo & 1ull) << (1 + o);
+    const uint64_t d1 = (ib.lo >> 1) & 0xFFull;  // input bits 1..8
+    const int pos = 9 + 8 * o;                   // output bits pos..pos+7
+    if (pos + 8 <= 64) {
+      lo |= d1 << pos;
+    } else if (pos >= 64) {
+      hi |= (uint32_t)(d1 << (pos - 64));
+    } else {
+      lo |= d1 << pos;
+      hi |= (uint32_t)(d1 >> (64 - pos));
+    }
+  }
+  uint4 w;
+  w.x = (uint32_t)lo;
+  w.y = (uint32_t)(lo >> 32);
+  w.z = hi & 0x1FFu;
+  w.w = 0u;
+  reinterpret_cast<uint4*>(out)[t] = w;
+  Bits ob;
+  ob.lo = lo;
+  ob.hi = w.z;
+  counts[t] = n_leaves_of(ob);
+}
+
+// Unpool structure, plain (Eq. 12): thread per output tree.
+__global__ void k_unpool_structure(const uint32_t* __restrict__ in, int64_t n_out, int gd, int gh,
+                                   int gw, uint32_t* __restrict__ out, int32_t* __restrict__ counts) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_out) return;
+  const TreePos p = tree_pos(t, 2 * gd, 2 * gh, 2 * gw);
+  const int o = ((p.d & 1) << 2) | ((p.h & 1) << 1) | (p.w & 1);
+  const int64_t ti = ((p.n * gd + (p.d >> 1)) * gh + (p.h >> 1)) * gw + (p.w >> 1);
+  const Bits ib = load_bits(in, ti);
+  uint32_t word = 0;
+  if ((ib.lo & 1ull) && bit(ib, 1 + o)) {
+    word = 1u;
+    for (int q = 0; q < 8; ++q) word |= (uint32_t)bit(ib, 9 + 8 * o + q) << (1 + q);
+  }
+  uint4 w;
+  w.x = word;
+  w.y = w.z = w.w = 0u;
+  reinterpret_cast<uint4*>(out)[t] = w;
+  counts[t] = 1 + 7 * __popc(word);
+}
+
+// Guided unpool: copy the guide and check that it pools to the input.
+__global__ void k_unpool_guided(const uint32_t* __restrict__ in, const uint32_t* __restrict__ guide,
+                                int64_t n_in, int gd, int gh, int gw, uint32_t* __restrict__ out,
+                                int32_t* __restrict__ counts, int32_t* __restrict__ mismatch) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // input tree
+  if (t >= n_in) return;
+  const TreePos p = tree_pos(t, gd, gh, gw);
+  const int Gd = 2 * gd, Gh = 2 * gh, Gw = 2 * gw;
+  uint64_t lo = 1ull;
+  uint32_t hi = 0;
+  for (int o = 0; o < 8; ++o) {
+    const int a = (o >> 2) & 1, bb = (o >> 1) & 1, c = o & 1;
+    const int64_t tg = ((p.n * Gd + 2 * p.d + a) * Gh + 2 * p.h + bb) * Gw + 2 * p.w + c;
+    const uint4 gw4 = reinterpret_cast<const uint4*>(guide)[tg];
+    reinterpret_cast<uint4*>(out)[tg] = gw4;
+    Bits gb;
+    gb.lo = (uint64_t)gw4.x | ((uint64_t)gw4.y << 32);
+    gb.hi = gw4.z & 0x1FFu;
+    counts[tg] = n_leaves_of(gb);
+    lo |= (gb.lo & 1ull) << (1 + o);
+    for (int q = 0; q < 8; ++q) {
+      const int pos = 9 + 8 * o + q;
+      const uint64_t v = (gb.lo >> (1 + q)) & 1ull;
+      if (pos < 64) lo |= v << pos;
+      else hi |= (uint32_t)v << (pos - 64);
+    }
+  }
+  const uint4 iw = reinterpret_cast<const uint4*>(in)[t];
+  const uint64_t ilo = (uint64_t)iw.x | ((uint64_t)iw.y << 32);
+  if (ilo != lo || (iw.z & 0x1FFu) != hi) atomicAdd(mismatch, 1);
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+namespace oci {
+
+size_t scan_workspace(int64_t n) {
+  const int64_t nb = (n + kScanChunk - 1) / kScanChunk;
+  return align256(sizeof(int32_t) * (size_t)n) + align256(sizeof(int64_t) * (size_t)(nb + 1)) + 256;
+}
+
+hipError_t scan_counts(const int32_t* counts, int64_t n, int64_t* prefix, void* ws,
+                       hipStream_t s) {
+  const int64_t nb = (n + kScanChunk - 1) / kScanChunk;
+  char* p = static_cast<char*>(ws) + align256(sizeof(int32_t) * (size_t)n);
+  int64_t* sums = reinterpret_cast<int64_t*>(p);
+  hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, counts, n, sums);
+  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kScanThreads), 0, s, sums, nb, prefix + n);
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kScanThreads), 0, s, counts, n, sums, prefix);
+  return hipGetLastError();
+}
+
+int32_t* scan_counts_buffer(void* ws) { return static_cast<int32_t*>(ws); }
+
+hipError_t launch_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule,
+                        uint32_t* trees, int32_t* counts, hipStream_t s) {
+  const int64_t nt = (int64_t)n * gd * gh * gw;
+  hipLaunchKernelGGL(k_build, dim3(blocks_for(nt, 4)), dim3(256), 0, s, occ, nt, gd, gh, gw, rule,
+                     trees, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_count(const uint32_t* trees, int64_t nt, int32_t* counts, hipStream_t s) {
+  hipLaunchKernelGGL(k_count, dim3(blocks_for(nt, 256)), dim3(256), 0, s, trees, nt, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_validate(const uint32_t* trees, int64_t nt, int32_t* bad, hipStream_t s) {
+  hipLaunchKernelGGL(k_validate, dim3(blocks_for(nt, 256)), dim3(256), 0, s, trees, nt, bad);
+  return hipGetLastError();
+}
+
+hipError_t launch_leaf_index(const uint32_t* trees, const int64_t* prefix, int64_t nt,
+                             uint64_t* info, hipStream_t s) {
+  hipLaunchKernelGGL(k_leaf_index, dim3(blocks_for(nt, 4)), dim3(256), 0, s, trees, prefix, nt, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_rowmap(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                         int gw, int64_t* rowmap, hipStream_t s) {
+  const int64_t nv = 512LL * n * gd * gh * gw;
+  hipLaunchKernelGGL(k_rowmap, dim3(blocks_for(nv, 256)), dim3(256), 0, s, trees, prefix, nv, gd,
+                     gh, gw, rowmap);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_structure(const uint32_t* in, int n, int gd, int gh, int gw, uint32_t* out,
+                                 int32_t* counts, hipStream_t s) {
+  const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
+  hipLaunchKernelGGL(k_pool_structure, dim3(blocks_for(no, 256)), dim3(256), 0, s, in, no, gd, gh,
+                     gw, out, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpool_structure(const uint32_t* in, const uint32_t* guide, int n, int gd, int gh,
+                                   int gw, uint32_t* out, int32_t* counts, int32_t* mismatch,
+                                   hipStream_t s) {
+  if (guide == nullptr) {
+    const int64_t no = 8LL * n * gd * gh * gw;
+    hipLaunchKernelGGL(k_unpool_structure, dim3(blocks_for(no, 256)), dim3(256), 0, s, in, no, gd,
+                       gh, gw, out, counts);
+  } else {
+    const int64_t ni = (int64_t)n * gd * gh * gw;
+    hipLaunchKernelGGL(k_unpool_guided, dim3(blocks_for(ni, 256)), dim3(256), 0, s, in, guide, ni,
+                       gd, gh, gw, out, counts, mismatch);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace oci

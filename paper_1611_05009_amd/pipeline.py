@@ -1,0 +1,106 @@
+"""One pass of the grid-octree hot path over a workload's batch.
+
+A step builds the octree from the resident occupancy grid, forms the input
+leaf features (ten2oc of a dense input, or resident per-leaf features), and
+runs the layer stack (conv3x3x3 with fused bias/ReLU, 2x2x2 max-pooling,
+plain or guided 2x2x2 unpooling).  Every op is a call into the HIP library.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+from . import octnet as oc
+from . import synth
+
+
+@dataclass
+class OpRecord:
+    op: str
+    g_in: oc.Octree
+    x_in: torch.Tensor
+    g_out: oc.Octree
+    x_out: torch.Tensor
+    params: dict = field(default_factory=dict)
+
+
+class Workload:
+    """Inputs of one workload, resident on the GPU, and its layer stack."""
+
+    def __init__(self, key: str, batch: int | None = None, device: str = "cuda"):
+        self.key = key
+        self.wl = synth.WORKLOADS[key]
+        self.batch = self.wl.batch if batch is None else batch
+        self.device = torch.device(device)
+        wl = self.wl
+        if wl.dense_features:
+            if key == "c1":
+                occ = synth.occupancy(wl, batch=self.batch)
+                dense = occ[..., None].astype(np.float32)
+            else:
+                occ, dense = synth.facade_input(wl, batch=self.batch)
+            self.dense = torch.from_numpy(dense).to(self.device)
+        else:
+            occ = synth.occupancy(wl, batch=self.batch)
+            self.dense = None
+        self.occ_np = occ
+        self.occ = torch.from_numpy(occ).to(self.device)
+        g = oc.build(self.occ)
+        self.n_leaves = g.n_leaves
+        self.features = None
+        if not wl.dense_features:
+            self.features = torch.from_numpy(synth.leaf_features(wl, g.n_leaves, wl.cin)).to(self.device)
+        # Conv layers with their fused ReLU flags.
+        self.layers = []
+        k = 0
+        ops = wl.layers
+        for i, L in enumerate(ops):
+            if L.op == "relu":
+                continue
+            if L.op == "conv":
+                w, b = synth.conv_weights(wl, k, L.cin, L.cout)
+                relu = i + 1 < len(ops) and ops[i + 1].op == "relu"
+                self.layers.append(("conv", dict(w=torch.from_numpy(w).to(self.device),
+                                                 b=torch.from_numpy(b).to(self.device),
+                                                 cin=L.cin, cout=L.cout, relu=relu, index=k)))
+                k += 1
+            else:
+                self.layers.append((L.op, {}))
+
+    @property
+    def dense_voxels(self) -> int:
+        return int(np.prod(self.occ_np.shape))
+
+
+def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: str = "auto"):
+    """One pass of the hot path.  Returns (structure, features) at the end.
+    conv_timer(start_event, end_event) brackets each convolution proper."""
+    g = oc.build(W.occ)
+    x = oc.ten2oc(g, W.dense, "avg") if W.dense is not None else W.features
+    if records is not None:
+        records.append(OpRecord("input", g, x, g, x))
+    guides = []
+    for op, p in W.layers:
+        g_in, x_in = g, x
+        if op == "conv":
+            ws = oc.conv3x3x3_prepare(g, p["w"])
+            if conv_timer is not None:
+                s, e = conv_timer()
+                s.record()
+            x = oc.conv3x3x3_execute(g, x, p["cout"], ws, p["b"], relu=p["relu"], impl=impl)
+            if conv_timer is not None:
+                e.record()
+        elif op == "pool":
+            guides.append(g)
+            g, x = oc.pool2(g, x)
+        elif op == "unpool":
+            g, x = oc.unpool2(g, x)
+        elif op == "unpool_guided":
+            g, x = oc.unpool2(g, x, guide=guides.pop())
+        else:
+            raise ValueError(op)
+        if records is not None:
+            records.append(OpRecord(op, g_in, x_in, g, x, p))
+    return g, x
