@@ -222,44 +222,61 @@ __device__ void window_sums(const LeafGeo& g, const uint32_t* __restrict__ trees
 }
 
 // ---------------------------------------------------------------------------
-// Generic kernel: tile of `tm` consecutive rows per block.  Waves compute
-// window sums into LDS, then all threads run the VALU contraction.
+// Generic kernel: tiles of `tm` rows, taken from `rows_list` (its length in
+// *n_list) or, without a list, rows 0..n_leaves-1.  Waves compute window sums
+// into LDS, then all threads run the VALU contraction.  Grid-stride over
+// tiles, so the grid does not depend on the list length.
 // ---------------------------------------------------------------------------
 __global__ void __launch_bounds__(kThreads) k_conv_generic(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
     const uint64_t* __restrict__ info, int64_t n_leaves, int gd, int gh, int gw,
     const float* __restrict__ in, int cin, const float* __restrict__ wt,
-    const float* __restrict__ bias, int cout, int relu, float* __restrict__ out, int tm) {
+    const float* __restrict__ bias, int cout, int relu, float* __restrict__ out, int tm,
+    const int32_t* __restrict__ rows_list, const int64_t* __restrict__ n_list) {
   extern __shared__ float smem[];
-  // layout: [4 waves][kSlots] entries, [4][27] counts, [tm][27*cin] sums, [tm] scale
+  // layout: [4 waves][kSlots] entries, [4][32] counts, [tm] rows, [tm][27*cin] sums, [tm] scale
   Entry* slots_all = reinterpret_cast<Entry*>(smem);
   int* counts_all = reinterpret_cast<int*>(slots_all + 4 * kSlots);
-  float* sums = reinterpret_cast<float*>(counts_all + 4 * 32);
+  int64_t* rowv = reinterpret_cast<int64_t*>(counts_all + 4 * 32);
+  float* sums = reinterpret_cast<float*>(rowv + 32);
   float* scale = sums + (int64_t)tm * 27 * cin;
   const int wv = threadIdx.x >> 6;
-  const int64_t row_base = (int64_t)blockIdx.x * tm;
-  for (int m = wv; m < tm; m += 4) {
-    const int64_t row = row_base + m;
-    if (row < n_leaves) {
-      const LeafGeo g = leaf_geo(info[row], row, gd, gh, gw);
-      window_sums(g, trees, prefix, gd, gh, gw, in, cin, slots_all + wv * kSlots,
-                  counts_all + wv * 32, sums + (int64_t)m * 27 * cin);
-      if (lane_id() == 0) scale[m] = 1.f / (float)(g.s * g.s * g.s);
-    }
-    __builtin_amdgcn_wave_barrier();
-  }
-  __syncthreads();
+  const int64_t n_rows = rows_list ? *n_list : n_leaves;
+  const int64_t n_tiles = (n_rows + tm - 1) / tm;
   const int K = 27 * cin;
-  for (int idx = threadIdx.x; idx < tm * cout; idx += kThreads) {
-    const int m = idx / cout, co = idx % cout;
-    const int64_t row = row_base + m;
-    if (row >= n_leaves) continue;
-    const float* sm = sums + (int64_t)m * K;
-    float acc = 0.f;
-    for (int k = 0; k < K; ++k) acc = fmaf(sm[k], wt[(int64_t)k * cout + co], acc);
-    float v = acc * scale[m] + (bias ? bias[co] : 0.f);
-    if (relu) v = fmaxf(v, 0.f);
-    out[row * cout + co] = v;
+  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const int64_t base = tile * tm;
+    for (int m = wv; m < tm; m += 4) {
+      const int64_t idx = base + m;
+      if (idx < n_rows) {
+        const int64_t row = rows_list ? (int64_t)rows_list[idx] : idx;
+        if (row < 0 || row >= n_leaves) {  // only a non-canonical structure gets here
+          if (lane_id() == 0) rowv[m] = -1;
+          __builtin_amdgcn_wave_barrier();
+          continue;
+        }
+        const LeafGeo g = leaf_geo(info[row], row, gd, gh, gw);
+        window_sums(g, trees, prefix, gd, gh, gw, in, cin, slots_all + wv * kSlots,
+                    counts_all + wv * 32, sums + (int64_t)m * K);
+        if (lane_id() == 0) {
+          scale[m] = 1.f / (float)(g.s * g.s * g.s);
+          rowv[m] = row;
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < tm * cout; idx += kThreads) {
+      const int m = idx / cout, co = idx % cout;
+      if (base + m >= n_rows || rowv[m] < 0) continue;
+      const float* sm = sums + (int64_t)m * K;
+      float acc = 0.f;
+      for (int k = 0; k < K; ++k) acc = fmaf(sm[k], wt[(int64_t)k * cout + co], acc);
+      float v = acc * scale[m] + (bias ? bias[co] : 0.f);
+      if (relu) v = fmaxf(v, 0.f);
+      out[rowv[m] * cout + co] = v;
+    }
+    __syncthreads();  // the next tile reuses the LDS
   }
 }
 
@@ -273,8 +290,8 @@ int generic_tile(int cin) {
 }
 
 size_t generic_smem(int cin, int tm) {
-  return sizeof(Entry) * 4 * kSlots + sizeof(int) * 4 * 32 + sizeof(float) * (size_t)tm * 27 * cin +
-         sizeof(float) * tm;
+  return sizeof(Entry) * 4 * kSlots + sizeof(int) * 4 * 32 + sizeof(int64_t) * 32 +
+         sizeof(float) * (size_t)tm * 27 * cin + sizeof(float) * tm;
 }
 
 bool g_slots_ready = false;
@@ -294,52 +311,462 @@ hipError_t init_slots() {
   return e;
 }
 
+// ---------------------------------------------------------------------------
+// Unit-voxel groups.
+// In breadth-first order the leaves of a tree with bit index < 73 (cells of
+// edge 2, 4, 8) come first, then the depth-3 voxels, eight consecutive rows
+// per split depth-2 node in ascending node order.  A group is one split
+// depth-2 node: key = tree << 6 | (node - 9); its rows are
+// prefix[tree] + n_big(tree) + 8k .. +8 for the k-th split depth-2 node.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int depth2_splits(const Bits& b) {
+  return __popcll(b.lo >> 9) + __popc(b.hi);
+}
+
+__global__ void k_group_count(const uint32_t* __restrict__ trees, int64_t n_trees,
+                              int32_t* __restrict__ n_grp, int32_t* __restrict__ n_big) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_trees) return;
+  const Bits b = load_bits(trees, t);
+  const int g = depth2_splits(b);
+  n_grp[t] = g;
+  n_big[t] = max(0, n_leaves_of(b) - 8 * g);
+}
+
+__global__ void k_group_fill(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                             const int64_t* __restrict__ gpre, const int64_t* __restrict__ bpre,
+                             int64_t n_trees, int64_t* __restrict__ gkey,
+                             int32_t* __restrict__ brow, int64_t gcap, int64_t bcap) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n_trees) return;
+  const Bits b = load_bits(trees, t);
+  const int64_t row0 = prefix[t];
+  // The capacities only matter for a non-canonical structure, whose counts
+  // need not match the leaf total the buffers were sized for.
+  for (int64_t k = bpre[t]; k < bpre[t + 1] && k < bcap; ++k) brow[k] = (int32_t)(row0 + k - bpre[t]);
+  int64_t k = gpre[t];
+  uint64_t m = b.lo >> 9;  // bits 9..63 -> positions 0..54
+  while (m && k < gcap) {
+    const int q = __ffsll((unsigned long long)m) - 1;
+    m &= m - 1;
+    gkey[k++] = (t << 6) | q;
+  }
+  uint32_t h = b.hi;  // bits 64..72 -> q = 55..63
+  while (h && k < gcap) {
+    const int q = __ffs(h) - 1;
+    h &= h - 1;
+    gkey[k++] = (t << 6) | (55 + q);
+  }
+}
+
+__global__ void k_zero(float* __restrict__ x, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) x[i] = 0.f;
+}
+
+// Row of the leaf holding voxel u (u = 16 ud + 4 uh + uw, each in 0..3) of
+// the 4^3 neighbourhood [p-1, p+3) of the group's 2^3 block at origin p;
+// -1 outside the grid (zero padding).
+__device__ __forceinline__ int32_t neighbour_row(const uint32_t* __restrict__ trees,
+                                                 const int64_t* __restrict__ prefix, int gd, int gh,
+                                                 int gw, int64_t key, int u) {
+  const int64_t t = key >> 6;
+  const int q = (int)(key & 63);
+  const TreePos p = tree_pos(t, gd, gh, gw);
+  const int o1 = q >> 3, o2 = q & 7;
+  const int vd = 8 * p.d + 4 * ((o1 >> 2) & 1) + 2 * ((o2 >> 2) & 1) - 1 + (u >> 4);
+  const int vh = 8 * p.h + 4 * ((o1 >> 1) & 1) + 2 * ((o2 >> 1) & 1) - 1 + ((u >> 2) & 3);
+  const int vw = 8 * p.w + 4 * (o1 & 1) + 2 * (o2 & 1) - 1 + (u & 3);
+  if (vd < 0 || vh < 0 || vw < 0 || vd >= 8 * gd || vh >= 8 * gh || vw >= 8 * gw) return -1;
+  const int64_t tt = ((p.n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
+  const Bits b = load_bits(trees, tt);
+  return (int32_t)(prefix[tt] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7)));
+}
+
+// ---------------------------------------------------------------------------
+// MFMA kernel for unit voxels.
+//
+// A wave owns a tile of MS rows = MS/8 groups.  For a unit voxel the window
+// sum S_delta is the input row of the leaf holding voxel o + delta, so the
+// contraction out = sum_delta W[1-delta] x(o+delta) is an implicit GEMM
+// (M = rows, K = 27 cin, N = cout) whose A rows are gathered from the input.
+//   MS = 32: v_mfma_f32_32x32x2_f32, lane l: A row l%32, k-slot l/32,
+//            B column l%32; D[8(r/4) + 4(l/32) + r%4][l%32] in register r.
+//   MS = 16: v_mfma_f32_16x16x4_f32, lane l: A row l%16, k-slot l/16,
+//            B column l%16; D[4(l/16) + r][l%16] in register r.
+// The K index (delta, ci) is ordered so that lane slot g feeds channels
+// CH*g .. CH*g + CH - 1 of every delta: one contiguous vector load per row.
+// Weights live in LDS already in B-operand order; NT N-tiles of MS columns
+// cover cout (padded with zero weights).
+// ---------------------------------------------------------------------------
+template <int CIN, int NT, int MS>
+struct MfmaCfg {
+  static constexpr int KS = MS == 32 ? 2 : 4;  // k-slots per MFMA
+  static constexpr int CH = CIN / KS;          // channels per lane per delta
+  static constexpr int VEC = CH % 4 == 0 ? 4 : (CH % 2 == 0 ? 2 : 1);
+  static constexpr int NV = CH / VEC;
+  static constexpr int GROUPS = MS / 8;
+  static constexpr int NCOL = MS * NT;
+  static constexpr int WFLOATS = 27 * CIN * NCOL;
+  static_assert(CIN % KS == 0, "cin must split over the k-slots");
+};
+
+template <int V> struct VecT;
+template <> struct VecT<1> { typedef float type; };
+template <> struct VecT<2> { typedef float __attribute__((ext_vector_type(2))) type; };
+template <> struct VecT<4> { typedef float __attribute__((ext_vector_type(4))) type; };
+
+template <int MS> struct AccT;
+template <> struct AccT<32> { typedef float __attribute__((ext_vector_type(16))) type; };
+template <> struct AccT<16> { typedef float __attribute__((ext_vector_type(4))) type; };
+
+template <int MS>
+__device__ __forceinline__ typename AccT<MS>::type mfma(float a, float b, typename AccT<MS>::type c);
+template <>
+__device__ __forceinline__ AccT<32>::type mfma<32>(float a, float b, AccT<32>::type c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+template <>
+__device__ __forceinline__ AccT<16>::type mfma<16>(float a, float b, AccT<16>::type c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int V>
+__device__ __forceinline__ float vget(const typename VecT<V>::type& v, int i) {
+  if constexpr (V == 1) return v;
+  else return v[i];
+}
+
+template <int CIN, int NT, int MS>
+__global__ void __launch_bounds__(512) k_conv_unit_mfma(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    int64_t n_leaves, const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
+    const float* __restrict__ in, const float* __restrict__ wm, const float* __restrict__ zero_row,
+    const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  using Vec = typename VecT<C::VEC>::type;
+  using Acc = typename AccT<MS>::type;
+  extern __shared__ float smem[];
+  float* wl = smem;
+  int32_t* nb_all = reinterpret_cast<int32_t*>(smem + C::WFLOATS);
+  {
+    typedef float __attribute__((ext_vector_type(4))) f4;
+    const f4* src = reinterpret_cast<const f4*>(wm);
+    f4* dst = reinterpret_cast<f4*>(wl);
+    for (int i = threadIdx.x; i < C::WFLOATS / 4; i += blockDim.x) dst[i] = src[i];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nwaves = blockDim.x >> 6;
+  int32_t* nb = nb_all + wave * (C::GROUPS * 64);
+  const int64_t G = min(*n_groups, n_leaves / 8);
+  const int64_t n_tiles = (G + C::GROUPS - 1) / C::GROUPS;
+  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
+  // contiguous run of chunks so that its L2 sees neighbouring groups.
+  const int nblk = gridDim.x;
+  const int xcd_blocks = nblk / 8;
+  const int chunk = (blockIdx.x % 8) * xcd_blocks + blockIdx.x / 8;
+  const int64_t per = (n_tiles + nblk - 1) / nblk;
+  const int64_t t_begin = (int64_t)chunk * per;
+  const int64_t t_end = min(n_tiles, t_begin + per);
+  // Lane roles.
+  const int m = lane % MS, g = lane / MS;
+  const int gi = m >> 3, o3 = m & 7;
+  const int ubase = gi * 64 + ((o3 >> 2) & 1) * 16 + ((o3 >> 1) & 1) * 4 + (o3 & 1);
+  const int col = lane % MS;
+  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
+#pragma unroll
+    for (int q = 0; q < C::GROUPS; ++q) {
+      const int64_t gidx = tile * C::GROUPS + q;
+      int32_t r = gidx < G ? neighbour_row(trees, prefix, gd, gh, gw, gkey[gidx], lane) : -1;
+      if (r >= n_leaves) r = -1;  // only a non-canonical structure gets here
+      nb[q * 64 + lane] = r;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    Acc acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
+    // Software pipeline: the gathered A rows of delta dl+2 and the B operands
+    // of delta dl+1 are in flight while the MFMAs of delta dl issue.  The
+    // scheduling barriers keep the compiler from sinking the loads back to
+    // their use.
+    Vec abuf[3][C::NV];
+    Vec bbuf[2][NT][C::NV];
+    auto load_a = [&](int dl, Vec* a) {
+      const int dd = dl / 9, dh = (dl / 3) % 3, dw = dl % 3;
+      const int row = nb[ubase + dd * 16 + dh * 4 + dw];
+      // Voxels outside the grid read a row of zeros (zero padding).
+      const float* base = row < 0 ? zero_row : in + (int64_t)row * CIN;
+      const Vec* src = reinterpret_cast<const Vec*>(base + C::CH * g);
+#pragma unroll
+      for (int v = 0; v < C::NV; ++v) a[v] = src[v];
+    };
+    auto load_b = [&](int dl, Vec (*b)[C::NV]) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const Vec* bsrc = reinterpret_cast<const Vec*>(wl) + ((dl * NT + nt) * C::NV) * 64 + lane;
+#pragma unroll
+        for (int v = 0; v < C::NV; ++v) b[nt][v] = bsrc[v * 64];
+      }
+    };
+    load_a(0, abuf[0]);
+    load_a(1, abuf[1]);
+    load_b(0, bbuf[0]);
+#pragma unroll
+    for (int dl = 0; dl < 27; ++dl) {
+      if (dl + 2 < 27) load_a(dl + 2, abuf[(dl + 2) % 3]);
+      if (dl + 1 < 27) load_b(dl + 1, bbuf[(dl + 1) % 2]);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int v = 0; v < C::NV; ++v)
+#pragma unroll
+          for (int e = 0; e < C::VEC; ++e)
+            acc[nt] = mfma<MS>(vget<C::VEC>(abuf[dl % 3][v], e),
+                               vget<C::VEC>(bbuf[dl % 2][nt][v], e), acc[nt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // Epilogue: unit cells need no 1/s^3 scaling.
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int co = MS * nt + col;
+      const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
+        const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
+        const int row0 = nb[(i >> 3) * 64 + 21];  // voxel (1,1,1): first row of the group
+        if (row0 < 0 || row0 + 8 > n_leaves || co >= cout) continue;
+        float v = acc[nt][r] + bv;
+        if (relu) v = fmaxf(v, 0.f);
+        out[(int64_t)(row0 + (i & 7)) * cout + co] = v;
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // nb is rewritten by the next tile
+  }
+}
+
+// Weights in B-operand order: for delta index dl, N-tile nt, vector jv, lane
+// and element e: column co = MS*nt + lane%MS, channel ci = CH*(lane/MS) +
+// VEC*jv + e, tap 26 - dl (Eq. 7 pairs input offset delta with tap 1 - delta).
+template <int CIN, int NT, int MS>
+__global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __restrict__ wm) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= C::WFLOATS) return;
+  int r = idx;
+  const int e = r % C::VEC; r /= C::VEC;
+  const int lane = r % 64; r /= 64;
+  const int jv = r % C::NV; r /= C::NV;
+  const int nt = r % NT; r /= NT;
+  const int dl = r;
+  const int co = MS * nt + lane % MS;
+  const int ci = C::CH * (lane / MS) + C::VEC * jv + e;
+  wm[idx] = co < cout ? w[((int64_t)co * CIN + ci) * 27 + (26 - dl)] : 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// Instantiated channel pairs.
+// ---------------------------------------------------------------------------
+typedef void (*MfmaFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const int64_t*,
+                       const int64_t*, const float*, const float*, const float*, const float*, int,
+                       int, float*);
+typedef void (*WeightFn)(const float*, int, float*);
+
+struct MfmaVariant {
+  int cin, cout_max, cout_min, ms, nt;
+  size_t wfloats;
+  MfmaFn kernel;
+  WeightFn weights;
+  int weight_total;
+};
+
+template <int CIN, int NT, int MS>
+MfmaVariant make_variant(int cout_min) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  MfmaVariant v;
+  v.cin = CIN;
+  v.cout_max = C::NCOL;
+  v.cout_min = cout_min;
+  v.ms = MS;
+  v.nt = NT;
+  v.wfloats = C::WFLOATS;
+  v.kernel = &k_conv_unit_mfma<CIN, NT, MS>;
+  v.weights = &k_mfma_weights<CIN, NT, MS>;
+  v.weight_total = C::WFLOATS;
+  return v;
+}
+
+// cout in [cout_min, cout_max]; 32-wide tiles for cout 17..32, 16-wide ones
+// for cout 5..16 (narrower outputs use the generic kernel).
+const MfmaVariant* find_variant(int cin, int cout) {
+  static const MfmaVariant table[] = {
+      make_variant<32, 1, 32>(17), make_variant<16, 1, 32>(17), make_variant<8, 1, 32>(17),
+      make_variant<4, 1, 32>(17),  make_variant<32, 1, 16>(5),  make_variant<16, 1, 16>(5),
+      make_variant<8, 1, 16>(5),   make_variant<4, 1, 16>(5),
+  };
+  for (const MfmaVariant& v : table)
+    if (v.cin == cin && cout >= v.cout_min && cout <= v.cout_max) return &v;
+  return nullptr;
+}
+
+constexpr int kMfmaThreads = 512;
+
+size_t mfma_smem(const MfmaVariant& v) {
+  return sizeof(float) * v.wfloats + sizeof(int32_t) * (kMfmaThreads / 64) * (v.ms / 8) * 64;
+}
+
+int g_num_cus = 0;
+size_t g_max_smem = 0;
+
+hipError_t device_limits() {
+  if (g_num_cus > 0) return hipSuccess;
+  int dev = 0, cus = 0, smem = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+  if (e != hipSuccess) return e;
+  g_num_cus = cus;
+  g_max_smem = (size_t)smem;
+  return hipSuccess;
+}
+
+// Workspace layout (each part 256-byte aligned):
+//   leaf_info  u64 [n_leaves]
+//   wt         f32 [27 cin cout]            generic-kernel weights
+//   wm         f32 [variant wfloats]        MFMA B operands (if a variant exists)
+//   scan_g     scan workspace (n_trees)     groups per tree -> gpre
+//   gpre       i64 [n_trees + 1]
+//   scan_b     scan workspace (n_trees)     big leaves per tree -> bpre
+//   bpre       i64 [n_trees + 1]
+//   gkey       i64 [n_leaves / 8 + 1]
+//   brow       i32 [n_leaves]
+//   zero       f32 [cin]                    a row of zeros (padding reads)
+struct ConvWs {
+  uint64_t* info;
+  float* wt;
+  float* wm;
+  char* scan_g;
+  int64_t* gpre;
+  char* scan_b;
+  int64_t* bpre;
+  int64_t* gkey;
+  int32_t* brow;
+  float* zero;
+  size_t total;
+};
+
+ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
+  using oci::align256;
+  char* p = static_cast<char*>(base);
+  size_t off = 0;
+  ConvWs w;
+  auto take = [&](size_t bytes) {
+    char* q = p ? p + off : nullptr;
+    off += align256(bytes);
+    return q;
+  };
+  const MfmaVariant* v = find_variant(cin, cout);
+  w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
+  w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
+  w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
+  w.scan_g = take(oci::scan_workspace(n_trees));
+  w.gpre = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
+  w.scan_b = take(oci::scan_workspace(n_trees));
+  w.bpre = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
+  w.gkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_leaves / 8 + 1)));
+  w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
+  w.zero = reinterpret_cast<float*>(take(sizeof(float) * (size_t)cin));
+  w.total = off + 256;
+  return w;
+}
+
 }  // namespace
 
 namespace oci {
 
 size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout) {
-  (void)n_trees;
-  return align256(sizeof(uint64_t) * (size_t)n_leaves) + align256(sizeof(float) * 27 * (size_t)cin * cout) +
-         256;
+  return carve(nullptr, n_trees, n_leaves, cin, cout).total;
 }
 
 bool conv_mfma_supported(int cin, int cout) {
-  (void)cin;
-  (void)cout;
-  return false;
+  const MfmaVariant* v = find_variant(cin, cout);
+  if (!v) return false;
+  // LDS: the whole weight set plus the neighbourhood rows of every wave must
+  // fit one workgroup (160 KB on gfx950; the device is asked when present).
+  const size_t limit = device_limits() == hipSuccess ? g_max_smem : 160 * 1024;
+  return mfma_smem(*v) <= limit;
 }
 
-// Workspace: [leaf_info: n_leaves x u64 | transposed weights: 27 cin cout f32]
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipError_t e = init_slots();
   if (e != hipSuccess) return e;
-  char* p = static_cast<char*>(ws);
-  uint64_t* info = reinterpret_cast<uint64_t*>(p);
-  p += align256(sizeof(uint64_t) * (size_t)a.n_leaves);
-  float* wt = reinterpret_cast<float*>(p);
-  e = launch_leaf_index(a.trees, a.prefix, a.n_trees, info, s);
+  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
+  e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
   if (e != hipSuccess) return e;
   const int64_t nw = 27LL * a.cin * a.cout;
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
-                     a.weight, a.cin, a.cout, wt);
+                     a.weight, a.cin, a.cout, w.wt);
+  const MfmaVariant* v = find_variant(a.cin, a.cout);
+  if (v == nullptr) return hipGetLastError();
+  hipLaunchKernelGGL(v->weights,
+                     dim3((unsigned)((v->weight_total + 255) / 256)), dim3(256), 0, s, a.weight,
+                     a.cout, w.wm);
+  const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
+  hipLaunchKernelGGL(k_group_count, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees,
+                     scan_counts_buffer(w.scan_g), scan_counts_buffer(w.scan_b));
+  e = scan_counts(scan_counts_buffer(w.scan_g), a.n_trees, w.gpre, w.scan_g, s);
+  if (e != hipSuccess) return e;
+  e = scan_counts(scan_counts_buffer(w.scan_b), a.n_trees, w.bpre, w.scan_b, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_group_fill, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.gpre, w.bpre,
+                     a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1, a.n_leaves);
+  hipLaunchKernelGGL(k_zero, dim3((unsigned)((a.cin + 255) / 256)), dim3(256), 0, s, w.zero,
+                     (int64_t)a.cin);
   return hipGetLastError();
 }
 
 hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s) {
-  (void)impl;
   hipError_t e = init_slots();
   if (e != hipSuccess) return e;
-  const char* p = static_cast<const char*>(ws);
-  const uint64_t* info = reinterpret_cast<const uint64_t*>(p);
-  p += align256(sizeof(uint64_t) * (size_t)a.n_leaves);
-  const float* wt = reinterpret_cast<const float*>(p);
+  const ConvWs w = carve(const_cast<void*>(ws), a.n_trees, a.n_leaves, a.cin, a.cout);
+  // The MFMA kernel reads input rows with 16-byte vector loads.
+  if (impl == 2 && (reinterpret_cast<uintptr_t>(a.in) & 15) != 0) impl = 1;
   const int tm = generic_tile(a.cin);
-  const size_t smem = generic_smem(a.cin, tm);
-  const int64_t blocks = (a.n_leaves + tm - 1) / tm;
-  hipLaunchKernelGGL(k_conv_generic, dim3((unsigned)blocks), dim3(kThreads), smem, s, a.trees,
-                     a.prefix, info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin, wt, a.bias, a.cout,
-                     a.relu, a.out, tm);
+  const size_t gsmem = generic_smem(a.cin, tm);
+  const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
+  if (impl != 2) {
+    const unsigned blocks = (unsigned)(all_tiles < 65536 ? all_tiles : 65536);
+    hipLaunchKernelGGL(k_conv_generic, dim3(blocks), dim3(kThreads), gsmem, s, a.trees, a.prefix,
+                       w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin, w.wt, a.bias, a.cout,
+                       a.relu, a.out, tm, (const int32_t*)nullptr, (const int64_t*)nullptr);
+    return hipGetLastError();
+  }
+  e = device_limits();
+  if (e != hipSuccess) return e;
+  const MfmaVariant* v = find_variant(a.cin, a.cout);
+  const size_t msmem = mfma_smem(*v);
+  if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
+  const int nblk = ((g_num_cus + 7) / 8) * 8;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kMfmaThreads), msmem, s,
+                     a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
+                     (const int64_t*)(w.gpre + a.n_trees), a.in, (const float*)w.wm,
+                     (const float*)w.zero, a.bias, a.cout, a.relu, a.out);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // Cells of edge 2, 4 and 8: at most one tile per leaf, grid-stride beyond.
+  const unsigned gblocks = (unsigned)(all_tiles < 8192 ? all_tiles : 8192);
+  hipLaunchKernelGGL(k_conv_generic, dim3(gblocks), dim3(kThreads), gsmem, s, a.trees, a.prefix,
+                     w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin, w.wt, a.bias, a.cout,
+                     a.relu, a.out, tm, (const int32_t*)w.brow,
+                     (const int64_t*)(w.bpre + a.n_trees));
   return hipGetLastError();
 }
 
