@@ -54,6 +54,23 @@ struct Entry {
 // voxels in the region.  Offsets are the running sums; the self entry uses
 // slot kSelfSlot.
 __constant__ int c_slot_off[27];
+
+// Edge-2 cells.  The shell is the 56 voxels u of the 4^3 block [o-1, o+3)
+// outside [o, o+2) (u in [0,4)^3 minus [1,2]^3); voxel u lies in the window
+// of delta iff u_a - delta_a - 1 is in {0, 1} on every axis.
+constexpr int shell2_u(int q) {
+  int k = 0;
+  for (int u = 0; u < 64; ++u) {
+    const int ud = u >> 4, uh = (u >> 2) & 3, uw = u & 3;
+    const bool inner = ud >= 1 && ud <= 2 && uh >= 1 && uh <= 2 && uw >= 1 && uw <= 2;
+    if (inner) continue;
+    if (k == q) return u;
+    ++k;
+  }
+  return -1;
+}
+
+__constant__ uint8_t c_shell2[56];
 constexpr int kSlots = 6 * 64 + 12 * 8 + 8 + 1;  // 489
 constexpr int kSelfSlot = kSlots - 1;
 
@@ -307,6 +324,10 @@ hipError_t init_slots() {
     acc += (dd == 0 ? 8 : 1) * (dh == 0 ? 8 : 1) * (dw == 0 ? 8 : 1);
   }
   hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(c_slot_off), off, sizeof(off));
+  if (e != hipSuccess) return e;
+  uint8_t sh2[56];
+  for (int q = 0; q < 56; ++q) sh2[q] = (uint8_t)shell2_u(q);
+  e = hipMemcpyToSymbol(HIP_SYMBOL(c_shell2), sh2, sizeof(sh2));
   if (e == hipSuccess) g_slots_ready = true;
   return e;
 }
@@ -323,27 +344,77 @@ __device__ __forceinline__ int depth2_splits(const Bits& b) {
   return __popcll(b.lo >> 9) + __popc(b.hi);
 }
 
-__global__ void k_group_count(const uint32_t* __restrict__ trees, int64_t n_trees,
-                              int32_t* __restrict__ n_grp, int32_t* __restrict__ n_big) {
+// Kinds of larger cells, in the order the lists hold them: edge-8 cells
+// whose 18 face and edge neighbours (inside the grid) are unsplit trees, the
+// other edge-8 cells, edge-4 cells, edge-2 cells.
+constexpr int kKinds = 4;
+
+// Per-tree counts: unit-voxel groups (split depth-2 nodes) and each kind of
+// larger cell.  Edge-8 cells are unsplit trees, edge-4 cells unsplit depth-1
+// nodes of a split root, edge-2 cells unsplit depth-2 nodes of a split
+// depth-1 node.
+__global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees, int gd, int gh,
+                             int gw, int32_t* __restrict__ n_grp, int32_t* __restrict__ n8t,
+                             int32_t* __restrict__ n8n, int32_t* __restrict__ n4,
+                             int32_t* __restrict__ n2) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
   const Bits b = load_bits(trees, t);
-  const int g = depth2_splits(b);
-  n_grp[t] = g;
-  n_big[t] = max(0, n_leaves_of(b) - 8 * g);
+  const int root = (int)(b.lo & 1ull);
+  const int p1 = __popc((uint32_t)(b.lo >> 1) & 0xFFu);
+  const int p2 = depth2_splits(b);
+  int trivial = 0;
+  if (!root) {
+    const TreePos p = tree_pos(t, gd, gh, gw);
+    trivial = 1;
+    for (int r = 0; r < 27 && trivial; ++r) {
+      const int dd = r / 9 - 1, dh = (r / 3) % 3 - 1, dw = r % 3 - 1;
+      if ((dd != 0) + (dh != 0) + (dw != 0) != 1 && (dd != 0) + (dh != 0) + (dw != 0) != 2) continue;
+      const int qd = p.d + dd, qh = p.h + dh, qw = p.w + dw;
+      if (qd < 0 || qh < 0 || qw < 0 || qd >= gd || qh >= gh || qw >= gw) continue;
+      const int64_t q = ((p.n * gd + qd) * gh + qh) * gw + qw;
+      if (trees[4 * q] & 1u) trivial = 0;
+    }
+  }
+  n_grp[t] = p2;
+  n8t[t] = (!root && trivial) ? 1 : 0;
+  n8n[t] = (!root && !trivial) ? 1 : 0;
+  n4[t] = root ? 8 - p1 : 0;
+  n2[t] = max(0, 8 * p1 - p2);
 }
 
-__global__ void k_group_fill(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
-                             const int64_t* __restrict__ gpre, const int64_t* __restrict__ bpre,
-                             int64_t n_trees, int64_t* __restrict__ gkey,
-                             int32_t* __restrict__ brow, int64_t gcap, int64_t bcap) {
+// Leaf lists.  gkey: one key per unit-voxel group.  brow: the rows of every
+// larger cell, grouped by kind (tree order within a kind), so that a tile of
+// consecutive entries of one kind holds cells of one size.
+// meta = {count of each kind, total}.
+__global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                             const int64_t* __restrict__ gpre, const int64_t* __restrict__ p8t,
+                             const int64_t* __restrict__ p8n, const int64_t* __restrict__ p4,
+                             const int64_t* __restrict__ p2, int64_t n_trees,
+                             int64_t* __restrict__ gkey, int32_t* __restrict__ brow, int64_t gcap,
+                             int64_t bcap, int64_t* __restrict__ meta) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
+  const int64_t c8t = p8t[n_trees], c8n = p8n[n_trees], c4 = p4[n_trees], c2 = p2[n_trees];
+  if (t == 0) {
+    meta[0] = c8t;
+    meta[1] = c8n;
+    meta[2] = c4;
+    meta[3] = c2;
+    meta[4] = c8t + c8n + c4 + c2;
+  }
   const Bits b = load_bits(trees, t);
   const int64_t row0 = prefix[t];
   // The capacities only matter for a non-canonical structure, whose counts
   // need not match the leaf total the buffers were sized for.
-  for (int64_t k = bpre[t]; k < bpre[t + 1] && k < bcap; ++k) brow[k] = (int32_t)(row0 + k - bpre[t]);
+  auto put = [&](int64_t k, int64_t row) {
+    if (k >= 0 && k < bcap) brow[k] = (int32_t)row;
+  };
+  if (p8t[t + 1] > p8t[t]) put(p8t[t], row0);
+  if (p8n[t + 1] > p8n[t]) put(c8t + p8n[t], row0);
+  const int64_t n4t = p4[t + 1] - p4[t];
+  for (int64_t k = p4[t]; k < p4[t + 1]; ++k) put(c8t + c8n + k, row0 + (k - p4[t]));
+  for (int64_t k = p2[t]; k < p2[t + 1]; ++k) put(c8t + c8n + c4 + k, row0 + n4t + (k - p2[t]));
   int64_t k = gpre[t];
   uint64_t m = b.lo >> 9;  // bits 9..63 -> positions 0..54
   while (m && k < gcap) {
@@ -550,6 +621,421 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
   }
 }
 
+// ---------------------------------------------------------------------------
+// MFMA kernels for cells of edge 2, 4 and 8.
+//
+// Same tile shape, lane roles and LDS weights as the unit-voxel kernel, but
+// each lane first builds the window sums of its own cell (origin o, edge SZ):
+//   S_delta = x_self * prod_a (SZ - |delta_a|) + sum of x over the one-voxel
+//             shell voxels that the window [o+delta, o+delta+SZ) covers,
+// VEC channels at a time, and the slice then enters the MFMA contraction.
+// All shell geometry is known at compile time for a given SZ, so every
+// S_delta stays in a fixed register.
+// ---------------------------------------------------------------------------
+template <int CIN, int NT, int MS>
+__device__ __forceinline__ void weights_to_lds(const float* __restrict__ wm, float* wl) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  typedef float __attribute__((ext_vector_type(4))) f4;
+  const f4* src = reinterpret_cast<const f4*>(wm);
+  f4* dst = reinterpret_cast<f4*>(wl);
+  for (int i = threadIdx.x; i < C::WFLOATS / 4; i += blockDim.x) dst[i] = src[i];
+  __syncthreads();
+}
+
+// Tiles [begin, end) of this workgroup: a contiguous chunk, chunks laid out
+// so that the workgroups of one XCD (dispatched round-robin) get neighbours.
+__device__ __forceinline__ void block_tiles(int64_t n_tiles, int64_t& begin, int64_t& end) {
+  const int nblk = gridDim.x;
+  const int chunk = (blockIdx.x % 8) * (nblk / 8) + blockIdx.x / 8;
+  const int64_t per = (n_tiles + nblk - 1) / nblk;
+  begin = (int64_t)chunk * per;
+  end = min(n_tiles, begin + per);
+}
+
+// Contract the window-sum slice cv (channels CH*g + VEC*cv ..) into acc.
+template <int CIN, int NT, int MS>
+__device__ __forceinline__ void contract_slice(const float (&S)[27][MfmaCfg<CIN, NT, MS>::VEC],
+                                               const float* wl, int cv, int lane,
+                                               typename AccT<MS>::type (&acc)[NT]) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  using Vec = typename VecT<C::VEC>::type;
+#pragma unroll
+  for (int dl = 0; dl < 27; ++dl) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const Vec bv = reinterpret_cast<const Vec*>(wl)[((dl * NT + nt) * C::NV + cv) * 64 + lane];
+#pragma unroll
+      for (int e = 0; e < C::VEC; ++e) acc[nt] = mfma<MS>(S[dl][e], vget<C::VEC>(bv, e), acc[nt]);
+    }
+    if (dl % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bounds the B loads in flight
+  }
+}
+
+// Store the tile: D row i belongs to the cell held by lane i.
+template <int MS, int NT>
+__device__ __forceinline__ void store_tile(const typename AccT<MS>::type (&acc)[NT], int row, float inv,
+                                           int lane, const float* __restrict__ bias, int cout,
+                                           int relu, float* __restrict__ out) {
+  const int g = lane / MS, col = lane % MS;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int co = MS * nt + col;
+    const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+#pragma unroll
+    for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
+      const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
+      const int rowi = __shfl(row, i, 64);
+      if (rowi < 0 || co >= cout) continue;
+      float v = fmaf(acc[nt][r], inv, bv);
+      if (relu) v = fmaxf(v, 0.f);
+      out[(int64_t)rowi * cout + co] = v;
+    }
+  }
+}
+
+// Range [begin, begin + count) of kind k in the larger-cell list.
+__device__ __forceinline__ void kind_range(const int64_t* __restrict__ meta, int kind, int64_t cap,
+                                           int64_t& begin, int64_t& count) {
+  begin = 0;
+  for (int k = 0; k < kind; ++k) begin += meta[k];
+  count = meta[kind];
+  if (begin > cap) begin = cap;
+  if (begin + count > cap) count = cap - begin;
+}
+
+
+// Adds the 56 shell voxels of an edge-2 cell into S, voxel by voxel, with
+// compile-time positions (template recursion keeps every index static).
+template <int Q, int CIN, int V>
+struct Shell2Loop {
+  __device__ __forceinline__ static void run(float (&S)[27][V], const int (&rows)[56],
+                                             const float* __restrict__ in,
+                                             const float* __restrict__ zero_row, int choff) {
+    using Vec = typename VecT<V>::type;
+    constexpr int u = shell2_u(Q);
+    constexpr int ud = u >> 4, uh = (u >> 2) & 3, uw = u & 3;
+    const Vec xv = *reinterpret_cast<const Vec*>(
+        (rows[Q] >= 0 ? in + (int64_t)rows[Q] * CIN : zero_row) + choff);
+#pragma unroll
+    for (int jd = 0; jd < 3; ++jd) {
+      if (ud - jd < 0 || ud - jd > 1) continue;  // delta_d = jd - 1
+#pragma unroll
+      for (int jh = 0; jh < 3; ++jh) {
+        if (uh - jh < 0 || uh - jh > 1) continue;
+#pragma unroll
+        for (int jw = 0; jw < 3; ++jw) {
+          if (uw - jw < 0 || uw - jw > 1) continue;
+#pragma unroll
+          for (int e = 0; e < V; ++e) S[jd * 9 + jh * 3 + jw][e] += vget<V>(xv, e);
+        }
+      }
+    }
+    if constexpr (Q % 8 == 7) __builtin_amdgcn_sched_barrier(0);  // bounds the loads in flight
+    Shell2Loop<Q + 1, CIN, V>::run(S, rows, in, zero_row, choff);
+  }
+};
+template <int CIN, int V>
+struct Shell2Loop<56, CIN, V> {
+  __device__ __forceinline__ static void run(float (&)[27][V], const int (&)[56], const float*,
+                                             const float*, int) {}
+};
+
+template <int CIN, int NT, int MS>
+__global__ void __launch_bounds__(512) k_conv_cell2_mfma(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
+    const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
+    const float* __restrict__ wm, const float* __restrict__ zero_row, const float* __restrict__ bias,
+    int cout, int relu, float* __restrict__ out) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  using Vec = typename VecT<C::VEC>::type;
+  using Acc = typename AccT<MS>::type;
+  constexpr int V = C::VEC;
+  constexpr int KS = C::KS;
+  extern __shared__ float smem[];
+  float* wl = smem;
+  weights_to_lds<CIN, NT, MS>(wm, wl);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  int64_t lbeg, lcnt;
+  kind_range(meta, kind, n_leaves, lbeg, lcnt);
+  int64_t t_begin, t_end;
+  block_tiles((lcnt + MS - 1) / MS, t_begin, t_end);
+  const int m = lane % MS, g = lane / MS;
+  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
+    const int64_t idx = tile * MS + m;
+    int row = idx < lcnt ? brow[lbeg + idx] : -1;
+    if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
+    // Shell rows: lane slot g resolves voxels q = j*KS + g, then the KS lanes
+    // of the cell exchange them.
+    int rows[56];
+    {
+      int mine[56 / KS];
+      int64_t n = 0;
+      int o0 = 0, o1 = 0, o2 = 0;
+      if (row >= 0) {
+        const uint64_t inf = info[row];
+        const TreePos p = tree_pos((int64_t)(inf >> 10), gd, gh, gw);
+        const Cell c = cell_of((int)(inf & 1023u));
+        n = p.n;
+        o0 = 8 * p.d + c.d;
+        o1 = 8 * p.h + c.h;
+        o2 = 8 * p.w + c.w;
+      }
+#pragma unroll
+      for (int j = 0; j < 56 / KS; ++j) {
+        const int u = c_shell2[j * KS + g];
+        const int vd = o0 - 1 + (u >> 4), vh = o1 - 1 + ((u >> 2) & 3), vw = o2 - 1 + (u & 3);
+        int r = -1;
+        if (row >= 0 && vd >= 0 && vh >= 0 && vw >= 0 && vd < 8 * gd && vh < 8 * gh && vw < 8 * gw) {
+          const int64_t tt = ((n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
+          const Bits b = load_bits(trees, tt);
+          const int64_t rr = prefix[tt] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7));
+          r = rr < n_leaves ? (int)rr : -1;
+        }
+        mine[j] = r;
+      }
+#pragma unroll
+      for (int j = 0; j < 56 / KS; ++j)
+#pragma unroll
+        for (int k = 0; k < KS; ++k) rows[j * KS + k] = __shfl(mine[j], m + MS * k, 64);
+    }
+    Acc acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
+#pragma unroll 1
+    for (int cv = 0; cv < C::NV; ++cv) {
+      const int choff = C::CH * g + V * cv;
+      float S[27][V];
+      {
+        const Vec xv = *reinterpret_cast<const Vec*>((row >= 0 ? in + (int64_t)row * CIN : zero_row) + choff);
+#pragma unroll
+        for (int dl = 0; dl < 27; ++dl) {
+          const float vol = (float)((2 - (dl / 9 == 1 ? 0 : 1)) * (2 - ((dl / 3) % 3 == 1 ? 0 : 1)) *
+                                    (2 - (dl % 3 == 1 ? 0 : 1)));
+#pragma unroll
+          for (int e = 0; e < V; ++e) S[dl][e] = vget<V>(xv, e) * vol;
+        }
+      }
+      Shell2Loop<0, CIN, V>::run(S, rows, in, zero_row, choff);
+      contract_slice<CIN, NT, MS>(S, wl, cv, lane, acc);
+    }
+    store_tile<MS, NT>(acc, row, 0.125f, lane, bias, cout, relu, out);
+  }
+}
+
+// Edge-4 and edge-8 cells.  The shell splits into 26 regions (faces, edges,
+// corners); region r lies inside one neighbouring tree.  If one leaf covers
+// the region (the neighbouring tree, or for SZ = 4 its depth-1 node, is not
+// split) it contributes once with the region's full overlap; otherwise the
+// region is walked in aligned 2x2x2 blocks of that tree, each either inside a
+// leaf of edge >= 2 or a split depth-2 node whose unit voxels are rows
+// first .. first+7.  Every contribution carries, per axis along which the
+// region extends, the interval [c0, c1) it covers relative to o; its weight
+// for delta is prod_a |[c0, c1) ^ [delta_a, delta_a + SZ)|.
+template <int R, int SZ, int V>
+__device__ __forceinline__ void region_add(float (&S)[27][V], const float (&x)[V], const int (&c0)[3],
+                                           const int (&c1)[3]) {
+  constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
+  float ov[3][3];
+#pragma unroll
+  for (int a = 0; a < 3; ++a)
+#pragma unroll
+    for (int j = 0; j < 3; ++j) ov[a][j] = (float)max(0, min(c1[a], j - 1 + SZ) - max(c0[a], j - 1));
+#pragma unroll
+  for (int j0 = 0; j0 < 3; ++j0) {
+    if (dir0 != 0 && j0 != dir0 + 1) continue;
+#pragma unroll
+    for (int j1 = 0; j1 < 3; ++j1) {
+      if (dir1 != 0 && j1 != dir1 + 1) continue;
+#pragma unroll
+      for (int j2 = 0; j2 < 3; ++j2) {
+        if (dir2 != 0 && j2 != dir2 + 1) continue;
+        float wgt = 1.f;
+        if (dir0 == 0) wgt *= ov[0][j0];
+        if (dir1 == 0) wgt *= ov[1][j1];
+        if (dir2 == 0) wgt *= ov[2][j2];
+#pragma unroll
+        for (int e = 0; e < V; ++e) S[j0 * 9 + j1 * 3 + j2][e] = fmaf(x[e], wgt, S[j0 * 9 + j1 * 3 + j2][e]);
+      }
+    }
+  }
+}
+
+template <int R, int SZ, int CIN, int V>
+__device__ __forceinline__ void region_sum(float (&S)[27][V], const uint32_t* __restrict__ trees,
+                                           const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+                                           int64_t n_leaves, int64_t n, const int (&o)[3],
+                                           const float* __restrict__ in, int choff) {
+  using Vec = typename VecT<V>::type;
+  constexpr int dir[3] = {R / 9 - 1, (R / 3) % 3 - 1, R % 3 - 1};
+  const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
+  int lo[3];
+  bool inside = true;
+#pragma unroll
+  for (int a = 0; a < 3; ++a) {
+    lo[a] = dir[a] < 0 ? o[a] - 1 : (dir[a] == 0 ? o[a] : o[a] + SZ);
+    const int hi = dir[a] < 0 ? o[a] : (dir[a] == 0 ? o[a] + SZ : o[a] + SZ + 1);
+    inside = inside && lo[a] >= 0 && hi <= lim[a];
+  }
+  if (!inside) return;  // zero padding
+  const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
+  const Bits b = load_bits(trees, tt);
+  const int64_t rbase = prefix[tt];
+  const int L[3] = {lo[0] & 7, lo[1] & 7, lo[2] & 7};
+  // A leaf covering the whole region?
+  int cover = -1;
+  if (!(b.lo & 1ull)) {
+    cover = 0;
+  } else if (SZ == 4) {
+    const int n1 = 1 + 4 * (L[0] >> 2) + 2 * (L[1] >> 2) + (L[2] >> 2);
+    if (!bit(b, n1)) cover = n1;
+  }
+  // 2x2x2 blocks along the axes the region extends on; one along the others.
+  constexpr int nb0 = dir[0] == 0 ? SZ / 2 : 1, nb1 = dir[1] == 0 ? SZ / 2 : 1,
+                nb2 = dir[2] == 0 ? SZ / 2 : 1;
+  const int nblocks = cover >= 0 ? 1 : nb0 * nb1 * nb2;
+  for (int bi = 0; bi < nblocks; ++bi) {
+    const int i0 = bi / (nb1 * nb2), i1 = (bi / nb2) % nb1, i2 = bi % nb2;
+    const int bix[3] = {i0, i1, i2};
+    int first;          // row of the block's leaf, or of its first unit voxel
+    int nsub = 1;       // contributions of this block
+    int bo[3];          // block origin in the neighbouring tree
+#pragma unroll
+    for (int a = 0; a < 3; ++a) bo[a] = dir[a] == 0 ? L[a] + 2 * bix[a] : (L[a] & ~1);
+    bool fine = false;
+    if (cover >= 0) {
+      first = (int)(rbase + data_idx(b, cover));
+    } else {
+      const int n1 = 1 + 4 * (bo[0] >> 2) + 2 * (bo[1] >> 2) + (bo[2] >> 2);
+      int node = n1;
+      if (bit(b, n1)) {
+        const int n2 = 8 * n1 + 1 + 4 * ((bo[0] >> 1) & 1) + 2 * ((bo[1] >> 1) & 1) + ((bo[2] >> 1) & 1);
+        node = n2;
+        if (bit(b, n2)) {
+          node = 8 * n2 + 1;
+          fine = true;
+          nsub = (dir[0] == 0 ? 2 : 1) * (dir[1] == 0 ? 2 : 1) * (dir[2] == 0 ? 2 : 1);
+        }
+      }
+      first = (int)(rbase + data_idx(b, node));
+    }
+    for (int sb = 0; sb < nsub; ++sb) {
+      int c0[3], c1[3], o3 = 0;
+      int k = sb;
+#pragma unroll
+      for (int a = 2; a >= 0; --a) {
+        int vbit;  // unit-voxel bit along axis a inside the block
+        if (dir[a] == 0) {
+          vbit = k & 1;
+          k >>= 1;
+        } else {
+          vbit = L[a] & 1;
+        }
+        o3 |= vbit << (2 - a);
+        if (cover >= 0) {
+          c0[a] = 0;
+          c1[a] = SZ;
+        } else if (fine) {
+          c0[a] = 2 * bix[a] + vbit;
+          c1[a] = c0[a] + 1;
+        } else {
+          c0[a] = 2 * bix[a];
+          c1[a] = c0[a] + 2;
+        }
+      }
+      const int64_t rr = (int64_t)first + (fine ? o3 : 0);
+      if (rr >= n_leaves) continue;  // only a non-canonical structure gets here
+      const Vec xv = *reinterpret_cast<const Vec*>(in + rr * CIN + choff);
+      float x[V];
+#pragma unroll
+      for (int e = 0; e < V; ++e) x[e] = vget<V>(xv, e);
+      region_add<R, SZ, V>(S, x, c0, c1);
+    }
+  }
+}
+
+template <int R, int SZ, int CIN, int V>
+struct RegionLoop {
+  __device__ __forceinline__ static void run(float (&S)[27][V], const uint32_t* trees,
+                                             const int64_t* prefix, int gd, int gh, int gw,
+                                             int64_t n_leaves, int64_t n, const int (&o)[3],
+                                             const float* in, int choff) {
+    if constexpr (R != 13)
+      region_sum<R, SZ, CIN, V>(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
+    RegionLoop<R + 1, SZ, CIN, V>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
+  }
+};
+template <int SZ, int CIN, int V>
+struct RegionLoop<27, SZ, CIN, V> {
+  __device__ __forceinline__ static void run(float (&)[27][V], const uint32_t*, const int64_t*, int,
+                                             int, int, int64_t, int64_t, const int (&)[3],
+                                             const float*, int) {}
+};
+
+template <int CIN, int NT, int MS, int SZ>
+__global__ void __launch_bounds__(512) k_conv_cellr_mfma(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
+    const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
+    const float* __restrict__ wm, const float* __restrict__ zero_row, const float* __restrict__ bias,
+    int cout, int relu, float* __restrict__ out) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  using Vec = typename VecT<C::VEC>::type;
+  using Acc = typename AccT<MS>::type;
+  constexpr int V = C::VEC;
+  extern __shared__ float smem[];
+  float* wl = smem;
+  weights_to_lds<CIN, NT, MS>(wm, wl);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  int64_t lbeg, lcnt;
+  kind_range(meta, kind, n_leaves, lbeg, lcnt);
+  int64_t t_begin, t_end;
+  block_tiles((lcnt + MS - 1) / MS, t_begin, t_end);
+  const int m = lane % MS, g = lane / MS;
+  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
+    const int64_t idx = tile * MS + m;
+    int row = idx < lcnt ? brow[lbeg + idx] : -1;
+    if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
+    int o[3] = {0, 0, 0};
+    int64_t n = 0;
+    if (row >= 0) {
+      const uint64_t inf = info[row];
+      const TreePos p = tree_pos((int64_t)(inf >> 10), gd, gh, gw);
+      const Cell c = cell_of((int)(inf & 1023u));
+      n = p.n;
+      o[0] = 8 * p.d + c.d;
+      o[1] = 8 * p.h + c.h;
+      o[2] = 8 * p.w + c.w;
+    }
+    Acc acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
+#pragma unroll 1
+    for (int cv = 0; cv < C::NV; ++cv) {
+      const int choff = C::CH * g + V * cv;
+      float S[27][V];
+      {
+        const Vec xv = *reinterpret_cast<const Vec*>((row >= 0 ? in + (int64_t)row * CIN : zero_row) + choff);
+#pragma unroll
+        for (int dl = 0; dl < 27; ++dl) {
+          const float vol = (float)((SZ - (dl / 9 == 1 ? 0 : 1)) * (SZ - ((dl / 3) % 3 == 1 ? 0 : 1)) *
+                                    (SZ - (dl % 3 == 1 ? 0 : 1)));
+#pragma unroll
+          for (int e = 0; e < V; ++e) S[dl][e] = vget<V>(xv, e) * vol;
+        }
+      }
+      if (row >= 0)
+        RegionLoop<0, SZ, CIN, V>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
+      contract_slice<CIN, NT, MS>(S, wl, cv, lane, acc);
+    }
+    store_tile<MS, NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bias, cout, relu, out);
+  }
+}
+
 // Weights in B-operand order: for delta index dl, N-tile nt, vector jv, lane
 // and element e: column co = MS*nt + lane%MS, channel ci = CH*(lane/MS) +
 // VEC*jv + e, tap 26 - dl (Eq. 7 pairs input offset delta with tap 1 - delta).
@@ -575,12 +1061,16 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 typedef void (*MfmaFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const int64_t*,
                        const int64_t*, const float*, const float*, const float*, const float*, int,
                        int, float*);
+typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
+                       const int32_t*, const int64_t*, int, const float*, const float*, const float*,
+                       const float*, int, int, float*);
 typedef void (*WeightFn)(const float*, int, float*);
 
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
   size_t wfloats;
   MfmaFn kernel;
+  CellFn cell2, cell4, cell8;
   WeightFn weights;
   int weight_total;
 };
@@ -596,6 +1086,9 @@ MfmaVariant make_variant(int cout_min) {
   v.nt = NT;
   v.wfloats = C::WFLOATS;
   v.kernel = &k_conv_unit_mfma<CIN, NT, MS>;
+  v.cell2 = &k_conv_cell2_mfma<CIN, NT, MS>;
+  v.cell4 = &k_conv_cellr_mfma<CIN, NT, MS, 4>;
+  v.cell8 = &k_conv_cellr_mfma<CIN, NT, MS, 8>;
   v.weights = &k_mfma_weights<CIN, NT, MS>;
   v.weight_total = C::WFLOATS;
   return v;
@@ -639,23 +1132,21 @@ hipError_t device_limits() {
 //   leaf_info  u64 [n_leaves]
 //   wt         f32 [27 cin cout]            generic-kernel weights
 //   wm         f32 [variant wfloats]        MFMA B operands (if a variant exists)
-//   scan_g     scan workspace (n_trees)     groups per tree -> gpre
-//   gpre       i64 [n_trees + 1]
-//   scan_b     scan workspace (n_trees)     big leaves per tree -> bpre
-//   bpre       i64 [n_trees + 1]
+//   5 x (scan workspace (n_trees), i64 [n_trees + 1])
+//              unit groups and each kind of larger cell per tree -> prefixes
 //   gkey       i64 [n_leaves / 8 + 1]
 //   brow       i32 [n_leaves]
+//   meta       i64 [kKinds + 1]
 //   zero       f32 [cin]                    a row of zeros (padding reads)
 struct ConvWs {
   uint64_t* info;
   float* wt;
   float* wm;
-  char* scan_g;
-  int64_t* gpre;
-  char* scan_b;
-  int64_t* bpre;
+  char* scan[1 + kKinds];
+  int64_t* pre[1 + kKinds];  // groups, then the kinds of larger cells
   int64_t* gkey;
   int32_t* brow;
+  int64_t* meta;
   float* zero;
   size_t total;
 };
@@ -674,12 +1165,13 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
   w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
-  w.scan_g = take(oci::scan_workspace(n_trees));
-  w.gpre = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
-  w.scan_b = take(oci::scan_workspace(n_trees));
-  w.bpre = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
+  for (int k = 0; k < 1 + kKinds; ++k) {
+    w.scan[k] = take(oci::scan_workspace(n_trees));
+    w.pre[k] = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
+  }
   w.gkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_leaves / 8 + 1)));
   w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
+  w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
   w.zero = reinterpret_cast<float*>(take(sizeof(float) * (size_t)cin));
   w.total = off + 256;
   return w;
@@ -717,14 +1209,17 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                      dim3((unsigned)((v->weight_total + 255) / 256)), dim3(256), 0, s, a.weight,
                      a.cout, w.wm);
   const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
-  hipLaunchKernelGGL(k_group_count, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees,
-                     scan_counts_buffer(w.scan_g), scan_counts_buffer(w.scan_b));
-  e = scan_counts(scan_counts_buffer(w.scan_g), a.n_trees, w.gpre, w.scan_g, s);
-  if (e != hipSuccess) return e;
-  e = scan_counts(scan_counts_buffer(w.scan_b), a.n_trees, w.bpre, w.scan_b, s);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_group_fill, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.gpre, w.bpre,
-                     a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1, a.n_leaves);
+  hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
+                     scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
+                     scan_counts_buffer(w.scan[2]), scan_counts_buffer(w.scan[3]),
+                     scan_counts_buffer(w.scan[4]));
+  for (int k = 0; k < 1 + kKinds; ++k) {
+    e = scan_counts(scan_counts_buffer(w.scan[k]), a.n_trees, w.pre[k], w.scan[k], s);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],
+                     w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
+                     a.n_leaves, w.meta);
   hipLaunchKernelGGL(k_zero, dim3((unsigned)((a.cin + 255) / 256)), dim3(256), 0, s, w.zero,
                      (int64_t)a.cin);
   return hipGetLastError();
@@ -749,24 +1244,33 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   e = device_limits();
   if (e != hipSuccess) return e;
   const MfmaVariant* v = find_variant(a.cin, a.cout);
+  const size_t wsmem = sizeof(float) * v->wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
   const int nblk = ((g_num_cus + 7) / 8) * 8;
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kMfmaThreads), msmem, s,
-                     a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
-                     (const int64_t*)(w.gpre + a.n_trees), a.in, (const float*)w.wm,
+  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kMfmaThreads), msmem, s, a.trees, a.prefix, a.gd,
+                     a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
+                     (const int64_t*)(w.pre[0] + a.n_trees), a.in, (const float*)w.wm,
                      (const float*)w.zero, a.bias, a.cout, a.relu, a.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Cells of edge 2, 4 and 8: at most one tile per leaf, grid-stride beyond.
-  const unsigned gblocks = (unsigned)(all_tiles < 8192 ? all_tiles : 8192);
-  hipLaunchKernelGGL(k_conv_generic, dim3(gblocks), dim3(kThreads), gsmem, s, a.trees, a.prefix,
-                     w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin, w.wt, a.bias, a.cout,
-                     a.relu, a.out, tm, (const int32_t*)w.brow,
-                     (const int64_t*)(w.bpre + a.n_trees));
+  // Larger cells, one launch per kind: trivial edge-8, other edge-8, edge-4,
+  // edge-2 (the lists are grouped by kind; the kernels read the counts).
+  const CellFn cells[kKinds] = {v->cell8, v->cell8, v->cell4, v->cell2};
+  for (int k = 0; k < kKinds; ++k) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)wsmem);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
+                       a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
+                       (const int64_t*)w.meta, k, a.in, (const float*)w.wm, (const float*)w.zero,
+                       a.bias, a.cout, a.relu, a.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   return hipGetLastError();
 }
 
