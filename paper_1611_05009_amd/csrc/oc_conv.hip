@@ -430,10 +430,6 @@ __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* 
   }
 }
 
-__global__ void k_zero(float* __restrict__ x, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) x[i] = 0.f;
-}
 
 // Row of the leaf holding voxel u (u = 16 ud + 4 uh + uw, each in 0..3) of
 // the 4^3 neighbourhood [p-1, p+3) of the group's 2^3 block at origin p;
@@ -508,13 +504,60 @@ __device__ __forceinline__ float vget(const typename VecT<V>::type& v, int i) {
   else return v[i];
 }
 
+// Tile schedule of a wave.  Workgroups are dispatched round-robin over the 8
+// XCDs, each with its own L2.  XCD x owns the x-th eighth of the tiles (a
+// compact region of space), and its waves interleave over that region, so
+// the tiles in flight on one XCD at any time are neighbours that share
+// gathered input rows in L2.  Tiles: first, first + stride, ... < end.
+struct WaveTiles {
+  int64_t first, end, stride;
+};
+
+__device__ __forceinline__ WaveTiles wave_tiles(int64_t n_tiles) {
+  const int nwaves = blockDim.x >> 6, wave = threadIdx.x >> 6;
+  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8, xblocks = gridDim.x / 8;
+  const int64_t per = (n_tiles + 7) / 8;
+  WaveTiles t;
+  t.end = min(n_tiles, (int64_t)(xcd + 1) * per);
+  t.first = (int64_t)xcd * per + (int64_t)slot * nwaves + wave;
+  t.stride = (int64_t)xblocks * nwaves;
+  return t;
+}
+
+// Gathers of input rows use raw buffer loads: one resource covers the input
+// (in_bytes valid bytes), offsets are 32-bit, and an offset past the end
+// reads as zero, which is the zero padding outside the grid.
+constexpr uint32_t kOutside = 0xFFFF0000u;  // offset of a voxel outside the grid
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t input_rsrc(const float* in, uint32_t in_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(in), (short)0, (int)in_bytes,
+                                           0x00020000);
+}
+
+template <int V>
+__device__ __forceinline__ typename VecT<V>::type gather(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  if constexpr (V == 4)
+    return __builtin_bit_cast(typename VecT<4>::type, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  else if constexpr (V == 2)
+    return __builtin_bit_cast(typename VecT<2>::type, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+  else
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+// Byte offset of channel ch of a row (kOutside for row < 0).
+template <int CIN>
+__device__ __forceinline__ uint32_t row_offset(int row, int ch) {
+  return row < 0 ? kOutside : (uint32_t)row * (uint32_t)(CIN * 4) + (uint32_t)(ch * 4);
+}
+
 template <int CIN, int NT, int MS>
 __global__ void __launch_bounds__(512) k_conv_unit_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
-    const float* __restrict__ in, const float* __restrict__ wm, const float* __restrict__ zero_row,
+    const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
     const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
   using C = MfmaCfg<CIN, NT, MS>;
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   using Vec = typename VecT<C::VEC>::type;
   using Acc = typename AccT<MS>::type;
   extern __shared__ float smem[];
@@ -529,24 +572,16 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
   int32_t* nb = nb_all + wave * (C::GROUPS * 64);
   const int64_t G = min(*n_groups, n_leaves / 8);
   const int64_t n_tiles = (G + C::GROUPS - 1) / C::GROUPS;
-  // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
-  // contiguous run of chunks so that its L2 sees neighbouring groups.
-  const int nblk = gridDim.x;
-  const int xcd_blocks = nblk / 8;
-  const int chunk = (blockIdx.x % 8) * xcd_blocks + blockIdx.x / 8;
-  const int64_t per = (n_tiles + nblk - 1) / nblk;
-  const int64_t t_begin = (int64_t)chunk * per;
-  const int64_t t_end = min(n_tiles, t_begin + per);
+  const WaveTiles wt = wave_tiles(n_tiles);
   // Lane roles.
   const int m = lane % MS, g = lane / MS;
   const int gi = m >> 3, o3 = m & 7;
   const int ubase = gi * 64 + ((o3 >> 2) & 1) * 16 + ((o3 >> 1) & 1) * 4 + (o3 & 1);
   const int col = lane % MS;
-  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
 #pragma unroll
     for (int q = 0; q < C::GROUPS; ++q) {
       const int64_t gidx = tile * C::GROUPS + q;
@@ -570,11 +605,9 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
     auto load_a = [&](int dl, Vec* a) {
       const int dd = dl / 9, dh = (dl / 3) % 3, dw = dl % 3;
       const int row = nb[ubase + dd * 16 + dh * 4 + dw];
-      // Voxels outside the grid read a row of zeros (zero padding).
-      const float* base = row < 0 ? zero_row : in + (int64_t)row * CIN;
-      const Vec* src = reinterpret_cast<const Vec*>(base + C::CH * g);
+      const uint32_t off = row_offset<CIN>(row, C::CH * g);
 #pragma unroll
-      for (int v = 0; v < C::NV; ++v) a[v] = src[v];
+      for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VEC * v);
     };
     auto load_b = [&](int dl, Vec (*b)[C::NV]) {
 #pragma unroll
@@ -624,13 +657,17 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
 // ---------------------------------------------------------------------------
 // MFMA kernels for cells of edge 2, 4 and 8.
 //
-// Same tile shape, lane roles and LDS weights as the unit-voxel kernel, but
-// each lane first builds the window sums of its own cell (origin o, edge SZ):
+// A wave takes 16 cells of one edge length SZ and contracts them with
+// v_mfma_f32_16x16x4_f32: lane (m = lane % 16, g = lane / 16) feeds channels
+// CH*g .. CH*g + CH - 1 (CH = cin/4) of cell m, and the weights sit in LDS in
+// the matching B-operand order.  Before they enter the MFMA, the lane builds
+// its cell's window sums (origin o):
 //   S_delta = x_self * prod_a (SZ - |delta_a|) + sum of x over the one-voxel
 //             shell voxels that the window [o+delta, o+delta+SZ) covers,
-// VEC channels at a time, and the slice then enters the MFMA contraction.
-// All shell geometry is known at compile time for a given SZ, so every
-// S_delta stays in a fixed register.
+// one delta_d layer (9 deltas x CH channels) at a time, so that every input
+// row a cell needs is gathered at most twice per tile, once per layer that
+// reaches it.  The shell geometry of each layer is fixed at compile time, so
+// every S_delta stays in a fixed register.
 // ---------------------------------------------------------------------------
 template <int CIN, int NT, int MS>
 __device__ __forceinline__ void weights_to_lds(const float* __restrict__ wm, float* wl) {
@@ -642,49 +679,66 @@ __device__ __forceinline__ void weights_to_lds(const float* __restrict__ wm, flo
   __syncthreads();
 }
 
-// Tiles [begin, end) of this workgroup: a contiguous chunk, chunks laid out
-// so that the workgroups of one XCD (dispatched round-robin) get neighbours.
-__device__ __forceinline__ void block_tiles(int64_t n_tiles, int64_t& begin, int64_t& end) {
-  const int nblk = gridDim.x;
-  const int chunk = (blockIdx.x % 8) * (nblk / 8) + blockIdx.x / 8;
-  const int64_t per = (n_tiles + nblk - 1) / nblk;
-  begin = (int64_t)chunk * per;
-  end = min(n_tiles, begin + per);
-}
+template <int CIN, int NT>
+struct CellCfg {
+  using C = MfmaCfg<CIN, NT, 16>;
+  static constexpr int CH = C::CH;
+  static constexpr int VEC = C::VEC;
+  static constexpr int NV = C::NV;
+  using Vec = typename VecT<VEC>::type;
+  using Acc = typename AccT<16>::type;
+};
 
-// Contract the window-sum slice cv (channels CH*g + VEC*cv ..) into acc.
-template <int CIN, int NT, int MS>
-__device__ __forceinline__ void contract_slice(const float (&S)[27][MfmaCfg<CIN, NT, MS>::VEC],
-                                               const float* wl, int cv, int lane,
-                                               typename AccT<MS>::type (&acc)[NT]) {
-  using C = MfmaCfg<CIN, NT, MS>;
-  using Vec = typename VecT<C::VEC>::type;
+// Contract layer JD (deltas 9 JD .. 9 JD + 8) into acc.
+template <int CIN, int NT, int JD>
+__device__ __forceinline__ void contract_layer(const float (&S)[9][CIN / 4],
+                                               const float* wl, int lane,
+                                               typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+  using K = CellCfg<CIN, NT>;
 #pragma unroll
-  for (int dl = 0; dl < 27; ++dl) {
+  for (int k = 0; k < 9; ++k) {
+    const int dl = 9 * JD + k;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const Vec bv = reinterpret_cast<const Vec*>(wl)[((dl * NT + nt) * C::NV + cv) * 64 + lane];
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int e = 0; e < C::VEC; ++e) acc[nt] = mfma<MS>(S[dl][e], vget<C::VEC>(bv, e), acc[nt]);
-    }
-    if (dl % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bounds the B loads in flight
+      for (int jv = 0; jv < K::NV; ++jv) {
+        const typename K::Vec bv =
+            reinterpret_cast<const typename K::Vec*>(wl)[((dl * NT + nt) * K::NV + jv) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < K::VEC; ++e)
+          acc[nt] = mfma<16>(S[k][K::VEC * jv + e], vget<K::VEC>(bv, e), acc[nt]);
+      }
+    if (k % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bounds the B loads in flight
   }
 }
 
-// Store the tile: D row i belongs to the cell held by lane i.
-template <int MS, int NT>
-__device__ __forceinline__ void store_tile(const typename AccT<MS>::type (&acc)[NT], int row, float inv,
-                                           int lane, const float* __restrict__ bias, int cout,
-                                           int relu, float* __restrict__ out) {
-  const int g = lane / MS, col = lane % MS;
+// The lane's CH channels of the row at byte offset off.
+template <int CIN>
+__device__ __forceinline__ void gather_channels(__amdgpu_buffer_rsrc_t rin, uint32_t off,
+                                                float (&x)[CIN / 4]) {
+  using K = CellCfg<CIN, 1>;
+#pragma unroll
+  for (int jv = 0; jv < K::NV; ++jv) {
+    const typename K::Vec v = gather<K::VEC>(rin, off + 4u * K::VEC * jv);
+#pragma unroll
+    for (int e = 0; e < K::VEC; ++e) x[K::VEC * jv + e] = vget<K::VEC>(v, e);
+  }
+}
+
+// Store the tile: D row i (= 4 (lane / 16) + r) belongs to the cell held by
+// lane i.
+template <int NT>
+__device__ __forceinline__ void store_tile16(const typename AccT<16>::type (&acc)[NT], int row,
+                                             float inv, int lane, const float* __restrict__ bias,
+                                             int cout, int relu, float* __restrict__ out) {
+  const int g = lane / 16, col = lane % 16;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const int co = MS * nt + col;
+    const int co = 16 * nt + col;
     const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
 #pragma unroll
-    for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
-      const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
-      const int rowi = __shfl(row, i, 64);
+    for (int r = 0; r < 4; ++r) {
+      const int rowi = __shfl(row, 4 * g + r, 64);
       if (rowi < 0 || co >= cout) continue;
       float v = fmaf(acc[nt][r], inv, bv);
       if (relu) v = fmaxf(v, 0.f);
@@ -703,22 +757,45 @@ __device__ __forceinline__ void kind_range(const int64_t* __restrict__ meta, int
   if (begin + count > cap) count = cap - begin;
 }
 
+// Cell of a list row: sample and global voxel origin (row < 0: none).
+__device__ __forceinline__ void cell_origin(const uint64_t* __restrict__ info, int row, int gd,
+                                            int gh, int gw, int64_t& n, int (&o)[3]) {
+  n = 0;
+  o[0] = o[1] = o[2] = 0;
+  if (row < 0) return;
+  const uint64_t inf = info[row];
+  const TreePos p = tree_pos((int64_t)(inf >> 10), gd, gh, gw);
+  const Cell c = cell_of((int)(inf & 1023u));
+  n = p.n;
+  o[0] = 8 * p.d + c.d;
+  o[1] = 8 * p.h + c.h;
+  o[2] = 8 * p.w + c.w;
+}
 
-// Adds the 56 shell voxels of an edge-2 cell into S, voxel by voxel, with
-// compile-time positions (template recursion keeps every index static).
-template <int Q, int CIN, int V>
-struct Shell2Loop {
-  __device__ __forceinline__ static void run(float (&S)[27][V], const int (&rows)[56],
-                                             const float* __restrict__ in,
-                                             const float* __restrict__ zero_row, int choff) {
-    using Vec = typename VecT<V>::type;
+template <int SZ, int JD, int CH>
+__device__ __forceinline__ void init_layer(float (&S)[9][CH], const float (&xs)[CH]) {
+  constexpr int fd = SZ - (JD == 1 ? 0 : 1);
+#pragma unroll
+  for (int k = 0; k < 9; ++k) {
+    const float vol = (float)(fd * (SZ - (k / 3 == 1 ? 0 : 1)) * (SZ - (k % 3 == 1 ? 0 : 1)));
+#pragma unroll
+    for (int e = 0; e < CH; ++e) S[k][e] = xs[e] * vol;
+  }
+}
+
+// Edge-2 cells.  Shell voxel u (of the 4^3 block [o-1, o+3) minus the cell)
+// lies in the window of delta iff u_a - delta_a - 1 is in {0, 1} on every
+// axis; layer JD (delta_d = JD - 1) reaches the voxel planes u_d = JD, JD + 1.
+template <int Q, int JD, int CIN>
+struct Shell2Layer {
+  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4],
+                                             const uint32_t (&offs)[56], __amdgpu_buffer_rsrc_t rin,
+                                             uint32_t choff) {
     constexpr int u = shell2_u(Q);
     constexpr int ud = u >> 4, uh = (u >> 2) & 3, uw = u & 3;
-    const Vec xv = *reinterpret_cast<const Vec*>(
-        (rows[Q] >= 0 ? in + (int64_t)rows[Q] * CIN : zero_row) + choff);
-#pragma unroll
-    for (int jd = 0; jd < 3; ++jd) {
-      if (ud - jd < 0 || ud - jd > 1) continue;  // delta_d = jd - 1
+    if constexpr (ud == JD || ud == JD + 1) {
+      float x[CIN / 4];
+      gather_channels<CIN>(rin, offs[Q] + choff, x);
 #pragma unroll
       for (int jh = 0; jh < 3; ++jh) {
         if (uh - jh < 0 || uh - jh > 1) continue;
@@ -726,65 +803,56 @@ struct Shell2Loop {
         for (int jw = 0; jw < 3; ++jw) {
           if (uw - jw < 0 || uw - jw > 1) continue;
 #pragma unroll
-          for (int e = 0; e < V; ++e) S[jd * 9 + jh * 3 + jw][e] += vget<V>(xv, e);
+          for (int e = 0; e < CIN / 4; ++e) S[jh * 3 + jw][e] += x[e];
         }
       }
+      if constexpr (Q % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bounds the loads in flight
     }
-    if constexpr (Q % 8 == 7) __builtin_amdgcn_sched_barrier(0);  // bounds the loads in flight
-    Shell2Loop<Q + 1, CIN, V>::run(S, rows, in, zero_row, choff);
+    Shell2Layer<Q + 1, JD, CIN>::run(S, offs, rin, choff);
   }
 };
-template <int CIN, int V>
-struct Shell2Loop<56, CIN, V> {
-  __device__ __forceinline__ static void run(float (&)[27][V], const int (&)[56], const float*,
-                                             const float*, int) {}
+template <int JD, int CIN>
+struct Shell2Layer<56, JD, CIN> {
+  __device__ __forceinline__ static void run(float (&)[9][CIN / 4],
+                                             const uint32_t (&)[56], __amdgpu_buffer_rsrc_t,
+                                             uint32_t) {}
 };
 
-template <int CIN, int NT, int MS>
+template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
-    const float* __restrict__ wm, const float* __restrict__ zero_row, const float* __restrict__ bias,
-    int cout, int relu, float* __restrict__ out) {
-  using C = MfmaCfg<CIN, NT, MS>;
-  using Vec = typename VecT<C::VEC>::type;
-  using Acc = typename AccT<MS>::type;
-  constexpr int V = C::VEC;
-  constexpr int KS = C::KS;
+    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
+    int relu, float* __restrict__ out) {
+  using K = CellCfg<CIN, NT>;
+  constexpr int CH = K::CH;
   extern __shared__ float smem[];
   float* wl = smem;
-  weights_to_lds<CIN, NT, MS>(wm, wl);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  weights_to_lds<CIN, NT, 16>(wm, wl);
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
-  int64_t t_begin, t_end;
-  block_tiles((lcnt + MS - 1) / MS, t_begin, t_end);
-  const int m = lane % MS, g = lane / MS;
-  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
-    const int64_t idx = tile * MS + m;
+  const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
+  const int m = lane % 16, g = lane / 16;
+  const uint32_t choff = 4u * (uint32_t)(CH * g);
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+    const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
     if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
-    // Shell rows: lane slot g resolves voxels q = j*KS + g, then the KS lanes
-    // of the cell exchange them.
-    int rows[56];
+    int64_t n;
+    int o[3];
+    cell_origin(info, row, gd, gh, gw, n, o);
+    // Shell rows as byte offsets: lane slot g resolves voxels q = 4 j + g,
+    // then the 4 lanes of the cell exchange them.
+    uint32_t offs[56];
     {
-      int mine[56 / KS];
-      int64_t n = 0;
-      int o0 = 0, o1 = 0, o2 = 0;
-      if (row >= 0) {
-        const uint64_t inf = info[row];
-        const TreePos p = tree_pos((int64_t)(inf >> 10), gd, gh, gw);
-        const Cell c = cell_of((int)(inf & 1023u));
-        n = p.n;
-        o0 = 8 * p.d + c.d;
-        o1 = 8 * p.h + c.h;
-        o2 = 8 * p.w + c.w;
-      }
+      int mine[14];
 #pragma unroll
-      for (int j = 0; j < 56 / KS; ++j) {
-        const int u = c_shell2[j * KS + g];
-        const int vd = o0 - 1 + (u >> 4), vh = o1 - 1 + ((u >> 2) & 3), vw = o2 - 1 + (u & 3);
+      for (int j = 0; j < 14; ++j) {
+        const int u = c_shell2[4 * j + g];
+        const int vd = o[0] - 1 + (u >> 4), vh = o[1] - 1 + ((u >> 2) & 3), vw = o[2] - 1 + (u & 3);
         int r = -1;
         if (row >= 0 && vd >= 0 && vh >= 0 && vw >= 0 && vd < 8 * gd && vh < 8 * gh && vw < 8 * gw) {
           const int64_t tt = ((n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
@@ -795,33 +863,36 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
         mine[j] = r;
       }
 #pragma unroll
-      for (int j = 0; j < 56 / KS; ++j)
+      for (int j = 0; j < 14; ++j)
 #pragma unroll
-        for (int k = 0; k < KS; ++k) rows[j * KS + k] = __shfl(mine[j], m + MS * k, 64);
+        for (int k = 0; k < 4; ++k) offs[4 * j + k] = row_offset<CIN>(__shfl(mine[j], m + 16 * k, 64), 0);
     }
-    Acc acc[NT];
+    float xs[CH];
+    gather_channels<CIN>(rin, row_offset<CIN>(row, 0) + choff, xs);
+    typename K::Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
-#pragma unroll 1
-    for (int cv = 0; cv < C::NV; ++cv) {
-      const int choff = C::CH * g + V * cv;
-      float S[27][V];
-      {
-        const Vec xv = *reinterpret_cast<const Vec*>((row >= 0 ? in + (int64_t)row * CIN : zero_row) + choff);
-#pragma unroll
-        for (int dl = 0; dl < 27; ++dl) {
-          const float vol = (float)((2 - (dl / 9 == 1 ? 0 : 1)) * (2 - ((dl / 3) % 3 == 1 ? 0 : 1)) *
-                                    (2 - (dl % 3 == 1 ? 0 : 1)));
-#pragma unroll
-          for (int e = 0; e < V; ++e) S[dl][e] = vget<V>(xv, e) * vol;
-        }
-      }
-      Shell2Loop<0, CIN, V>::run(S, rows, in, zero_row, choff);
-      contract_slice<CIN, NT, MS>(S, wl, cv, lane, acc);
+      for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
+    {
+      float S[9][CH];
+      init_layer<2, 0>(S, xs);
+      Shell2Layer<0, 0, CIN>::run(S, offs, rin, choff);
+      contract_layer<CIN, NT, 0>(S, wl, lane, acc);
     }
-    store_tile<MS, NT>(acc, row, 0.125f, lane, bias, cout, relu, out);
+    {
+      float S[9][CH];
+      init_layer<2, 1>(S, xs);
+      Shell2Layer<0, 1, CIN>::run(S, offs, rin, choff);
+      contract_layer<CIN, NT, 1>(S, wl, lane, acc);
+    }
+    {
+      float S[9][CH];
+      init_layer<2, 2>(S, xs);
+      Shell2Layer<0, 2, CIN>::run(S, offs, rin, choff);
+      contract_layer<CIN, NT, 2>(S, wl, lane, acc);
+    }
+    store_tile16<NT>(acc, row, 0.125f, lane, bias, cout, relu, out);
   }
 }
 
@@ -833,9 +904,10 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
 // leaf of edge >= 2 or a split depth-2 node whose unit voxels are rows
 // first .. first+7.  Every contribution carries, per axis along which the
 // region extends, the interval [c0, c1) it covers relative to o; its weight
-// for delta is prod_a |[c0, c1) ^ [delta_a, delta_a + SZ)|.
-template <int R, int SZ, int V>
-__device__ __forceinline__ void region_add(float (&S)[27][V], const float (&x)[V], const int (&c0)[3],
+// for delta is prod_a |[c0, c1) ^ [delta_a, delta_a + SZ)|.  Layer JD takes
+// the regions with dir_d in {0, JD - 1}.
+template <int R, int JD, int SZ, int CH>
+__device__ __forceinline__ void region_add(float (&S)[9][CH], const float (&x)[CH], const int (&c0)[3],
                                            const int (&c1)[3]) {
   constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
   float ov[3][3];
@@ -844,31 +916,28 @@ __device__ __forceinline__ void region_add(float (&S)[27][V], const float (&x)[V
 #pragma unroll
     for (int j = 0; j < 3; ++j) ov[a][j] = (float)max(0, min(c1[a], j - 1 + SZ) - max(c0[a], j - 1));
 #pragma unroll
-  for (int j0 = 0; j0 < 3; ++j0) {
-    if (dir0 != 0 && j0 != dir0 + 1) continue;
+  for (int j1 = 0; j1 < 3; ++j1) {
+    if (dir1 != 0 && j1 != dir1 + 1) continue;
 #pragma unroll
-    for (int j1 = 0; j1 < 3; ++j1) {
-      if (dir1 != 0 && j1 != dir1 + 1) continue;
+    for (int j2 = 0; j2 < 3; ++j2) {
+      if (dir2 != 0 && j2 != dir2 + 1) continue;
+      float wgt = 1.f;
+      if (dir0 == 0) wgt *= ov[0][JD];
+      if (dir1 == 0) wgt *= ov[1][j1];
+      if (dir2 == 0) wgt *= ov[2][j2];
 #pragma unroll
-      for (int j2 = 0; j2 < 3; ++j2) {
-        if (dir2 != 0 && j2 != dir2 + 1) continue;
-        float wgt = 1.f;
-        if (dir0 == 0) wgt *= ov[0][j0];
-        if (dir1 == 0) wgt *= ov[1][j1];
-        if (dir2 == 0) wgt *= ov[2][j2];
-#pragma unroll
-        for (int e = 0; e < V; ++e) S[j0 * 9 + j1 * 3 + j2][e] = fmaf(x[e], wgt, S[j0 * 9 + j1 * 3 + j2][e]);
-      }
+      for (int e = 0; e < CH; ++e) S[j1 * 3 + j2][e] = fmaf(x[e], wgt, S[j1 * 3 + j2][e]);
     }
   }
 }
 
-template <int R, int SZ, int CIN, int V>
-__device__ __forceinline__ void region_sum(float (&S)[27][V], const uint32_t* __restrict__ trees,
+template <int R, int JD, int SZ, int CIN>
+__device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4],
+                                           const uint32_t* __restrict__ trees,
                                            const int64_t* __restrict__ prefix, int gd, int gh, int gw,
                                            int64_t n_leaves, int64_t n, const int (&o)[3],
-                                           const float* __restrict__ in, int choff) {
-  using Vec = typename VecT<V>::type;
+                                           __amdgpu_buffer_rsrc_t rin, uint32_t choff) {
+  constexpr int CH = CIN / 4;
   constexpr int dir[3] = {R / 9 - 1, (R / 3) % 3 - 1, R % 3 - 1};
   const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
   int lo[3];
@@ -897,11 +966,10 @@ __device__ __forceinline__ void region_sum(float (&S)[27][V], const uint32_t* __
                 nb2 = dir[2] == 0 ? SZ / 2 : 1;
   const int nblocks = cover >= 0 ? 1 : nb0 * nb1 * nb2;
   for (int bi = 0; bi < nblocks; ++bi) {
-    const int i0 = bi / (nb1 * nb2), i1 = (bi / nb2) % nb1, i2 = bi % nb2;
-    const int bix[3] = {i0, i1, i2};
-    int first;          // row of the block's leaf, or of its first unit voxel
-    int nsub = 1;       // contributions of this block
-    int bo[3];          // block origin in the neighbouring tree
+    const int bix[3] = {bi / (nb1 * nb2), (bi / nb2) % nb1, bi % nb2};
+    int first;     // row of the block's leaf, or of its first unit voxel
+    int nsub = 1;  // contributions of this block
+    int bo[3];     // block origin in the neighbouring tree
 #pragma unroll
     for (int a = 0; a < 3; ++a) bo[a] = dir[a] == 0 ? L[a] + 2 * bix[a] : (L[a] & ~1);
     bool fine = false;
@@ -947,92 +1015,94 @@ __device__ __forceinline__ void region_sum(float (&S)[27][V], const uint32_t* __
       }
       const int64_t rr = (int64_t)first + (fine ? o3 : 0);
       if (rr >= n_leaves) continue;  // only a non-canonical structure gets here
-      const Vec xv = *reinterpret_cast<const Vec*>(in + rr * CIN + choff);
-      float x[V];
-#pragma unroll
-      for (int e = 0; e < V; ++e) x[e] = vget<V>(xv, e);
-      region_add<R, SZ, V>(S, x, c0, c1);
+      float x[CH];
+      gather_channels<CIN>(rin, row_offset<CIN>((int)rr, 0) + choff, x);
+      region_add<R, JD, SZ, CH>(S, x, c0, c1);
     }
   }
 }
 
-template <int R, int SZ, int CIN, int V>
-struct RegionLoop {
-  __device__ __forceinline__ static void run(float (&S)[27][V], const uint32_t* trees,
-                                             const int64_t* prefix, int gd, int gh, int gw,
-                                             int64_t n_leaves, int64_t n, const int (&o)[3],
-                                             const float* in, int choff) {
-    if constexpr (R != 13)
-      region_sum<R, SZ, CIN, V>(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
-    RegionLoop<R + 1, SZ, CIN, V>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
+template <int R, int JD, int SZ, int CIN>
+struct RegionLayer {
+  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4],
+                                             const uint32_t* trees, const int64_t* prefix, int gd,
+                                             int gh, int gw, int64_t n_leaves, int64_t n,
+                                             const int (&o)[3], __amdgpu_buffer_rsrc_t rin,
+                                             uint32_t choff) {
+    constexpr int dir0 = R / 9 - 1;
+    if constexpr (R != 13 && (dir0 == 0 || dir0 == JD - 1)) {
+      region_sum<R, JD, SZ, CIN>(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+      __builtin_amdgcn_sched_barrier(0);  // one region's loads in flight at a time
+    }
+    RegionLayer<R + 1, JD, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
   }
 };
-template <int SZ, int CIN, int V>
-struct RegionLoop<27, SZ, CIN, V> {
-  __device__ __forceinline__ static void run(float (&)[27][V], const uint32_t*, const int64_t*, int,
-                                             int, int, int64_t, int64_t, const int (&)[3],
-                                             const float*, int) {}
+template <int JD, int SZ, int CIN>
+struct RegionLayer<27, JD, SZ, CIN> {
+  __device__ __forceinline__ static void run(float (&)[9][CIN / 4], const uint32_t*,
+                                             const int64_t*, int, int, int, int64_t, int64_t,
+                                             const int (&)[3], __amdgpu_buffer_rsrc_t, uint32_t) {}
 };
 
-template <int CIN, int NT, int MS, int SZ>
+template <int CIN, int NT, int SZ>
 __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
-    const float* __restrict__ wm, const float* __restrict__ zero_row, const float* __restrict__ bias,
-    int cout, int relu, float* __restrict__ out) {
-  using C = MfmaCfg<CIN, NT, MS>;
-  using Vec = typename VecT<C::VEC>::type;
-  using Acc = typename AccT<MS>::type;
-  constexpr int V = C::VEC;
+    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
+    int relu, float* __restrict__ out) {
+  using K = CellCfg<CIN, NT>;
+  constexpr int CH = K::CH;
   extern __shared__ float smem[];
   float* wl = smem;
-  weights_to_lds<CIN, NT, MS>(wm, wl);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  weights_to_lds<CIN, NT, 16>(wm, wl);
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
-  int64_t t_begin, t_end;
-  block_tiles((lcnt + MS - 1) / MS, t_begin, t_end);
-  const int m = lane % MS, g = lane / MS;
-  for (int64_t tile = t_begin + wave; tile < t_end; tile += nwaves) {
-    const int64_t idx = tile * MS + m;
+  const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
+  const int m = lane % 16, g = lane / 16;
+  const uint32_t choff = 4u * (uint32_t)(CH * g);
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+    const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
     if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
-    int o[3] = {0, 0, 0};
-    int64_t n = 0;
-    if (row >= 0) {
-      const uint64_t inf = info[row];
-      const TreePos p = tree_pos((int64_t)(inf >> 10), gd, gh, gw);
-      const Cell c = cell_of((int)(inf & 1023u));
-      n = p.n;
-      o[0] = 8 * p.d + c.d;
-      o[1] = 8 * p.h + c.h;
-      o[2] = 8 * p.w + c.w;
-    }
-    Acc acc[NT];
+    int64_t n;
+    int o[3];
+    cell_origin(info, row, gd, gh, gw, n, o);
+    float xs[CH];
+    gather_channels<CIN>(rin, row_offset<CIN>(row, 0) + choff, xs);
+    typename K::Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
-#pragma unroll 1
-    for (int cv = 0; cv < C::NV; ++cv) {
-      const int choff = C::CH * g + V * cv;
-      float S[27][V];
-      {
-        const Vec xv = *reinterpret_cast<const Vec*>((row >= 0 ? in + (int64_t)row * CIN : zero_row) + choff);
-#pragma unroll
-        for (int dl = 0; dl < 27; ++dl) {
-          const float vol = (float)((SZ - (dl / 9 == 1 ? 0 : 1)) * (SZ - ((dl / 3) % 3 == 1 ? 0 : 1)) *
-                                    (SZ - (dl % 3 == 1 ? 0 : 1)));
-#pragma unroll
-          for (int e = 0; e < V; ++e) S[dl][e] = vget<V>(xv, e) * vol;
-        }
-      }
+      for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
+    // Each layer re-derives the region geometry instead of keeping it live
+    // across layers (which would spill).
+    {
+      float S[9][CH];
+      init_layer<SZ, 0>(S, xs);
       if (row >= 0)
-        RegionLoop<0, SZ, CIN, V>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, in, choff);
-      contract_slice<CIN, NT, MS>(S, wl, cv, lane, acc);
+        RegionLayer<0, 0, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+      contract_layer<CIN, NT, 0>(S, wl, lane, acc);
     }
-    store_tile<MS, NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bias, cout, relu, out);
+    asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
+    {
+      float S[9][CH];
+      init_layer<SZ, 1>(S, xs);
+      if (row >= 0)
+        RegionLayer<0, 1, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+      contract_layer<CIN, NT, 1>(S, wl, lane, acc);
+    }
+    asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
+    {
+      float S[9][CH];
+      init_layer<SZ, 2>(S, xs);
+      if (row >= 0)
+        RegionLayer<0, 2, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+      contract_layer<CIN, NT, 2>(S, wl, lane, acc);
+    }
+    store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bias, cout, relu, out);
   }
 }
 
@@ -1059,20 +1129,21 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 // Instantiated channel pairs.
 // ---------------------------------------------------------------------------
 typedef void (*MfmaFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const int64_t*,
-                       const int64_t*, const float*, const float*, const float*, const float*, int,
+                       const int64_t*, const float*, const float*, uint32_t, const float*, int,
                        int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
-                       const int32_t*, const int64_t*, int, const float*, const float*, const float*,
+                       const int32_t*, const int64_t*, int, const float*, const float*, uint32_t,
                        const float*, int, int, float*);
 typedef void (*WeightFn)(const float*, int, float*);
 
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
-  size_t wfloats;
+  size_t wfloats;       // unit-voxel kernel weights (MS-row tiles)
   MfmaFn kernel;
-  CellFn cell2, cell4, cell8;
   WeightFn weights;
-  int weight_total;
+  size_t cell_wfloats;  // cell kernels' weights (16-row tiles)
+  CellFn cell2, cell4, cell8;
+  WeightFn cell_weights;
 };
 
 template <int CIN, int NT, int MS>
@@ -1086,11 +1157,13 @@ MfmaVariant make_variant(int cout_min) {
   v.nt = NT;
   v.wfloats = C::WFLOATS;
   v.kernel = &k_conv_unit_mfma<CIN, NT, MS>;
-  v.cell2 = &k_conv_cell2_mfma<CIN, NT, MS>;
-  v.cell4 = &k_conv_cellr_mfma<CIN, NT, MS, 4>;
-  v.cell8 = &k_conv_cellr_mfma<CIN, NT, MS, 8>;
   v.weights = &k_mfma_weights<CIN, NT, MS>;
-  v.weight_total = C::WFLOATS;
+  constexpr int CNT = (C::NCOL + 15) / 16;
+  v.cell_wfloats = MfmaCfg<CIN, CNT, 16>::WFLOATS;
+  v.cell2 = &k_conv_cell2_mfma<CIN, CNT>;
+  v.cell4 = &k_conv_cellr_mfma<CIN, CNT, 4>;
+  v.cell8 = &k_conv_cellr_mfma<CIN, CNT, 8>;
+  v.cell_weights = &k_mfma_weights<CIN, CNT, 16>;
   return v;
 }
 
@@ -1131,23 +1204,23 @@ hipError_t device_limits() {
 // Workspace layout (each part 256-byte aligned):
 //   leaf_info  u64 [n_leaves]
 //   wt         f32 [27 cin cout]            generic-kernel weights
-//   wm         f32 [variant wfloats]        MFMA B operands (if a variant exists)
+//   wm         f32 [variant wfloats]        unit-voxel kernel B operands (if a variant exists)
+//   wc         f32 [variant cell_wfloats]   cell kernels' B operands
 //   5 x (scan workspace (n_trees), i64 [n_trees + 1])
 //              unit groups and each kind of larger cell per tree -> prefixes
 //   gkey       i64 [n_leaves / 8 + 1]
 //   brow       i32 [n_leaves]
 //   meta       i64 [kKinds + 1]
-//   zero       f32 [cin]                    a row of zeros (padding reads)
 struct ConvWs {
   uint64_t* info;
   float* wt;
   float* wm;
+  float* wc;
   char* scan[1 + kKinds];
   int64_t* pre[1 + kKinds];  // groups, then the kinds of larger cells
   int64_t* gkey;
   int32_t* brow;
   int64_t* meta;
-  float* zero;
   size_t total;
 };
 
@@ -1165,6 +1238,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
   w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
+  w.wc = reinterpret_cast<float*>(take(v ? sizeof(float) * v->cell_wfloats : 0));
   for (int k = 0; k < 1 + kKinds; ++k) {
     w.scan[k] = take(oci::scan_workspace(n_trees));
     w.pre[k] = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
@@ -1172,7 +1246,6 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.gkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_leaves / 8 + 1)));
   w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
   w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
-  w.zero = reinterpret_cast<float*>(take(sizeof(float) * (size_t)cin));
   w.total = off + 256;
   return w;
 }
@@ -1205,9 +1278,10 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                      a.weight, a.cin, a.cout, w.wt);
   const MfmaVariant* v = find_variant(a.cin, a.cout);
   if (v == nullptr) return hipGetLastError();
-  hipLaunchKernelGGL(v->weights,
-                     dim3((unsigned)((v->weight_total + 255) / 256)), dim3(256), 0, s, a.weight,
-                     a.cout, w.wm);
+  hipLaunchKernelGGL(v->weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
+                     a.weight, a.cout, w.wm);
+  hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256)), dim3(256), 0,
+                     s, a.weight, a.cout, w.wc);
   const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
@@ -1220,8 +1294,6 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],
                      w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
                      a.n_leaves, w.meta);
-  hipLaunchKernelGGL(k_zero, dim3((unsigned)((a.cin + 255) / 256)), dim3(256), 0, s, w.zero,
-                     (int64_t)a.cin);
   return hipGetLastError();
 }
 
@@ -1229,8 +1301,11 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   hipError_t e = init_slots();
   if (e != hipSuccess) return e;
   const ConvWs w = carve(const_cast<void*>(ws), a.n_trees, a.n_leaves, a.cin, a.cout);
-  // The MFMA kernel reads input rows with 16-byte vector loads.
-  if (impl == 2 && (reinterpret_cast<uintptr_t>(a.in) & 15) != 0) impl = 1;
+  // The MFMA kernels gather input rows with 16-byte buffer loads at 32-bit
+  // offsets below kOutside; otherwise the generic kernel runs.
+  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)a.cin * 4u;
+  if (impl == 2 && ((reinterpret_cast<uintptr_t>(a.in) & 15) != 0 || in_bytes64 >= kOutside)) impl = 1;
+  const uint32_t in_bytes = (uint32_t)(in_bytes64 < kOutside ? in_bytes64 : 0);
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
   const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
@@ -1244,7 +1319,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   e = device_limits();
   if (e != hipSuccess) return e;
   const MfmaVariant* v = find_variant(a.cin, a.cout);
-  const size_t wsmem = sizeof(float) * v->wfloats;
+  const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
   const int nblk = ((g_num_cus + 7) / 8) * 8;
@@ -1253,8 +1328,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kMfmaThreads), msmem, s, a.trees, a.prefix, a.gd,
                      a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
-                     (const int64_t*)(w.pre[0] + a.n_trees), a.in, (const float*)w.wm,
-                     (const float*)w.zero, a.bias, a.cout, a.relu, a.out);
+                     (const int64_t*)(w.pre[0] + a.n_trees), a.in, (const float*)w.wm, in_bytes,
+                     a.bias, a.cout, a.relu, a.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // Larger cells, one launch per kind: trivial edge-8, other edge-8, edge-4,
@@ -1266,8 +1341,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
-                       (const int64_t*)w.meta, k, a.in, (const float*)w.wm, (const float*)w.zero,
-                       a.bias, a.cout, a.relu, a.out);
+                       (const int64_t*)w.meta, k, a.in, (const float*)w.wc, in_bytes, a.bias,
+                       a.cout, a.relu, a.out);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
