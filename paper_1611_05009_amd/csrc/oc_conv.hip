@@ -13,6 +13,15 @@
 // window sums followed by one (27*Cin) x Cout contraction per leaf.
 #include "oc_internal.h"
 
+// Tuning knobs (compile-time): deltas of gathered A rows in flight in the
+// unit-voxel kernel; shell voxels / regions per scheduling group in the cell
+// kernels.
+#ifndef OC_UNIT_ACCS
+#define OC_UNIT_ACCS 1
+#endif
+#ifndef OC_UNIT_PREFETCH
+#define OC_UNIT_PREFETCH 2
+#endif
 using namespace ocd;
 
 namespace {
@@ -67,6 +76,13 @@ constexpr int shell2_u(int q) {
     if (k == q) return u;
     ++k;
   }
+  return -1;
+}
+
+// Index in that list of shell voxel u (-1 for the cell's own voxels).
+constexpr int shell2_q(int u) {
+  for (int q = 0; q < 56; ++q)
+    if (shell2_u(q) == u) return q;
   return -1;
 }
 
@@ -431,6 +447,32 @@ __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* 
 }
 
 
+// Voxel u of the 4^3 neighbourhood of group `key`, split into its tree (-1
+// outside the grid) and its local position (d<<6 | h<<3 | w): the address
+// part of neighbour_row, so that the tree loads can be issued early.
+struct NbProbe {
+  int64_t tt;
+  int local;
+};
+
+__device__ __forceinline__ NbProbe neighbour_probe(int gd, int gh, int gw, int64_t key, int u) {
+  NbProbe r;
+  r.tt = -1;
+  r.local = 0;
+  if (key < 0) return r;
+  const int64_t t = key >> 6;
+  const int q = (int)(key & 63);
+  const TreePos p = tree_pos(t, gd, gh, gw);
+  const int o1 = q >> 3, o2 = q & 7;
+  const int vd = 8 * p.d + 4 * ((o1 >> 2) & 1) + 2 * ((o2 >> 2) & 1) - 1 + (u >> 4);
+  const int vh = 8 * p.h + 4 * ((o1 >> 1) & 1) + 2 * ((o2 >> 1) & 1) - 1 + ((u >> 2) & 3);
+  const int vw = 8 * p.w + 4 * (o1 & 1) + 2 * (o2 & 1) - 1 + (u & 3);
+  if (vd < 0 || vh < 0 || vw < 0 || vd >= 8 * gd || vh >= 8 * gh || vw >= 8 * gw) return r;
+  r.tt = ((p.n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
+  r.local = ((vd & 7) << 6) | ((vh & 7) << 3) | (vw & 7);
+  return r;
+}
+
 // Row of the leaf holding voxel u (u = 16 ud + 4 uh + uw, each in 0..3) of
 // the 4^3 neighbourhood [p-1, p+3) of the group's 2^3 block at origin p;
 // -1 outside the grid (zero padding).
@@ -572,7 +614,9 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
   __syncthreads();
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  int32_t* nb = nb_all + wave * (C::GROUPS * 64);
+  // Two neighbourhood tables per wave: the current tile's, and the next
+  // tile's, which is resolved in stages between the MFMAs of this one.
+  int32_t* nb_w = nb_all + wave * (2 * C::GROUPS * 64);
   const int64_t G = min(*n_groups, n_leaves / 8);
   const int64_t n_tiles = (G + C::GROUPS - 1) / C::GROUPS;
   const WaveTiles wt = wave_tiles(n_tiles);
@@ -581,31 +625,95 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
   const int gi = m >> 3, o3 = m & 7;
   const int ubase = gi * 64 + ((o3 >> 2) & 1) * 16 + ((o3 >> 1) & 1) * 4 + (o3 & 1);
   const int col = lane % MS;
-  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+  // Staged lookup of the neighbourhood rows of tile t into table nbt.
+  int64_t keys[C::GROUPS];
+  NbProbe probe[C::GROUPS];
+  Bits pbits[C::GROUPS];
+  int64_t pbase[C::GROUPS];
+  auto stage_keys = [&](int64_t t) {
 #pragma unroll
     for (int q = 0; q < C::GROUPS; ++q) {
-      const int64_t gidx = tile * C::GROUPS + q;
-      int32_t r = gidx < G ? neighbour_row(trees, prefix, gd, gh, gw, gkey[gidx], lane) : -1;
-      if (r >= n_leaves) r = -1;  // only a non-canonical structure gets here
-      nb[q * 64 + lane] = r;
+      const int64_t gidx = t * C::GROUPS + q;
+      keys[q] = (t < wt.end && gidx < G) ? gkey[gidx] : -1;
+    }
+  };
+  auto stage_trees = [&]() {
+#pragma unroll
+    for (int q = 0; q < C::GROUPS; ++q) {
+      probe[q] = neighbour_probe(gd, gh, gw, keys[q], lane);
+      const int64_t tt = probe[q].tt < 0 ? 0 : probe[q].tt;
+      pbits[q] = load_bits(trees, tt);
+      pbase[q] = prefix[tt];
+    }
+  };
+  auto stage_rows = [&](int32_t* nbt) {
+#pragma unroll
+    for (int q = 0; q < C::GROUPS; ++q) {
+      int32_t r = -1;
+      if (probe[q].tt >= 0) {
+        const int l = probe[q].local;
+        const int64_t rr =
+            pbase[q] + data_idx(pbits[q], leaf_at(pbits[q], (l >> 6) & 7, (l >> 3) & 7, l & 7));
+        r = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
+      }
+      nbt[q * 64 + lane] = r;
     }
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    Acc acc[NT];
+  };
+  // Epilogue of a finished tile (unit cells need no 1/s^3 scaling).
+  auto store_unit_tile = [&](const Acc (&res)[NT], const int32_t* tnb) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt) {
+      const int co = MS * nt + col;
+      const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
 #pragma unroll
-      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
+        const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
+        const int row0 = tnb[(i >> 3) * 64 + 21];  // voxel (1,1,1): first row of the group
+        if (row0 < 0 || row0 + 8 > n_leaves || co >= cout) continue;
+        float v = res[nt][r] + bv;
+        if (relu) v = fmaxf(v, 0.f);
+        out[(int64_t)(row0 + (i & 7)) * cout + co] = v;
+      }
+    }
+  };
+  Acc pacc[NT];
+  const int32_t* pnb = nb_w;
+  bool have_prev = false;
+  int cur = 0;
+  stage_keys(wt.first);
+  stage_trees();
+  stage_rows(nb_w);
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+    int32_t* nb = nb_w + cur * (C::GROUPS * 64);
+    int32_t* nb_next = nb_w + (cur ^ 1) * (C::GROUPS * 64);
+    const int64_t next = tile + wt.stride;
+    // OC_UNIT_ACCS independent accumulator sets (deltas alternate between
+    // them) so that consecutive MFMAs do not wait on each other's results.
+    constexpr int NA = OC_UNIT_ACCS;
+    Acc acc2[NA][NT];
+#pragma unroll
+    for (int a2 = 0; a2 < NA; ++a2)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc2[a2][nt][r] = 0.f;
     // Software pipeline: the gathered A rows of delta dl+2 and the B operands
     // of delta dl+1 are in flight while the MFMAs of delta dl issue.  The
     // scheduling barriers keep the compiler from sinking the loads back to
     // their use.
-    Vec abuf[3][C::NV];
+    constexpr int PD = OC_UNIT_PREFETCH;  // deltas of gathers in flight
+    Vec abuf[PD + 1][C::NV];
     Vec bbuf[2][NT][C::NV];
+    // The 27 A-row offsets of this lane, read from the table up front so that
+    // no LDS round trip sits between a delta's MFMAs and its gathers.
+    uint32_t aoff[27];
+#pragma unroll
+    for (int dl = 0; dl < 27; ++dl)
+      aoff[dl] = row_offset<CIN>(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3], C::CH * g);
     auto load_a = [&](int dl, Vec* a) {
-      const int dd = dl / 9, dh = (dl / 3) % 3, dw = dl % 3;
-      const int row = nb[ubase + dd * 16 + dh * 4 + dw];
-      const uint32_t off = row_offset<CIN>(row, C::CH * g);
+      const uint32_t off = aoff[dl];
 #pragma unroll
       for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VEC * v);
     };
@@ -617,13 +725,20 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
         for (int v = 0; v < C::NV; ++v) b[nt][v] = bsrc[v * 64];
       }
     };
-    load_a(0, abuf[0]);
-    load_a(1, abuf[1]);
+#pragma unroll
+    for (int k = 0; k < PD; ++k) load_a(k, abuf[k]);
     load_b(0, bbuf[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (have_prev) store_unit_tile(pacc, pnb);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int dl = 0; dl < 27; ++dl) {
-      if (dl + 2 < 27) load_a(dl + 2, abuf[(dl + 2) % 3]);
+      if (dl + PD < 27) load_a(dl + PD, abuf[(dl + PD) % (PD + 1)]);
       if (dl + 1 < 27) load_b(dl + 1, bbuf[(dl + 1) % 2]);
+      // The next tile's lookups: keys, then tree bits and prefixes, then rows.
+      if (dl == 3) stage_keys(next);
+      if (dl == 9) stage_trees();
+      if (dl == 18) stage_rows(nb_next);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
@@ -631,27 +746,29 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
         for (int v = 0; v < C::NV; ++v)
 #pragma unroll
           for (int e = 0; e < C::VEC; ++e)
-            acc[nt] = mfma<MS>(vget<C::VEC>(abuf[dl % 3][v], e),
-                               vget<C::VEC>(bbuf[dl % 2][nt][v], e), acc[nt]);
+            acc2[(v * C::VEC + e) % NA][nt] =
+                mfma<MS>(vget<C::VEC>(abuf[dl % (PD + 1)][v], e),
+                         vget<C::VEC>(bbuf[dl % 2][nt][v], e), acc2[(v * C::VEC + e) % NA][nt]);
       __builtin_amdgcn_sched_barrier(0);
     }
-    // Epilogue: unit cells need no 1/s^3 scaling.
+    Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const int co = MS * nt + col;
-      const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+      acc[nt] = acc2[0][nt];
 #pragma unroll
-      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
-        const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
-        const int row0 = nb[(i >> 3) * 64 + 21];  // voxel (1,1,1): first row of the group
-        if (row0 < 0 || row0 + 8 > n_leaves || co >= cout) continue;
-        float v = acc[nt][r] + bv;
-        if (relu) v = fmaxf(v, 0.f);
-        out[(int64_t)(row0 + (i & 7)) * cout + co] = v;
-      }
+      for (int a2 = 1; a2 < NA; ++a2) acc[nt] += acc2[a2][nt];
     }
+    // The stores of this tile are issued after the next tile's first
+    // gathers: stores share the load counter, so storing now would make the
+    // next tile's first waits wait for them too.
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) pacc[nt] = acc[nt];
+    pnb = nb;
+    have_prev = true;
+    cur ^= 1;
     __builtin_amdgcn_wave_barrier();  // nb is rewritten by the next tile
   }
+  if (have_prev) store_unit_tile(pacc, pnb);
 }
 
 // ---------------------------------------------------------------------------
@@ -669,6 +786,13 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
 // reaches it.  The shell geometry of each layer is fixed at compile time, so
 // every S_delta stays in a fixed register.
 // ---------------------------------------------------------------------------
+#ifndef OC_REGION_GROUP
+#define OC_REGION_GROUP 3
+#endif
+#ifndef OC_SHELL_GROUP
+#define OC_SHELL_GROUP 8
+#endif
+
 template <int CIN, int NT, int MS>
 __device__ __forceinline__ void weights_to_lds(const float* __restrict__ wm, float* wl) {
   using C = MfmaCfg<CIN, NT, MS>;
@@ -786,37 +910,74 @@ __device__ __forceinline__ void init_layer(float (&S)[9][CH], const float (&xs)[
 // Edge-2 cells.  Shell voxel u (of the 4^3 block [o-1, o+3) minus the cell)
 // lies in the window of delta iff u_a - delta_a - 1 is in {0, 1} on every
 // axis; layer JD (delta_d = JD - 1) reaches the voxel planes u_d = JD, JD + 1.
-template <int Q, int JD, int CIN>
-struct Shell2Layer {
-  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4],
-                                             const uint32_t (&offs)[56], __amdgpu_buffer_rsrc_t rin,
-                                             uint32_t choff) {
-    constexpr int u = shell2_u(Q);
-    constexpr int ud = u >> 4, uh = (u >> 2) & 3, uw = u & 3;
-    if constexpr (ud == JD || ud == JD + 1) {
-      float x[CIN / 4];
-      gather_channels<CIN>(rin, offs[Q] + choff, x);
-#pragma unroll
-      for (int jh = 0; jh < 3; ++jh) {
-        if (uh - jh < 0 || uh - jh > 1) continue;
-#pragma unroll
-        for (int jw = 0; jw < 3; ++jw) {
-          if (uw - jw < 0 || uw - jw > 1) continue;
-#pragma unroll
-          for (int e = 0; e < CIN / 4; ++e) S[jh * 3 + jw][e] += x[e];
-        }
-      }
-      if constexpr (Q % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bounds the loads in flight
+// Within a layer the voxels are taken one h-row (u_h = UH) at a time: the
+// 8 voxels (u_d in {JD, JD + 1}, u_w = 0..3) of a row are gathered into X,
+// and once rows 0..JH+1 are added the window sums of delta-row JH
+// (delta_h = JH - 1) are complete and can enter the MFMA while the next
+// row's gathers are in flight.
+constexpr bool shell2_inner(int u) {
+  return (u >> 4) >= 1 && (u >> 4) <= 2 && ((u >> 2) & 3) >= 1 && ((u >> 2) & 3) <= 2 &&
+         (u & 3) >= 1 && (u & 3) <= 2;
+}
+
+template <int JD, int UH, int K, int CIN>
+struct Shell2RowLoad {
+  __device__ __forceinline__ static void run(float (&X)[8][CIN / 4], const uint32_t (&offs)[56],
+                                             __amdgpu_buffer_rsrc_t rin, uint32_t choff) {
+    constexpr int u = (JD + K / 4) * 16 + UH * 4 + (K % 4);
+    if constexpr (!shell2_inner(u)) {
+      constexpr int q = shell2_q(u);
+      gather_channels<CIN>(rin, offs[q] + choff, X[K]);
     }
-    Shell2Layer<Q + 1, JD, CIN>::run(S, offs, rin, choff);
+    Shell2RowLoad<JD, UH, K + 1, CIN>::run(X, offs, rin, choff);
   }
 };
-template <int JD, int CIN>
-struct Shell2Layer<56, JD, CIN> {
-  __device__ __forceinline__ static void run(float (&)[9][CIN / 4],
-                                             const uint32_t (&)[56], __amdgpu_buffer_rsrc_t,
-                                             uint32_t) {}
+template <int JD, int UH, int CIN>
+struct Shell2RowLoad<JD, UH, 8, CIN> {
+  __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t (&)[56],
+                                             __amdgpu_buffer_rsrc_t, uint32_t) {}
 };
+
+template <int JD, int UH, int CIN>
+__device__ __forceinline__ void shell2_row_add(float (&S)[9][CIN / 4], const float (&X)[8][CIN / 4]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const int u = (JD + k / 4) * 16 + UH * 4 + (k % 4);
+    if (shell2_inner(u)) continue;
+    const int uw = k % 4;
+#pragma unroll
+    for (int jh = 0; jh < 3; ++jh) {
+      if (UH - jh < 0 || UH - jh > 1) continue;
+#pragma unroll
+      for (int jw = 0; jw < 3; ++jw) {
+        if (uw - jw < 0 || uw - jw > 1) continue;
+#pragma unroll
+        for (int e = 0; e < CIN / 4; ++e) S[jh * 3 + jw][e] += X[k][e];
+      }
+    }
+  }
+}
+
+// Contract delta-row JH (delta_h = JH - 1) of layer JD into acc.
+template <int CIN, int NT, int JD, int JH>
+__device__ __forceinline__ void contract_row(const float (&S)[9][CIN / 4], const float* wl, int lane,
+                                             typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+  using K = CellCfg<CIN, NT>;
+#pragma unroll
+  for (int jw = 0; jw < 3; ++jw) {
+    const int k = JH * 3 + jw, dl = 9 * JD + k;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int jv = 0; jv < K::NV; ++jv) {
+        const typename K::Vec bv =
+            reinterpret_cast<const typename K::Vec*>(wl)[((dl * NT + nt) * K::NV + jv) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < K::VEC; ++e)
+          acc[nt] = mfma<16>(S[k][K::VEC * jv + e], vget<K::VEC>(bv, e), acc[nt]);
+      }
+  }
+}
 
 template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
@@ -874,24 +1035,32 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
-    {
-      float S[9][CH];
-      init_layer<2, 0>(S, xs);
-      Shell2Layer<0, 0, CIN>::run(S, offs, rin, choff);
-      contract_layer<CIN, NT, 0>(S, wl, lane, acc);
-    }
-    {
-      float S[9][CH];
-      init_layer<2, 1>(S, xs);
-      Shell2Layer<0, 1, CIN>::run(S, offs, rin, choff);
-      contract_layer<CIN, NT, 1>(S, wl, lane, acc);
-    }
-    {
-      float S[9][CH];
-      init_layer<2, 2>(S, xs);
-      Shell2Layer<0, 2, CIN>::run(S, offs, rin, choff);
-      contract_layer<CIN, NT, 2>(S, wl, lane, acc);
-    }
+    float S[9][CH];
+    float X[8][CH];
+#define OC_LOAD(JD, UH) \
+  Shell2RowLoad<JD, UH, 0, CIN>::run(X, offs, rin, choff); \
+  __builtin_amdgcn_sched_barrier(0)
+#define OC_ADD(JD, UH) \
+  __builtin_amdgcn_sched_barrier(0); \
+  shell2_row_add<JD, UH, CIN>(S, X)
+#define OC_MMA(JD, JH) contract_row<CIN, NT, JD, JH>(S, wl, lane, acc)
+    init_layer<2, 0>(S, xs);
+    OC_LOAD(0, 0); OC_ADD(0, 0);
+    OC_LOAD(0, 1); OC_ADD(0, 1);
+    OC_LOAD(0, 2); OC_MMA(0, 0); OC_ADD(0, 2);
+    OC_LOAD(0, 3); OC_MMA(0, 1); OC_ADD(0, 3);
+    OC_LOAD(1, 0); OC_MMA(0, 2); __builtin_amdgcn_sched_barrier(0); init_layer<2, 1>(S, xs); OC_ADD(1, 0);
+    OC_LOAD(1, 1); OC_ADD(1, 1);
+    OC_LOAD(1, 2); OC_MMA(1, 0); OC_ADD(1, 2);
+    OC_LOAD(1, 3); OC_MMA(1, 1); OC_ADD(1, 3);
+    OC_LOAD(2, 0); OC_MMA(1, 2); __builtin_amdgcn_sched_barrier(0); init_layer<2, 2>(S, xs); OC_ADD(2, 0);
+    OC_LOAD(2, 1); OC_ADD(2, 1);
+    OC_LOAD(2, 2); OC_MMA(2, 0); OC_ADD(2, 2);
+    OC_LOAD(2, 3); OC_MMA(2, 1); OC_ADD(2, 3);
+    OC_MMA(2, 2);
+#undef OC_LOAD
+#undef OC_ADD
+#undef OC_MMA
     store_tile16<NT>(acc, row, 0.125f, lane, bias, cout, relu, out);
   }
 }
@@ -1032,7 +1201,8 @@ struct RegionLayer {
     constexpr int dir0 = R / 9 - 1;
     if constexpr (R != 13 && (dir0 == 0 || dir0 == JD - 1)) {
       region_sum<R, JD, SZ, CIN>(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
-      __builtin_amdgcn_sched_barrier(0);  // one region's loads in flight at a time
+      // A few regions' loads in flight at a time (more would spill).
+      if constexpr (R % OC_REGION_GROUP == OC_REGION_GROUP - 1) __builtin_amdgcn_sched_barrier(0);
     }
     RegionLayer<R + 1, JD, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
   }
@@ -1053,9 +1223,13 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     int relu, float* __restrict__ out) {
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
+#ifdef OC_EXP_BGLOBAL
+  const float* wl = wm;
+#else
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
+#endif
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
@@ -1183,7 +1357,7 @@ const MfmaVariant* find_variant(int cin, int cout) {
 constexpr int kMfmaThreads = 512;
 
 size_t mfma_smem(const MfmaVariant& v) {
-  return sizeof(float) * v.wfloats + sizeof(int32_t) * (kMfmaThreads / 64) * (v.ms / 8) * 64;
+  return sizeof(float) * v.wfloats + sizeof(int32_t) * (kMfmaThreads / 64) * 2 * (v.ms / 8) * 64;
 }
 
 int g_num_cus = 0;
@@ -1339,7 +1513,13 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)wsmem);
     if (e != hipSuccess) return e;
+#ifdef OC_EXP_BGLOBAL
+    const bool glob = k != 3;
+    hipLaunchKernelGGL(cells[k], dim3(glob ? OC_EXP_BLOCKS * nblk : nblk), dim3(glob ? OC_EXP_THREADS : kMfmaThreads),
+                       glob ? 0 : wsmem, s, a.trees, a.prefix, a.gd,
+#else
     hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
+#endif
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
                        (const int64_t*)w.meta, k, a.in, (const float*)w.wc, in_bytes, a.bias,
                        a.cout, a.relu, a.out);

@@ -132,40 +132,110 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
   }
 }
 
-// Eq. 12 data (plain or guided): one wave per output tree.
+// Row copies for the leaves marked in m (lane j of m holds out_row, src_row):
+// the leaves are compacted into the wave's LDS slots, then copied W floats
+// per lane with several rows side by side (8 rows per instruction for 32
+// channels and W = 4).
+template <int W>
+__device__ __forceinline__ void copy_leaf_rows(uint64_t m, int64_t out_row, int64_t src_row,
+                                               const float* __restrict__ in, int c,
+                                               float* __restrict__ out, int64_t* slots) {
+  const int nl = __popcll(m);
+  if (nl == 0) return;
+  const int lane = lane_id();
+  if ((m >> lane) & 1ull) {
+    const int k = __popcll(m & lanemask_lt());
+    slots[2 * k] = out_row;
+    slots[2 * k + 1] = src_row;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  const int ne = c / W;  // W-float elements per row
+  const int lpr = ne < 64 ? ne : 64;
+  const int rpi = 64 / lpr;
+  const int q0 = lane % lpr, rsub = lane / lpr;
+  for (int r0 = 0; r0 < nl; r0 += rpi) {
+    const int r = r0 + rsub;
+    if (rsub < rpi && r < nl) {
+      const int64_t o = slots[2 * r], sr = slots[2 * r + 1];
+      for (int q = q0; q < ne; q += lpr) {
+        if constexpr (W == 4)
+          reinterpret_cast<float4*>(out + o * c)[q] = reinterpret_cast<const float4*>(in + sr * c)[q];
+        else
+          out[o * c + q] = in[sr * c + q];
+      }
+    }
+  }
+  __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next call
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+}
+
+// Eq. 12 data (plain or guided): one wave per input tree and its 8 output
+// trees.  An output tree with a single leaf copies the input leaf that holds
+// it (the input node 1 + o, or the input root when that is unsplit); the
+// leaves of a split output tree are enumerated 64 positions at a time and
+// each copies the input leaf holding its voxels at half resolution.
+template <int W>
 __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_trees,
-                                                const int64_t* __restrict__ in_prefix, int64_t n_out,
+                                                const int64_t* __restrict__ in_prefix, int64_t n_in,
                                                 int gd, int gh, int gw, const float* __restrict__ in,
                                                 int c, const uint32_t* __restrict__ out_trees,
                                                 const int64_t* __restrict__ out_prefix,
                                                 float* __restrict__ out) {
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= n_out) return;
-  const TreePos p = tree_pos(t, 2 * gd, 2 * gh, 2 * gw);
-  const int o = ((p.d & 1) << 2) | ((p.h & 1) << 1) | (p.w & 1);
-  const int64_t ti = ((p.n * gd + (p.d >> 1)) * gh + (p.h >> 1)) * gw + (p.w >> 1);
+  __shared__ int64_t slots_all[4][128];
+  const int wave = threadIdx.x >> 6;
+  const int64_t ti = (int64_t)blockIdx.x * 4 + wave;
+  if (ti >= n_in) return;  // whole wave exits together
+  int64_t* slots = slots_all[wave];
+  const int lane = lane_id();
+  const TreePos p = tree_pos(ti, gd, gh, gw);
   const Bits ib = load_bits(in_trees, ti);
   const int64_t in_row0 = in_prefix[ti];
-  const Bits ob = load_bits(out_trees, t);
-  const int64_t row0 = out_prefix[t];
-  int base = 0;
-  for (int c0 = 0; c0 < kNodes; c0 += 64) {
-    const int i = c0 + lane_id();
-    const bool leaf = i < kNodes && is_leaf(ob, i);
-    const uint64_t m = __ballot(leaf);
-    int64_t orow = 0, srow = 0;
-    if (leaf) {
-      orow = row0 + base + __popcll(m & lanemask_lt());
-      int node;
-      if (!(ib.lo & 1ull)) node = 0;                      // unsplit input tree
-      else if (i == 0) node = 1 + o;                      // output root <- input depth 1
-      else if (i < 9) node = 9 + 8 * o + (i - 1);         // depth 1 <- depth 2
-      else if (i < 73) node = 73 + 64 * o + (i - 9);      // depth 2 <- depth-3 voxel
-      else node = 73 + 64 * o + ((i - 73) >> 3);          // guided depth 3 <- same voxel
-      srow = in_row0 + data_idx(ib, node);
+  const bool in_split = (ib.lo & 1ull) != 0;
+  const int Gh = 2 * gh, Gw = 2 * gw, Gd = 2 * gd;
+  auto out_tree = [&](int o) {
+    return ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw + 2 * p.w +
+           (o & 1);
+  };
+  // Output trees with a single leaf.
+  bool single = false;
+  int64_t orow = 0, srow = 0;
+  if (lane < 8) {
+    const int64_t t = out_tree(lane);
+    const Bits ob = load_bits(out_trees, t);
+    single = !(ob.lo & 1ull);
+    if (single) {
+      orow = out_prefix[t];
+      srow = in_row0 + data_idx(ib, in_split ? 1 + lane : 0);
     }
-    copy_rows(m, orow, srow, 1, in, c, out);
-    base += __popcll(m);
+  }
+  const uint64_t singles = __ballot(single);
+  const uint64_t split = __ballot(lane < 8 && !single);
+  copy_leaf_rows<W>(singles, orow, srow, in, c, out, slots);
+  // Split output trees.
+  for (uint32_t sm = (uint32_t)split; sm; sm &= sm - 1) {
+    const int o = __ffs(sm) - 1;
+    const int64_t t = out_tree(o);
+    const Bits ob = load_bits(out_trees, t);
+    const int64_t row0 = out_prefix[t];
+    int base = 0;
+    for (int c0 = 1; c0 < kNodes; c0 += 64) {
+      const int i = c0 + lane;
+      const bool leaf = i < kNodes && is_leaf(ob, i);
+      const uint64_t m = __ballot(leaf);
+      int64_t lo = 0, ls = 0;
+      if (leaf) {
+        lo = row0 + base + __popcll(m & lanemask_lt());
+        int node;
+        if (!in_split) node = 0;                       // unsplit input tree (guided only)
+        else if (i < 9) node = 9 + 8 * o + (i - 1);    // depth 1 <- depth 2
+        else if (i < 73) node = 73 + 64 * o + (i - 9); // depth 2 <- depth-3 voxel
+        else node = 73 + 64 * o + ((i - 73) >> 3);     // guided depth 3 <- same voxel
+        ls = in_row0 + data_idx(ib, node);
+      }
+      copy_leaf_rows<W>(m, lo, ls, in, c, out, slots);
+      base += __popcll(m);
+    }
   }
 }
 
@@ -220,9 +290,15 @@ hipError_t launch_pool_max(const uint32_t* in_trees, const int64_t* in_prefix, i
 hipError_t launch_unpool(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
                          int gw, const float* in, int c, const uint32_t* out_trees,
                          const int64_t* out_prefix, float* out, hipStream_t s) {
-  const int64_t no = 8LL * n * gd * gh * gw;
-  hipLaunchKernelGGL(k_unpool, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
-                     gd, gh, gw, in, c, out_trees, out_prefix, out);
+  const int64_t ni = (int64_t)n * gd * gh * gw;
+  const bool vec = c % 4 == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_unpool<4>, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
+                       gd, gh, gw, in, c, out_trees, out_prefix, out);
+  else
+    hipLaunchKernelGGL(k_unpool<1>, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
+                       gd, gh, gw, in, c, out_trees, out_prefix, out);
   return hipGetLastError();
 }
 
