@@ -365,14 +365,15 @@ __device__ __forceinline__ int depth2_splits(const Bits& b) {
 // other edge-8 cells, edge-4 cells, edge-2 cells.
 constexpr int kKinds = 4;
 
-// Per-tree counts: unit-voxel groups (split depth-2 nodes) and each kind of
-// larger cell.  Edge-8 cells are unsplit trees, edge-4 cells unsplit depth-1
-// nodes of a split root, edge-2 cells unsplit depth-2 nodes of a split
-// depth-1 node.
+// Per-tree counts: unit-voxel groups (split depth-2 nodes), each kind of
+// larger cell, and boundary-sum slots.  Edge-8 cells are unsplit trees,
+// edge-4 cells unsplit depth-1 nodes of a split root, edge-2 cells unsplit
+// depth-2 nodes of a split depth-1 node.  A split tree has one slot for
+// itself and one per split depth-1 node.
 __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees, int gd, int gh,
                              int gw, int32_t* __restrict__ n_grp, int32_t* __restrict__ n8t,
                              int32_t* __restrict__ n8n, int32_t* __restrict__ n4,
-                             int32_t* __restrict__ n2) {
+                             int32_t* __restrict__ n2, int32_t* __restrict__ nslot) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
   const Bits b = load_bits(trees, t);
@@ -397,18 +398,20 @@ __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees
   n8n[t] = (!root && !trivial) ? 1 : 0;
   n4[t] = root ? 8 - p1 : 0;
   n2[t] = max(0, 8 * p1 - p2);
+  nslot[t] = root ? 1 + p1 : 0;
 }
 
 // Leaf lists.  gkey: one key per unit-voxel group.  brow: the rows of every
 // larger cell, grouped by kind (tree order within a kind), so that a tile of
-// consecutive entries of one kind holds cells of one size.
+// consecutive entries of one kind holds cells of one size.  stl: the split
+// trees in order (there are n_trees - meta[0] - meta[1]).
 // meta = {count of each kind, total}.
 __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
                              const int64_t* __restrict__ gpre, const int64_t* __restrict__ p8t,
                              const int64_t* __restrict__ p8n, const int64_t* __restrict__ p4,
                              const int64_t* __restrict__ p2, int64_t n_trees,
                              int64_t* __restrict__ gkey, int32_t* __restrict__ brow, int64_t gcap,
-                             int64_t bcap, int64_t* __restrict__ meta) {
+                             int64_t bcap, int32_t* __restrict__ stl, int64_t* __restrict__ meta) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
   const int64_t c8t = p8t[n_trees], c8n = p8n[n_trees], c4 = p4[n_trees], c2 = p2[n_trees];
@@ -428,6 +431,7 @@ __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* 
   };
   if (p8t[t + 1] > p8t[t]) put(p8t[t], row0);
   if (p8n[t + 1] > p8n[t]) put(c8t + p8n[t], row0);
+  if (b.lo & 1ull) stl[t - p8t[t] - p8n[t]] = (int32_t)t;
   const int64_t n4t = p4[t + 1] - p4[t];
   for (int64_t k = p4[t]; k < p4[t + 1]; ++k) put(c8t + c8n + k, row0 + (k - p4[t]));
   for (int64_t k = p2[t]; k < p2[t + 1]; ++k) put(c8t + c8n + c4 + k, row0 + n4t + (k - p2[t]));
@@ -983,7 +987,8 @@ template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
+    const int64_t* __restrict__ meta, int kind, const int64_t* __restrict__,
+    const float* __restrict__, int64_t, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
   using K = CellCfg<CIN, NT>;
@@ -1065,49 +1070,222 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Boundary sums.  Boundary set e (e in {-1, 0, 1}^3, e != 0) of an aligned
+// cubic block holds the voxels whose coordinate along every axis with
+// e_a != 0 is the block's first (e_a = -1) or last (e_a = +1): 6 faces, 12
+// edge lines and 8 corners.  Once per convolution the input is summed over
+// every boundary set of every split tree and every split depth-1 node, per
+// voxel (a leaf counts once for each of its voxels in the set).  A split
+// tree t owns slot sbase[t] and, for its k-th split depth-1 node, slot
+// sbase[t] + 1 + k; slot s holds 26 rows of cin floats at
+// bsum[(26 s + set) cin].
+// ---------------------------------------------------------------------------
+constexpr int kSets = 26;
+
+__host__ __device__ constexpr int bset(int ed, int eh, int ew) {
+  return (ed + 1) * 9 + (eh + 1) * 3 + (ew + 1) - ((ed + 1) * 9 + (eh + 1) * 3 + (ew + 1) > 13);
+}
+
+// Is coordinate x (of a block of edge B) inside set component e?
+__host__ __device__ constexpr bool in_set(int e, int x, int B) {
+  return e == 0 || (e < 0 ? x == 0 : x == B - 1);
+}
+
+// The 56 boundary voxels V (= 16 x0 + 4 x1 + x2) of a 4^3 block, K-th in
+// ascending order: load reads each from its leaf (r2: row of each 2^3
+// octant's leaf or first unit voxel, sp: which octants are split), add puts
+// each into the sets that hold it.
+constexpr bool interior4(int v) {
+  return (v >> 4) % 3 != 0 && ((v >> 2) & 3) % 3 != 0 && (v & 3) % 3 != 0;
+}
+
+template <int V, int K>
+struct BoundaryVoxels {
+  static constexpr int x0 = V >> 4, x1 = (V >> 2) & 3, x2 = V & 3;
+  static constexpr bool skip = interior4(V);
+  static constexpr int NK = skip ? K : K + 1;
+  template <int CIN>
+  __device__ __forceinline__ static void load(float (&xv)[56], const int (&r2)[8], int sp,
+                                              __amdgpu_buffer_rsrc_t rin, int c) {
+    if constexpr (!skip) {
+      constexpr int o2 = 4 * (x0 >> 1) + 2 * (x1 >> 1) + (x2 >> 1);
+      constexpr int u = 4 * (x0 & 1) + 2 * (x1 & 1) + (x2 & 1);
+      xv[K] = gather<1>(rin, row_offset<CIN>(r2[o2] + (((sp >> o2) & 1) ? u : 0), c));
+    }
+    BoundaryVoxels<V + 1, NK>::template load<CIN>(xv, r2, sp, rin, c);
+  }
+  __device__ __forceinline__ static void add(float (&cs)[kSets], const float (&xv)[56]) {
+    if constexpr (!skip) {
+#pragma unroll
+      for (int r = 0; r < 27; ++r) {
+        if (r == 13) continue;
+        if (in_set(r / 9 - 1, x0, 4) && in_set((r / 3) % 3 - 1, x1, 4) && in_set(r % 3 - 1, x2, 4))
+          cs[r - (r > 13)] += xv[K];
+      }
+    }
+    BoundaryVoxels<V + 1, NK>::add(cs, xv);
+  }
+};
+template <int K>
+struct BoundaryVoxels<64, K> {
+  template <int CIN>
+  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int,
+                                              __amdgpu_buffer_rsrc_t, int) {}
+  __device__ __forceinline__ static void add(float (&)[kSets], const float (&)[56]) {}
+};
+
+// CIN lanes per split tree (lane = channel).  Each depth-1 child is summed
+// from its 56 boundary voxels, each read from the leaf that holds it (an
+// unsplit child reads its one row 56 times, from cache), all 56 loads in
+// flight before the sums; a tree set is the sum of the same set over the
+// children on that side.
+template <int CIN>
+__global__ void __launch_bounds__(256) k_boundary_sums(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+    const int32_t* __restrict__ stl, const int64_t* __restrict__ meta,
+    const int64_t* __restrict__ sbase, int64_t n_trees, int64_t cap, const float* __restrict__ in,
+    uint32_t in_bytes, float* __restrict__ bsum) {
+  constexpr int TPW = 64 / CIN;
+  const int lane = threadIdx.x & 63, c = lane % CIN, sub = lane / CIN;
+  int64_t n_split = n_trees - meta[0] - meta[1];
+  n_split = n_split < 0 ? 0 : (n_split > n_trees ? n_trees : n_split);
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
+  for (int64_t j = wave * TPW + sub; j < n_split; j += nwaves * TPW) {
+    const int64_t t = stl[j];
+    const Bits b = load_bits(trees, t);
+    const int rbase = (int)prefix[t];
+    const int64_t s0 = sbase[t];
+    float ts[kSets];
+#pragma unroll
+    for (int s = 0; s < kSets; ++s) ts[s] = 0.f;
+#pragma unroll
+    for (int o1 = 0; o1 < 8; ++o1) {
+      const bool split1 = bit(b, 1 + o1);
+      const int r1 = rbase + data_idx(b, 1 + o1);
+      int r2[8];
+      int sp = 0;
+#pragma unroll
+      for (int o2 = 0; o2 < 8; ++o2) {
+        const int n2 = 9 + 8 * o1 + o2;
+        const int s2 = bit(b, n2);
+        sp |= s2 << o2;
+        r2[o2] = split1 ? rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2) : r1;
+      }
+      float xv[56];
+      BoundaryVoxels<0, 0>::load<CIN>(xv, r2, sp, rin, c);
+      __builtin_amdgcn_sched_barrier(0);
+      float cs[kSets];
+#pragma unroll
+      for (int s = 0; s < kSets; ++s) cs[s] = 0.f;
+      BoundaryVoxels<0, 0>::add(cs, xv);
+      if (split1) {
+        const int64_t slot = s0 + 1 + __popc((uint32_t)(b.lo >> 1) & ((1u << o1) - 1u));
+        if (slot < cap) {
+          float* dst = bsum + slot * (kSets * CIN) + c;
+#pragma unroll
+          for (int s = 0; s < kSets; ++s) dst[s * CIN] = cs[s];
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 27; ++r) {
+        if (r == 13) continue;
+        if (in_set(r / 9 - 1, (o1 >> 2) & 1, 2) && in_set((r / 3) % 3 - 1, (o1 >> 1) & 1, 2) &&
+            in_set(r % 3 - 1, o1 & 1, 2))
+          ts[r - (r > 13)] += cs[r - (r > 13)];
+      }
+    }
+    if (s0 < cap) {
+      float* dst = bsum + s0 * (kSets * CIN) + c;
+#pragma unroll
+      for (int s = 0; s < kSets; ++s) dst[s * CIN] = ts[s];
+    }
+  }
+}
+
 // Edge-4 and edge-8 cells.  The shell splits into 26 regions (faces, edges,
-// corners); region r lies inside one neighbouring tree.  If one leaf covers
-// the region (the neighbouring tree, or for SZ = 4 its depth-1 node, is not
-// split) it contributes once with the region's full overlap; otherwise the
-// region is walked in aligned 2x2x2 blocks of that tree, each either inside a
-// leaf of edge >= 2 or a split depth-2 node whose unit voxels are rows
-// first .. first+7.  Every contribution carries, per axis along which the
-// region extends, the interval [c0, c1) it covers relative to o; its weight
-// for delta is prod_a |[c0, c1) ^ [delta_a, delta_a + SZ)|.  Layer JD takes
-// the regions with dir_d in {0, JD - 1}.
+// corners).  Region dir lies in the neighbouring block at offset dir (a
+// tree for SZ = 8, a depth-1 node for SZ = 4) and is that block's boundary
+// set -dir.  Along an axis with dir_a != 0 it lies in the window of delta
+// only for delta_a = dir_a; along the others it spans the cell, and the
+// window cuts off its last voxel plane (delta_a = -1) or its first
+// (delta_a = +1).  If one leaf covers the block, the region adds that leaf's
+// row times the number of its voxels in the window; otherwise the block's
+// boundary sums give it by inclusion-exclusion: set -dir, minus for each cut
+// axis the set that also fixes that axis to the cut side, plus the sets that
+// fix two or three cut axes.  Layer JD takes the regions with dir_d in
+// {0, JD - 1}.
 template <int R, int JD, int SZ, int CH>
-__device__ __forceinline__ void region_add(float (&S)[9][CH], const float (&x)[CH], const int (&c0)[3],
-                                           const int (&c1)[3]) {
+__device__ __forceinline__ void region_add(float (&S)[9][CH], const float (&x)[CH]) {
   constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
-  float ov[3][3];
-#pragma unroll
-  for (int a = 0; a < 3; ++a)
-#pragma unroll
-    for (int j = 0; j < 3; ++j) ov[a][j] = (float)max(0, min(c1[a], j - 1 + SZ) - max(c0[a], j - 1));
 #pragma unroll
   for (int j1 = 0; j1 < 3; ++j1) {
     if (dir1 != 0 && j1 != dir1 + 1) continue;
 #pragma unroll
     for (int j2 = 0; j2 < 3; ++j2) {
       if (dir2 != 0 && j2 != dir2 + 1) continue;
-      float wgt = 1.f;
-      if (dir0 == 0) wgt *= ov[0][JD];
-      if (dir1 == 0) wgt *= ov[1][j1];
-      if (dir2 == 0) wgt *= ov[2][j2];
+      const float wgt = (float)((dir0 == 0 ? SZ - (JD != 1) : 1) * (dir1 == 0 ? SZ - (j1 != 1) : 1) *
+                                (dir2 == 0 ? SZ - (j2 != 1) : 1));
 #pragma unroll
       for (int e = 0; e < CH; ++e) S[j1 * 3 + j2][e] = fmaf(x[e], wgt, S[j1 * 3 + j2][e]);
     }
   }
 }
 
-template <int R, int JD, int SZ, int CIN>
+template <int R, int JD, int CIN>
+__device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float* __restrict__ p) {
+  using K = CellCfg<CIN, 1>;
+  constexpr int CH = CIN / 4;
+  constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
+#pragma unroll
+  for (int ed = -1; ed <= 1; ++ed) {
+    if (dir0 != 0 ? ed != -dir0 : (ed != 0 && ed != 1 - JD)) continue;
+#pragma unroll
+    for (int eh = -1; eh <= 1; ++eh) {
+      if (dir1 != 0 && eh != -dir1) continue;
+#pragma unroll
+      for (int ew = -1; ew <= 1; ++ew) {
+        if (dir2 != 0 && ew != -dir2) continue;
+        float v[CH];
+#pragma unroll
+        for (int jv = 0; jv < K::NV; ++jv) {
+          const typename K::Vec q =
+              *reinterpret_cast<const typename K::Vec*>(p + bset(ed, eh, ew) * CIN + K::VEC * jv);
+#pragma unroll
+          for (int e = 0; e < K::VEC; ++e) v[K::VEC * jv + e] = vget<K::VEC>(q, e);
+        }
+        const bool n0 = dir0 == 0 && ed != 0;
+#pragma unroll
+        for (int j1 = 0; j1 < 3; ++j1) {
+          if (dir1 != 0 ? j1 != dir1 + 1 : (eh != 0 && j1 != 1 - eh)) continue;
+          const bool n1 = n0 != (dir1 == 0 && eh != 0);
+#pragma unroll
+          for (int j2 = 0; j2 < 3; ++j2) {
+            if (dir2 != 0 ? j2 != dir2 + 1 : (ew != 0 && j2 != 1 - ew)) continue;
+            const bool neg = n1 != (dir2 == 0 && ew != 0);
+#pragma unroll
+            for (int e = 0; e < CH; ++e) S[j1 * 3 + j2][e] += neg ? -v[e] : v[e];
+          }
+        }
+      }
+    }
+  }
+}
+
+// TRIV: the cell's face and edge neighbour trees are known to be unsplit.
+template <int R, int JD, int SZ, int CIN, bool TRIV>
 __device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4],
                                            const uint32_t* __restrict__ trees,
-                                           const int64_t* __restrict__ prefix, int gd, int gh, int gw,
-                                           int64_t n_leaves, int64_t n, const int (&o)[3],
-                                           __amdgpu_buffer_rsrc_t rin, uint32_t choff) {
+                                           const int64_t* __restrict__ prefix,
+                                           const int64_t* __restrict__ sbase, int gd, int gh, int gw,
+                                           int64_t cap, int64_t n, const int (&o)[3],
+                                           __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
+                                           int choff) {
   constexpr int CH = CIN / 4;
   constexpr int dir[3] = {R / 9 - 1, (R / 3) % 3 - 1, R % 3 - 1};
+  constexpr int nz = (dir[0] != 0) + (dir[1] != 0) + (dir[2] != 0);
   const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
   int lo[3];
   bool inside = true;
@@ -1119,124 +1297,76 @@ __device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4],
   }
   if (!inside) return;  // zero padding
   const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
-  const Bits b = load_bits(trees, tt);
-  const int64_t rbase = prefix[tt];
-  const int L[3] = {lo[0] & 7, lo[1] & 7, lo[2] & 7};
-  // A leaf covering the whole region?
-  int cover = -1;
-  if (!(b.lo & 1ull)) {
-    cover = 0;
-  } else if (SZ == 4) {
-    const int n1 = 1 + 4 * (L[0] >> 2) + 2 * (L[1] >> 2) + (L[2] >> 2);
-    if (!bit(b, n1)) cover = n1;
+  int row = (int)prefix[tt];
+  int64_t slot = -1;
+  if constexpr (!TRIV || nz == 3) {
+    const uint32_t w0 = trees[4 * tt];  // split bits 0..31
+    if (w0 & 1u) {
+      if constexpr (SZ == 8) {
+        slot = sbase[tt];
+      } else {
+        const int o1 = 4 * ((lo[0] >> 2) & 1) + 2 * ((lo[1] >> 2) & 1) + ((lo[2] >> 2) & 1);
+        const int m = __popc((w0 >> 1) & ((1u << o1) - 1u));  // split depth-1 nodes before it
+        if ((w0 >> (1 + o1)) & 1u) slot = sbase[tt] + 1 + m;
+        else row += o1 - m;  // Eq. 3 for a depth-1 leaf
+      }
+    }
   }
-  // 2x2x2 blocks along the axes the region extends on; one along the others.
-  constexpr int nb0 = dir[0] == 0 ? SZ / 2 : 1, nb1 = dir[1] == 0 ? SZ / 2 : 1,
-                nb2 = dir[2] == 0 ? SZ / 2 : 1;
-  const int nblocks = cover >= 0 ? 1 : nb0 * nb1 * nb2;
-  for (int bi = 0; bi < nblocks; ++bi) {
-    const int bix[3] = {bi / (nb1 * nb2), (bi / nb2) % nb1, bi % nb2};
-    int first;     // row of the block's leaf, or of its first unit voxel
-    int nsub = 1;  // contributions of this block
-    int bo[3];     // block origin in the neighbouring tree
-#pragma unroll
-    for (int a = 0; a < 3; ++a) bo[a] = dir[a] == 0 ? L[a] + 2 * bix[a] : (L[a] & ~1);
-    bool fine = false;
-    if (cover >= 0) {
-      first = (int)(rbase + data_idx(b, cover));
-    } else {
-      const int n1 = 1 + 4 * (bo[0] >> 2) + 2 * (bo[1] >> 2) + (bo[2] >> 2);
-      int node = n1;
-      if (bit(b, n1)) {
-        const int n2 = 8 * n1 + 1 + 4 * ((bo[0] >> 1) & 1) + 2 * ((bo[1] >> 1) & 1) + ((bo[2] >> 1) & 1);
-        node = n2;
-        if (bit(b, n2)) {
-          node = 8 * n2 + 1;
-          fine = true;
-          nsub = (dir[0] == 0 ? 2 : 1) * (dir[1] == 0 ? 2 : 1) * (dir[2] == 0 ? 2 : 1);
-        }
-      }
-      first = (int)(rbase + data_idx(b, node));
-    }
-    for (int sb = 0; sb < nsub; ++sb) {
-      int c0[3], c1[3], o3 = 0;
-      int k = sb;
-#pragma unroll
-      for (int a = 2; a >= 0; --a) {
-        int vbit;  // unit-voxel bit along axis a inside the block
-        if (dir[a] == 0) {
-          vbit = k & 1;
-          k >>= 1;
-        } else {
-          vbit = L[a] & 1;
-        }
-        o3 |= vbit << (2 - a);
-        if (cover >= 0) {
-          c0[a] = 0;
-          c1[a] = SZ;
-        } else if (fine) {
-          c0[a] = 2 * bix[a] + vbit;
-          c1[a] = c0[a] + 1;
-        } else {
-          c0[a] = 2 * bix[a];
-          c1[a] = c0[a] + 2;
-        }
-      }
-      const int64_t rr = (int64_t)first + (fine ? o3 : 0);
-      if (rr >= n_leaves) continue;  // only a non-canonical structure gets here
-      float x[CH];
-      gather_channels<CIN>(rin, row_offset<CIN>((int)rr, 0) + choff, x);
-      region_add<R, JD, SZ, CH>(S, x, c0, c1);
-    }
+  if (slot < 0) {
+    float x[CH];
+    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), x);
+    region_add<R, JD, SZ, CH>(S, x);
+  } else if (slot < cap) {
+    summary_add<R, JD, CIN>(S, bsum + slot * (kSets * CIN) + choff);
   }
 }
 
-template <int R, int JD, int SZ, int CIN>
+template <int R, int JD, int SZ, int CIN, bool TRIV>
 struct RegionLayer {
-  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4],
-                                             const uint32_t* trees, const int64_t* prefix, int gd,
-                                             int gh, int gw, int64_t n_leaves, int64_t n,
+  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], const uint32_t* trees,
+                                             const int64_t* prefix, const int64_t* sbase, int gd,
+                                             int gh, int gw, int64_t cap, int64_t n,
                                              const int (&o)[3], __amdgpu_buffer_rsrc_t rin,
-                                             uint32_t choff) {
+                                             const float* bsum, int choff) {
     constexpr int dir0 = R / 9 - 1;
     if constexpr (R != 13 && (dir0 == 0 || dir0 == JD - 1)) {
-      region_sum<R, JD, SZ, CIN>(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+      region_sum<R, JD, SZ, CIN, TRIV>(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin, bsum,
+                                       choff);
       // A few regions' loads in flight at a time (more would spill).
       if constexpr (R % OC_REGION_GROUP == OC_REGION_GROUP - 1) __builtin_amdgcn_sched_barrier(0);
     }
-    RegionLayer<R + 1, JD, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
+                                               bsum, choff);
   }
 };
-template <int JD, int SZ, int CIN>
-struct RegionLayer<27, JD, SZ, CIN> {
+template <int JD, int SZ, int CIN, bool TRIV>
+struct RegionLayer<27, JD, SZ, CIN, TRIV> {
   __device__ __forceinline__ static void run(float (&)[9][CIN / 4], const uint32_t*,
-                                             const int64_t*, int, int, int, int64_t, int64_t,
-                                             const int (&)[3], __amdgpu_buffer_rsrc_t, uint32_t) {}
+                                             const int64_t*, const int64_t*, int, int, int, int64_t,
+                                             int64_t, const int (&)[3], __amdgpu_buffer_rsrc_t,
+                                             const float*, int) {}
 };
 
-template <int CIN, int NT, int SZ>
+template <int CIN, int NT, int SZ, bool TRIV>
 __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, int kind, const float* __restrict__ in,
+    const int64_t* __restrict__ meta, int kind, const int64_t* __restrict__ sbase,
+    const float* __restrict__ bsum, int64_t cap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
-#ifdef OC_EXP_BGLOBAL
-  const float* wl = wm;
-#else
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
-#endif
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
   const int m = lane % 16, g = lane / 16;
-  const uint32_t choff = 4u * (uint32_t)(CH * g);
+  const int choff = CH * g;  // the lane's first channel
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
@@ -1245,7 +1375,7 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     int o[3];
     cell_origin(info, row, gd, gh, gw, n, o);
     float xs[CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(row, 0) + choff, xs);
+    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), xs);
     typename K::Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -1257,7 +1387,8 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
       float S[9][CH];
       init_layer<SZ, 0>(S, xs);
       if (row >= 0)
-        RegionLayer<0, 0, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+        RegionLayer<0, 0, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
+                                              bsum, choff);
       contract_layer<CIN, NT, 0>(S, wl, lane, acc);
     }
     asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
@@ -1265,7 +1396,8 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
       float S[9][CH];
       init_layer<SZ, 1>(S, xs);
       if (row >= 0)
-        RegionLayer<0, 1, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+        RegionLayer<0, 1, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
+                                              bsum, choff);
       contract_layer<CIN, NT, 1>(S, wl, lane, acc);
     }
     asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
@@ -1273,7 +1405,8 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
       float S[9][CH];
       init_layer<SZ, 2>(S, xs);
       if (row >= 0)
-        RegionLayer<0, 2, SZ, CIN>::run(S, trees, prefix, gd, gh, gw, n_leaves, n, o, rin, choff);
+        RegionLayer<0, 2, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
+                                              bsum, choff);
       contract_layer<CIN, NT, 2>(S, wl, lane, acc);
     }
     store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bias, cout, relu, out);
@@ -1306,9 +1439,11 @@ typedef void (*MfmaFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, 
                        const int64_t*, const float*, const float*, uint32_t, const float*, int,
                        int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
-                       const int32_t*, const int64_t*, int, const float*, const float*, uint32_t,
-                       const float*, int, int, float*);
+                       const int32_t*, const int64_t*, int, const int64_t*, const float*, int64_t,
+                       const float*, const float*, uint32_t, const float*, int, int, float*);
 typedef void (*WeightFn)(const float*, int, float*);
+typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
+                      const int64_t*, int64_t, int64_t, const float*, uint32_t, float*);
 
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
@@ -1316,8 +1451,9 @@ struct MfmaVariant {
   MfmaFn kernel;
   WeightFn weights;
   size_t cell_wfloats;  // cell kernels' weights (16-row tiles)
-  CellFn cell2, cell4, cell8;
+  CellFn cell2, cell4, cell8, cell8t;
   WeightFn cell_weights;
+  SumFn sums;
 };
 
 template <int CIN, int NT, int MS>
@@ -1335,9 +1471,11 @@ MfmaVariant make_variant(int cout_min) {
   constexpr int CNT = (C::NCOL + 15) / 16;
   v.cell_wfloats = MfmaCfg<CIN, CNT, 16>::WFLOATS;
   v.cell2 = &k_conv_cell2_mfma<CIN, CNT>;
-  v.cell4 = &k_conv_cellr_mfma<CIN, CNT, 4>;
-  v.cell8 = &k_conv_cellr_mfma<CIN, CNT, 8>;
+  v.cell4 = &k_conv_cellr_mfma<CIN, CNT, 4, false>;
+  v.cell8 = &k_conv_cellr_mfma<CIN, CNT, 8, false>;
+  v.cell8t = &k_conv_cellr_mfma<CIN, CNT, 8, true>;
   v.cell_weights = &k_mfma_weights<CIN, CNT, 16>;
+  v.sums = &k_boundary_sums<CIN>;
   return v;
 }
 
@@ -1380,21 +1518,33 @@ hipError_t device_limits() {
 //   wt         f32 [27 cin cout]            generic-kernel weights
 //   wm         f32 [variant wfloats]        unit-voxel kernel B operands (if a variant exists)
 //   wc         f32 [variant cell_wfloats]   cell kernels' B operands
-//   5 x (scan workspace (n_trees), i64 [n_trees + 1])
-//              unit groups and each kind of larger cell per tree -> prefixes
+//   6 x (scan workspace (n_trees), i64 [n_trees + 1])
+//              per tree: unit groups, each kind of larger cell, boundary-sum
+//              slots -> prefixes
 //   gkey       i64 [n_leaves / 8 + 1]
 //   brow       i32 [n_leaves]
+//   stl        i32 [n_trees]                split trees
 //   meta       i64 [kKinds + 1]
+//   bsum       f32 [cap][26][cin]           boundary sums (if a variant exists)
+// A slot belongs to a split node of depth 0 or 1 and every split node adds 7
+// leaves, so cap = (n_leaves - n_trees) / 7 slots hold every canonical
+// structure of that size.
+constexpr int kScans = 2 + kKinds;  // groups, the kinds, slots
+constexpr int kSlotScan = 1 + kKinds;
+
 struct ConvWs {
   uint64_t* info;
   float* wt;
   float* wm;
   float* wc;
-  char* scan[1 + kKinds];
-  int64_t* pre[1 + kKinds];  // groups, then the kinds of larger cells
+  char* scan[kScans];
+  int64_t* pre[kScans];
   int64_t* gkey;
   int32_t* brow;
+  int32_t* stl;
   int64_t* meta;
+  float* bsum;
+  int64_t cap;
   size_t total;
 };
 
@@ -1413,13 +1563,16 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
   w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
   w.wc = reinterpret_cast<float*>(take(v ? sizeof(float) * v->cell_wfloats : 0));
-  for (int k = 0; k < 1 + kKinds; ++k) {
+  for (int k = 0; k < kScans; ++k) {
     w.scan[k] = take(oci::scan_workspace(n_trees));
     w.pre[k] = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
   }
   w.gkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_leaves / 8 + 1)));
   w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
+  w.stl = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_trees));
   w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
+  w.cap = v && n_leaves > n_trees ? (n_leaves - n_trees) / 7 : 0;
+  w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)cin * (size_t)w.cap));
   w.total = off + 256;
   return w;
 }
@@ -1460,14 +1613,14 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
                      scan_counts_buffer(w.scan[2]), scan_counts_buffer(w.scan[3]),
-                     scan_counts_buffer(w.scan[4]));
-  for (int k = 0; k < 1 + kKinds; ++k) {
+                     scan_counts_buffer(w.scan[4]), scan_counts_buffer(w.scan[kSlotScan]));
+  for (int k = 0; k < kScans; ++k) {
     e = scan_counts(scan_counts_buffer(w.scan[k]), a.n_trees, w.pre[k], w.scan[k], s);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],
                      w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
-                     a.n_leaves, w.meta);
+                     a.n_leaves, w.stl, w.meta);
   return hipGetLastError();
 }
 
@@ -1506,22 +1659,30 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
                      a.bias, a.cout, a.relu, a.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Larger cells, one launch per kind: trivial edge-8, other edge-8, edge-4,
-  // edge-2 (the lists are grouped by kind; the kernels read the counts).
-  const CellFn cells[kKinds] = {v->cell8, v->cell8, v->cell4, v->cell2};
+  // Boundary sums of the split trees and split depth-1 nodes.
+  {
+    const int64_t per_block = 4 * (64 / a.cin);  // trees per pass of a 256-thread block
+    int64_t blocks = (a.n_trees + per_block - 1) / per_block;
+    if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
+                       (const int32_t*)w.stl, (const int64_t*)w.meta,
+                       (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, a.in, in_bytes, w.bsum);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // Larger cells, one launch per kind: edge-8 with unsplit face and edge
+  // neighbours, other edge-8, edge-4, edge-2 (the lists are grouped by kind;
+  // the kernels read the counts).
+  const CellFn cells[kKinds] = {v->cell8t, v->cell8, v->cell4, v->cell2};
   for (int k = 0; k < kKinds; ++k) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)wsmem);
     if (e != hipSuccess) return e;
-#ifdef OC_EXP_BGLOBAL
-    const bool glob = k != 3;
-    hipLaunchKernelGGL(cells[k], dim3(glob ? OC_EXP_BLOCKS * nblk : nblk), dim3(glob ? OC_EXP_THREADS : kMfmaThreads),
-                       glob ? 0 : wsmem, s, a.trees, a.prefix, a.gd,
-#else
     hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
-#endif
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
-                       (const int64_t*)w.meta, k, a.in, (const float*)w.wc, in_bytes, a.bias,
+                       (const int64_t*)w.meta, k, (const int64_t*)w.pre[kSlotScan],
+                       (const float*)w.bsum, w.cap, a.in, (const float*)w.wc, in_bytes, a.bias,
                        a.cout, a.relu, a.out);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
