@@ -507,8 +507,11 @@ __device__ __forceinline__ int32_t neighbour_row(const uint32_t* __restrict__ tr
 //            B column l%32; D[8(r/4) + 4(l/32) + r%4][l%32] in register r.
 //   MS = 16: v_mfma_f32_16x16x4_f32, lane l: A row l%16, k-slot l/16,
 //            B column l%16; D[4(l/16) + r][l%16] in register r.
-// The K index (delta, ci) is ordered so that lane slot g feeds channels
-// CH*g .. CH*g + CH - 1 of every delta: one contiguous vector load per row.
+// The K index (delta, ci) is ordered so that a lane of k-slot g holds CH
+// channels of its row in NV vectors of VEC: vector v holds channels
+// VEC (KS v + g) .. + VEC - 1 (KS = k-slots).  One load instruction then
+// reads, per row, KS * VEC consecutive channels, whole 64-byte sectors where
+// the row allows, instead of touching every sector of the row each time.
 // Weights live in LDS already in B-operand order; NT N-tiles of MS columns
 // cover cout (padded with zero weights).
 // ---------------------------------------------------------------------------
@@ -518,6 +521,7 @@ struct MfmaCfg {
   static constexpr int CH = CIN / KS;          // channels per lane per delta
   static constexpr int VEC = CH % 4 == 0 ? 4 : (CH % 2 == 0 ? 2 : 1);
   static constexpr int NV = CH / VEC;
+  static constexpr int VSTRIDE = KS * VEC;     // channels between a lane's vectors
   static constexpr int GROUPS = MS / 8;
   static constexpr int NCOL = MS * NT;
   static constexpr int WFLOATS = 27 * CIN * NCOL;
@@ -596,8 +600,13 @@ __device__ __forceinline__ uint32_t row_offset(int row, int ch) {
   return row < 0 ? kOutside : (uint32_t)row * (uint32_t)(CIN * 4) + (uint32_t)(ch * 4);
 }
 
+#ifndef OC_UNIT_THREADS
+#define OC_UNIT_THREADS 512
+#endif
+constexpr int kUnitThreads = OC_UNIT_THREADS;
+
 template <int CIN, int NT, int MS>
-__global__ void __launch_bounds__(512) k_conv_unit_mfma(
+__global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
     const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
@@ -665,12 +674,20 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   };
+  // The lane's bias values, read once (a load in the epilogue would make it
+  // wait for the next tile's gathers as well).
+  float bvals[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int co = MS * nt + col;
+    bvals[nt] = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+  }
   // Epilogue of a finished tile (unit cells need no 1/s^3 scaling).
   auto store_unit_tile = [&](const Acc (&res)[NT], const int32_t* tnb) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
       const int co = MS * nt + col;
-      const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+      const float bv = bvals[nt];
 #pragma unroll
       for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
         const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
@@ -715,11 +732,11 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
     uint32_t aoff[27];
 #pragma unroll
     for (int dl = 0; dl < 27; ++dl)
-      aoff[dl] = row_offset<CIN>(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3], C::CH * g);
+      aoff[dl] = row_offset<CIN>(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3], C::VEC * g);
     auto load_a = [&](int dl, Vec* a) {
       const uint32_t off = aoff[dl];
 #pragma unroll
-      for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VEC * v);
+      for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
     };
     auto load_b = [&](int dl, Vec (*b)[C::NV]) {
 #pragma unroll
@@ -779,9 +796,9 @@ __global__ void __launch_bounds__(512) k_conv_unit_mfma(
 // MFMA kernels for cells of edge 2, 4 and 8.
 //
 // A wave takes 16 cells of one edge length SZ and contracts them with
-// v_mfma_f32_16x16x4_f32: lane (m = lane % 16, g = lane / 16) feeds channels
-// CH*g .. CH*g + CH - 1 (CH = cin/4) of cell m, and the weights sit in LDS in
-// the matching B-operand order.  Before they enter the MFMA, the lane builds
+// v_mfma_f32_16x16x4_f32: lane (m = lane % 16, g = lane / 16) feeds CH =
+// cin/4 channels of cell m (vector jv: channels VEC (4 jv + g) ..), and the
+// weights sit in LDS in the matching B-operand order.  Before they enter the MFMA, the lane builds
 // its cell's window sums (origin o):
 //   S_delta = x_self * prod_a (SZ - |delta_a|) + sum of x over the one-voxel
 //             shell voxels that the window [o+delta, o+delta+SZ) covers,
@@ -812,6 +829,7 @@ struct CellCfg {
   using C = MfmaCfg<CIN, NT, 16>;
   static constexpr int CH = C::CH;
   static constexpr int VEC = C::VEC;
+  static constexpr int VSTRIDE = C::VSTRIDE;
   static constexpr int NV = C::NV;
   using Vec = typename VecT<VEC>::type;
   using Acc = typename AccT<16>::type;
@@ -847,9 +865,20 @@ __device__ __forceinline__ void gather_channels(__amdgpu_buffer_rsrc_t rin, uint
   using K = CellCfg<CIN, 1>;
 #pragma unroll
   for (int jv = 0; jv < K::NV; ++jv) {
-    const typename K::Vec v = gather<K::VEC>(rin, off + 4u * K::VEC * jv);
+    const typename K::Vec v = gather<K::VEC>(rin, off + 4u * K::VSTRIDE * jv);
 #pragma unroll
     for (int e = 0; e < K::VEC; ++e) x[K::VEC * jv + e] = vget<K::VEC>(v, e);
+  }
+}
+
+// The lane's bias values for 16-column tiles (column 16 nt + lane % 16).
+template <int NT>
+__device__ __forceinline__ void bias16(const float* __restrict__ bias, int cout, int lane,
+                                       float (&bv)[NT]) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int co = 16 * nt + lane % 16;
+    bv[nt] = (bias != nullptr && co < cout) ? bias[co] : 0.f;
   }
 }
 
@@ -857,13 +886,13 @@ __device__ __forceinline__ void gather_channels(__amdgpu_buffer_rsrc_t rin, uint
 // lane i.
 template <int NT>
 __device__ __forceinline__ void store_tile16(const typename AccT<16>::type (&acc)[NT], int row,
-                                             float inv, int lane, const float* __restrict__ bias,
+                                             float inv, int lane, const float (&bvals)[NT],
                                              int cout, int relu, float* __restrict__ out) {
   const int g = lane / 16, col = lane % 16;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int co = 16 * nt + col;
-    const float bv = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+    const float bv = bvals[nt];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int rowi = __shfl(row, 4 * g + r, 64);
@@ -1002,7 +1031,9 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
   const int m = lane % 16, g = lane / 16;
-  const uint32_t choff = 4u * (uint32_t)(CH * g);
+  const uint32_t choff = 4u * (uint32_t)(K::VEC * g);  // the lane's first channel
+  float bvals[NT];
+  bias16<NT>(bias, cout, lane, bvals);
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
@@ -1066,7 +1097,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
 #undef OC_LOAD
 #undef OC_ADD
 #undef OC_MMA
-    store_tile16<NT>(acc, row, 0.125f, lane, bias, cout, relu, out);
+    store_tile16<NT>(acc, row, 0.125f, lane, bvals, cout, relu, out);
   }
 }
 
@@ -1252,7 +1283,7 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
 #pragma unroll
         for (int jv = 0; jv < K::NV; ++jv) {
           const typename K::Vec q =
-              *reinterpret_cast<const typename K::Vec*>(p + bset(ed, eh, ew) * CIN + K::VEC * jv);
+              *reinterpret_cast<const typename K::Vec*>(p + bset(ed, eh, ew) * CIN + K::VSTRIDE * jv);
 #pragma unroll
           for (int e = 0; e < K::VEC; ++e) v[K::VEC * jv + e] = vget<K::VEC>(q, e);
         }
@@ -1366,7 +1397,9 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
   const int m = lane % 16, g = lane / 16;
-  const int choff = CH * g;  // the lane's first channel
+  const int choff = K::VEC * g;  // the lane's first channel
+  float bvals[NT];
+  bias16<NT>(bias, cout, lane, bvals);
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
@@ -1409,13 +1442,13 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
                                               bsum, choff);
       contract_layer<CIN, NT, 2>(S, wl, lane, acc);
     }
-    store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bias, cout, relu, out);
+    store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu, out);
   }
 }
 
 // Weights in B-operand order: for delta index dl, N-tile nt, vector jv, lane
-// and element e: column co = MS*nt + lane%MS, channel ci = CH*(lane/MS) +
-// VEC*jv + e, tap 26 - dl (Eq. 7 pairs input offset delta with tap 1 - delta).
+// and element e: column co = MS*nt + lane%MS, channel ci = VEC*(KS*jv +
+// lane/MS) + e, tap 26 - dl (Eq. 7 pairs input offset delta with tap 1 - delta).
 template <int CIN, int NT, int MS>
 __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __restrict__ wm) {
   using C = MfmaCfg<CIN, NT, MS>;
@@ -1428,7 +1461,7 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
   const int nt = r % NT; r /= NT;
   const int dl = r;
   const int co = MS * nt + lane % MS;
-  const int ci = C::CH * (lane / MS) + C::VEC * jv + e;
+  const int ci = C::VEC * (C::KS * jv + lane / MS) + e;
   wm[idx] = co < cout ? w[((int64_t)co * CIN + ci) * 27 + (26 - dl)] : 0.f;
 }
 
@@ -1483,8 +1516,14 @@ MfmaVariant make_variant(int cout_min) {
 // for cout 5..16 (narrower outputs use the generic kernel).
 const MfmaVariant* find_variant(int cin, int cout) {
   static const MfmaVariant table[] = {
+#ifdef OC_UNIT_MS16
+      make_variant<32, 2, 16>(17), make_variant<16, 2, 16>(17), make_variant<8, 2, 16>(17),
+      make_variant<4, 2, 16>(17),
+#else
       make_variant<32, 1, 32>(17), make_variant<16, 1, 32>(17), make_variant<8, 1, 32>(17),
-      make_variant<4, 1, 32>(17),  make_variant<32, 1, 16>(5),  make_variant<16, 1, 16>(5),
+      make_variant<4, 1, 32>(17),
+#endif
+      make_variant<32, 1, 16>(5),  make_variant<16, 1, 16>(5),
       make_variant<8, 1, 16>(5),   make_variant<4, 1, 16>(5),
   };
   for (const MfmaVariant& v : table)
@@ -1495,7 +1534,7 @@ const MfmaVariant* find_variant(int cin, int cout) {
 constexpr int kMfmaThreads = 512;
 
 size_t mfma_smem(const MfmaVariant& v) {
-  return sizeof(float) * v.wfloats + sizeof(int32_t) * (kMfmaThreads / 64) * 2 * (v.ms / 8) * 64;
+  return sizeof(float) * v.wfloats + sizeof(int32_t) * (kUnitThreads / 64) * 2 * (v.ms / 8) * 64;
 }
 
 int g_num_cus = 0;
@@ -1653,7 +1692,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kMfmaThreads), msmem, s, a.trees, a.prefix, a.gd,
+  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.trees, a.prefix, a.gd,
                      a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
                      (const int64_t*)(w.pre[0] + a.n_trees), a.in, (const float*)w.wm, in_bytes,
                      a.bias, a.cout, a.relu, a.out);
