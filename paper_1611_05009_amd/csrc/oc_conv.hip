@@ -496,6 +496,20 @@ __device__ __forceinline__ int32_t neighbour_row(const uint32_t* __restrict__ tr
   return (int32_t)(prefix[tt] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7)));
 }
 
+// Neighbourhood table of the unit-voxel groups (structure only, built once
+// per structure): nbt[64 k + u] = neighbour_row(group k, u), -1 outside the
+// grid, for the G = min(n_groups, n_leaves / 8) groups.
+__global__ void k_unit_table(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                             int gd, int gh, int gw, int64_t n_leaves,
+                             const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
+                             int32_t* __restrict__ nbt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t G = min(*n_groups, n_leaves / 8);
+  if (i >= G * 64) return;
+  const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, gkey[i >> 6], (int)(i & 63));
+  nbt[i] = r < n_leaves ? r : -1;  // only a non-canonical structure exceeds
+}
+
 // ---------------------------------------------------------------------------
 // MFMA kernel for unit voxels.
 //
@@ -607,8 +621,7 @@ constexpr int kUnitThreads = OC_UNIT_THREADS;
 
 template <int CIN, int NT, int MS>
 __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
-    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
-    int64_t n_leaves, const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
+    int64_t n_leaves, const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups,
     const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
     const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
   using C = MfmaCfg<CIN, NT, MS>;
@@ -628,7 +641,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   // Two neighbourhood tables per wave: the current tile's, and the next
-  // tile's, which is resolved in stages between the MFMAs of this one.
+  // tile's, which is staged between the MFMAs of this one.
   int32_t* nb_w = nb_all + wave * (2 * C::GROUPS * 64);
   const int64_t G = min(*n_groups, n_leaves / 8);
   const int64_t n_tiles = (G + C::GROUPS - 1) / C::GROUPS;
@@ -638,39 +651,20 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
   const int gi = m >> 3, o3 = m & 7;
   const int ubase = gi * 64 + ((o3 >> 2) & 1) * 16 + ((o3 >> 1) & 1) * 4 + (o3 & 1);
   const int col = lane % MS;
-  // Staged lookup of the neighbourhood rows of tile t into table nbt.
-  int64_t keys[C::GROUPS];
-  NbProbe probe[C::GROUPS];
-  Bits pbits[C::GROUPS];
-  int64_t pbase[C::GROUPS];
-  auto stage_keys = [&](int64_t t) {
+  // The neighbourhood rows of tile t: loaded from the table (one coalesced
+  // load per group) well before they are needed, then written to the LDS
+  // table of the wave.
+  int32_t tbl[C::GROUPS];
+  auto stage_load = [&](int64_t t) {
 #pragma unroll
     for (int q = 0; q < C::GROUPS; ++q) {
       const int64_t gidx = t * C::GROUPS + q;
-      keys[q] = (t < wt.end && gidx < G) ? gkey[gidx] : -1;
+      tbl[q] = (t < wt.end && gidx < G) ? nbt[gidx * 64 + lane] : -1;
     }
   };
-  auto stage_trees = [&]() {
+  auto stage_rows = [&](int32_t* nbl) {
 #pragma unroll
-    for (int q = 0; q < C::GROUPS; ++q) {
-      probe[q] = neighbour_probe(gd, gh, gw, keys[q], lane);
-      const int64_t tt = probe[q].tt < 0 ? 0 : probe[q].tt;
-      pbits[q] = load_bits(trees, tt);
-      pbase[q] = prefix[tt];
-    }
-  };
-  auto stage_rows = [&](int32_t* nbt) {
-#pragma unroll
-    for (int q = 0; q < C::GROUPS; ++q) {
-      int32_t r = -1;
-      if (probe[q].tt >= 0) {
-        const int l = probe[q].local;
-        const int64_t rr =
-            pbase[q] + data_idx(pbits[q], leaf_at(pbits[q], (l >> 6) & 7, (l >> 3) & 7, l & 7));
-        r = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
-      }
-      nbt[q * 64 + lane] = r;
-    }
+    for (int q = 0; q < C::GROUPS; ++q) nbl[q * 64 + lane] = tbl[q];
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   };
@@ -699,13 +693,39 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
       }
     }
   };
+  // Software pipeline: the gathered A rows of delta dl+PD and the B operands
+  // of delta dl+1 are in flight while the MFMAs of delta dl issue; the
+  // gathers of a tile's first PD deltas are issued during the previous
+  // tile's last ones (PD + 1 divides 27, so the buffer ring lines up).  The
+  // scheduling barriers keep the compiler from sinking the loads back to
+  // their use.
+  constexpr int PD = OC_UNIT_PREFETCH;  // deltas of gathers in flight
+  static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
+  Vec abuf[PD + 1][C::NV];
+  auto gather_row = [&](uint32_t off, Vec* a) {
+#pragma unroll
+    for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
+  };
+  // Byte offsets of the lane's A rows for the first PD deltas of a table.
+  uint32_t noff[PD];
+  auto first_offsets = [&](const int32_t* t) {
+#pragma unroll
+    for (int k = 0; k < PD; ++k)
+      noff[k] = row_offset<CIN>(t[ubase + (k / 9) * 16 + ((k / 3) % 3) * 4 + k % 3], C::VEC * g);
+  };
+  // A finished tile is stored during the next tile's fifth delta: its stores
+  // then queue behind gathers that are already consumed, and the gathers
+  // issued after them are consumed deltas later (the memory counter is
+  // in issue order).
   Acc pacc[NT];
   const int32_t* pnb = nb_w;
   bool have_prev = false;
   int cur = 0;
-  stage_keys(wt.first);
-  stage_trees();
+  stage_load(wt.first);
   stage_rows(nb_w);
+  first_offsets(nb_w);
+#pragma unroll
+  for (int k = 0; k < PD; ++k) gather_row(noff[k], abuf[k]);
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     int32_t* nb = nb_w + cur * (C::GROUPS * 64);
     int32_t* nb_next = nb_w + (cur ^ 1) * (C::GROUPS * 64);
@@ -720,12 +740,6 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
         for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc2[a2][nt][r] = 0.f;
-    // Software pipeline: the gathered A rows of delta dl+2 and the B operands
-    // of delta dl+1 are in flight while the MFMAs of delta dl issue.  The
-    // scheduling barriers keep the compiler from sinking the loads back to
-    // their use.
-    constexpr int PD = OC_UNIT_PREFETCH;  // deltas of gathers in flight
-    Vec abuf[PD + 1][C::NV];
     Vec bbuf[2][NT][C::NV];
     // The 27 A-row offsets of this lane, read from the table up front so that
     // no LDS round trip sits between a delta's MFMAs and its gathers.
@@ -733,11 +747,6 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
 #pragma unroll
     for (int dl = 0; dl < 27; ++dl)
       aoff[dl] = row_offset<CIN>(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3], C::VEC * g);
-    auto load_a = [&](int dl, Vec* a) {
-      const uint32_t off = aoff[dl];
-#pragma unroll
-      for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
-    };
     auto load_b = [&](int dl, Vec (*b)[C::NV]) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -746,20 +755,20 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
         for (int v = 0; v < C::NV; ++v) b[nt][v] = bsrc[v * 64];
       }
     };
-#pragma unroll
-    for (int k = 0; k < PD; ++k) load_a(k, abuf[k]);
     load_b(0, bbuf[0]);
-    __builtin_amdgcn_sched_barrier(0);
-    if (have_prev) store_unit_tile(pacc, pnb);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int dl = 0; dl < 27; ++dl) {
-      if (dl + PD < 27) load_a(dl + PD, abuf[(dl + PD) % (PD + 1)]);
+      if (dl + PD < 27) gather_row(aoff[dl + PD], abuf[(dl + PD) % (PD + 1)]);
+      else gather_row(noff[dl + PD - 27], abuf[(dl + PD) % (PD + 1)]);  // next tile
       if (dl + 1 < 27) load_b(dl + 1, bbuf[(dl + 1) % 2]);
-      // The next tile's lookups: keys, then tree bits and prefixes, then rows.
-      if (dl == 3) stage_keys(next);
-      if (dl == 9) stage_trees();
-      if (dl == 18) stage_rows(nb_next);
+      // The next tile's neighbourhood rows.
+      if (dl == 3) stage_load(next);
+      if (dl == 4 && have_prev) store_unit_tile(pacc, pnb);
+      if (dl == 18) {
+        stage_rows(nb_next);
+        first_offsets(nb_next);
+      }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
@@ -779,9 +788,6 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
 #pragma unroll
       for (int a2 = 1; a2 < NA; ++a2) acc[nt] += acc2[a2][nt];
     }
-    // The stores of this tile are issued after the next tile's first
-    // gathers: stores share the load counter, so storing now would make the
-    // next tile's first waits wait for them too.
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) pacc[nt] = acc[nt];
     pnb = nb;
@@ -1016,7 +1022,7 @@ template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, int kind, const int64_t* __restrict__,
+    const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__,
     const float* __restrict__, int64_t, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
@@ -1236,6 +1242,63 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
   }
 }
 
+// Region codes of the edge-4 and edge-8 cells (structure only, built once per
+// structure).  For list entry j (the first three kinds) and shell region r
+// (the 27 offsets dir without the centre, r = index of dir minus one past
+// the centre), codes[r ccap + j] = the row of the leaf that covers the
+// neighbouring block at offset dir (the tree for an edge-8 cell, the depth-1
+// node for an edge-4 one), -2 - s if that block is split and has
+// boundary-sum slot s, -1 outside the grid.
+__global__ void k_region_codes(const uint32_t* __restrict__ trees,
+                               const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+                               int64_t n_leaves, const uint64_t* __restrict__ info,
+                               const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
+                               const int64_t* __restrict__ sbase, int64_t cap, int64_t ccap,
+                               int32_t* __restrict__ codes) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t n8 = meta[0] + meta[1], nbig = n8 + meta[2];
+  if (nbig > ccap) nbig = ccap;
+  if (nbig > n_leaves) nbig = n_leaves;
+  if (j >= nbig) return;
+  const int sz = j < n8 ? 8 : 4;
+  int row = brow[j];
+  if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
+  int64_t n;
+  int o[3];
+  cell_origin(info, row, gd, gh, gw, n, o);
+  const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
+  for (int r = 0; r < 27; ++r) {
+    if (r == 13) continue;
+    const int dir[3] = {r / 9 - 1, (r / 3) % 3 - 1, r % 3 - 1};
+    int lo[3];
+    bool inside = row >= 0;
+    for (int a = 0; a < 3; ++a) {
+      lo[a] = dir[a] < 0 ? o[a] - 1 : (dir[a] == 0 ? o[a] : o[a] + sz);
+      const int hi = dir[a] < 0 ? o[a] : (dir[a] == 0 ? o[a] + sz : o[a] + sz + 1);
+      inside = inside && lo[a] >= 0 && hi <= lim[a];
+    }
+    int32_t code = -1;
+    if (inside) {
+      const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
+      const uint32_t w0 = trees[4 * tt];  // split bits 0..31
+      int64_t rr = prefix[tt], slot = -1;
+      if (w0 & 1u) {
+        if (sz == 8) {
+          slot = sbase[tt];
+        } else {
+          const int o1 = 4 * ((lo[0] >> 2) & 1) + 2 * ((lo[1] >> 2) & 1) + ((lo[2] >> 2) & 1);
+          const int m = __popc((w0 >> 1) & ((1u << o1) - 1u));  // split depth-1 nodes before it
+          if ((w0 >> (1 + o1)) & 1u) slot = sbase[tt] + 1 + m;
+          else rr += o1 - m;  // Eq. 3 for a depth-1 leaf
+        }
+      }
+      if (slot >= 0) code = slot < cap && slot < 0x7FFFFFF0LL ? (int32_t)(-2 - slot) : -1;
+      else code = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
+    }
+    codes[(int64_t)(r - (r > 13)) * ccap + j] = code;
+  }
+}
+
 // Edge-4 and edge-8 cells.  The shell splits into 26 regions (faces, edges,
 // corners).  Region dir lies in the neighbouring block at offset dir (a
 // tree for SZ = 8, a depth-1 node for SZ = 4) and is that block's boundary
@@ -1305,85 +1368,61 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
   }
 }
 
-// TRIV: the cell's face and edge neighbour trees are known to be unsplit.
+// TRIV: the cell's face and edge neighbour trees are known to be unsplit, so
+// their codes are rows.
 template <int R, int JD, int SZ, int CIN, bool TRIV>
-__device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4],
-                                           const uint32_t* __restrict__ trees,
-                                           const int64_t* __restrict__ prefix,
-                                           const int64_t* __restrict__ sbase, int gd, int gh, int gw,
-                                           int64_t cap, int64_t n, const int (&o)[3],
+__device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4], int32_t code,
                                            __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
                                            int choff) {
   constexpr int CH = CIN / 4;
-  constexpr int dir[3] = {R / 9 - 1, (R / 3) % 3 - 1, R % 3 - 1};
-  constexpr int nz = (dir[0] != 0) + (dir[1] != 0) + (dir[2] != 0);
-  const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
-  int lo[3];
-  bool inside = true;
-#pragma unroll
-  for (int a = 0; a < 3; ++a) {
-    lo[a] = dir[a] < 0 ? o[a] - 1 : (dir[a] == 0 ? o[a] : o[a] + SZ);
-    const int hi = dir[a] < 0 ? o[a] : (dir[a] == 0 ? o[a] + SZ : o[a] + SZ + 1);
-    inside = inside && lo[a] >= 0 && hi <= lim[a];
-  }
-  if (!inside) return;  // zero padding
-  const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
-  int row = (int)prefix[tt];
-  int64_t slot = -1;
-  if constexpr (!TRIV || nz == 3) {
-    const uint32_t w0 = trees[4 * tt];  // split bits 0..31
-    if (w0 & 1u) {
-      if constexpr (SZ == 8) {
-        slot = sbase[tt];
-      } else {
-        const int o1 = 4 * ((lo[0] >> 2) & 1) + 2 * ((lo[1] >> 2) & 1) + ((lo[2] >> 2) & 1);
-        const int m = __popc((w0 >> 1) & ((1u << o1) - 1u));  // split depth-1 nodes before it
-        if ((w0 >> (1 + o1)) & 1u) slot = sbase[tt] + 1 + m;
-        else row += o1 - m;  // Eq. 3 for a depth-1 leaf
-      }
-    }
-  }
-  if (slot < 0) {
+  constexpr int nz = (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1);
+  if (code >= 0) {
     float x[CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), x);
+    gather_channels<CIN>(rin, row_offset<CIN>(code, choff), x);
     region_add<R, JD, SZ, CH>(S, x);
-  } else if (slot < cap) {
-    summary_add<R, JD, CIN>(S, bsum + slot * (kSets * CIN) + choff);
+  } else if (!TRIV || nz == 3) {
+    if (code <= -2) summary_add<R, JD, CIN>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff);
   }
+}
+
+// The regions of layer JD (those with dir_d in {0, JD - 1}), R ascending:
+// their codes are loaded first, then the regions are added a few at a time.
+template <int JD>
+constexpr bool in_layer(int R) {
+  return R != 13 && (R / 9 - 1 == 0 || R / 9 - 1 == JD - 1);
 }
 
 template <int R, int JD, int SZ, int CIN, bool TRIV>
 struct RegionLayer {
-  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], const uint32_t* trees,
-                                             const int64_t* prefix, const int64_t* sbase, int gd,
-                                             int gh, int gw, int64_t cap, int64_t n,
-                                             const int (&o)[3], __amdgpu_buffer_rsrc_t rin,
-                                             const float* bsum, int choff) {
-    constexpr int dir0 = R / 9 - 1;
-    if constexpr (R != 13 && (dir0 == 0 || dir0 == JD - 1)) {
-      region_sum<R, JD, SZ, CIN, TRIV>(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin, bsum,
-                                       choff);
+  __device__ __forceinline__ static void codes(int32_t (&c)[27], const int32_t* __restrict__ col,
+                                               int64_t ccap) {
+    if constexpr (in_layer<JD>(R)) c[R] = col[(int64_t)(R - (R > 13)) * ccap];
+    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::codes(c, col, ccap);
+  }
+  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], const int32_t (&c)[27],
+                                             __amdgpu_buffer_rsrc_t rin, const float* bsum,
+                                             int choff) {
+    if constexpr (in_layer<JD>(R)) {
+      region_sum<R, JD, SZ, CIN, TRIV>(S, c[R], rin, bsum, choff);
       // A few regions' loads in flight at a time (more would spill).
       if constexpr (R % OC_REGION_GROUP == OC_REGION_GROUP - 1) __builtin_amdgcn_sched_barrier(0);
     }
-    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
-                                               bsum, choff);
+    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
   }
 };
 template <int JD, int SZ, int CIN, bool TRIV>
 struct RegionLayer<27, JD, SZ, CIN, TRIV> {
-  __device__ __forceinline__ static void run(float (&)[9][CIN / 4], const uint32_t*,
-                                             const int64_t*, const int64_t*, int, int, int, int64_t,
-                                             int64_t, const int (&)[3], __amdgpu_buffer_rsrc_t,
-                                             const float*, int) {}
+  __device__ __forceinline__ static void codes(int32_t (&)[27], const int32_t*, int64_t) {}
+  __device__ __forceinline__ static void run(float (&)[9][CIN / 4], const int32_t (&)[27],
+                                             __amdgpu_buffer_rsrc_t, const float*, int) {}
 };
 
 template <int CIN, int NT, int SZ, bool TRIV>
 __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, int kind, const int64_t* __restrict__ sbase,
-    const float* __restrict__ bsum, int64_t cap, const float* __restrict__ in,
+    const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
+    const float* __restrict__ bsum, int64_t ccap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
   using K = CellCfg<CIN, NT>;
@@ -1403,10 +1442,8 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
-    if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
-    int64_t n;
-    int o[3];
-    cell_origin(info, row, gd, gh, gw, n, o);
+    if (row >= n_leaves || lbeg + idx >= ccap) row = -1;  // only a non-canonical structure
+    const int32_t* col = codes + (lbeg + idx);  // the cell's column of region codes
     float xs[CH];
     gather_channels<CIN>(rin, row_offset<CIN>(row, choff), xs);
     typename K::Acc acc[NT];
@@ -1414,32 +1451,34 @@ __global__ void __launch_bounds__(512) k_conv_cellr_mfma(
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
-    // Each layer re-derives the region geometry instead of keeping it live
-    // across layers (which would spill).
     {
       float S[9][CH];
+      int32_t c[27];
       init_layer<SZ, 0>(S, xs);
-      if (row >= 0)
-        RegionLayer<0, 0, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
-                                              bsum, choff);
+      if (row >= 0) {
+        RegionLayer<0, 0, SZ, CIN, TRIV>::codes(c, col, ccap);
+        RegionLayer<0, 0, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
+      }
       contract_layer<CIN, NT, 0>(S, wl, lane, acc);
     }
-    asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
     {
       float S[9][CH];
+      int32_t c[27];
       init_layer<SZ, 1>(S, xs);
-      if (row >= 0)
-        RegionLayer<0, 1, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
-                                              bsum, choff);
+      if (row >= 0) {
+        RegionLayer<0, 1, SZ, CIN, TRIV>::codes(c, col, ccap);
+        RegionLayer<0, 1, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
+      }
       contract_layer<CIN, NT, 1>(S, wl, lane, acc);
     }
-    asm volatile("" : "+v"(o[0]), "+v"(o[1]), "+v"(o[2]));
     {
       float S[9][CH];
+      int32_t c[27];
       init_layer<SZ, 2>(S, xs);
-      if (row >= 0)
-        RegionLayer<0, 2, SZ, CIN, TRIV>::run(S, trees, prefix, sbase, gd, gh, gw, cap, n, o, rin,
-                                              bsum, choff);
+      if (row >= 0) {
+        RegionLayer<0, 2, SZ, CIN, TRIV>::codes(c, col, ccap);
+        RegionLayer<0, 2, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
+      }
       contract_layer<CIN, NT, 2>(S, wl, lane, acc);
     }
     store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu, out);
@@ -1468,11 +1507,10 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 // ---------------------------------------------------------------------------
 // Instantiated channel pairs.
 // ---------------------------------------------------------------------------
-typedef void (*MfmaFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const int64_t*,
-                       const int64_t*, const float*, const float*, uint32_t, const float*, int,
-                       int, float*);
+typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, const float*,
+                       uint32_t, const float*, int, int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
-                       const int32_t*, const int64_t*, int, const int64_t*, const float*, int64_t,
+                       const int32_t*, const int64_t*, int, const int32_t*, const float*, int64_t,
                        const float*, const float*, uint32_t, const float*, int, int, float*);
 typedef void (*WeightFn)(const float*, int, float*);
 typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
@@ -1565,9 +1603,12 @@ hipError_t device_limits() {
 //   stl        i32 [n_trees]                split trees
 //   meta       i64 [kKinds + 1]
 //   bsum       f32 [cap][26][cin]           boundary sums (if a variant exists)
+//   nbt        i32 [(n_leaves / 8 + 1) 64]  unit-group neighbourhood rows (if a variant exists)
+//   codes      i32 [26][ccap]               region codes of edge-4/8 cells (if a variant exists)
 // A slot belongs to a split node of depth 0 or 1 and every split node adds 7
 // leaves, so cap = (n_leaves - n_trees) / 7 slots hold every canonical
-// structure of that size.
+// structure of that size; a tree holds at most 8 cells of edge 4 or 8, so
+// ccap = min(8 n_trees, n_leaves).
 constexpr int kScans = 2 + kKinds;  // groups, the kinds, slots
 constexpr int kSlotScan = 1 + kKinds;
 
@@ -1584,6 +1625,9 @@ struct ConvWs {
   int64_t* meta;
   float* bsum;
   int64_t cap;
+  int32_t* nbt;
+  int32_t* codes;
+  int64_t ccap;
   size_t total;
 };
 
@@ -1612,6 +1656,9 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
   w.cap = v && n_leaves > n_trees ? (n_leaves - n_trees) / 7 : 0;
   w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)cin * (size_t)w.cap));
+  w.nbt = reinterpret_cast<int32_t*>(take(v ? sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1) : 0));
+  w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
+  w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
   w.total = off + 256;
   return w;
 }
@@ -1660,6 +1707,17 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],
                      w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
                      a.n_leaves, w.stl, w.meta);
+  // Neighbourhood tables of the MFMA kernels.
+  const int64_t nt_threads = 64 * (a.n_leaves / 8);
+  if (nt_threads > 0)
+    hipLaunchKernelGGL(k_unit_table, dim3((unsigned)((nt_threads + 255) / 256)), dim3(256), 0, s,
+                       a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
+                       (const int64_t*)(w.pre[0] + a.n_trees), w.nbt);
+  if (w.ccap > 0)
+    hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256)), dim3(256), 0, s,
+                       a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
+                       (const int32_t*)w.brow, (const int64_t*)w.meta,
+                       (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes);
   return hipGetLastError();
 }
 
@@ -1692,10 +1750,9 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.trees, a.prefix, a.gd,
-                     a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
-                     (const int64_t*)(w.pre[0] + a.n_trees), a.in, (const float*)w.wm, in_bytes,
-                     a.bias, a.cout, a.relu, a.out);
+  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.n_leaves,
+                     (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), a.in,
+                     (const float*)w.wm, in_bytes, a.bias, a.cout, a.relu, a.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // Boundary sums of the split trees and split depth-1 nodes.
@@ -1720,8 +1777,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
-                       (const int64_t*)w.meta, k, (const int64_t*)w.pre[kSlotScan],
-                       (const float*)w.bsum, w.cap, a.in, (const float*)w.wc, in_bytes, a.bias,
+                       (const int64_t*)w.meta, k, (const int32_t*)w.codes,
+                       (const float*)w.bsum, w.ccap, a.in, (const float*)w.wc, in_bytes, a.bias,
                        a.cout, a.relu, a.out);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
