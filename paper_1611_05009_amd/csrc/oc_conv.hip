@@ -961,7 +961,7 @@ constexpr bool shell2_inner(int u) {
 
 template <int JD, int UH, int K, int CIN>
 struct Shell2RowLoad {
-  __device__ __forceinline__ static void run(float (&X)[8][CIN / 4], const uint32_t (&offs)[56],
+  __device__ __forceinline__ static void run(float (&X)[8][CIN / 4], const uint32_t* offs,
                                              __amdgpu_buffer_rsrc_t rin, uint32_t choff) {
     constexpr int u = (JD + K / 4) * 16 + UH * 4 + (K % 4);
     if constexpr (!shell2_inner(u)) {
@@ -973,9 +973,12 @@ struct Shell2RowLoad {
 };
 template <int JD, int UH, int CIN>
 struct Shell2RowLoad<JD, UH, 8, CIN> {
-  __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t (&)[56],
+  __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t*,
                                              __amdgpu_buffer_rsrc_t, uint32_t) {}
 };
+
+// LDS bytes per wave for the shell offsets of a 16-cell tile.
+constexpr int kShell2Lds = 16 * 56 * 4;
 
 template <int JD, int UH, int CIN>
 __device__ __forceinline__ void shell2_row_add(float (&S)[9][CIN / 4], const float (&X)[8][CIN / 4]) {
@@ -1018,6 +1021,42 @@ __device__ __forceinline__ void contract_row(const float (&S)[9][CIN / 4], const
   }
 }
 
+// As contract_row, for window sums held in the gather layout: the A operand
+// of MFMA lane L is fetched from lane perm / 4 (see k_conv_cell2_mfma).
+template <int CIN, int NT, int JD, int JH>
+__device__ __forceinline__ void contract_row_perm(const float (&S)[9][CIN / 4], const float* wl,
+                                                  int lane, int perm,
+                                                  typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+  float P[3][CIN / 4];
+#pragma unroll
+  for (int jw = 0; jw < 3; ++jw)
+#pragma unroll
+    for (int e = 0; e < CIN / 4; ++e)
+      P[jw][e] = __builtin_bit_cast(
+          float, __builtin_amdgcn_ds_bpermute(perm, __builtin_bit_cast(int, S[JH * 3 + jw][e])));
+  using K = CellCfg<CIN, NT>;
+#pragma unroll
+  for (int jw = 0; jw < 3; ++jw) {
+    const int dl = 9 * JD + JH * 3 + jw;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int jv = 0; jv < K::NV; ++jv) {
+        const typename K::Vec bv =
+            reinterpret_cast<const typename K::Vec*>(wl)[((dl * NT + nt) * K::NV + jv) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < K::VEC; ++e)
+          acc[nt] = mfma<16>(P[jw][K::VEC * jv + e], vget<K::VEC>(bv, e), acc[nt]);
+      }
+  }
+}
+
+// Edge-2 cells.  The window sums are built in a gather layout and moved to
+// the MFMA layout before each contraction: in the MFMA layout lane
+// m + 16 g holds channel chunk g of cell m, so the 16 lanes that the memory
+// pipeline serves together would read 16 different rows; in the gather
+// layout lane l holds chunk l % 4 of cell 4 (l / 16) + (l / 4) % 4, so
+// those 16 lanes read 4 rows, 64 contiguous bytes each.
 template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
@@ -1036,25 +1075,30 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
-  const int m = lane % 16, g = lane / 16;
-  const uint32_t choff = 4u * (uint32_t)(K::VEC * g);  // the lane's first channel
+  // Gather layout: cell cl, chunk q.  MFMA lane (m, g) takes its operands
+  // from lane 16 (m / 4) + 4 (m % 4) + g.
+  const int cl = 4 * (lane >> 4) + ((lane >> 2) & 3), q = lane & 3;
+  const int perm = 4 * (16 * ((lane & 15) >> 2) + 4 * (lane & 3) + (lane >> 4));
+  const uint32_t choff = 4u * (uint32_t)(K::VEC * q);  // the lane's first channel
   float bvals[NT];
   bias16<NT>(bias, cout, lane, bvals);
+  // The wave's shell offsets: 56 per cell, after the weights.
+  uint32_t* offm = reinterpret_cast<uint32_t*>(smem + MfmaCfg<CIN, NT, 16>::WFLOATS) +
+                   (threadIdx.x >> 6) * (kShell2Lds / 4) + cl * 56;
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
-    const int64_t idx = tile * 16 + m;
+    const int64_t idx = tile * 16 + cl;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
     if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
     int64_t n;
     int o[3];
     cell_origin(info, row, gd, gh, gw, n, o);
-    // Shell rows as byte offsets: lane slot g resolves voxels q = 4 j + g,
-    // then the 4 lanes of the cell exchange them.
-    uint32_t offs[56];
+    // Shell rows as byte offsets, in the wave's LDS area: lane chunk q
+    // resolves shell voxels 4 j + q of its cell.
     {
       int mine[14];
 #pragma unroll
       for (int j = 0; j < 14; ++j) {
-        const int u = c_shell2[4 * j + g];
+        const int u = c_shell2[4 * j + q];
         const int vd = o[0] - 1 + (u >> 4), vh = o[1] - 1 + ((u >> 2) & 3), vw = o[2] - 1 + (u & 3);
         int r = -1;
         if (row >= 0 && vd >= 0 && vh >= 0 && vw >= 0 && vd < 8 * gd && vh < 8 * gh && vw < 8 * gw) {
@@ -1066,9 +1110,9 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
         mine[j] = r;
       }
 #pragma unroll
-      for (int j = 0; j < 14; ++j)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) offs[4 * j + k] = row_offset<CIN>(__shfl(mine[j], m + 16 * k, 64), 0);
+      for (int j = 0; j < 14; ++j) offm[4 * j + q] = row_offset<CIN>(mine[j], 0);
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
     float xs[CH];
     gather_channels<CIN>(rin, row_offset<CIN>(row, 0) + choff, xs);
@@ -1077,33 +1121,43 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
+    // The 12 row steps (layer JD, h-row UH) run two deep: the gathers of
+    // step k + 2 are issued once step k's rows are added.
     float S[9][CH];
-    float X[8][CH];
-#define OC_LOAD(JD, UH) \
-  Shell2RowLoad<JD, UH, 0, CIN>::run(X, offs, rin, choff); \
+    float X[2][8][CH];
+#define OC_LOAD(JD, UH, B) \
+  Shell2RowLoad<JD, UH, 0, CIN>::run(X[B], offm, rin, choff); \
   __builtin_amdgcn_sched_barrier(0)
-#define OC_ADD(JD, UH) \
+#define OC_ADD(JD, UH, B) \
   __builtin_amdgcn_sched_barrier(0); \
-  shell2_row_add<JD, UH, CIN>(S, X)
-#define OC_MMA(JD, JH) contract_row<CIN, NT, JD, JH>(S, wl, lane, acc)
+  shell2_row_add<JD, UH, CIN>(S, X[B])
+#define OC_MMA(JD, JH) contract_row_perm<CIN, NT, JD, JH>(S, wl, lane, perm, acc)
+#define OC_INIT(JD) \
+  __builtin_amdgcn_sched_barrier(0); \
+  init_layer<2, JD>(S, xs)
     init_layer<2, 0>(S, xs);
-    OC_LOAD(0, 0); OC_ADD(0, 0);
-    OC_LOAD(0, 1); OC_ADD(0, 1);
-    OC_LOAD(0, 2); OC_MMA(0, 0); OC_ADD(0, 2);
-    OC_LOAD(0, 3); OC_MMA(0, 1); OC_ADD(0, 3);
-    OC_LOAD(1, 0); OC_MMA(0, 2); __builtin_amdgcn_sched_barrier(0); init_layer<2, 1>(S, xs); OC_ADD(1, 0);
-    OC_LOAD(1, 1); OC_ADD(1, 1);
-    OC_LOAD(1, 2); OC_MMA(1, 0); OC_ADD(1, 2);
-    OC_LOAD(1, 3); OC_MMA(1, 1); OC_ADD(1, 3);
-    OC_LOAD(2, 0); OC_MMA(1, 2); __builtin_amdgcn_sched_barrier(0); init_layer<2, 2>(S, xs); OC_ADD(2, 0);
-    OC_LOAD(2, 1); OC_ADD(2, 1);
-    OC_LOAD(2, 2); OC_MMA(2, 0); OC_ADD(2, 2);
-    OC_LOAD(2, 3); OC_MMA(2, 1); OC_ADD(2, 3);
+    OC_LOAD(0, 0, 0); OC_LOAD(0, 1, 1);
+    OC_ADD(0, 0, 0); OC_LOAD(0, 2, 0);
+    OC_ADD(0, 1, 1); OC_LOAD(0, 3, 1);
+    OC_MMA(0, 0); OC_ADD(0, 2, 0); OC_LOAD(1, 0, 0);
+    OC_MMA(0, 1); OC_ADD(0, 3, 1); OC_LOAD(1, 1, 1);
+    OC_MMA(0, 2); OC_INIT(1); OC_ADD(1, 0, 0); OC_LOAD(1, 2, 0);
+    OC_ADD(1, 1, 1); OC_LOAD(1, 3, 1);
+    OC_MMA(1, 0); OC_ADD(1, 2, 0); OC_LOAD(2, 0, 0);
+    OC_MMA(1, 1); OC_ADD(1, 3, 1); OC_LOAD(2, 1, 1);
+    OC_MMA(1, 2); OC_INIT(2); OC_ADD(2, 0, 0); OC_LOAD(2, 2, 0);
+    OC_ADD(2, 1, 1); OC_LOAD(2, 3, 1);
+    OC_MMA(2, 0); OC_ADD(2, 2, 0);
+    OC_MMA(2, 1); OC_ADD(2, 3, 1);
     OC_MMA(2, 2);
 #undef OC_LOAD
 #undef OC_ADD
 #undef OC_MMA
-    store_tile16<NT>(acc, row, 0.125f, lane, bvals, cout, relu, out);
+#undef OC_INIT
+    __builtin_amdgcn_wave_barrier();  // offm is rewritten by the next tile
+    // The row of cell m, for the store's MFMA layout.
+    const int row_m = __builtin_amdgcn_ds_bpermute(perm, row);
+    store_tile16<NT>(acc, row_m, 0.125f, lane, bvals, cout, relu, out);
   }
 }
 
@@ -1772,10 +1826,13 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   // the kernels read the counts).
   const CellFn cells[kKinds] = {v->cell8t, v->cell8, v->cell4, v->cell2};
   for (int k = 0; k < kKinds; ++k) {
+    // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
+    const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
+    if (smem > g_max_smem) return hipErrorInvalidConfiguration;
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)wsmem);
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), wsmem, s, a.trees, a.prefix, a.gd,
+    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), smem, s, a.trees, a.prefix, a.gd,
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
                        (const int64_t*)w.meta, k, (const int32_t*)w.codes,
                        (const float*)w.bsum, w.ccap, a.in, (const float*)w.wc, in_bytes, a.bias,
