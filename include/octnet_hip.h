@@ -117,7 +117,10 @@ int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int g
               const float* dense, int c, int pool, float* data, void* stream);
 
 /* Bytes of workspace for oc_conv3x3x3 on a structure with n_trees trees and
- * n_leaves leaves.  *bytes [host]. */
+ * n_leaves leaves.  *bytes [host].  The size is a bound that holds for every
+ * canonical structure of that size; on the MFMA path it is dominated by the
+ * per-call boundary sums of split nodes, 26*cin*4*(n_leaves - n_trees)/7
+ * bytes. */
 int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes);
 
 /*

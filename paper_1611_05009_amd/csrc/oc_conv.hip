@@ -1382,8 +1382,10 @@ __device__ __forceinline__ void region_add(float (&S)[9][CH], const float (&x)[C
   }
 }
 
+// use = false: the loads still happen (at a valid address) but add nothing.
 template <int R, int JD, int CIN>
-__device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float* __restrict__ p) {
+__device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float* __restrict__ p,
+                                            bool use) {
   using K = CellCfg<CIN, 1>;
   constexpr int CH = CIN / 4;
   constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
@@ -1402,7 +1404,7 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
           const typename K::Vec q =
               *reinterpret_cast<const typename K::Vec*>(p + bset(ed, eh, ew) * CIN + K::VSTRIDE * jv);
 #pragma unroll
-          for (int e = 0; e < K::VEC; ++e) v[K::VEC * jv + e] = vget<K::VEC>(q, e);
+          for (int e = 0; e < K::VEC; ++e) v[K::VEC * jv + e] = use ? vget<K::VEC>(q, e) : 0.f;
         }
         const bool n0 = dir0 == 0 && ed != 0;
 #pragma unroll
@@ -1423,19 +1425,33 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
 }
 
 // TRIV: the cell's face and edge neighbour trees are known to be unsplit, so
-// their codes are rows.
+// their codes are rows; then the row gather is issued whatever the code (a
+// code that is not a row reads zeros), so that it need not wait behind a
+// branch, and a corner's boundary sum is read only if some lane of the wave
+// needs it.
 template <int R, int JD, int SZ, int CIN, bool TRIV>
 __device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4], int32_t code,
                                            __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
                                            int choff) {
   constexpr int CH = CIN / 4;
   constexpr int nz = (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1);
-  if (code >= 0) {
+  if constexpr (TRIV) {
+    float x[CH];
+    gather_channels<CIN>(rin, code >= 0 ? row_offset<CIN>(code, choff) : kOutside, x);
+    region_add<R, JD, SZ, CH>(S, x);
+    if constexpr (nz == 3) {
+      const bool use = code <= -2;
+      if (__builtin_amdgcn_ballot_w64(use) != 0) {
+        const int64_t slot = use ? (int64_t)(-2 - code) : 0;  // slot 0 always exists
+        summary_add<R, JD, CIN>(S, bsum + slot * (kSets * CIN) + choff, use);
+      }
+    }
+  } else if (code >= 0) {
     float x[CH];
     gather_channels<CIN>(rin, row_offset<CIN>(code, choff), x);
     region_add<R, JD, SZ, CH>(S, x);
-  } else if (!TRIV || nz == 3) {
-    if (code <= -2) summary_add<R, JD, CIN>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff);
+  } else if (code <= -2) {
+    summary_add<R, JD, CIN>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff, true);
   }
 }
 
@@ -1471,8 +1487,13 @@ struct RegionLayer<27, JD, SZ, CIN, TRIV> {
                                              __amdgpu_buffer_rsrc_t, const float*, int) {}
 };
 
+#ifndef OC_CELLR_THREADS
+#define OC_CELLR_THREADS 512
+#endif
+constexpr int kCellrThreads = OC_CELLR_THREADS;
+
 template <int CIN, int NT, int SZ, bool TRIV>
-__global__ void __launch_bounds__(512) k_conv_cellr_mfma(
+__global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
@@ -1708,7 +1729,9 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
   w.stl = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_trees));
   w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
-  w.cap = v && n_leaves > n_trees ? (n_leaves - n_trees) / 7 : 0;
+  // At least one slot where a variant exists: the cell kernels may read slot
+  // 0 (and discard it) when no cell of a wave needs boundary sums.
+  w.cap = v ? (n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1) : 0;
   w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)cin * (size_t)w.cap));
   w.nbt = reinterpret_cast<int32_t*>(take(v ? sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1) : 0));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
@@ -1832,7 +1855,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(kMfmaThreads), smem, s, a.trees, a.prefix, a.gd,
+    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s,
+                       a.trees, a.prefix, a.gd,
                        a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
                        (const int64_t*)w.meta, k, (const int32_t*)w.codes,
                        (const float*)w.bsum, w.ccap, a.in, (const float*)w.wc, in_bytes, a.bias,

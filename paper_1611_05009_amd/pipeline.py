@@ -74,9 +74,12 @@ class Workload:
         return int(np.prod(self.occ_np.shape))
 
 
-def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: str = "auto"):
+def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: str = "auto",
+             prep_timer=None):
     """One pass of the hot path.  Returns (structure, features) at the end.
-    conv_timer(start_event, end_event) brackets each convolution proper."""
+    conv_timer() returns a (start, end) event pair that brackets each
+    convolution proper (execute); prep_timer() one that brackets each
+    convolution's prepare (structure- and weight-dependent tables)."""
     g = oc.build(W.occ)
     x = oc.ten2oc(g, W.dense, "avg") if W.dense is not None else W.features
     if records is not None:
@@ -85,7 +88,12 @@ def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: st
     for op, p in W.layers:
         g_in, x_in = g, x
         if op == "conv":
+            if prep_timer is not None:
+                ps, pe = prep_timer()
+                ps.record()
             ws = oc.conv3x3x3_prepare(g, p["w"])
+            if prep_timer is not None:
+                pe.record()
             if conv_timer is not None:
                 s, e = conv_timer()
                 s.record()
