@@ -1302,7 +1302,8 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
 // the centre), codes[r ccap + j] = the row of the leaf that covers the
 // neighbouring block at offset dir (the tree for an edge-8 cell, the depth-1
 // node for an edge-4 one), -2 - s if that block is split and has
-// boundary-sum slot s, -1 outside the grid.
+// boundary-sum slot s, -1 outside the grid.  A corner region is one voxel,
+// so its code is always the row of the leaf that holds that voxel.
 __global__ void k_region_codes(const uint32_t* __restrict__ trees,
                                const int64_t* __restrict__ prefix, int gd, int gh, int gw,
                                int64_t n_leaves, const uint64_t* __restrict__ info,
@@ -1336,7 +1337,11 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
       const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
       const uint32_t w0 = trees[4 * tt];  // split bits 0..31
       int64_t rr = prefix[tt], slot = -1;
-      if (w0 & 1u) {
+      const bool corner = dir[0] != 0 && dir[1] != 0 && dir[2] != 0;
+      if (corner) {
+        const Bits b = load_bits(trees, tt);
+        rr += data_idx(b, leaf_at(b, lo[0] & 7, lo[1] & 7, lo[2] & 7));
+      } else if (w0 & 1u) {
         if (sz == 8) {
           slot = sbase[tt];
         } else {
@@ -1425,27 +1430,19 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
 }
 
 // TRIV: the cell's face and edge neighbour trees are known to be unsplit, so
-// their codes are rows; then the row gather is issued whatever the code (a
-// code that is not a row reads zeros), so that it need not wait behind a
-// branch, and a corner's boundary sum is read only if some lane of the wave
-// needs it.
+// all its codes are rows, as corner codes always are; then the row gather is
+// issued whatever the code (a code that is not a row reads zeros), so that
+// it need not wait behind a branch.
 template <int R, int JD, int SZ, int CIN, bool TRIV>
 __device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4], int32_t code,
                                            __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
                                            int choff) {
   constexpr int CH = CIN / 4;
   constexpr int nz = (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1);
-  if constexpr (TRIV) {
+  if constexpr (TRIV || nz == 3) {  // codes are rows (or outside)
     float x[CH];
     gather_channels<CIN>(rin, code >= 0 ? row_offset<CIN>(code, choff) : kOutside, x);
     region_add<R, JD, SZ, CH>(S, x);
-    if constexpr (nz == 3) {
-      const bool use = code <= -2;
-      if (__builtin_amdgcn_ballot_w64(use) != 0) {
-        const int64_t slot = use ? (int64_t)(-2 - code) : 0;  // slot 0 always exists
-        summary_add<R, JD, CIN>(S, bsum + slot * (kSets * CIN) + choff, use);
-      }
-    }
   } else if (code >= 0) {
     float x[CH];
     gather_channels<CIN>(rin, row_offset<CIN>(code, choff), x);
@@ -1560,6 +1557,174 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
   }
 }
 
+// Edge-8 cells whose face and edge neighbour trees are unsplit.  Every shell
+// region is then one leaf's row (corners always are), so
+// S_delta = sum_r w(delta, r) x_r over the cell's own row (r = 13) and its 26
+// region rows, w(delta, r) being the number of region r's voxels in the
+// window of delta, and Eq. 8 becomes out = b + sum_r W8_r x_r with effective
+// weights W8_r = (1/512) sum_delta w(delta, r) W[1 - delta], formed once per
+// weight set.  That is the unit voxels' gather-GEMM (K = 27 cin): MS cells
+// per tile, term r's rows gathered into the A operand two terms ahead, the
+// next tile's term rows loaded during this one.
+template <int CIN, int NT, int MS>
+__global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
+    int64_t n_leaves, const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
+    const int32_t* __restrict__ codes, int64_t ccap, const float* __restrict__ in,
+    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
+    int relu, float* __restrict__ out) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  using Vec = typename VecT<C::VEC>::type;
+  using Acc = typename AccT<MS>::type;
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  extern __shared__ float smem[];
+  float* wl = smem;
+  weights_to_lds<CIN, NT, MS>(wm, wl);
+  const int lane = threadIdx.x & 63;
+  const int m = lane % MS, g = lane / MS, col = lane % MS;
+  int64_t cnt = meta[0];  // the kind comes first in the lists
+  if (cnt > ccap) cnt = ccap;
+  if (cnt > n_leaves) cnt = n_leaves;
+  const WaveTiles wt = wave_tiles((cnt + MS - 1) / MS);
+  float bvals[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int co = MS * nt + col;
+    bvals[nt] = (bias != nullptr && co < cout) ? bias[co] : 0.f;
+  }
+  // Term rows of the lane's cell in tile t (-1: none).
+  int32_t trow[27];
+  auto stage_load = [&](int64_t t) {
+    const int64_t idx = t * MS + m;
+    const bool ok = t < wt.end && idx < cnt;
+#pragma unroll
+    for (int r = 0; r < 27; ++r) {
+      int32_t v = -1;
+      if (ok) v = r == 13 ? brow[idx] : codes[(int64_t)(r - (r > 13)) * ccap + idx];
+      trow[r] = v < n_leaves ? v : -1;  // only a non-canonical structure exceeds
+    }
+  };
+  auto store_tile = [&](const Acc (&res)[NT], int srow) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int co = MS * nt + col;
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) {
+        const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
+        const int rowi = __shfl(srow, i, 64);
+        if (rowi < 0 || co >= cout) continue;
+        float v = res[nt][r] + bvals[nt];
+        if (relu) v = fmaxf(v, 0.f);
+        out[(int64_t)rowi * cout + co] = v;
+      }
+    }
+  };
+  constexpr int PD = OC_UNIT_PREFETCH;
+  static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
+  Vec abuf[PD + 1][C::NV];
+  auto gather_row = [&](uint32_t off, Vec* a) {
+#pragma unroll
+    for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
+  };
+  uint32_t aoff[27];
+  auto offsets = [&]() {
+#pragma unroll
+    for (int r = 0; r < 27; ++r) aoff[r] = row_offset<CIN>(trow[r], C::VEC * g);
+  };
+  Acc pacc[NT];
+  int psrow = -1;
+  bool have_prev = false;
+  stage_load(wt.first);
+  offsets();
+#pragma unroll
+  for (int k = 0; k < PD; ++k) gather_row(aoff[k], abuf[k]);
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+    const int srow = trow[13];
+    Vec bbuf[2][NT][C::NV];
+    auto load_b = [&](int dl, Vec (*b)[C::NV]) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const Vec* bsrc = reinterpret_cast<const Vec*>(wl) + ((dl * NT + nt) * C::NV) * 64 + lane;
+#pragma unroll
+        for (int v = 0; v < C::NV; ++v) b[nt][v] = bsrc[v * 64];
+      }
+    };
+    Acc acc[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc[nt][r] = 0.f;
+    load_b(0, bbuf[0]);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int dl = 0; dl < 27; ++dl) {
+      if (dl + PD < 27) gather_row(aoff[dl + PD], abuf[(dl + PD) % (PD + 1)]);
+      else gather_row(aoff[dl + PD - 27], abuf[(dl + PD) % (PD + 1)]);  // next tile
+      if (dl + 1 < 27) load_b(dl + 1, bbuf[(dl + 1) % 2]);
+      if (dl == 3) stage_load(tile + wt.stride);
+      if (dl == 4 && have_prev) store_tile(pacc, psrow);
+      if (dl == 22) {
+        // The next tile's offsets (this tile's are no longer needed past
+        // the gathers already issued).
+#pragma unroll
+        for (int k = 0; k < PD; ++k) aoff[k] = row_offset<CIN>(trow[k], C::VEC * g);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int v = 0; v < C::NV; ++v)
+#pragma unroll
+          for (int e = 0; e < C::VEC; ++e)
+            acc[nt] = mfma<MS>(vget<C::VEC>(abuf[dl % (PD + 1)][v], e),
+                               vget<C::VEC>(bbuf[dl % 2][nt][v], e), acc[nt]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) pacc[nt] = acc[nt];
+    psrow = srow;
+    have_prev = true;
+    offsets();  // the next tile's
+  }
+  if (have_prev) store_tile(pacc, psrow);
+}
+
+// Effective weights of the edge-8 gather-GEMM, in the unit kernel's B-operand
+// order: term r (region dir = (r/9 - 1, (r/3)%3 - 1, r%3 - 1), r = 13 the cell
+// itself) takes (1/sz^3) sum_delta w(delta, r) W[tap 1 - delta], where
+// w(delta, r) = 0 unless delta_a = dir_a wherever dir_a != 0, and is the
+// product of sz - |delta_a| over the other axes.
+template <int CIN, int NT, int MS>
+__global__ void k_eff_weights(const float* __restrict__ w, int cout, int sz,
+                              float* __restrict__ wm) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= C::WFLOATS) return;
+  int q = idx;
+  const int e = q % C::VEC; q /= C::VEC;
+  const int lane = q % 64; q /= 64;
+  const int jv = q % C::NV; q /= C::NV;
+  const int nt = q % NT; q /= NT;
+  const int r = q;
+  const int co = MS * nt + lane % MS;
+  const int ci = C::VEC * (C::KS * jv + lane / MS) + e;
+  if (co >= cout) {
+    wm[idx] = 0.f;
+    return;
+  }
+  const int dir[3] = {r / 9 - 1, (r / 3) % 3 - 1, r % 3 - 1};
+  double acc = 0.0;
+  for (int dl = 0; dl < 27; ++dl) {
+    const int dlt[3] = {dl / 9 - 1, (dl / 3) % 3 - 1, dl % 3 - 1};
+    int wgt = 1;
+    for (int a = 0; a < 3; ++a) {
+      if (dir[a] != 0) wgt *= dlt[a] == dir[a] ? 1 : 0;
+      else wgt *= sz - (dlt[a] != 0 ? 1 : 0);
+    }
+    if (wgt != 0) acc += (double)wgt * (double)w[((int64_t)co * CIN + ci) * 27 + (26 - dl)];
+  }
+  wm[idx] = (float)(acc / ((double)sz * sz * sz));
+}
+
 // Weights in B-operand order: for delta index dl, N-tile nt, vector jv, lane
 // and element e: column co = MS*nt + lane%MS, channel ci = VEC*(KS*jv +
 // lane/MS) + e, tap 26 - dl (Eq. 7 pairs input offset delta with tap 1 - delta).
@@ -1588,6 +1753,9 @@ typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, 
                        const int32_t*, const int64_t*, int, const int32_t*, const float*, int64_t,
                        const float*, const float*, uint32_t, const float*, int, int, float*);
 typedef void (*WeightFn)(const float*, int, float*);
+typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*, int64_t,
+                        const float*, const float*, uint32_t, const float*, int, int, float*);
+typedef void (*EffWeightFn)(const float*, int, int, float*);
 typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
                       const int64_t*, int64_t, int64_t, const float*, uint32_t, float*);
 
@@ -1597,9 +1765,11 @@ struct MfmaVariant {
   MfmaFn kernel;
   WeightFn weights;
   size_t cell_wfloats;  // cell kernels' weights (16-row tiles)
-  CellFn cell2, cell4, cell8, cell8t;
+  CellFn cell2, cell4, cell8;
   WeightFn cell_weights;
   SumFn sums;
+  Cell8Fn cell8g;          // edge-8 cells with unsplit face/edge neighbours
+  EffWeightFn eff_weights; // their effective weights (unit-kernel layout)
 };
 
 template <int CIN, int NT, int MS>
@@ -1619,9 +1789,10 @@ MfmaVariant make_variant(int cout_min) {
   v.cell2 = &k_conv_cell2_mfma<CIN, CNT>;
   v.cell4 = &k_conv_cellr_mfma<CIN, CNT, 4, false>;
   v.cell8 = &k_conv_cellr_mfma<CIN, CNT, 8, false>;
-  v.cell8t = &k_conv_cellr_mfma<CIN, CNT, 8, true>;
   v.cell_weights = &k_mfma_weights<CIN, CNT, 16>;
   v.sums = &k_boundary_sums<CIN>;
+  v.cell8g = &k_conv_cell8t_gemm<CIN, NT, MS>;
+  v.eff_weights = &k_eff_weights<CIN, NT, MS>;
   return v;
 }
 
@@ -1670,6 +1841,7 @@ hipError_t device_limits() {
 //   wt         f32 [27 cin cout]            generic-kernel weights
 //   wm         f32 [variant wfloats]        unit-voxel kernel B operands (if a variant exists)
 //   wc         f32 [variant cell_wfloats]   cell kernels' B operands
+//   w8         f32 [variant wfloats]        edge-8 effective weights (unit layout)
 //   6 x (scan workspace (n_trees), i64 [n_trees + 1])
 //              per tree: unit groups, each kind of larger cell, boundary-sum
 //              slots -> prefixes
@@ -1692,6 +1864,7 @@ struct ConvWs {
   float* wt;
   float* wm;
   float* wc;
+  float* w8;
   char* scan[kScans];
   int64_t* pre[kScans];
   int64_t* gkey;
@@ -1721,6 +1894,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
   w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
   w.wc = reinterpret_cast<float*>(take(v ? sizeof(float) * v->cell_wfloats : 0));
+  w.w8 = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
   for (int k = 0; k < kScans; ++k) {
     w.scan[k] = take(oci::scan_workspace(n_trees));
     w.pre[k] = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
@@ -1772,6 +1946,8 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                      a.weight, a.cout, w.wm);
   hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256)), dim3(256), 0,
                      s, a.weight, a.cout, w.wc);
+  hipLaunchKernelGGL(v->eff_weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
+                     a.weight, a.cout, 8, w.w8);
   const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
@@ -1844,11 +2020,23 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // Larger cells, one launch per kind: edge-8 with unsplit face and edge
-  // neighbours, other edge-8, edge-4, edge-2 (the lists are grouped by kind;
-  // the kernels read the counts).
-  const CellFn cells[kKinds] = {v->cell8t, v->cell8, v->cell4, v->cell2};
-  for (int k = 0; k < kKinds; ++k) {
+  // Edge-8 cells with unsplit face and edge neighbours: the gather-GEMM with
+  // effective weights (same LDS footprint as the unit kernel, no tables).
+  {
+    const size_t gsm = sizeof(float) * v->wfloats;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(v->cell8g, dim3(nblk), dim3(kUnitThreads), gsm, s, a.n_leaves,
+                       (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes,
+                       w.ccap, a.in, (const float*)w.w8, in_bytes, a.bias, a.cout, a.relu, a.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // The other larger cells, one launch per kind: other edge-8, edge-4,
+  // edge-2 (the lists are grouped by kind; the kernels read the counts).
+  const CellFn cells[kKinds] = {nullptr, v->cell8, v->cell4, v->cell2};
+  for (int k = 1; k < kKinds; ++k) {
     // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
     const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
     if (smem > g_max_smem) return hipErrorInvalidConfiguration;
