@@ -1064,7 +1064,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__,
     const float* __restrict__, int64_t, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
-    int relu, float* __restrict__ out) {
+    int relu, float* __restrict__ out, const int64_t* __restrict__, int64_t, int64_t) {
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
   extern __shared__ float smem[];
@@ -1236,15 +1236,19 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
     const int32_t* __restrict__ stl, const int64_t* __restrict__ meta,
     const int64_t* __restrict__ sbase, int64_t n_trees, int64_t cap, const float* __restrict__ in,
-    uint32_t in_bytes, float* __restrict__ bsum) {
+    uint32_t in_bytes, float* __restrict__ bsum, const int64_t* __restrict__ p8t,
+    const int64_t* __restrict__ p8n, int64_t t0, int64_t t1) {
   constexpr int TPW = 64 / CIN;
   const int lane = threadIdx.x & 63, c = lane % CIN, sub = lane / CIN;
   int64_t n_split = n_trees - meta[0] - meta[1];
   n_split = n_split < 0 ? 0 : (n_split > n_trees ? n_trees : n_split);
+  // The split trees among trees [t0, t1): list entries [j0, j1).
+  const int64_t j0 = min(n_split, max((int64_t)0, t0 - p8t[t0] - p8n[t0]));
+  const int64_t j1 = min(n_split, max(j0, t1 - p8t[t1] - p8n[t1]));
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
-  for (int64_t j = wave * TPW + sub; j < n_split; j += nwaves * TPW) {
+  for (int64_t j = j0 + wave * TPW + sub; j < j1; j += nwaves * TPW) {
     const int64_t t = stl[j];
     const Bits b = load_bits(trees, t);
     const int rbase = (int)prefix[t];
@@ -1496,7 +1500,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
     const float* __restrict__ bsum, int64_t ccap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
-    int relu, float* __restrict__ out) {
+    int relu, float* __restrict__ out, const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
   extern __shared__ float smem[];
@@ -1506,6 +1510,13 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
+  {
+    // Only the cells of trees [t0, t1) (kpre: the kind's per-tree prefix).
+    const int64_t a = min(lcnt, max((int64_t)0, kpre[t0]));
+    const int64_t b = min(lcnt, max(a, kpre[t1]));
+    lbeg += a;
+    lcnt = b - a;
+  }
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
   const int m = lane % 16, g = lane / 16;
   const int choff = K::VEC * g;  // the lane's first channel
@@ -1751,13 +1762,15 @@ typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, co
                        uint32_t, const float*, int, int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
                        const int32_t*, const int64_t*, int, const int32_t*, const float*, int64_t,
-                       const float*, const float*, uint32_t, const float*, int, int, float*);
+                       const float*, const float*, uint32_t, const float*, int, int, float*,
+                       const int64_t*, int64_t, int64_t);
 typedef void (*WeightFn)(const float*, int, float*);
 typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*, int64_t,
                         const float*, const float*, uint32_t, const float*, int, int, float*);
 typedef void (*EffWeightFn)(const float*, int, int, float*);
 typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
-                      const int64_t*, int64_t, int64_t, const float*, uint32_t, float*);
+                      const int64_t*, int64_t, int64_t, const float*, uint32_t, float*,
+                      const int64_t*, const int64_t*, int64_t, int64_t);
 
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
@@ -1816,6 +1829,14 @@ const MfmaVariant* find_variant(int cin, int cout) {
 }
 
 constexpr int kMfmaThreads = 512;
+
+// Chunks of trees for the boundary sums and the cells that read them (one:
+// more chunks keep the sums in cache for their readers, but each chunk's
+// launches then hold too few tiles per wave to hide their latency).
+#ifndef OC_SUM_CHUNKS
+#define OC_SUM_CHUNKS 1
+#endif
+constexpr int kSumChunks = OC_SUM_CHUNKS;
 
 size_t mfma_smem(const MfmaVariant& v) {
   return sizeof(float) * v.wfloats + sizeof(int32_t) * (kUnitThreads / 64) * 2 * (v.ms / 8) * 64;
@@ -2008,18 +2029,6 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
                      (const float*)w.wm, in_bytes, a.bias, a.cout, a.relu, a.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Boundary sums of the split trees and split depth-1 nodes.
-  {
-    const int64_t per_block = 4 * (64 / a.cin);  // trees per pass of a 256-thread block
-    int64_t blocks = (a.n_trees + per_block - 1) / per_block;
-    if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
-                       (const int32_t*)w.stl, (const int64_t*)w.meta,
-                       (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, a.in, in_bytes, w.bsum);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   // Edge-8 cells with unsplit face and edge neighbours: the gather-GEMM with
   // effective weights (same LDS footprint as the unit kernel, no tables).
   {
@@ -2033,24 +2042,51 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // The other larger cells, one launch per kind: other edge-8, edge-4,
-  // edge-2 (the lists are grouped by kind; the kernels read the counts).
-  const CellFn cells[kKinds] = {nullptr, v->cell8, v->cell4, v->cell2};
-  for (int k = 1; k < kKinds; ++k) {
+  auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
     const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
     if (smem > g_max_smem) return hipErrorInvalidConfiguration;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(cells[k]),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(cells[k], dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s,
-                       a.trees, a.prefix, a.gd,
-                       a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info, (const int32_t*)w.brow,
-                       (const int64_t*)w.meta, k, (const int32_t*)w.codes,
+    const CellFn f = k == 1 || k == 0 ? v->cell8 : (k == 2 ? v->cell4 : v->cell2);
+    hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (r != hipSuccess) return r;
+    hipLaunchKernelGGL(f, dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
+                       a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
+                       (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
                        (const float*)w.bsum, w.ccap, a.in, (const float*)w.wc, in_bytes, a.bias,
-                       a.cout, a.relu, a.out);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+                       a.cout, a.relu, a.out, (const int64_t*)w.pre[1 + k], t0, t1);
+    return hipGetLastError();
+  };
+  // Edge-2 cells (no boundary sums).
+  e = launch_cells(3, 0, a.n_trees);
+  if (e != hipSuccess) return e;
+  // Boundary sums and the cells that read them (other edge-8, edge-4), in
+  // chunks of trees: the sums of the trees up to a chunk's end plus one tree
+  // plane (every neighbour of its cells), then the chunk's cells, so that the
+  // sums they read were written moments before and are still cached.
+  const int64_t plane = (int64_t)a.gh * a.gw + a.gw + 1;
+  const int64_t per_block = 4 * (64 / a.cin);  // trees per pass of a 256-thread block
+  int64_t done = 0;
+  for (int c = 0; c < kSumChunks; ++c) {
+    const int64_t t0 = a.n_trees * c / kSumChunks, t1 = a.n_trees * (c + 1) / kSumChunks;
+    const int64_t need = c + 1 == kSumChunks ? a.n_trees : min(a.n_trees, t1 + plane);
+    if (need > done) {
+      int64_t blocks = (need - done + per_block - 1) / per_block;
+      if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
+      hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
+                         (const int32_t*)w.stl, (const int64_t*)w.meta,
+                         (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, a.in, in_bytes,
+                         w.bsum, (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      done = need;
+    }
+    if (t1 > t0) {
+      e = launch_cells(1, t0, t1);
+      if (e != hipSuccess) return e;
+      e = launch_cells(2, t0, t1);
+      if (e != hipSuccess) return e;
+    }
   }
   return hipGetLastError();
 }

@@ -313,3 +313,23 @@ def random_occupancy(rng: np.random.Generator, n: int, gd: int, gh: int, gw: int
         ext = [int(rng.integers(1, x)) for x in (D, H, W)]
         occ[s, lo[0]:lo[0] + ext[0], lo[1]:lo[1] + ext[1], lo[2]:lo[2] + ext[2]] = 0
     return occ
+
+
+def random_trees(rng: np.random.Generator, n: int, gd: int, gh: int, gw: int,
+                 p_root: float = 0.5, p_d1: float = 0.5, p_d2: float = 0.5) -> np.ndarray:
+    """uint32 [n*gd*gh*gw, 4]: canonical split strings drawn node by node (a
+    root splits with p_root, a depth-1 node of a split root with p_d1, a
+    depth-2 node of a split depth-1 node with p_d2), bit j at word j >> 5,
+    position j & 31.  Gives every cell size next to every kind of neighbour
+    on small grids."""
+    nt = n * gd * gh * gw
+    bits = np.zeros((nt, 73), dtype=bool)
+    bits[:, 0] = rng.random(nt) < p_root
+    for i in range(1, 9):
+        bits[:, i] = bits[:, 0] & (rng.random(nt) < p_d1)
+    for i in range(9, 73):
+        bits[:, i] = bits[:, (i - 1) // 8] & (rng.random(nt) < p_d2)
+    words = np.zeros((nt, 4), dtype=np.uint32)
+    for j in range(73):
+        words[:, j >> 5] |= bits[:, j].astype(np.uint32) << np.uint32(j & 31)
+    return words
