@@ -841,6 +841,12 @@ struct CellCfg {
   using Acc = typename AccT<16>::type;
 };
 
+// Channels per lane vector of the 16-row cell kernels.
+template <int CIN>
+constexpr int cell_vec() {
+  return MfmaCfg<CIN, 1, 16>::VEC;
+}
+
 // Contract layer JD (deltas 9 JD .. 9 JD + 8) into acc.
 template <int CIN, int NT, int JD>
 __device__ __forceinline__ void contract_layer(const float (&S)[9][CIN / 4],
@@ -1391,12 +1397,14 @@ __device__ __forceinline__ void region_add(float (&S)[9][CH], const float (&x)[C
   }
 }
 
-// use = false: the loads still happen (at a valid address) but add nothing.
-template <int R, int JD, int CIN>
-__device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float* __restrict__ p,
-                                            bool use) {
+// Pass P of the window sums covers the lane's channel vectors P PV .. P PV +
+// PV - 1 (W = PV VEC channels).  use = false: the loads still happen (at a
+// valid address) but add nothing.
+template <int R, int JD, int CIN, int PV, int P>
+__device__ __forceinline__ void summary_add(float (&S)[9][PV * cell_vec<CIN>()],
+                                            const float* __restrict__ p, bool use) {
   using K = CellCfg<CIN, 1>;
-  constexpr int CH = CIN / 4;
+  constexpr int CH = PV * K::VEC;
   constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
 #pragma unroll
   for (int ed = -1; ed <= 1; ++ed) {
@@ -1409,11 +1417,11 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
         if (dir2 != 0 && ew != -dir2) continue;
         float v[CH];
 #pragma unroll
-        for (int jv = 0; jv < K::NV; ++jv) {
-          const typename K::Vec q =
-              *reinterpret_cast<const typename K::Vec*>(p + bset(ed, eh, ew) * CIN + K::VSTRIDE * jv);
+        for (int i = 0; i < PV; ++i) {
+          const typename K::Vec q = *reinterpret_cast<const typename K::Vec*>(
+              p + bset(ed, eh, ew) * CIN + K::VSTRIDE * (P * PV + i));
 #pragma unroll
-          for (int e = 0; e < K::VEC; ++e) v[K::VEC * jv + e] = use ? vget<K::VEC>(q, e) : 0.f;
+          for (int e = 0; e < K::VEC; ++e) v[K::VEC * i + e] = use ? vget<K::VEC>(q, e) : 0.f;
         }
         const bool n0 = dir0 == 0 && ed != 0;
 #pragma unroll
@@ -1437,22 +1445,35 @@ __device__ __forceinline__ void summary_add(float (&S)[9][CIN / 4], const float*
 // all its codes are rows, as corner codes always are; then the row gather is
 // issued whatever the code (a code that is not a row reads zeros), so that
 // it need not wait behind a branch.
-template <int R, int JD, int SZ, int CIN, bool TRIV>
-__device__ __forceinline__ void region_sum(float (&S)[9][CIN / 4], int32_t code,
+// The lane's channel vectors P PV .. P PV + PV - 1 of the row at byte offset off.
+template <int CIN, int PV, int P>
+__device__ __forceinline__ void gather_pass(__amdgpu_buffer_rsrc_t rin, uint32_t off,
+                                            float (&x)[PV * cell_vec<CIN>()]) {
+  using K = CellCfg<CIN, 1>;
+#pragma unroll
+  for (int i = 0; i < PV; ++i) {
+    const typename K::Vec v = gather<K::VEC>(rin, off + 4u * K::VSTRIDE * (P * PV + i));
+#pragma unroll
+    for (int e = 0; e < K::VEC; ++e) x[K::VEC * i + e] = vget<K::VEC>(v, e);
+  }
+}
+
+template <int R, int JD, int SZ, int CIN, bool TRIV, int PV, int P>
+__device__ __forceinline__ void region_sum(float (&S)[9][PV * cell_vec<CIN>()], int32_t code,
                                            __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
                                            int choff) {
-  constexpr int CH = CIN / 4;
+  constexpr int CH = PV * cell_vec<CIN>();
   constexpr int nz = (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1);
   if constexpr (TRIV || nz == 3) {  // codes are rows (or outside)
     float x[CH];
-    gather_channels<CIN>(rin, code >= 0 ? row_offset<CIN>(code, choff) : kOutside, x);
+    gather_pass<CIN, PV, P>(rin, code >= 0 ? row_offset<CIN>(code, choff) : kOutside, x);
     region_add<R, JD, SZ, CH>(S, x);
   } else if (code >= 0) {
     float x[CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(code, choff), x);
+    gather_pass<CIN, PV, P>(rin, row_offset<CIN>(code, choff), x);
     region_add<R, JD, SZ, CH>(S, x);
   } else if (code <= -2) {
-    summary_add<R, JD, CIN>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff, true);
+    summary_add<R, JD, CIN, PV, P>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff, true);
   }
 }
 
@@ -1463,33 +1484,87 @@ constexpr bool in_layer(int R) {
   return R != 13 && (R / 9 - 1 == 0 || R / 9 - 1 == JD - 1);
 }
 
-template <int R, int JD, int SZ, int CIN, bool TRIV>
+template <int R, int JD, int SZ, int CIN, bool TRIV, int PV, int P>
 struct RegionLayer {
+  static constexpr int W = PV * cell_vec<CIN>();
   __device__ __forceinline__ static void codes(int32_t (&c)[27], const int32_t* __restrict__ col,
                                                int64_t ccap) {
     if constexpr (in_layer<JD>(R)) c[R] = col[(int64_t)(R - (R > 13)) * ccap];
-    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::codes(c, col, ccap);
+    RegionLayer<R + 1, JD, SZ, CIN, TRIV, PV, P>::codes(c, col, ccap);
   }
-  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], const int32_t (&c)[27],
+  __device__ __forceinline__ static void run(float (&S)[9][W], const int32_t (&c)[27],
                                              __amdgpu_buffer_rsrc_t rin, const float* bsum,
                                              int choff) {
     if constexpr (in_layer<JD>(R)) {
-      region_sum<R, JD, SZ, CIN, TRIV>(S, c[R], rin, bsum, choff);
+      region_sum<R, JD, SZ, CIN, TRIV, PV, P>(S, c[R], rin, bsum, choff);
       // A few regions' loads in flight at a time (more would spill).
       if constexpr (R % OC_REGION_GROUP == OC_REGION_GROUP - 1) __builtin_amdgcn_sched_barrier(0);
     }
-    RegionLayer<R + 1, JD, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
+    RegionLayer<R + 1, JD, SZ, CIN, TRIV, PV, P>::run(S, c, rin, bsum, choff);
   }
 };
-template <int JD, int SZ, int CIN, bool TRIV>
-struct RegionLayer<27, JD, SZ, CIN, TRIV> {
+template <int JD, int SZ, int CIN, bool TRIV, int PV, int P>
+struct RegionLayer<27, JD, SZ, CIN, TRIV, PV, P> {
+  static constexpr int W = PV * cell_vec<CIN>();
   __device__ __forceinline__ static void codes(int32_t (&)[27], const int32_t*, int64_t) {}
-  __device__ __forceinline__ static void run(float (&)[9][CIN / 4], const int32_t (&)[27],
+  __device__ __forceinline__ static void run(float (&)[9][W], const int32_t (&)[27],
                                              __amdgpu_buffer_rsrc_t, const float*, int) {}
+};
+
+// Contract pass P (vectors P PV .. + PV - 1) of layer JD into acc.
+template <int CIN, int NT, int JD, int PV, int P>
+__device__ __forceinline__ void contract_pass(const float (&S)[9][PV * cell_vec<CIN>()],
+                                              const float* wl, int lane,
+                                              typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+  using K = CellCfg<CIN, NT>;
+#pragma unroll
+  for (int k = 0; k < 9; ++k) {
+    const int dl = 9 * JD + k;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < PV; ++i) {
+        const int jv = P * PV + i;
+        const typename K::Vec bv =
+            reinterpret_cast<const typename K::Vec*>(wl)[((dl * NT + nt) * K::NV + jv) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < K::VEC; ++e)
+          acc[nt] = mfma<16>(S[k][K::VEC * i + e], vget<K::VEC>(bv, e), acc[nt]);
+      }
+    if (k % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bounds the B loads in flight
+  }
+}
+
+// One layer of the window sums, in NV / PV passes over the lane's channel
+// vectors (fewer registers per pass; the codes are loaded once per layer).
+template <int CIN, int NT, int SZ, bool TRIV, int JD, int PV, int P>
+struct LayerPasses {
+  __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
+                                             bool live, __amdgpu_buffer_rsrc_t rin,
+                                             const float* bsum, int choff, const float* wl,
+                                             int lane, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+    using K = CellCfg<CIN, NT>;
+    constexpr int W = PV * K::VEC;
+    if constexpr (P * PV < K::NV) {
+      float xp[W];
+#pragma unroll
+      for (int e = 0; e < W; ++e) xp[e] = xs[P * W + e];
+      float S[9][W];
+      init_layer<SZ, JD>(S, xp);
+      if (live) RegionLayer<0, JD, SZ, CIN, TRIV, PV, P>::run(S, c, rin, bsum, choff);
+      contract_pass<CIN, NT, JD, PV, P>(S, wl, lane, acc);
+      __builtin_amdgcn_sched_barrier(0);
+      LayerPasses<CIN, NT, SZ, TRIV, JD, PV, P + 1>::run(c, xs, live, rin, bsum, choff, wl, lane,
+                                                        acc);
+    }
+  }
 };
 
 #ifndef OC_CELLR_THREADS
 #define OC_CELLR_THREADS 512
+#endif
+#ifndef OC_CELLR_PV
+#define OC_CELLR_PV 2
 #endif
 constexpr int kCellrThreads = OC_CELLR_THREADS;
 
@@ -1503,6 +1578,8 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     int relu, float* __restrict__ out, const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
+  // Channel vectors per window-sum pass.
+  constexpr int PV = OC_CELLR_PV < K::NV ? OC_CELLR_PV : K::NV;
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
@@ -1534,35 +1611,18 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
-    {
-      float S[9][CH];
+#pragma unroll
+    for (int jd = 0; jd < 3; ++jd) {
       int32_t c[27];
-      init_layer<SZ, 0>(S, xs);
       if (row >= 0) {
-        RegionLayer<0, 0, SZ, CIN, TRIV>::codes(c, col, ccap);
-        RegionLayer<0, 0, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
+        if (jd == 0) RegionLayer<0, 0, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
+        if (jd == 1) RegionLayer<0, 1, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
+        if (jd == 2) RegionLayer<0, 2, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
       }
-      contract_layer<CIN, NT, 0>(S, wl, lane, acc);
-    }
-    {
-      float S[9][CH];
-      int32_t c[27];
-      init_layer<SZ, 1>(S, xs);
-      if (row >= 0) {
-        RegionLayer<0, 1, SZ, CIN, TRIV>::codes(c, col, ccap);
-        RegionLayer<0, 1, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
-      }
-      contract_layer<CIN, NT, 1>(S, wl, lane, acc);
-    }
-    {
-      float S[9][CH];
-      int32_t c[27];
-      init_layer<SZ, 2>(S, xs);
-      if (row >= 0) {
-        RegionLayer<0, 2, SZ, CIN, TRIV>::codes(c, col, ccap);
-        RegionLayer<0, 2, SZ, CIN, TRIV>::run(S, c, rin, bsum, choff);
-      }
-      contract_layer<CIN, NT, 2>(S, wl, lane, acc);
+      if (jd == 0) LayerPasses<CIN, NT, SZ, TRIV, 0, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
+      if (jd == 1) LayerPasses<CIN, NT, SZ, TRIV, 1, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
+      if (jd == 2) LayerPasses<CIN, NT, SZ, TRIV, 2, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
+      __builtin_amdgcn_sched_barrier(0);  // keeps the next layer's loads out of this one
     }
     store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu, out);
   }
