@@ -505,8 +505,14 @@ __global__ void k_unit_table(const uint32_t* __restrict__ trees, const int64_t* 
                              int32_t* __restrict__ nbt) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t G = min(*n_groups, n_leaves / 8);
-  if (i >= G * 64) return;
-  const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, gkey[i >> 6], (int)(i & 63));
+  if (i >= G * 64) return;  // G * 64 is a multiple of 64: whole waves exit
+  // One group per wave: its key is wave-uniform, so the tree position is
+  // derived once per wave on the scalar unit.
+  const uint64_t k64 = (uint64_t)gkey[i >> 6];
+  const uint32_t klo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)k64);
+  const uint32_t khi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(k64 >> 32));
+  const int64_t key = (int64_t)(((uint64_t)khi << 32) | klo);
+  const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, key, (int)(i & 63));
   nbt[i] = r < n_leaves ? r : -1;  // only a non-canonical structure exceeds
 }
 
