@@ -2040,8 +2040,14 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
                      scan_counts_buffer(w.scan[2]), scan_counts_buffer(w.scan[3]),
                      scan_counts_buffer(w.scan[4]), scan_counts_buffer(w.scan[kSlotScan]));
-  for (int k = 0; k < kScans; ++k) {
-    e = scan_counts(scan_counts_buffer(w.scan[k]), a.n_trees, w.pre[k], w.scan[k], s);
+  {
+    void* sws[kScans];
+    int64_t* spre[kScans];
+    for (int k = 0; k < kScans; ++k) {
+      sws[k] = w.scan[k];
+      spre[k] = w.pre[k];
+    }
+    e = scan_counts_set(kScans, sws, a.n_trees, spre, s);
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],

@@ -15,6 +15,10 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t scan_workspace(int64_t n);
 int32_t* scan_counts_buffer(void* ws);
 hipError_t scan_counts(const int32_t* counts, int64_t n, int64_t* prefix, void* ws, hipStream_t s);
+// k (<= kMaxScans) scans of length n in three launches: ws[i] is a scan
+// workspace whose counts buffer holds the counts, prefix[i] the output.
+constexpr int kMaxScans = 8;
+hipError_t scan_counts_set(int k, void* const* ws, int64_t n, int64_t* const* prefix, hipStream_t s);
 
 hipError_t launch_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule,
                         uint32_t* trees, int32_t* counts, hipStream_t s);

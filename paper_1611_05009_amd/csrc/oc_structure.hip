@@ -121,6 +121,13 @@ __device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t* sh_waves,
   return off + incl - v;
 }
 
+// Several scans of the same length at once (blockIdx.y selects the array).
+struct ScanSet {
+  const int32_t* counts[oci::kMaxScans];
+  int64_t* prefix[oci::kMaxScans];
+  int64_t* sums[oci::kMaxScans];
+};
+
 __global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const int32_t* __restrict__ counts,
                                                               int64_t n, int64_t* __restrict__ sums) {
   __shared__ int64_t sh[kScanThreads / 64];
@@ -132,6 +139,19 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const int32_t* __r
   int64_t tot;
   block_excl_scan(s, sh, &tot);
   if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_reduce_set(ScanSet set, int64_t n) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  const int32_t* __restrict__ counts = set.counts[blockIdx.y];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k)
+    if (base + k < n) s += counts[base + k];
+  int64_t tot;
+  block_excl_scan(s, sh, &tot);
+  if (threadIdx.x == 0) set.sums[blockIdx.y][blockIdx.x] = tot;
 }
 
 // Single block: exclusive scan of the per-chunk sums in place; total -> *total.
@@ -148,6 +168,42 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_sums(int64_t* __restrict_
     carry += tot;
   }
   if (threadIdx.x == 0) *total = carry;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_sums_set(ScanSet set, int64_t nb, int64_t n) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  int64_t* __restrict__ sums = set.sums[blockIdx.y];
+  int64_t carry = 0;
+  for (int64_t b0 = 0; b0 < nb; b0 += kScanThreads) {
+    const int64_t i = b0 + threadIdx.x;
+    const int64_t v = i < nb ? sums[i] : 0;
+    int64_t tot;
+    const int64_t ex = block_excl_scan(v, sh, &tot);
+    if (i < nb) sums[i] = carry + ex;
+    carry += tot;
+  }
+  if (threadIdx.x == 0) set.prefix[blockIdx.y][n] = carry;
+}
+
+__global__ void __launch_bounds__(kScanThreads) k_scan_apply_set(ScanSet set, int64_t n) {
+  __shared__ int64_t sh[kScanThreads / 64];
+  const int32_t* __restrict__ counts = set.counts[blockIdx.y];
+  int64_t* __restrict__ prefix = set.prefix[blockIdx.y];
+  const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    v[k] = base + k < n ? counts[base + k] : 0;
+    s += v[k];
+  }
+  int64_t tot;
+  int64_t run = block_excl_scan(s, sh, &tot) + set.sums[blockIdx.y][blockIdx.x];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    if (base + k < n) prefix[base + k] = run;
+    run += v[k];
+  }
 }
 
 __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const int32_t* __restrict__ counts,
@@ -326,6 +382,26 @@ hipError_t scan_counts(const int32_t* counts, int64_t n, int64_t* prefix, void* 
   hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)nb), dim3(kScanThreads), 0, s, counts, n, sums);
   hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(kScanThreads), 0, s, sums, nb, prefix + n);
   hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)nb), dim3(kScanThreads), 0, s, counts, n, sums, prefix);
+  return hipGetLastError();
+}
+
+hipError_t scan_counts_set(int k, void* const* ws, int64_t n, int64_t* const* prefix,
+                           hipStream_t s) {
+  if (k < 1 || k > kMaxScans) return hipErrorInvalidValue;
+  const int64_t nb = (n + kScanChunk - 1) / kScanChunk;
+  ScanSet set;
+  for (int i = 0; i < kMaxScans; ++i) {
+    const int j = i < k ? i : 0;
+    set.counts[i] = static_cast<const int32_t*>(ws[j]);
+    set.prefix[i] = prefix[j];
+    set.sums[i] = reinterpret_cast<int64_t*>(static_cast<char*>(ws[j]) +
+                                             align256(sizeof(int32_t) * (size_t)n));
+  }
+  hipLaunchKernelGGL(k_scan_reduce_set, dim3((unsigned)nb, (unsigned)k), dim3(kScanThreads), 0, s,
+                     set, n);
+  hipLaunchKernelGGL(k_scan_sums_set, dim3(1, (unsigned)k), dim3(kScanThreads), 0, s, set, nb, n);
+  hipLaunchKernelGGL(k_scan_apply_set, dim3((unsigned)nb, (unsigned)k), dim3(kScanThreads), 0, s,
+                     set, n);
   return hipGetLastError();
 }
 
