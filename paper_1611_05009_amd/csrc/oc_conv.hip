@@ -992,22 +992,32 @@ struct Shell2RowLoad<JD, UH, 8, CIN> {
 // LDS bytes per wave for the shell offsets of a 16-cell tile.
 constexpr int kShell2Lds = 16 * 56 * 4;
 
+// The box sums are separable: the two planes of the row are summed first,
+// then neighbouring pairs along w, and each pair sum goes to the two
+// delta-rows that reach h-row UH (the cell's own voxels are left out here;
+// init_layer counts them).
 template <int JD, int UH, int CIN>
 __device__ __forceinline__ void shell2_row_add(float (&S)[9][CIN / 4], const float (&X)[8][CIN / 4]) {
+  constexpr int CH = CIN / 4;
+  float D[4][CH];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const int u = (JD + k / 4) * 16 + UH * 4 + (k % 4);
-    if (shell2_inner(u)) continue;
-    const int uw = k % 4;
+  for (int uw = 0; uw < 4; ++uw) {
+    const bool a = !shell2_inner(JD * 16 + UH * 4 + uw);        // plane JD
+    const bool b = !shell2_inner((JD + 1) * 16 + UH * 4 + uw);  // plane JD + 1
+#pragma unroll
+    for (int e = 0; e < CH; ++e)
+      D[uw][e] = a && b ? X[uw][e] + X[4 + uw][e] : (a ? X[uw][e] : (b ? X[4 + uw][e] : 0.f));
+  }
+#pragma unroll
+  for (int jw = 0; jw < 3; ++jw) {
+    float P[CH];
+#pragma unroll
+    for (int e = 0; e < CH; ++e) P[e] = D[jw][e] + D[jw + 1][e];
 #pragma unroll
     for (int jh = 0; jh < 3; ++jh) {
       if (UH - jh < 0 || UH - jh > 1) continue;
 #pragma unroll
-      for (int jw = 0; jw < 3; ++jw) {
-        if (uw - jw < 0 || uw - jw > 1) continue;
-#pragma unroll
-        for (int e = 0; e < CIN / 4; ++e) S[jh * 3 + jw][e] += X[k][e];
-      }
+      for (int e = 0; e < CH; ++e) S[jh * 3 + jw][e] += P[e];
     }
   }
 }
