@@ -1259,7 +1259,7 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
     const int32_t* __restrict__ stl, const int64_t* __restrict__ meta,
     const int64_t* __restrict__ sbase, int64_t n_trees, int64_t cap, const float* __restrict__ in,
     uint32_t in_bytes, float* __restrict__ bsum, const int64_t* __restrict__ p8t,
-    const int64_t* __restrict__ p8n, int64_t t0, int64_t t1) {
+    const int64_t* __restrict__ p8n, int64_t t0, int64_t t1, const uint32_t* __restrict__ smask) {
   constexpr int TPW = 64 / CIN;
   const int lane = threadIdx.x & 63, c = lane % CIN, sub = lane / CIN;
   int64_t n_split = n_trees - meta[0] - meta[1];
@@ -1301,9 +1301,11 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
       if (split1) {
         const int64_t slot = s0 + 1 + __popc((uint32_t)(b.lo >> 1) & ((1u << o1) - 1u));
         if (slot < cap) {
+          const uint32_t mk = smask[slot];  // only the sets some cell reads
           float* dst = bsum + slot * (kSets * CIN) + c;
 #pragma unroll
-          for (int s = 0; s < kSets; ++s) dst[s * CIN] = cs[s];
+          for (int s = 0; s < kSets; ++s)
+            if ((mk >> s) & 1u) dst[s * CIN] = cs[s];
         }
       }
 #pragma unroll
@@ -1315,11 +1317,18 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
       }
     }
     if (s0 < cap) {
+      const uint32_t mk = smask[s0];
       float* dst = bsum + s0 * (kSets * CIN) + c;
 #pragma unroll
-      for (int s = 0; s < kSets; ++s) dst[s * CIN] = ts[s];
+      for (int s = 0; s < kSets; ++s)
+        if ((mk >> s) & 1u) dst[s * CIN] = ts[s];
     }
   }
+}
+
+__global__ void k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
 }
 
 // Region codes of the edge-4 and edge-8 cells (structure only, built once per
@@ -1329,13 +1338,14 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
 // neighbouring block at offset dir (the tree for an edge-8 cell, the depth-1
 // node for an edge-4 one), -2 - s if that block is split and has
 // boundary-sum slot s, -1 outside the grid.  A corner region is one voxel,
-// so its code is always the row of the leaf that holds that voxel.
+// so its code is always the row of the leaf that holds that voxel.  smask[s]
+// collects the boundary sets of slot s that some cell reads.
 __global__ void k_region_codes(const uint32_t* __restrict__ trees,
                                const int64_t* __restrict__ prefix, int gd, int gh, int gw,
                                int64_t n_leaves, const uint64_t* __restrict__ info,
                                const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
                                const int64_t* __restrict__ sbase, int64_t cap, int64_t ccap,
-                               int32_t* __restrict__ codes) {
+                               int32_t* __restrict__ codes, uint32_t* __restrict__ smask) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t n8 = meta[0] + meta[1], nbig = n8 + meta[2];
   if (nbig > ccap) nbig = ccap;
@@ -1378,6 +1388,19 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
         }
       }
       if (slot >= 0) code = slot < cap && slot < 0x7FFFFFF0LL ? (int32_t)(-2 - slot) : -1;
+      if (code <= -2) {
+        // The sets a cell reads for region dir: e_a = -dir_a where dir_a != 0,
+        // any value on the other axes.
+        uint32_t mk = 0;
+        for (int q = 0; q < 27; ++q) {
+          if (q == 13) continue;
+          const int e3[3] = {q / 9 - 1, (q / 3) % 3 - 1, q % 3 - 1};
+          if ((dir[0] == 0 || e3[0] == -dir[0]) && (dir[1] == 0 || e3[1] == -dir[1]) &&
+              (dir[2] == 0 || e3[2] == -dir[2]))
+            mk |= 1u << (q - (q > 13));
+        }
+        atomicOr(&smask[slot], mk);
+      }
       else code = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
     }
     codes[(int64_t)(r - (r > 13)) * ccap + j] = code;
@@ -1846,7 +1869,7 @@ typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*,
 typedef void (*EffWeightFn)(const float*, int, int, float*);
 typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
                       const int64_t*, int64_t, int64_t, const float*, uint32_t, float*,
-                      const int64_t*, const int64_t*, int64_t, int64_t);
+                      const int64_t*, const int64_t*, int64_t, int64_t, const uint32_t*);
 
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
@@ -1949,6 +1972,7 @@ hipError_t device_limits() {
 //   bsum       f32 [cap][26][cin]           boundary sums (if a variant exists)
 //   nbt        i32 [(n_leaves / 8 + 1) 64]  unit-group neighbourhood rows (if a variant exists)
 //   codes      i32 [26][ccap]               region codes of edge-4/8 cells (if a variant exists)
+//   smask      u32 [cap]                    boundary sets read per slot
 // A slot belongs to a split node of depth 0 or 1 and every split node adds 7
 // leaves, so cap = (n_leaves - n_trees) / 7 slots hold every canonical
 // structure of that size; a tree holds at most 8 cells of edge 4 or 8, so
@@ -1973,6 +1997,7 @@ struct ConvWs {
   int32_t* nbt;
   int32_t* codes;
   int64_t ccap;
+  uint32_t* smask;
   size_t total;
 };
 
@@ -2007,6 +2032,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.nbt = reinterpret_cast<int32_t*>(take(v ? sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1) : 0));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
+  w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.total = off + 256;
   return w;
 }
@@ -2069,11 +2095,14 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
     hipLaunchKernelGGL(k_unit_table, dim3((unsigned)((nt_threads + 255) / 256)), dim3(256), 0, s,
                        a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
                        (const int64_t*)(w.pre[0] + a.n_trees), w.nbt);
+  if (w.cap > 0)
+    hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((w.cap + 255) / 256)), dim3(256), 0, s, w.smask,
+                       w.cap);
   if (w.ccap > 0)
     hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256)), dim3(256), 0, s,
                        a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta,
-                       (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes);
+                       (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes, w.smask);
   return hipGetLastError();
 }
 
@@ -2158,7 +2187,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
       hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
                          (const int32_t*)w.stl, (const int64_t*)w.meta,
                          (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, a.in, in_bytes,
-                         w.bsum, (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need);
+                         w.bsum, (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need,
+                         (const uint32_t*)w.smask);
       e = hipGetLastError();
       if (e != hipSuccess) return e;
       done = need;
