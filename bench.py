@@ -158,6 +158,14 @@ def main():
         prep_events.append((s, e))
         return s, e
 
+    op_events = []
+
+    def op_timer(name):
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        op_events.append((name, s, e))
+        return s, e
+
     for _ in range(args.warmup):
         pipeline.run_step(W, impl=args.impl)
     torch.cuda.synchronize()
@@ -165,10 +173,12 @@ def main():
 
     events.clear()
     prep_events.clear()
+    op_events.clear()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        pipeline.run_step(W, conv_timer=timer, impl=args.impl, prep_timer=prep_timer)
+        pipeline.run_step(W, conv_timer=timer, impl=args.impl, prep_timer=prep_timer,
+                          op_timer=op_timer)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_step = 1e3 * dt / args.steps
@@ -181,6 +191,11 @@ def main():
     prep_ms = [0.0] * n_conv
     for k, (s, e) in enumerate(prep_events):
         prep_ms[k % n_conv] += s.elapsed_time(e) / args.steps
+    # Build, pool and unpool, each summed over its calls in a step (the
+    # structure calls synchronize to return leaf counts to the host).
+    op_ms = {}
+    for name, s, e in op_events:
+        op_ms[name] = op_ms.get(name, 0.0) + s.elapsed_time(e) / args.steps
     # Dominant kernel: the first conv layer (the only one in the 256^3 workload).
     p0 = convs[0][1]
     gd = W.occ_np.shape[1] // 8
@@ -213,6 +228,7 @@ def main():
         },
         "conv_ms": per_layer_ms,
         "conv_prepare_ms": prep_ms,
+        "op_ms": op_ms,
         "conv_leaf_cells_per_s": W.n_leaves / t_conv,
         "dense_voxels_per_s": W.dense_voxels / t_conv,
         "roofline": {

@@ -75,12 +75,23 @@ class Workload:
 
 
 def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: str = "auto",
-             prep_timer=None):
+             prep_timer=None, op_timer=None):
     """One pass of the hot path.  Returns (structure, features) at the end.
     conv_timer() returns a (start, end) event pair that brackets each
     convolution proper (execute); prep_timer() one that brackets each
-    convolution's prepare (structure- and weight-dependent tables)."""
-    g = oc.build(W.occ)
+    convolution's prepare (structure- and weight-dependent tables);
+    op_timer(name) one that brackets the build ("build") and each pool or
+    unpool ("pool", "unpool", "unpool_guided")."""
+    def timed(name, fn):
+        if op_timer is None:
+            return fn()
+        s, e = op_timer(name)
+        s.record()
+        r = fn()
+        e.record()
+        return r
+
+    g = timed("build", lambda: oc.build(W.occ))
     x = oc.ten2oc(g, W.dense, "avg") if W.dense is not None else W.features
     if records is not None:
         records.append(OpRecord("input", g, x, g, x))
@@ -102,11 +113,12 @@ def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: st
                 e.record()
         elif op == "pool":
             guides.append(g)
-            g, x = oc.pool2(g, x)
+            g, x = timed("pool", lambda: oc.pool2(g_in, x_in))
         elif op == "unpool":
-            g, x = oc.unpool2(g, x)
+            g, x = timed("unpool", lambda: oc.unpool2(g_in, x_in))
         elif op == "unpool_guided":
-            g, x = oc.unpool2(g, x, guide=guides.pop())
+            guide = guides.pop()
+            g, x = timed("unpool_guided", lambda: oc.unpool2(g_in, x_in, guide=guide))
         else:
             raise ValueError(op)
         if records is not None:
