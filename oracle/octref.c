@@ -549,6 +549,186 @@ void ocref_unpool2(const int64_t *in_rowmap, int gd, int gh, int gw, const doubl
   }
 }
 
+/* ------------------------------------------------------------------------- */
+/* Gradients (backward passes) of the convolution, pooling and unpooling.     */
+/* Each is the adjoint of the forward map as the forward is defined above:    */
+/* the convolution of Eq. 8 is linear in the input and in the weights, pool   */
+/* (Eq. 10) selects one input value per output value, unpool (Eq. 12) copies. */
+/* ------------------------------------------------------------------------- */
+
+static double leaf_volume(const uint64_t *leaf_info, long row) {
+  int dep, a, b, e, s;
+  node_geom((int)(leaf_info[row] & 1023), &dep, &a, &b, &e, &s);
+  return (double)s * s * s;
+}
+
+/* Input gradient of Eq. 8 (bias and ReLU excluded).  Output voxel v of leaf l
+ * receives dy[l] / |l| (the average of Eq. 8 spreads it over the cell), and
+ * reads input voxel v - (tap - 1) with tap weight W[co][ci][tap] (Eq. 7).
+ * So input voxel u collects sum over taps of W^T dy[leaf(u + tap - 1)] /
+ * |leaf(u + tap - 1)|, and input leaf l' sums that over its voxels.
+ * rowmap holds every sample; dx [n_leaves][cin] is overwritten. */
+void ocref_conv3_bwd_data(const uint64_t *leaf_info, const int64_t *rowmap, int n, int gd,
+                          int gh, int gw, const double *dy, int cout, const double *w, int cin,
+                          long n_leaves, double *dx) {
+  long D = 8L * gd, H = 8L * gh, W = 8L * gw;
+  (void)n;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (long r = 0; r < n_leaves; ++r) {
+    uint64_t info = leaf_info[r];
+    long t = (long)(info >> 10);
+    int bit = (int)(info & 1023);
+    long rem = t;
+    int tw = rem % gw; rem /= gw;
+    int th = rem % gh; rem /= gh;
+    int td = rem % gd; rem /= gd;
+    long sample = rem;
+    const int64_t *rm = rowmap + sample * D * H * W;
+    int dep, od, oh, ow, s;
+    node_geom(bit, &dep, &od, &oh, &ow, &s);
+    double *acc = dx + r * cin;
+    for (int ci = 0; ci < cin; ++ci) acc[ci] = 0.0;
+    for (int a = 0; a < s; ++a)
+      for (int b = 0; b < s; ++b)
+        for (int e = 0; e < s; ++e) {
+          long i = 8L * td + od + a, j = 8L * th + oh + b, k = 8L * tw + ow + e;
+          for (int l = 0; l < 3; ++l)
+            for (int m = 0; m < 3; ++m)
+              for (int q = 0; q < 3; ++q) {
+                long vi = i + l - 1, vj = j + m - 1, vk = k + q - 1;  /* output voxel */
+                if (vi < 0 || vi >= D || vj < 0 || vj >= H || vk < 0 || vk >= W) continue;
+                long ol = rm[(vi * H + vj) * W + vk];
+                double inv = 1.0 / leaf_volume(leaf_info, ol);
+                const double *g = dy + ol * cout;
+                for (int ci = 0; ci < cin; ++ci) {
+                  double sum = 0.0;
+                  for (int co = 0; co < cout; ++co)
+                    sum += w[((long)co * cin + ci) * 27 + l * 9 + m * 3 + q] * g[co];
+                  acc[ci] += sum * inv;
+                }
+              }
+        }
+  }
+}
+
+/* Weight and bias gradients of Eq. 8: dw[co][ci][tap] = sum over leaves l of
+ * dy[l][co] / |l| times the sum over l's voxels v of x at v - (tap - 1)
+ * (zero outside the grid); db[co] = sum over leaves of dy[l][co].  Summed in
+ * row order, one output channel per thread. */
+void ocref_conv3_bwd_weight(const uint64_t *leaf_info, const int64_t *rowmap, int n, int gd,
+                            int gh, int gw, const double *x, int cin, const double *dy, int cout,
+                            long n_leaves, double *dw, double *db) {
+  long D = 8L * gd, H = 8L * gh, W = 8L * gw;
+  (void)n;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int co = 0; co < cout; ++co) {
+    double *dwc = dw + (long)co * cin * 27;
+    for (long z = 0; z < (long)cin * 27; ++z) dwc[z] = 0.0;
+    double bsum = 0.0;
+    for (long r = 0; r < n_leaves; ++r) {
+      uint64_t info = leaf_info[r];
+      long t = (long)(info >> 10);
+      int bit = (int)(info & 1023);
+      long rem = t;
+      int tw = rem % gw; rem /= gw;
+      int th = rem % gh; rem /= gh;
+      int td = rem % gd; rem /= gd;
+      long sample = rem;
+      const int64_t *rm = rowmap + sample * D * H * W;
+      int dep, od, oh, ow, s;
+      node_geom(bit, &dep, &od, &oh, &ow, &s);
+      double g = dy[r * cout + co];
+      bsum += g;
+      g /= (double)s * s * s;
+      for (int a = 0; a < s; ++a)
+        for (int b = 0; b < s; ++b)
+          for (int e = 0; e < s; ++e) {
+            long i = 8L * td + od + a, j = 8L * th + oh + b, k = 8L * tw + ow + e;
+            for (int l = 0; l < 3; ++l)
+              for (int m = 0; m < 3; ++m)
+                for (int q = 0; q < 3; ++q) {
+                  long ii = i - l + 1, jj = j - m + 1, kk = k - q + 1;
+                  if (ii < 0 || ii >= D || jj < 0 || jj >= H || kk < 0 || kk >= W) continue;
+                  const double *xi = x + rm[(ii * H + jj) * W + kk] * cin;
+                  for (int ci = 0; ci < cin; ++ci) dwc[(long)ci * 27 + l * 9 + m * 3 + q] += g * xi[ci];
+                }
+          }
+    }
+    db[co] = bsum;
+  }
+}
+
+/* Gradient of Eq. 10: an output value that copies an input cell passes its
+ * gradient to that cell; one that is the maximum of 8 depth-3 voxels passes
+ * it to the first of them (order l, m, n) that attains the maximum, per
+ * channel.  dx [in_rows][c] is overwritten. */
+void ocref_pool2_max_bwd(const uint64_t *in_leaf_info, const int64_t *in_rowmap, int n,
+                         int gd, int gh, int gw, const double *in_data, int c,
+                         const uint64_t *out_leaf_info, long out_rows, const double *dy,
+                         long in_rows, double *dx) {
+  long D = 8L * gd, H = 8L * gh, W = 8L * gw;
+  int ogd = gd / 2, ogh = gh / 2, ogw = gw / 2;
+  (void)n;
+  for (long z = 0; z < in_rows * c; ++z) dx[z] = 0.0;
+  for (long r = 0; r < out_rows; ++r) {
+    long t = (long)(out_leaf_info[r] >> 10);
+    int bit = (int)(out_leaf_info[r] & 1023);
+    long rem = t;
+    int tw = rem % ogw; rem /= ogw;
+    int th = rem % ogh; rem /= ogh;
+    int td = rem % ogd; rem /= ogd;
+    long sample = rem;
+    const int64_t *rm = in_rowmap + sample * D * H * W;
+    int dep, od, oh, ow, s;
+    node_geom(bit, &dep, &od, &oh, &ow, &s);
+    long i = 2 * (8L * td + od), j = 2 * (8L * th + oh), k = 2 * (8L * tw + ow);
+    for (int ch = 0; ch < c; ++ch) {
+      int vd;
+      double v = oc_value(rm, H, W, in_leaf_info, in_data, c, ch, i, j, k, &vd);
+      long best = rm[(i * H + j) * W + k];
+      if (vd >= 3) {
+        for (int l = 0; l < 2; ++l)
+          for (int m = 0; m < 2; ++m)
+            for (int q = 0; q < 2; ++q) {
+              double xv = oc_value(rm, H, W, in_leaf_info, in_data, c, ch, i + l, j + m, k + q, NULL);
+              if (xv > v) {
+                v = xv;
+                best = rm[((i + l) * H + j + m) * W + k + q];
+              }
+            }
+      }
+      dx[best * c + ch] += dy[r * c + ch];
+    }
+  }
+}
+
+/* Gradient of Eq. 12 (plain or guided): every output leaf copies the input
+ * leaf holding floor(v / 2) of its first voxel v, so that input leaf sums
+ * the gradients of all output leaves that copy it, in output row order.
+ * dx [in_rows][c] is overwritten. */
+void ocref_unpool2_bwd(const int64_t *in_rowmap, int gd, int gh, int gw, int c,
+                       const uint64_t *out_leaf_info, long out_rows, const double *dy,
+                       long in_rows, double *dx) {
+  long D = 8L * gd, H = 8L * gh, W = 8L * gw;
+  int Gd = 2 * gd, Gh = 2 * gh, Gw = 2 * gw;
+  for (long z = 0; z < in_rows * c; ++z) dx[z] = 0.0;
+  for (long r = 0; r < out_rows; ++r) {
+    long t = (long)(out_leaf_info[r] >> 10);
+    int bit = (int)(out_leaf_info[r] & 1023);
+    long rem = t;
+    int tw = rem % Gw; rem /= Gw;
+    int th = rem % Gh; rem /= Gh;
+    int td = rem % Gd; rem /= Gd;
+    long sample = rem;
+    const int64_t *rm = in_rowmap + sample * D * H * W;
+    int dep, od, oh, ow, s;
+    node_geom(bit, &dep, &od, &oh, &ow, &s);
+    long i = 8L * td + od, j = 8L * th + oh, k = 8L * tw + ow;
+    long row = rm[((i / 2) * H + j / 2) * W + k / 2];
+    for (int ch = 0; ch < c; ++ch) dx[row * c + ch] += dy[r * c + ch];
+  }
+}
+
 /* Element-wise rectifier (pointwise ops act on leaf data unchanged, Sec. 3.2). */
 void ocref_relu(double *x, long count) {
   for (long i = 0; i < count; ++i)

@@ -17,6 +17,10 @@ Every function follows a passage of the OctNet paper (Riegler et al., CVPR
   to oc2ten of the input (the wrapper of Eq. 6).
 - ``pool2_structure`` / ``pool2_max``: Eq. 10 (Sec. 3.2, "Pooling").
 - ``unpool2_structure`` / ``unpool2``: Eq. 12 and the guided remark after it.
+- ``conv3_bwd_data`` / ``conv3_bwd_weight`` / ``pool2_max_bwd`` /
+  ``unpool2_bwd`` / ``relu_bwd``: the gradients of those maps (their
+  adjoints: Eq. 8 is linear in the input and in the weights, Eq. 10 selects
+  one input value per output value, Eq. 12 copies).
 """
 from __future__ import annotations
 
@@ -77,6 +81,10 @@ def lib():
             "ocref_unpool2_structure": (None, [P, i32, i32, i32, i32, P]),
             "ocref_unpool2": (None, [P, i32, i32, i32, P, i32, P, i64, P]),
             "ocref_relu": (None, [P, i64]),
+            "ocref_conv3_bwd_data": (None, [P, P, i32, i32, i32, i32, P, i32, P, i32, i64, P]),
+            "ocref_conv3_bwd_weight": (None, [P, P, i32, i32, i32, i32, P, i32, P, i32, i64, P, P]),
+            "ocref_pool2_max_bwd": (None, [P, P, i32, i32, i32, i32, P, i32, P, i64, P, i64, P]),
+            "ocref_unpool2_bwd": (None, [P, i32, i32, i32, i32, P, i64, P, i64, P]),
             "ocref_num_threads": (i32, []),
             "ocref_set_num_threads": (None, [i32]),
         }
@@ -387,3 +395,68 @@ def num_threads() -> int:
 
 def set_num_threads(n: int) -> None:
     lib().ocref_set_num_threads(int(n))
+
+
+# ----------------------------------------------------------------------------
+# Gradients
+# ----------------------------------------------------------------------------
+
+
+def conv3_bwd_data(g: Grid, dy: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """Input gradient of Eq. 8 (bias and ReLU excluded): [n_leaves, Cin]."""
+    dy = _c(dy, np.float64)
+    w = _c(w, np.float64)
+    cout, cin = w.shape[0], w.shape[1]
+    assert dy.shape == (g.n_leaves, cout)
+    info, rm = leaf_info(g), rowmap(g)
+    dx = np.zeros((g.n_leaves, cin), dtype=np.float64)
+    lib().ocref_conv3_bwd_data(_p(info), _p(rm), g.n, g.gd, g.gh, g.gw, _p(dy), cout, _p(w),
+                               cin, g.n_leaves, _p(dx))
+    return dx
+
+
+def conv3_bwd_weight(g: Grid, x: np.ndarray, dy: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """Weight and bias gradients of Eq. 8: ([Cout, Cin, 3, 3, 3], [Cout])."""
+    x = _c(x, np.float64)
+    dy = _c(dy, np.float64)
+    cin, cout = x.shape[1], dy.shape[1]
+    assert x.shape[0] == g.n_leaves and dy.shape[0] == g.n_leaves
+    info, rm = leaf_info(g), rowmap(g)
+    dw = np.zeros((cout, cin, 3, 3, 3), dtype=np.float64)
+    db = np.zeros(cout, dtype=np.float64)
+    lib().ocref_conv3_bwd_weight(_p(info), _p(rm), g.n, g.gd, g.gh, g.gw, _p(x), cin, _p(dy),
+                                 cout, g.n_leaves, _p(dw), _p(db))
+    return dw, db
+
+
+def pool2_max_bwd(g: Grid, x: np.ndarray, dy: np.ndarray, out_g: Grid | None = None) -> np.ndarray:
+    """Gradient of Eq. 10 with respect to the input leaves: [n_leaves(g), C]."""
+    x = _c(x, np.float64)
+    dy = _c(dy, np.float64)
+    c = x.shape[1]
+    out_g = pool2_structure(g) if out_g is None else out_g
+    info_in, info_out, rm = leaf_info(g), leaf_info(out_g), rowmap(g)
+    assert dy.shape == (out_g.n_leaves, c)
+    dx = np.zeros((g.n_leaves, c), dtype=np.float64)
+    lib().ocref_pool2_max_bwd(_p(info_in), _p(rm), g.n, g.gd, g.gh, g.gw, _p(x), c, _p(info_out),
+                              info_out.size, _p(dy), g.n_leaves, _p(dx))
+    return dx
+
+
+def unpool2_bwd(g: Grid, dy: np.ndarray, out_g: Grid) -> np.ndarray:
+    """Gradient of Eq. 12 (plain or guided; out_g is the output structure)
+    with respect to the input leaves: [n_leaves(g), C]."""
+    dy = _c(dy, np.float64)
+    c = dy.shape[1]
+    info_out, rm = leaf_info(out_g), rowmap(g)
+    assert dy.shape[0] == out_g.n_leaves
+    dx = np.zeros((g.n_leaves, c), dtype=np.float64)
+    lib().ocref_unpool2_bwd(_p(rm), g.gd, g.gh, g.gw, c, _p(info_out), info_out.size, _p(dy),
+                            g.n_leaves, _p(dx))
+    return dx
+
+
+def relu_bwd(y: np.ndarray, dy: np.ndarray) -> np.ndarray:
+    """Gradient of max(0, .) given its output y: dy where y > 0, else 0."""
+    y = np.asarray(y, dtype=np.float64)
+    return np.where(y > 0.0, np.asarray(dy, dtype=np.float64), 0.0)
