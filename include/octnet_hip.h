@@ -29,7 +29,7 @@
  * `stream` is a hipStream_t (NULL = the default stream).  Calls are
  * asynchronous on that stream except where marked "synchronizes".  The caller
  * owns every buffer; no call allocates or frees device memory.  Outputs must
- * not alias inputs (except oc_relu).  Argument errors are detected on the host
+ * not alias inputs (except oc_relu and oc_relu_backward).  Argument errors are detected on the host
  * before any launch and leave every buffer untouched.
  */
 #ifndef OCTNET_HIP_H
@@ -205,6 +205,62 @@ int oc_unpool2(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd
 /* Pointwise max(0, x) on leaf data (pointwise ops act on leaf data alone,
  * Sec. 3.2).  In place allowed. */
 int oc_relu(float* data, int64_t count, void* stream);
+
+/*
+ * Gradients.  Each takes the output gradient (dout, laid out as the forward
+ * output) and writes gradients laid out as the forward operands; the caller
+ * owns every buffer, and outputs must not alias inputs except in
+ * oc_relu_backward.  They follow from the forward definitions by the chain
+ * rule (back-propagation through the layers of Sec. 3, trained end to end as
+ * in Sec. 5).
+ */
+
+/* Bytes of workspace for oc_conv3x3x3_backward.  *bytes [host]. */
+int oc_conv3x3x3_backward_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout,
+                                    size_t* bytes);
+
+/*
+ * Gradient of oc_conv3x3x3 (Eq. 8 with average pooling) without its ReLU:
+ * apply oc_relu_backward to dout first when the forward call fused one.
+ *   dout:    float [n_leaves][cout], the gradient of the convolution output.
+ *   din:     float [n_leaves][cin] or NULL: the input gradient.  With
+ *            g_l = dout_l / |l| spread over the voxels of output leaf l, input
+ *            leaf l' receives |l'| times the convolution of g with the
+ *            flipped, channel-transposed kernel (the adjoint of Eq. 7 summed
+ *            over the cell).  Needs weight.
+ *   dweight: float [cout][cin][3][3][3] or NULL (overwritten, not
+ *            accumulated): sum over leaves of g_l times the window sums of
+ *            the forward input.  Needs in.
+ *   dbias:   float [cout] or NULL: the column sums of dout.
+ * cin, cout in [1, 256]; n_leaves < 2^31.  ws: at least
+ * oc_conv3x3x3_backward_workspace bytes.  Deterministic: the sums run in a
+ * fixed order.
+ */
+int oc_conv3x3x3_backward(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                          int gw, int64_t n_leaves, const float* in, int cin, const float* weight,
+                          int cout, const float* dout, float* din, float* dweight, float* dbias,
+                          void* ws, size_t ws_bytes, void* stream);
+
+/* Gradient of oc_pool2_max (Eq. 10).  Arguments as oc_pool2_max; in is the
+ * forward input, dout [out leaves][c], din [in leaves][c] (every row
+ * written).  An output leaf that copies an input leaf passes its gradient
+ * through; one that takes the maximum of 8 unit voxels passes it, channel by
+ * channel, to the first of them (in child order) holding the maximum. */
+int oc_pool2_max_backward(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                          int gw, const float* in, int c, const uint32_t* out_trees,
+                          const int64_t* out_prefix, const float* dout, float* din, void* stream);
+
+/* Gradient of oc_unpool2 (Eq. 12, plain or guided).  Arguments as
+ * oc_unpool2, plus in_n_leaves, the row count of din [in_n_leaves][c]: every
+ * input leaf receives the sum of dout over the output leaves that copy it
+ * (in output row order). */
+int oc_unpool2_backward(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                        int gw, int64_t in_n_leaves, int c, const uint32_t* out_trees,
+                        const int64_t* out_prefix, const float* dout, float* din, void* stream);
+
+/* Gradient of oc_relu given its output: din = dout where out > 0, else 0.
+ * din may alias dout; count 0 does nothing (the pointers may then be NULL). */
+int oc_relu_backward(const float* out, const float* dout, float* din, int64_t count, void* stream);
 
 #ifdef __cplusplus
 }

@@ -359,4 +359,85 @@ int oc_relu(float* data, int64_t count, void* stream) {
   return OC_OK;
 }
 
+int oc_conv3x3x3_backward_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout,
+                                    size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(OC_EINVAL, "oc_conv3x3x3_backward_workspace: null pointer");
+  if (n_trees <= 0 || n_leaves <= 0 || cin <= 0 || cout <= 0)
+    return fail(OC_EINVAL, "oc_conv3x3x3_backward_workspace: non-positive size");
+  *bytes = oci::conv_backward_workspace(n_trees, n_leaves, cin, cout);
+  return OC_OK;
+}
+
+int oc_conv3x3x3_backward(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
+                          int gw, int64_t n_leaves, const float* in, int cin, const float* weight,
+                          int cout, const float* dout, float* din, float* dweight, float* dbias,
+                          void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  const char* who = "oc_conv3x3x3_backward";
+  if (!trees || !prefix || !ws || !dout) return fail(OC_EINVAL, "%s: null pointer", who);
+  if (din && !weight) return fail(OC_EINVAL, "%s: din needs weight", who);
+  if (dweight && !in) return fail(OC_EINVAL, "%s: dweight needs in", who);
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "%s: non-positive dims", who);
+  if (cin <= 0 || cout <= 0 || cin > 256 || cout > 256)
+    return fail(OC_EINVAL, "%s: channels (%d, %d) outside [1,256] x [1,256]", who, cin, cout);
+  if (n_leaves <= 0) return fail(OC_EINVAL, "%s: n_leaves <= 0", who);
+  if (n_leaves >= (1LL << 31)) return fail(OC_EOVERFLOW, "%s: n_leaves >= 2^31", who);
+  const int64_t nt = n_trees_of(n, gd, gh, gw);
+  if (n_leaves > 512 * nt) return fail(OC_EINVAL, "%s: n_leaves > 512 * n_trees", who);
+  const size_t need = oci::conv_backward_workspace(nt, n_leaves, cin, cout);
+  if (ws_bytes < need) return fail(OC_EWORKSPACE, "%s: workspace %zu < %zu", who, ws_bytes, need);
+  if (dweight && !oci::conv_backward_supported(cin, cout))
+    return fail(OC_EINVAL, "%s: no weight-gradient kernel for (%d, %d)", who, cin, cout);
+  oci::ConvBwdArgs a;
+  a.trees = trees; a.prefix = prefix;
+  a.n = n; a.gd = gd; a.gh = gh; a.gw = gw;
+  a.n_trees = nt; a.n_leaves = n_leaves;
+  a.in = in; a.cin = cin; a.weight = weight; a.cout = cout;
+  a.dy = dout; a.dx = din; a.dweight = dweight; a.dbias = dbias;
+  OC_CHECK_HIP(oci::launch_conv_backward(a, ws, as_stream(stream)), who);
+  return OC_OK;
+}
+
+int oc_pool2_max_backward(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                          int gw, const float* in, int c, const uint32_t* out_trees,
+                          const int64_t* out_prefix, const float* dout, float* din, void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !in_prefix || !in || !out_trees || !out_prefix || !dout || !din)
+    return fail(OC_EINVAL, "oc_pool2_max_backward: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0)
+    return fail(OC_EINVAL, "oc_pool2_max_backward: non-positive dims");
+  if ((gd | gh | gw) & 1) return fail(OC_EINVAL, "oc_pool2_max_backward: odd tree grid");
+  OC_CHECK_HIP(oci::launch_pool_max_bwd(in_trees, in_prefix, n, gd, gh, gw, in, c, out_trees,
+                                        out_prefix, dout, din, as_stream(stream)),
+               "oc_pool2_max_backward");
+  return OC_OK;
+}
+
+int oc_unpool2_backward(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd, int gh,
+                        int gw, int64_t in_n_leaves, int c, const uint32_t* out_trees,
+                        const int64_t* out_prefix, const float* dout, float* din, void* stream) {
+  g_last_error.clear();
+  if (!in_trees || !in_prefix || !out_trees || !out_prefix || !dout || !din)
+    return fail(OC_EINVAL, "oc_unpool2_backward: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || c <= 0 || in_n_leaves <= 0)
+    return fail(OC_EINVAL, "oc_unpool2_backward: non-positive dims");
+  if (in_n_leaves > 512 * n_trees_of(n, gd, gh, gw))
+    return fail(OC_EINVAL, "oc_unpool2_backward: in_n_leaves > 512 * n_trees");
+  if (!sizes_ok(n, 2 * gd, 2 * gh, 2 * gw)) return fail(OC_EOVERFLOW, "oc_unpool2_backward: grid too large");
+  OC_CHECK_HIP(oci::launch_unpool_bwd(in_trees, in_prefix, n, gd, gh, gw, in_n_leaves, c, out_trees,
+                                      out_prefix, dout, din, as_stream(stream)),
+               "oc_unpool2_backward");
+  return OC_OK;
+}
+
+int oc_relu_backward(const float* out, const float* dout, float* din, int64_t count, void* stream) {
+  g_last_error.clear();
+  if (count < 0) return fail(OC_EINVAL, "oc_relu_backward: negative count");
+  if (count == 0) return OC_OK;
+  if (!out || !dout || !din) return fail(OC_EINVAL, "oc_relu_backward: null pointer");
+  OC_CHECK_HIP(oci::launch_relu_bwd(out, dout, din, count, as_stream(stream)), "oc_relu_backward");
+  return OC_OK;
+}
+
 }  // extern "C"

@@ -1855,6 +1855,131 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 }
 
 // ---------------------------------------------------------------------------
+// Gradients of the convolution (bias and ReLU excluded).
+//
+// Input gradient.  The forward output of leaf l is (1/|l|) sum over l's
+// voxels v of sum_delta W[1-delta] x(v + delta), so input voxel u receives
+// sum_delta W[1-delta]^T g(u - delta) with g = dy / |l| spread over every
+// voxel of leaf l, and input leaf l' sums that over its |l'| voxels.  With
+// delta' = -delta that is |l'| times the forward convolution, with the
+// flipped and transposed kernel W'[tap] = W[2 - tap]^T, of the leaf features
+// g: the forward kernels compute it between two per-row scalings.
+//
+// Weight gradient.  dW[co][ci][1-delta] = sum over leaves l of
+// (dy_l[co] / |l|) S_delta(l)[ci], S the forward window sums of the input.
+// ---------------------------------------------------------------------------
+
+// w' [cin][cout][27] from w [cout][cin][27]: swap the channel roles, flip the taps.
+__global__ void k_flip_transpose(const float* __restrict__ w, int cin, int cout,
+                                 float* __restrict__ wt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = 27LL * cin * cout;
+  if (i >= total) return;
+  const int tap = (int)(i % 27);
+  const int64_t r = i / 27;
+  const int co = (int)(r % cout), ci = (int)(r / cout);  // wt[ci][co][tap]
+  wt[i] = w[((int64_t)co * cin + ci) * 27 + (26 - tap)];
+}
+
+// dst[row][k] = src[row][k] * |leaf|^(+1 or -1) (edge^3 is a power of two,
+// so both are exact).  In place allowed.
+__global__ void k_scale_rows(const float* src, float* dst, const uint64_t* __restrict__ info,
+                             int64_t n_leaves, int c, int mul) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_leaves * c) return;
+  const int64_t row = i / c;
+  const int sz = cell_of((int)(info[row] & 1023u)).size;
+  const float v = (float)(sz * sz * sz);
+  dst[i] = mul ? src[i] * v : src[i] / v;
+}
+
+// Weight-gradient partials.  Block (x, y) takes leaf chunk x and entry slice
+// y (`slice` entries) of the flattened (delta, ci, co) index: window sums of
+// a tile of tm leaves go to LDS (as in the generic forward kernel), dy / |l|
+// beside them, and each thread accumulates its entries of the slice in LDS
+// over the chunk, in leaf order.  partial: [chunks][27 * cin * cout].
+__global__ void __launch_bounds__(kThreads) k_conv_wgrad(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+    const uint64_t* __restrict__ info, int64_t n_leaves, int gd, int gh, int gw,
+    const float* __restrict__ in, int cin, const float* __restrict__ dy, int cout, int tm,
+    int slice, float* __restrict__ partial) {
+  extern __shared__ float smem[];
+  Entry* slots_all = reinterpret_cast<Entry*>(smem);
+  int* counts_all = reinterpret_cast<int*>(slots_all + 4 * kSlots);
+  float* acc = reinterpret_cast<float*>(counts_all + 4 * 32);
+  float* sums = acc + slice;
+  float* gs = sums + (int64_t)tm * 27 * cin;
+  const int wv = threadIdx.x >> 6;
+  const int K = 27 * cin;
+  const int64_t n_ent = (int64_t)K * cout;
+  const int64_t e0 = (int64_t)blockIdx.y * slice;
+  const int ne = (int)min((int64_t)slice, n_ent - e0);
+  for (int e = threadIdx.x; e < ne; e += kThreads) acc[e] = 0.f;
+  const int64_t per = (n_leaves + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = min(n_leaves, (int64_t)blockIdx.x * per), hi = min(n_leaves, lo + per);
+  __syncthreads();
+  for (int64_t base = lo; base < hi; base += tm) {
+    const int mt = (int)min((int64_t)tm, hi - base);
+    for (int m = wv; m < mt; m += 4) {
+      const int64_t row = base + m;
+      const LeafGeo g = leaf_geo(info[row], row, gd, gh, gw);
+      window_sums(g, trees, prefix, gd, gh, gw, in, cin, slots_all + wv * kSlots,
+                  counts_all + wv * 32, sums + (int64_t)m * K);
+      const float inv = 1.f / (float)(g.s * g.s * g.s);
+      for (int co = lane_id(); co < cout; co += 64) gs[m * cout + co] = dy[row * cout + co] * inv;
+      __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < ne; e += kThreads) {
+      const int64_t f = e0 + e;  // (dl, ci, co) flattened, co fastest
+      const int co = (int)(f % cout);
+      const int k = (int)(f / cout);  // dl * cin + ci
+      float a = acc[e];
+      for (int m = 0; m < mt; ++m) a = fmaf(sums[(int64_t)m * K + k], gs[m * cout + co], a);
+      acc[e] = a;
+    }
+    __syncthreads();  // the next tile reuses the LDS
+  }
+  float* dst = partial + (int64_t)blockIdx.x * n_ent + e0;
+  for (int e = threadIdx.x; e < ne; e += kThreads) dst[e] = acc[e];
+}
+
+// dw[co][ci][26 - dl] = sum over chunks, in chunk order, of the partials.
+__global__ void k_wgrad_reduce(const float* __restrict__ partial, int chunks, int cin, int cout,
+                               float* __restrict__ dw) {
+  const int64_t f = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n_ent = 27LL * cin * cout;
+  if (f >= n_ent) return;
+  float a = 0.f;
+  for (int x = 0; x < chunks; ++x) a += partial[(int64_t)x * n_ent + f];
+  const int co = (int)(f % cout);
+  const int k = (int)(f / cout);
+  const int dl = k / cin, ci = k % cin;
+  dw[((int64_t)co * cin + ci) * 27 + (26 - dl)] = a;
+}
+
+// Column sums of dy over row chunks (bias gradient), then over chunks in order.
+__global__ void k_colsum_partial(const float* __restrict__ dy, int64_t n_rows, int c,
+                                 float* __restrict__ partial) {
+  const int64_t per = (n_rows + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per, hi = min(n_rows, lo + per);
+  for (int co = threadIdx.x; co < c; co += blockDim.x) {
+    float a = 0.f;
+    for (int64_t r = lo; r < hi; ++r) a += dy[r * c + co];
+    partial[(int64_t)blockIdx.x * c + co] = a;
+  }
+}
+
+__global__ void k_colsum_reduce(const float* __restrict__ partial, int chunks, int c,
+                                float* __restrict__ out) {
+  const int co = blockIdx.x * blockDim.x + threadIdx.x;
+  if (co >= c) return;
+  float a = 0.f;
+  for (int x = 0; x < chunks; ++x) a += partial[(int64_t)x * c + co];
+  out[co] = a;
+}
+
+// ---------------------------------------------------------------------------
 // Instantiated channel pairs.
 // ---------------------------------------------------------------------------
 typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, const float*,
@@ -2199,6 +2324,158 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
       e = launch_cells(2, t0, t1);
       if (e != hipSuccess) return e;
     }
+  }
+  return hipGetLastError();
+}
+
+}  // namespace oci
+
+// ---------------------------------------------------------------------------
+// Convolution gradients.  Workspace: leaf_info, w', the rows g = dy / |l|,
+// the forward workspace of the (cout -> cin) convolution, weight-gradient
+// and bias partials.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr int kBiasChunks = 256;  // row chunks of the bias gradient
+
+// Leaf chunks of the weight gradient: one per compute unit, fewer when the
+// partials ([chunks][27 cin cout] floats) would pass 64 MB.
+int wgrad_chunks(int cin, int cout) {
+  const int64_t n_ent = 27LL * cin * cout;
+  int64_t c = (16LL << 20) / n_ent;
+  if (c > 256) c = 256;
+  if (c < 8) c = 8;
+  return (int)c;
+}
+
+struct BwdWs {
+  uint64_t* info;
+  float* wt;
+  float* g;
+  float* wpart;
+  float* bpart;
+  void* fws;
+  size_t fws_bytes;
+  size_t total;
+};
+
+BwdWs carve_bwd(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
+  char* p = static_cast<char*>(base);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    char* q = p ? p + off : nullptr;
+    off += oci::align256(bytes);
+    return q;
+  };
+  BwdWs w;
+  w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
+  w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
+  w.g = reinterpret_cast<float*>(take(sizeof(float) * (size_t)n_leaves * cout));
+  w.wpart = reinterpret_cast<float*>(
+      take(sizeof(float) * (size_t)wgrad_chunks(cin, cout) * 27 * (size_t)cin * cout));
+  w.bpart = reinterpret_cast<float*>(take(sizeof(float) * (size_t)kBiasChunks * cout));
+  w.fws_bytes = oci::conv_workspace(n_trees, n_leaves, cout, cin);
+  w.fws = take(w.fws_bytes);
+  w.total = off + 256;
+  return w;
+}
+
+// LDS plan of k_conv_wgrad: shell entries, the accumulator slice, and tm
+// rows of window sums and scaled dy.  The slice takes what leaves at least
+// 8 rows (or the whole entry range when that fits); tm then takes the rest.
+struct WgradPlan {
+  int tm, slice, slices;
+  size_t smem;
+};
+
+WgradPlan wgrad_plan(int cin, int cout, size_t budget) {
+  WgradPlan pl{0, 0, 0, 0};
+  const size_t fixed = sizeof(Entry) * 4 * kSlots + sizeof(int) * 4 * 32;
+  const size_t per = sizeof(float) * (27 * (size_t)cin + cout);
+  const int64_t n_ent = 27LL * cin * cout;
+  if (budget < fixed + per + sizeof(float) * kThreads) return pl;
+  int64_t room = (int64_t)((budget - fixed) / sizeof(float));
+  int64_t want = room - 8 * (int64_t)(per / sizeof(float));
+  if (want < kThreads) want = kThreads;
+  int64_t slice = n_ent < want ? n_ent : want;
+  const int64_t slices = (n_ent + slice - 1) / slice;
+  slice = (n_ent + slices - 1) / slices;
+  const int64_t left = room - slice;
+  int64_t tm = left / (int64_t)(per / sizeof(float));
+  if (tm > 32) tm = 32;
+  if (tm < 1) return pl;
+  pl.tm = (int)tm;
+  pl.slice = (int)slice;
+  pl.slices = (int)slices;
+  pl.smem = fixed + sizeof(float) * ((size_t)slice + (size_t)tm * (27 * (size_t)cin + cout));
+  return pl;
+}
+}  // namespace
+
+namespace oci {
+
+size_t conv_backward_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout) {
+  return carve_bwd(nullptr, n_trees, n_leaves, cin, cout).total;
+}
+
+bool conv_backward_supported(int cin, int cout) {
+  const size_t limit = device_limits() == hipSuccess ? g_max_smem : 160 * 1024;
+  return wgrad_plan(cin, cout, limit).tm >= 1;
+}
+
+hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
+  hipError_t e = init_slots();
+  if (e != hipSuccess) return e;
+  const BwdWs w = carve_bwd(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
+  e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
+  if (e != hipSuccess) return e;
+  const int64_t nyc = a.n_leaves * a.cout, nxc = a.n_leaves * a.cin;
+  if (a.dx) {
+    // |l'| * conv_{W'}(dy / |l|): the forward convolution from cout to cin
+    // channels with the flipped, transposed kernel.
+    const int64_t nw = 27LL * a.cin * a.cout;
+    hipLaunchKernelGGL(k_flip_transpose, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
+                       a.weight, a.cin, a.cout, w.wt);
+    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nyc + 255) / 256)), dim3(256), 0, s, a.dy,
+                       w.g, (const uint64_t*)w.info, a.n_leaves, a.cout, 0);
+    ConvArgs f;
+    f.trees = a.trees; f.prefix = a.prefix;
+    f.n = a.n; f.gd = a.gd; f.gh = a.gh; f.gw = a.gw;
+    f.n_trees = a.n_trees; f.n_leaves = a.n_leaves;
+    f.in = w.g; f.cin = a.cout; f.weight = w.wt; f.bias = nullptr; f.cout = a.cin;
+    f.relu = 0; f.out = a.dx;
+    e = launch_conv_prepare(f, w.fws, s);
+    if (e != hipSuccess) return e;
+    e = launch_conv_execute(f, w.fws, conv_mfma_supported(a.cout, a.cin) ? 2 : 1, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nxc + 255) / 256)), dim3(256), 0, s,
+                       (const float*)a.dx, a.dx, (const uint64_t*)w.info, a.n_leaves, a.cin, 1);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.dweight) {
+    e = device_limits();
+    if (e != hipSuccess) return e;
+    const WgradPlan pl = wgrad_plan(a.cin, a.cout, g_max_smem);
+    if (pl.tm < 1) return hipErrorInvalidConfiguration;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_wgrad),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.smem);
+    if (e != hipSuccess) return e;
+    const int chunks = wgrad_chunks(a.cin, a.cout);
+    const int64_t n_ent = 27LL * a.cin * a.cout;
+    hipLaunchKernelGGL(k_conv_wgrad, dim3(chunks, pl.slices), dim3(kThreads), pl.smem, s, a.trees,
+                       a.prefix, (const uint64_t*)w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin,
+                       a.dy, a.cout, pl.tm, pl.slice, w.wpart);
+    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((n_ent + 255) / 256)), dim3(256), 0, s,
+                       (const float*)w.wpart, chunks, a.cin, a.cout, a.dweight);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (a.dbias) {
+    hipLaunchKernelGGL(k_colsum_partial, dim3(kBiasChunks), dim3(64), 0, s, a.dy, a.n_leaves,
+                       a.cout, w.bpart);
+    hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)((a.cout + 63) / 64)), dim3(64), 0, s,
+                       (const float*)w.bpart, kBiasChunks, a.cout, a.dbias);
   }
   return hipGetLastError();
 }

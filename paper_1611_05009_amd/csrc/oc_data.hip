@@ -258,6 +258,147 @@ __global__ void k_relu_scalar(float* __restrict__ x, int64_t count) {
     x[i] = fmaxf(x[i], 0.f);
 }
 
+// ---------------------------------------------------------------------------
+// Gradients of pooling, unpooling and ReLU.
+// ---------------------------------------------------------------------------
+
+// Gradient of Eq. 10: an output leaf that copies one input leaf passes dy to
+// it; one that takes the maximum of 8 unit voxels passes dy, per channel, to
+// the first voxel (in child order) holding the maximum and 0 to the others.
+// Every input leaf has exactly one output leaf, so every row of din is
+// written once.  One wave per output tree, as the forward kernel.
+__global__ void __launch_bounds__(256) k_pool_max_bwd(
+    const uint32_t* __restrict__ in_trees, const int64_t* __restrict__ in_prefix, int64_t n_out,
+    int gd, int gh, int gw, const float* __restrict__ in, int c,
+    const uint32_t* __restrict__ out_trees, const int64_t* __restrict__ out_prefix,
+    const float* __restrict__ dy, float* __restrict__ din) {
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= n_out) return;
+  const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
+  const Bits ob = load_bits(out_trees, t);
+  const int64_t row0 = out_prefix[t];
+  int base = 0;
+  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+    const int i = c0 + lane_id();
+    const bool leaf = i < kNodes && is_leaf(ob, i);
+    uint64_t m = __ballot(leaf);
+    const int nleaf = __popcll(m);
+    int64_t orow = 0, srow = 0;
+    int nmax = 1;
+    if (leaf) {
+      orow = row0 + base + __popcll(m & lanemask_lt());
+      int o, node;
+      if (i < 9) {
+        o = i - 1; node = 0;
+      } else if (i < 73) {
+        o = (i - 9) >> 3; node = 1 + ((i - 9) & 7);
+      } else {
+        o = (i - 73) >> 6; node = 9 + ((i - 73) & 63);
+      }
+      const int64_t ti = ((p.n * gd + 2 * p.d + ((o >> 2) & 1)) * gh + 2 * p.h + ((o >> 1) & 1)) * gw +
+                         2 * p.w + (o & 1);
+      const Bits ib = load_bits(in_trees, ti);
+      if (node >= 9 && bit(ib, node)) {
+        node = 8 * node + 1;
+        nmax = 8;
+      }
+      srow = in_prefix[ti] + data_idx(ib, node);
+    }
+    while (m) {
+      const int j = __ffsll((unsigned long long)m) - 1;
+      m &= m - 1;
+      const int64_t orj = __shfl(orow, j, 64);
+      const int64_t srj = __shfl(srow, j, 64);
+      const int nm = __shfl(nmax, j, 64);
+      for (int k = lane_id(); k < c; k += 64) {
+        const float g = dy[orj * c + k];
+        if (nm == 1) {
+          din[srj * c + k] = g;
+        } else {
+          const float* sx = in + srj * c + k;
+          float v = sx[0];
+          int arg = 0;
+          for (int r = 1; r < 8; ++r) {
+            const float x = sx[(int64_t)r * c];
+            if (x > v) { v = x; arg = r; }
+          }
+          for (int r = 0; r < 8; ++r) din[(srj + r) * c + k] = r == arg ? g : 0.f;
+        }
+      }
+    }
+    base += nleaf;
+  }
+}
+
+// Gradient of Eq. 12 (plain or guided): every input leaf receives the sum of
+// dy over the output leaves that copy it.  One wave per input tree walks its
+// 8 output trees in row order, as the forward kernel, and adds each output
+// row into its source row; the wave owns every source row it touches, so the
+// sums need no atomics and come out in the same order on every run.  din
+// must be zero on entry.
+__global__ void __launch_bounds__(256) k_unpool_bwd(
+    const uint32_t* __restrict__ in_trees, const int64_t* __restrict__ in_prefix, int64_t n_in,
+    int gd, int gh, int gw, int c, const uint32_t* __restrict__ out_trees,
+    const int64_t* __restrict__ out_prefix, const float* __restrict__ dy, float* __restrict__ din) {
+  const int64_t ti = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (ti >= n_in) return;
+  const int lane = lane_id();
+  const TreePos p = tree_pos(ti, gd, gh, gw);
+  const Bits ib = load_bits(in_trees, ti);
+  const int64_t in_row0 = in_prefix[ti];
+  const bool in_split = (ib.lo & 1ull) != 0;
+  const int Gh = 2 * gh, Gw = 2 * gw, Gd = 2 * gd;
+  auto add_rows = [&](uint64_t m, int64_t lo, int64_t ls) {
+    while (m) {
+      const int j = __ffsll((unsigned long long)m) - 1;
+      m &= m - 1;
+      const int64_t orj = __shfl(lo, j, 64);
+      const int64_t srj = __shfl(ls, j, 64);
+      for (int k = lane; k < c; k += 64) din[srj * c + k] += dy[orj * c + k];
+    }
+  };
+  for (int o = 0; o < 8; ++o) {
+    const int64_t t = ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw +
+                      2 * p.w + (o & 1);
+    const Bits ob = load_bits(out_trees, t);
+    const int64_t row0 = out_prefix[t];
+    if (!(ob.lo & 1ull)) {  // a single output leaf
+      add_rows(1ull, row0, in_row0 + data_idx(ib, in_split ? 1 + o : 0));
+      continue;
+    }
+    int base = 0;
+    for (int c0 = 1; c0 < kNodes; c0 += 64) {
+      const int i = c0 + lane;
+      const bool leaf = i < kNodes && is_leaf(ob, i);
+      const uint64_t m = __ballot(leaf);
+      int64_t lo = 0, ls = 0;
+      if (leaf) {
+        lo = row0 + base + __popcll(m & lanemask_lt());
+        int node;
+        if (!in_split) node = 0;
+        else if (i < 9) node = 9 + 8 * o + (i - 1);
+        else if (i < 73) node = 73 + 64 * o + (i - 9);
+        else node = 73 + 64 * o + ((i - 73) >> 3);
+        ls = in_row0 + data_idx(ib, node);
+      }
+      add_rows(m, lo, ls);
+      base += __popcll(m);
+    }
+  }
+}
+
+__global__ void k_fill_zero(float* __restrict__ x, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) x[i] = 0.f;
+}
+
+// din = dy where the ReLU output y is positive, else 0.  din may alias dy.
+__global__ void k_relu_bwd(const float* y, const float* dy, float* din, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    din[i] = y[i] > 0.f ? dy[i] : 0.f;
+}
+
 }  // namespace
 
 namespace oci {
@@ -312,6 +453,40 @@ hipError_t launch_relu(float* x, int64_t count, hipStream_t s) {
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_relu, dim3((unsigned)blocks), dim3(256), 0, s, x, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_pool_max_bwd(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                               int gh, int gw, const float* in, int c, const uint32_t* out_trees,
+                               const int64_t* out_prefix, const float* dy, float* din,
+                               hipStream_t s) {
+  const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
+  hipLaunchKernelGGL(k_pool_max_bwd, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix,
+                     no, gd, gh, gw, in, c, out_trees, out_prefix, dy, din);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpool_bwd(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                             int gh, int gw, int64_t in_n_leaves, int c, const uint32_t* out_trees,
+                             const int64_t* out_prefix, const float* dy, float* din,
+                             hipStream_t s) {
+  const int64_t ni = (int64_t)n * gd * gh * gw;
+  const int64_t count = in_n_leaves * c;
+  int64_t zb = (count + 255) / 256;
+  if (zb > 8192) zb = 8192;
+  if (zb < 1) zb = 1;
+  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)zb), dim3(256), 0, s, din, count);
+  hipLaunchKernelGGL(k_unpool_bwd, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
+                     gd, gh, gw, c, out_trees, out_prefix, dy, din);
+  return hipGetLastError();
+}
+
+hipError_t launch_relu_bwd(const float* y, const float* dy, float* din, int64_t count,
+                           hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(k_relu_bwd, dim3((unsigned)blocks), dim3(256), 0, s, y, dy, din, count);
   return hipGetLastError();
 }
 

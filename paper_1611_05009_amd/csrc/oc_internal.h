@@ -45,6 +45,18 @@ hipError_t launch_unpool(const uint32_t* in_trees, const int64_t* in_prefix, int
                          int gw, const float* in, int c, const uint32_t* out_trees,
                          const int64_t* out_prefix, float* out, hipStream_t s);
 hipError_t launch_relu(float* x, int64_t count, hipStream_t s);
+// Gradients (the arguments mirror the forward calls; dy/din are the output
+// and input gradients).  din of the unpool gradient is cleared first.
+hipError_t launch_pool_max_bwd(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                               int gh, int gw, const float* in, int c, const uint32_t* out_trees,
+                               const int64_t* out_prefix, const float* dy, float* din,
+                               hipStream_t s);
+hipError_t launch_unpool_bwd(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
+                             int gh, int gw, int64_t in_n_leaves, int c, const uint32_t* out_trees,
+                             const int64_t* out_prefix, const float* dy, float* din,
+                             hipStream_t s);
+hipError_t launch_relu_bwd(const float* y, const float* dy, float* din, int64_t count,
+                           hipStream_t s);
 
 // Convolution.
 struct ConvArgs {
@@ -67,5 +79,25 @@ bool conv_mfma_supported(int cin, int cout);
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
 // The convolution proper; impl: 1 generic, 2 mfma (caller checked support).
 hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s);
+
+// Convolution gradients (bias and ReLU excluded): any of dx, dweight, dbias
+// may be null.
+struct ConvBwdArgs {
+  const uint32_t* trees;
+  const int64_t* prefix;
+  int n, gd, gh, gw;
+  int64_t n_trees, n_leaves;
+  const float* in;      // forward input [n_leaves][cin] (for dweight)
+  int cin;
+  const float* weight;  // [cout][cin][27] (for dx)
+  int cout;
+  const float* dy;      // [n_leaves][cout]
+  float* dx;            // [n_leaves][cin]
+  float* dweight;       // [cout][cin][27]
+  float* dbias;         // [cout]
+};
+size_t conv_backward_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout);
+bool conv_backward_supported(int cin, int cout);
+hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s);
 
 }  // namespace oci

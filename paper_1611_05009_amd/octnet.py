@@ -54,6 +54,12 @@ SIGNATURES = {
     "oc_unpool2_structure": (_I, [_P, _I, _I, _I, _I, _P, _P, _P, _P, _P, _S, _P]),
     "oc_unpool2": (_I, [_P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P]),
     "oc_relu": (_I, [_P, _L, _P]),
+    "oc_conv3x3x3_backward_workspace": (_I, [_L, _L, _I, _I, _P]),
+    "oc_conv3x3x3_backward": (_I, [_P, _P, _I, _I, _I, _I, _L, _P, _I, _P, _I, _P, _P, _P, _P, _P,
+                                   _S, _P]),
+    "oc_pool2_max_backward": (_I, [_P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
+    "oc_unpool2_backward": (_I, [_P, _P, _I, _I, _I, _I, _L, _I, _P, _P, _P, _P, _P]),
+    "oc_relu_backward": (_I, [_P, _P, _P, _L, _P]),
 }
 
 _lib = None
@@ -320,3 +326,71 @@ def unpool2(g: Octree, data: torch.Tensor, guide: Octree | None = None):
 def relu_(data: torch.Tensor) -> torch.Tensor:
     _check(lib().oc_relu(_ptr(data), data.numel(), _stream()), "oc_relu")
     return data
+
+
+def conv_backward_workspace_bytes(g: Octree, cin: int, cout: int) -> int:
+    nb = ctypes.c_size_t(0)
+    _check(lib().oc_conv3x3x3_backward_workspace(g.n_trees, g.n_leaves, cin, cout, ctypes.byref(nb)),
+           "oc_conv3x3x3_backward_workspace")
+    return nb.value
+
+
+def conv3x3x3_backward(g: Octree, data: torch.Tensor | None, weight: torch.Tensor, dout: torch.Tensor,
+                       need_input: bool = True, need_weight: bool = True, need_bias: bool = True,
+                       ws: torch.Tensor | None = None):
+    """Gradients of conv3x3x3 (without its ReLU) from dout [n_leaves, Cout]:
+    (d input [n_leaves, Cin], d weight [Cout, Cin, 3, 3, 3], d bias [Cout]),
+    None for each one not asked for."""
+    cout, cin = weight.shape[0], weight.shape[1]
+    if tuple(weight.shape) != (cout, cin, 3, 3, 3):
+        raise OctNetError("weight must be [Cout, Cin, 3, 3, 3]")
+    if tuple(dout.shape) != (g.n_leaves, cout):
+        raise OctNetError("dout must be [n_leaves, Cout]")
+    dev = dout.device
+    din = torch.empty((g.n_leaves, cin), dtype=torch.float32, device=dev) if need_input else None
+    dw = torch.empty((cout, cin, 3, 3, 3), dtype=torch.float32, device=dev) if need_weight else None
+    db = torch.empty(cout, dtype=torch.float32, device=dev) if need_bias else None
+    if need_weight and (data is None or tuple(data.shape) != (g.n_leaves, cin)):
+        raise OctNetError("the weight gradient needs the input [n_leaves, Cin]")
+    if ws is None:
+        ws = torch.empty(conv_backward_workspace_bytes(g, cin, cout), dtype=torch.uint8, device=dev)
+    _check(lib().oc_conv3x3x3_backward(_ptr(g.trees), _ptr(g.prefix), *g.dims(), g.n_leaves,
+                                       _ptr(data) if need_weight else None, cin, _ptr(weight), cout,
+                                       _ptr(dout), _ptr(din), _ptr(dw), _ptr(db), _ptr(ws), ws.numel(),
+                                       _stream()), "oc_conv3x3x3_backward")
+    return din, dw, db
+
+
+def pool2_max_backward(g: Octree, data: torch.Tensor, out_g: Octree, dout: torch.Tensor) -> torch.Tensor:
+    """Gradient of pool2_max with respect to its input leaves."""
+    c = data.shape[1]
+    if tuple(dout.shape) != (out_g.n_leaves, c):
+        raise OctNetError("dout must be [out leaves, C]")
+    din = torch.empty((g.n_leaves, c), dtype=torch.float32, device=data.device)
+    _check(lib().oc_pool2_max_backward(_ptr(g.trees), _ptr(g.prefix), *g.dims(), _ptr(data), c,
+                                       _ptr(out_g.trees), _ptr(out_g.prefix), _ptr(dout), _ptr(din),
+                                       _stream()), "oc_pool2_max_backward")
+    return din
+
+
+def unpool2_backward(g: Octree, out_g: Octree, dout: torch.Tensor) -> torch.Tensor:
+    """Gradient of unpool2_data (plain or guided) with respect to its input leaves."""
+    c = dout.shape[1]
+    if dout.shape[0] != out_g.n_leaves:
+        raise OctNetError("dout must be [out leaves, C]")
+    din = torch.empty((g.n_leaves, c), dtype=torch.float32, device=dout.device)
+    _check(lib().oc_unpool2_backward(_ptr(g.trees), _ptr(g.prefix), *g.dims(), g.n_leaves, c,
+                                     _ptr(out_g.trees), _ptr(out_g.prefix), _ptr(dout), _ptr(din),
+                                     _stream()), "oc_unpool2_backward")
+    return din
+
+
+def relu_backward(out: torch.Tensor, dout: torch.Tensor, din: torch.Tensor | None = None) -> torch.Tensor:
+    """dout where the ReLU output is positive, else 0 (din may be dout)."""
+    if out.shape != dout.shape:
+        raise OctNetError("out and dout must have one shape")
+    if din is None:
+        din = torch.empty_like(dout)
+    _check(lib().oc_relu_backward(_ptr(out), _ptr(dout), _ptr(din), dout.numel(), _stream()),
+           "oc_relu_backward")
+    return din
