@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     ap.add_argument("--impl", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--bwd-steps", type=int, default=3,
+                    help="backward passes timed after the forward steps (0: none)")
     ap.add_argument("--cpu-rows", type=int, default=6000,
                     help="leaves in the oracle's timed sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -120,6 +122,37 @@ def cpu_baseline(W, rows_wanted):
         "sample": "conv layer 0 on %d uniformly drawn leaves of %d (%.1f s, fp64, rowmaps built per sample)"
                   % (rows.size, ref.n_leaves, dt),
     }
+
+
+def backward_times(W, steps):
+    """Milliseconds per backward pass of the step's layers, by op (HIP events
+    around each call), after one untimed warmup pass.  Outside the forward's
+    timed region and not part of `value`."""
+    import torch
+    from paper_1611_05009_amd import pipeline
+
+    recs = []
+    g, x = pipeline.run_step(W, recs)
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    dy = torch.randn(x.shape, generator=gen, device="cuda", dtype=torch.float32)
+    pipeline.run_backward(W, recs, dy)
+    torch.cuda.synchronize()
+    evs = []
+
+    def op_timer(name):
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        evs.append((name, s, e))
+        return s, e
+
+    for _ in range(steps):
+        pipeline.run_backward(W, recs, dy, op_timer=op_timer)
+    torch.cuda.synchronize()
+    ms = {}
+    for name, s, e in evs:
+        ms[name] = ms.get(name, 0.0) + s.elapsed_time(e) / steps
+    print("backward timed: %s" % ms, file=sys.stderr, flush=True)
+    return ms
 
 
 def main():
@@ -244,6 +277,8 @@ def main():
             "hbm_frac": nbytes / t_conv / 1e9 / PEAK_HBM_GBS,
         },
     }
+    if args.bwd_steps > 0:
+        out["backward_ms"] = backward_times(W, args.bwd_steps)
     if not args.no_cpu_baseline:
         print("timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_rows)

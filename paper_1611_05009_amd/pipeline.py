@@ -124,3 +124,50 @@ def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: st
         if records is not None:
             records.append(OpRecord(op, g_in, x_in, g, x, p))
     return g, x
+
+
+def run_backward(W: Workload, records: list, dy: torch.Tensor, op_timer=None, trace: list | None = None):
+    """Gradients of one pass, from dy (the gradient of the last output)
+    back through the layer stack recorded by run_step(W, records).  Returns
+    (gradient of the input leaf features, {conv index: (dweight, dbias)}).
+    op_timer(name), as in run_step, brackets each call: "unpool_bwd",
+    "pool_bwd", "relu_bwd", "conv_bwd_input" and "conv_bwd_weight" (the
+    weight and bias gradients).  trace, when given, receives (record,
+    gradient in, gradients out) for each op: out is the input gradient, or
+    (relu-masked gradient, input gradient, dweight, dbias) for a conv."""
+    def timed(name, fn):
+        if op_timer is None:
+            return fn()
+        s, e = op_timer(name)
+        s.record()
+        r = fn()
+        e.record()
+        return r
+
+    grads = {}
+    for rec in reversed(records):
+        if rec.op == "input":
+            break
+        dy_in = dy
+        if rec.op in ("unpool", "unpool_guided"):
+            dy = timed("unpool_bwd", lambda: oc.unpool2_backward(rec.g_in, rec.g_out, dy))
+            out = dy
+        elif rec.op == "pool":
+            dy = timed("pool_bwd", lambda: oc.pool2_max_backward(rec.g_in, rec.x_in, rec.g_out, dy))
+            out = dy
+        elif rec.op == "conv":
+            p = rec.params
+            if p["relu"]:
+                dy = timed("relu_bwd", lambda: oc.relu_backward(rec.x_out, dy))
+            dyc = dy
+            _, dw, db = timed("conv_bwd_weight", lambda: oc.conv3x3x3_backward(
+                rec.g_in, rec.x_in, p["w"], dyc, need_input=False))
+            grads[p["index"]] = (dw, db)
+            dy = timed("conv_bwd_input", lambda: oc.conv3x3x3_backward(
+                rec.g_in, None, p["w"], dyc, need_weight=False, need_bias=False)[0])
+            out = (dyc, dy, dw, db)
+        else:
+            raise ValueError(rec.op)
+        if trace is not None:
+            trace.append((rec, dy_in, out))
+    return dy, grads

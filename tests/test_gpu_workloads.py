@@ -81,3 +81,97 @@ def test_workload_chain(key):
             assert np.array_equal(host(r.x_out)[rows], want.astype(np.float32))
         else:
             raise AssertionError(r.op)
+
+
+def vol_of(info):
+    bits = (info & np.uint64(1023)).astype(np.int64)
+    return np.where(bits == 0, 512.0, np.where(bits < 9, 64.0, np.where(bits < 73, 8.0, 1.0)))
+
+
+def flipped_kernel(w):
+    return np.ascontiguousarray(np.flip(w, axis=(2, 3, 4)).transpose(1, 0, 2, 3, 4))
+
+
+def close_sum(got, want, absum, what):
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    lim = 1e-5 + 1e-4 * (np.abs(want) + absum)
+    bad = np.abs(got - want) > lim
+    assert not bad.any(), "%s: %d/%d out of tolerance" % (what, int(bad.sum()), bad.size)
+
+
+@pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5"])
+def test_workload_backward_chain(key):
+    """The gradients of a full-size pass, op by op in reverse, each checked
+    against the oracle fed the GPU's own gradient into that op: ReLU and pool
+    routing exact, unpool sums in full, the conv input gradient on sampled
+    rows (as |l| times the oracle's forward convolution with the flipped
+    kernel of dy / |l|, an identity pinned on the CPU), the bias gradient as
+    fp64 column sums.  The weight gradient at full size is checked by
+    test_conv_backward_full_size_adjoint."""
+    from paper_1611_05009_amd import pipeline
+    W = pipeline.Workload(key)
+    recs = []
+    g, x = pipeline.run_step(W, recs)
+    gen = torch.Generator(device="cuda").manual_seed(3)
+    dy = torch.randn(x.shape, generator=gen, device="cuda", dtype=torch.float32)
+    trace = []
+    pipeline.run_backward(W, recs, dy, trace=trace)
+    torch.cuda.synchronize()
+    log("workload %s backward: %d ops" % (key, len(trace)))
+    for k, (r, d_in, out) in enumerate(trace):
+        log("  bwd op %d %s" % (k, r.op))
+        gi = ref_grid(r.g_in)
+        di = host(d_in)
+        if r.op == "pool":
+            want = O.pool2_max_bwd(gi, host(r.x_in), di, ref_grid(r.g_out))
+            assert np.array_equal(host(out), want.astype(np.float32))
+        elif r.op in ("unpool", "unpool_guided"):
+            go = ref_grid(r.g_out)
+            want = O.unpool2_bwd(gi, di, go)
+            close_sum(host(out), want, O.unpool2_bwd(gi, np.abs(di), go), "%s unpool bwd" % key)
+        elif r.op == "conv":
+            dyc, dx, dw, db = out
+            dyc_h = host(dyc)
+            if r.params["relu"]:
+                assert np.array_equal(dyc_h, O.relu_bwd(host(r.x_out), di).astype(np.float32))
+            info = O.leaf_info(gi)
+            vol = vol_of(info)
+            rows = sample_rows(gi.n_leaves, info, 1500, seed=100 + k)
+            w = host(r.params["w"])
+            gsc = dyc_h.astype(np.float64) / vol[:, None]
+            want = vol[rows, None] * O.conv3_sampled(gi, gsc, flipped_kernel(w), None, False, rows, info=info)
+            absum = vol[rows, None] * O.conv3_sampled(gi, np.abs(gsc), np.abs(flipped_kernel(w)), None,
+                                                      False, rows, info=info)
+            close_sum(host(dx)[rows], want, absum, "%s conv input gradient" % key)
+            close_sum(host(db), dyc_h.astype(np.float64).sum(0), np.abs(dyc_h).astype(np.float64).sum(0),
+                      "%s bias gradient" % key)
+            assert np.isfinite(host(dw)).all()
+        else:
+            raise AssertionError(r.op)
+
+
+def test_conv_backward_full_size_adjoint():
+    """At the benchmark's full size (256^3 batch 16, 32->32): with
+    y = conv(x) (no bias) and dy = y, the input and weight gradients must
+    satisfy <x, dx> = <w, dw> = <y, y> (Eq. 8 is linear in x and in w), each
+    within 1e-4 relative; the terms of <y, y> are all positive, so the
+    identity is not lost in cancellation."""
+    from paper_1611_05009_amd import octnet as oc
+    from paper_1611_05009_amd import pipeline
+    W = pipeline.Workload("c4")
+    recs = []
+    pipeline.run_step(W, recs)
+    conv = next(r for r in recs if r.op == "conv")
+    x, w = conv.x_in, conv.params["w"]
+    y = oc.conv3x3x3(conv.g_in, x, w)
+    dx, dw, db = oc.conv3x3x3_backward(conv.g_in, x, w, y)
+    torch.cuda.synchronize()
+    yy = float((y.double() ** 2).sum())
+    xdx = float((x.double() * dx.double()).sum())
+    wdw = float((w.double() * dw.double()).sum())
+    log("full-size adjoint: <y,y> %.9g <x,dx> %.9g <w,dw> %.9g" % (yy, xdx, wdw))
+    assert abs(xdx - yy) <= 1e-4 * yy
+    assert abs(wdw - yy) <= 1e-4 * yy
+    s = y.double().sum(0)
+    assert bool(((db.double() - s).abs() <= 1e-4 * (s.abs() + y.double().abs().sum(0))).all())

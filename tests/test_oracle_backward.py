@@ -138,3 +138,32 @@ def test_relu_gradient():
     y = np.array([[-1.0, 0.0, 2.0]])
     dy = np.array([[5.0, 6.0, 7.0]])
     np.testing.assert_array_equal(O.relu_bwd(y, dy), [[0.0, 0.0, 7.0]])
+
+
+def flipped_kernel(w):
+    """W'[ci][co][tap] = W[co][ci][26 - tap]: channels swapped, taps mirrored."""
+    return np.ascontiguousarray(np.flip(w, axis=(2, 3, 4)).transpose(1, 0, 2, 3, 4))
+
+
+def leaf_volumes(g):
+    sizes = {0: 512, 1: 64, 2: 8, 3: 1}
+    bits = (O.leaf_info(g) & np.uint64(1023)).astype(np.int64)
+    depth = np.where(bits == 0, 0, np.where(bits < 9, 1, np.where(bits < 73, 2, 3)))
+    return np.vectorize(sizes.get)(depth).astype(np.float64)
+
+
+@pytest.mark.parametrize("case", STRUCTS)
+def test_input_gradient_is_the_flipped_convolution(case):
+    """The input gradient equals |l'| times the forward convolution with the
+    flipped, channel-swapped kernel of dy / |l|: the form the GPU computes,
+    and the one the full-size checks evaluate on sampled rows."""
+    rng, g = grid_of(case)
+    cin, cout = 3, 4
+    w = rng.standard_normal((cout, cin, 3, 3, 3))
+    dy = rng.standard_normal((g.n_leaves, cout))
+    vol = leaf_volumes(g)
+    via_fwd = vol[:, None] * O.conv3(g, dy / vol[:, None], flipped_kernel(w))
+    np.testing.assert_allclose(via_fwd, O.conv3_bwd_data(g, dy, w), rtol=1e-12, atol=1e-12)
+    rows = np.array([0, g.n_leaves // 2, g.n_leaves - 1])
+    samp = vol[rows, None] * O.conv3_sampled(g, dy / vol[:, None], flipped_kernel(w), None, False, rows)
+    np.testing.assert_allclose(samp, O.conv3_bwd_data(g, dy, w)[rows], rtol=1e-12, atol=1e-12)
