@@ -1902,7 +1902,8 @@ __global__ void __launch_bounds__(kThreads) k_conv_wgrad(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
     const uint64_t* __restrict__ info, int64_t n_leaves, int gd, int gh, int gw,
     const float* __restrict__ in, int cin, const float* __restrict__ dy, int cout, int tm,
-    int slice, float* __restrict__ partial) {
+    int slice, float* __restrict__ partial, const int32_t* __restrict__ rows,
+    const int64_t* __restrict__ meta) {
   extern __shared__ float smem[];
   Entry* slots_all = reinterpret_cast<Entry*>(smem);
   int* counts_all = reinterpret_cast<int*>(slots_all + 4 * kSlots);
@@ -1915,13 +1916,17 @@ __global__ void __launch_bounds__(kThreads) k_conv_wgrad(
   const int64_t e0 = (int64_t)blockIdx.y * slice;
   const int ne = (int)min((int64_t)slice, n_ent - e0);
   for (int e = threadIdx.x; e < ne; e += kThreads) acc[e] = 0.f;
-  const int64_t per = (n_leaves + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = min(n_leaves, (int64_t)blockIdx.x * per), hi = min(n_leaves, lo + per);
+  // With a list: the edge-8 cells with a split neighbour and the edge-4
+  // cells (rows[meta[0] ..), meta[1] + meta[2] of them); else every leaf.
+  const int64_t n_items = rows ? min(meta[1] + meta[2], n_leaves - meta[0]) : n_leaves;
+  const int32_t* list = rows ? rows + meta[0] : nullptr;
+  const int64_t per = (n_items + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = min(n_items, (int64_t)blockIdx.x * per), hi = min(n_items, lo + per);
   __syncthreads();
   for (int64_t base = lo; base < hi; base += tm) {
     const int mt = (int)min((int64_t)tm, hi - base);
     for (int m = wv; m < mt; m += 4) {
-      const int64_t row = base + m;
+      const int64_t row = list ? (int64_t)list[base + m] : base + m;
       const LeafGeo g = leaf_geo(info[row], row, gd, gh, gw);
       window_sums(g, trees, prefix, gd, gh, gw, in, cin, slots_all + wv * kSlots,
                   counts_all + wv * 32, sums + (int64_t)m * K);
@@ -1956,6 +1961,222 @@ __global__ void k_wgrad_reduce(const float* __restrict__ partial, int chunks, in
   const int k = (int)(f / cout);
   const int dl = k / cin, ci = k % cin;
   dw[((int64_t)co * cin + ci) * 27 + (26 - dl)] = a;
+}
+
+// ---------------------------------------------------------------------------
+// Weight gradient on the matrix cores.  dW_delta = sum over items of
+// g_item (x) B_item,delta, the item sum being the K dimension of
+// v_mfma_f32_16x16x4_f32 (4 items per instruction): lane l supplies g of
+// item l/16 at output channel 16 mt + l%16 (A) and B of item l/16 at input
+// channel 16 nt + l%16 (B), and holds D[co = 16 mt + 4 (l/16) + r][ci = 16 nt
+// + l%16] in register r.  The three waves of a workgroup take one layer dd
+// of the offsets each (9 offsets, MT x NT tiles); every workgroup leaves its
+// sums in a partial set [(delta, ci, co)], the layout of the window-sum
+// kernel above, reduced afterwards in a fixed order.
+//
+// Items: the unit voxels and, as 8 voxels sharing one g = dy / 8, the
+// edge-2 cells, both taken as 2^3 blocks whose 4^3 neighbourhood rows give
+// B = x(v + delta) directly; and the edge-8 cells whose 26 neighbouring
+// regions are single leaves, whose window sums are weighted sums of those
+// 27 rows.
+// ---------------------------------------------------------------------------
+typedef float __attribute__((ext_vector_type(4))) wg_f4;
+
+template <int MT, int NT>
+__device__ __forceinline__ void wgrad_store(const wg_f4 (&acc)[9][MT][NT], int dd, int cin,
+                                            int cout, float* __restrict__ dst) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    const int dl = (dd + 1) * 9 + t;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int co = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + (lane & 15);
+          if (co < cout && ci < cin) dst[((int64_t)dl * cin + ci) * cout + co] = acc[t][mt][nt][r];
+        }
+  }
+}
+
+template <int MT, int NT>
+__global__ void __launch_bounds__(192) k_wgrad_blocks(
+    const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups, int64_t n_leaves,
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
+    const int64_t* __restrict__ meta, const float* __restrict__ in, uint32_t in_bytes, int cin,
+    const float* __restrict__ dy, uint32_t dy_bytes, int cout, float* __restrict__ partial) {
+  const int lane = lane_id();
+  const int dd = (int)(threadIdx.x >> 6) - 1;
+  const int q = lane >> 4, c16 = lane & 15;
+  const int64_t ng = min(*n_groups, n_leaves / 8);
+  const int64_t off2 = meta[0] + meta[1] + meta[2];
+  const int64_t nblk = ng + min(meta[3], n_leaves - off2);
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
+  // Position in the 4^3 neighbourhood of the voxel of item slot q in each
+  // half of the block (voxels 4j + q, octant order).
+  int uc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int v = 4 * j + q;
+    uc[j] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
+  }
+  wg_f4 acc[9][MT][NT];
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t b = blockIdx.x; b < nblk; b += gridDim.x) {
+    int nbv;
+    float sc;
+    if (b < ng) {
+      nbv = nbt[64 * b + lane];
+      sc = 1.f;
+    } else {
+      // An edge-2 cell: its depth-2 node fixes the block's position.
+      const int32_t row = brow[off2 + (b - ng)];
+      const uint64_t inf = info[row];
+      const int64_t key = ((int64_t)(inf >> 10) << 6) | (int64_t)((int)(inf & 1023u) - 9);
+      nbv = neighbour_row(trees, prefix, gd, gh, gw, key, lane);
+      sc = 0.125f;
+    }
+    float A[2][MT];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int rv = __shfl(nbv, uc[j], 64);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int co = 16 * mt + c16;
+        const uint32_t off = co < cout ? (uint32_t)rv * (uint32_t)(cout * 4) + (uint32_t)(co * 4) : kOutside;
+        A[j][mt] = gather<1>(rdy, off) * sc;
+      }
+    }
+    float B[9][2][NT];
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int u = uc[j] + dd * 16 + (t / 3 - 1) * 4 + (t % 3 - 1);
+        const int row = __shfl(nbv, u, 64);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int ci = 16 * nt + c16;
+          const uint32_t off = (row < 0 || ci >= cin) ? kOutside
+                                                      : (uint32_t)row * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
+          B[t][j][nt] = gather<1>(rin, off);
+        }
+      }
+#pragma unroll
+    for (int t = 0; t < 9; ++t)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[j][mt], B[t][j][nt], acc[t][mt][nt], 0, 0, 0);
+  }
+  wgrad_store<MT, NT>(acc, dd, cin, cout, partial + (int64_t)blockIdx.x * 27 * cin * cout);
+}
+
+// Edge-8 cells whose face and edge neighbours are unsplit trees: each of the
+// 27 regions around the cell (itself included) is one leaf, so along each
+// axis the window shifted by delta_a overlaps the cell's own span by
+// 8 - |delta_a| voxels and the neighbour on side delta_a by one voxel, and
+// S_delta = sum over regions of the product of those overlaps times the
+// region's row, evaluated axis by axis.
+template <int MT, int NT>
+__global__ void __launch_bounds__(192) k_wgrad_cells8t(
+    const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
+    const int32_t* __restrict__ codes, int64_t ccap, int64_t n_leaves,
+    const float* __restrict__ in, uint32_t in_bytes, int cin, const float* __restrict__ dy,
+    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
+  const int lane = lane_id();
+  const int dd = (int)(threadIdx.x >> 6) - 1;
+  const int q = lane >> 4, c16 = lane & 15;
+  const int64_t n8 = min(min(meta[0], ccap), n_leaves);
+  const int64_t ngrp = (n8 + 3) / 4;
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
+  constexpr float kInv = 1.f / 512.f;
+  const float wd0 = dd == 0 ? 8.f : 7.f;  // overlap with the cell's own span along d
+  wg_f4 acc[9][MT][NT];
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
+  for (int64_t b = blockIdx.x; b < ngrp; b += gridDim.x) {
+    const int64_t j = 4 * b + q;
+    const bool ok = j < n8;
+    const int row = ok ? brow[j] : -1;
+    float A[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int co = 16 * mt + c16;
+      const uint32_t off = (row >= 0 && co < cout) ? (uint32_t)row * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
+                                                   : kOutside;
+      A[mt] = gather<1>(rdy, off) * kInv;
+    }
+    // Rows of the regions in layer 0 (the cell's d span) and layer dd.
+    float X[2][3][3][NT];
+#pragma unroll
+    for (int L = 0; L < 2; ++L)
+#pragma unroll
+      for (int rh = 0; rh < 3; ++rh)
+#pragma unroll
+        for (int rw = 0; rw < 3; ++rw) {
+          const int rd = L == 0 ? 0 : dd;
+          const int r = (rd + 1) * 9 + rh * 3 + rw;
+          int code = -1;
+          if (ok && (L == 0 || dd != 0))
+            code = r == 13 ? row : codes[(int64_t)(r - (r > 13)) * ccap + j];
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const int ci = 16 * nt + c16;
+            const uint32_t off = (code < 0 || ci >= cin)
+                                     ? kOutside
+                                     : (uint32_t)code * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
+            X[L][rh][rw][nt] = gather<1>(rin, off);
+          }
+        }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      // d: the cell's layer weighted by its overlap plus the dd layer.
+      float Y[3][3];
+#pragma unroll
+      for (int rh = 0; rh < 3; ++rh)
+#pragma unroll
+        for (int rw = 0; rw < 3; ++rw) Y[rh][rw] = wd0 * X[0][rh][rw][nt] + X[1][rh][rw][nt];
+      // w: for each offset dw, the own column weighted 8 - |dw| plus column dw.
+      float Z[3][3];  // [rh][dw]
+#pragma unroll
+      for (int rh = 0; rh < 3; ++rh) {
+        Z[rh][0] = 7.f * Y[rh][1] + Y[rh][0];
+        Z[rh][1] = 8.f * Y[rh][1];
+        Z[rh][2] = 7.f * Y[rh][1] + Y[rh][2];
+      }
+#pragma unroll
+      for (int dw = 0; dw < 3; ++dw) {
+        const float s_m = 7.f * Z[1][dw] + Z[0][dw];
+        const float s_0 = 8.f * Z[1][dw];
+        const float s_p = 7.f * Z[1][dw] + Z[2][dw];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          acc[0 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_m, acc[0 + dw][mt][nt], 0, 0, 0);
+          acc[3 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_0, acc[3 + dw][mt][nt], 0, 0, 0);
+          acc[6 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_p, acc[6 + dw][mt][nt], 0, 0, 0);
+        }
+      }
+    }
+  }
+  wgrad_store<MT, NT>(acc, dd, cin, cout, partial + (int64_t)blockIdx.x * 27 * cin * cout);
 }
 
 // Column sums of dy over row chunks (bias gradient), then over chunks in order.
@@ -2348,6 +2569,37 @@ int wgrad_chunks(int cin, int cout) {
   return (int)c;
 }
 
+// The matrix-core weight gradient: input and output channels up to 32, and
+// the neighbourhood tables of the (cout -> cin) forward preparation (built
+// where that direction has an MFMA variant).
+constexpr int kWgBlockGroups = 1024;  // workgroups of the 2^3-block kernel
+constexpr int kWgCellGroups = 256;    // workgroups of the edge-8 kernel
+
+bool wgrad_mfma_ok(int cin, int cout) {
+  return cin <= 32 && cout <= 32 && find_variant(cout, cin) != nullptr;
+}
+
+// Partial sets of the weight gradient, each [27 cin cout].
+int wgrad_sets(int cin, int cout) {
+  return wgrad_chunks(cin, cout) + (wgrad_mfma_ok(cin, cout) ? kWgBlockGroups + kWgCellGroups : 0);
+}
+
+typedef void (*WgBlocksFn)(const int32_t*, const int64_t*, int64_t, const uint32_t*, const int64_t*,
+                           int, int, int, const uint64_t*, const int32_t*, const int64_t*,
+                           const float*, uint32_t, int, const float*, uint32_t, int, float*);
+typedef void (*WgCellsFn)(const int32_t*, const int64_t*, const int32_t*, int64_t, int64_t,
+                          const float*, uint32_t, int, const float*, uint32_t, int, float*);
+
+WgBlocksFn wg_blocks_fn(int mt, int nt) {
+  if (mt == 1) return nt == 1 ? &k_wgrad_blocks<1, 1> : &k_wgrad_blocks<1, 2>;
+  return nt == 1 ? &k_wgrad_blocks<2, 1> : &k_wgrad_blocks<2, 2>;
+}
+
+WgCellsFn wg_cells_fn(int mt, int nt) {
+  if (mt == 1) return nt == 1 ? &k_wgrad_cells8t<1, 1> : &k_wgrad_cells8t<1, 2>;
+  return nt == 1 ? &k_wgrad_cells8t<2, 1> : &k_wgrad_cells8t<2, 2>;
+}
+
 struct BwdWs {
   uint64_t* info;
   float* wt;
@@ -2372,7 +2624,7 @@ BwdWs carve_bwd(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
   w.g = reinterpret_cast<float*>(take(sizeof(float) * (size_t)n_leaves * cout));
   w.wpart = reinterpret_cast<float*>(
-      take(sizeof(float) * (size_t)wgrad_chunks(cin, cout) * 27 * (size_t)cin * cout));
+      take(sizeof(float) * (size_t)wgrad_sets(cin, cout) * 27 * (size_t)cin * cout));
   w.bpart = reinterpret_cast<float*>(take(sizeof(float) * (size_t)kBiasChunks * cout));
   w.fws_bytes = oci::conv_workspace(n_trees, n_leaves, cout, cin);
   w.fws = take(w.fws_bytes);
@@ -2430,22 +2682,30 @@ hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
   e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
   if (e != hipSuccess) return e;
   const int64_t nyc = a.n_leaves * a.cout, nxc = a.n_leaves * a.cin;
-  if (a.dx) {
-    // |l'| * conv_{W'}(dy / |l|): the forward convolution from cout to cin
-    // channels with the flipped, transposed kernel.
+  const uint64_t x_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cin * 4u;
+  const uint64_t y_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cout * 4u;
+  const bool mfma_wg = a.dweight && a.in && wgrad_mfma_ok(a.cin, a.cout) && x_bytes < kOutside &&
+                       y_bytes < kOutside;
+  // The (cout -> cin) forward convolution with the flipped, transposed
+  // kernel: its preparation also builds the structure tables (unit-group
+  // neighbourhoods, cell lists, region codes) the weight gradient reads.
+  ConvArgs f;
+  f.trees = a.trees; f.prefix = a.prefix;
+  f.n = a.n; f.gd = a.gd; f.gh = a.gh; f.gw = a.gw;
+  f.n_trees = a.n_trees; f.n_leaves = a.n_leaves;
+  f.in = w.g; f.cin = a.cout; f.weight = w.wt; f.bias = nullptr; f.cout = a.cin;
+  f.relu = 0; f.out = a.dx;
+  if (a.dx || mfma_wg) {
     const int64_t nw = 27LL * a.cin * a.cout;
     hipLaunchKernelGGL(k_flip_transpose, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
                        a.weight, a.cin, a.cout, w.wt);
-    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nyc + 255) / 256)), dim3(256), 0, s, a.dy,
-                       w.g, (const uint64_t*)w.info, a.n_leaves, a.cout, 0);
-    ConvArgs f;
-    f.trees = a.trees; f.prefix = a.prefix;
-    f.n = a.n; f.gd = a.gd; f.gh = a.gh; f.gw = a.gw;
-    f.n_trees = a.n_trees; f.n_leaves = a.n_leaves;
-    f.in = w.g; f.cin = a.cout; f.weight = w.wt; f.bias = nullptr; f.cout = a.cin;
-    f.relu = 0; f.out = a.dx;
     e = launch_conv_prepare(f, w.fws, s);
     if (e != hipSuccess) return e;
+  }
+  if (a.dx) {
+    // |l'| * conv_{W'}(dy / |l|).
+    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nyc + 255) / 256)), dim3(256), 0, s, a.dy,
+                       w.g, (const uint64_t*)w.info, a.n_leaves, a.cout, 0);
     e = launch_conv_execute(f, w.fws, conv_mfma_supported(a.cout, a.cin) ? 2 : 1, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nxc + 255) / 256)), dim3(256), 0, s,
@@ -2463,11 +2723,35 @@ hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
     if (e != hipSuccess) return e;
     const int chunks = wgrad_chunks(a.cin, a.cout);
     const int64_t n_ent = 27LL * a.cin * a.cout;
+    int sets = chunks;
+    const int32_t* rows = nullptr;
+    const int64_t* meta = nullptr;
+    if (mfma_wg) {
+      // Unit voxels, edge-2 cells and edge-8 cells with unsplit neighbours
+      // on the matrix cores; the other edge-8 and the edge-4 cells by
+      // window sums.
+      const ConvWs fw = carve(w.fws, a.n_trees, a.n_leaves, a.cout, a.cin);
+      const int mt = a.cout > 16 ? 2 : 1, nt = a.cin > 16 ? 2 : 1;
+      float* pb = w.wpart + (int64_t)chunks * n_ent;
+      float* pc = pb + (int64_t)kWgBlockGroups * n_ent;
+      hipLaunchKernelGGL(wg_blocks_fn(mt, nt), dim3(kWgBlockGroups), dim3(192), 0, s,
+                         (const int32_t*)fw.nbt, (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves,
+                         a.trees, a.prefix, a.gd, a.gh, a.gw, (const uint64_t*)w.info,
+                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, a.in, (uint32_t)x_bytes,
+                         a.cin, a.dy, (uint32_t)y_bytes, a.cout, pb);
+      hipLaunchKernelGGL(wg_cells_fn(mt, nt), dim3(kWgCellGroups), dim3(192), 0, s,
+                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, (const int32_t*)fw.codes,
+                         fw.ccap, a.n_leaves, a.in, (uint32_t)x_bytes, a.cin, a.dy, (uint32_t)y_bytes,
+                         a.cout, pc);
+      sets += kWgBlockGroups + kWgCellGroups;
+      rows = fw.brow;
+      meta = fw.meta;
+    }
     hipLaunchKernelGGL(k_conv_wgrad, dim3(chunks, pl.slices), dim3(kThreads), pl.smem, s, a.trees,
                        a.prefix, (const uint64_t*)w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin,
-                       a.dy, a.cout, pl.tm, pl.slice, w.wpart);
+                       a.dy, a.cout, pl.tm, pl.slice, w.wpart, rows, meta);
     hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((n_ent + 255) / 256)), dim3(256), 0, s,
-                       (const float*)w.wpart, chunks, a.cin, a.cout, a.dweight);
+                       (const float*)w.wpart, sets, a.cin, a.cout, a.dweight);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
