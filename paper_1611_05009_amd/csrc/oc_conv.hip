@@ -1882,15 +1882,20 @@ __global__ void k_flip_transpose(const float* __restrict__ w, int cin, int cout,
 }
 
 // dst[row][k] = src[row][k] * |leaf|^(+1 or -1) (edge^3 is a power of two,
-// so both are exact).  In place allowed.
+// so both are exact).  In place allowed.  V channels per thread (c % V == 0).
+template <int V>
 __global__ void k_scale_rows(const float* src, float* dst, const uint64_t* __restrict__ info,
                              int64_t n_leaves, int c, int mul) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n_leaves * c) return;
-  const int64_t row = i / c;
+  const int cv = c / V;
+  if (i >= n_leaves * cv) return;
+  const int64_t row = i / cv;
   const int sz = cell_of((int)(info[row] & 1023u)).size;
-  const float v = (float)(sz * sz * sz);
-  dst[i] = mul ? src[i] * v : src[i] / v;
+  const float f = mul ? (float)(sz * sz * sz) : 1.f / (float)(sz * sz * sz);
+  typedef typename VecT<V>::type T;
+  T v = reinterpret_cast<const T*>(src)[i];
+  v *= f;
+  reinterpret_cast<T*>(dst)[i] = v;
 }
 
 // Weight-gradient partials.  Block (x, y) takes leaf chunk x and entry slice
@@ -2179,15 +2184,147 @@ __global__ void __launch_bounds__(192) k_wgrad_cells8t(
   wgrad_store<MT, NT>(acc, dd, cin, cout, partial + (int64_t)blockIdx.x * 27 * cin * cout);
 }
 
-// Column sums of dy over row chunks (bias gradient), then over chunks in order.
-__global__ void k_colsum_partial(const float* __restrict__ dy, int64_t n_rows, int c,
-                                 float* __restrict__ partial) {
+// Edge-8 cells with a split neighbour and edge-4 cells: the window sums of
+// the forward cell kernel (the cell's own row, region rows and boundary
+// sums of split neighbours, layer by layer), written to LDS per tile of 16
+// cells and read back in the B-operand layout.  Wave jd of a workgroup
+// computes layer jd (offsets delta_d = jd - 1) of every cell of the tile.
+template <int CIN, int SZ, int JD, int PV, int P>
+struct LayerSumsLds {
+  __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
+                                             bool live, __amdgpu_buffer_rsrc_t rin,
+                                             const float* bsum, int choff, float* sl) {
+    using K = CellCfg<CIN, 1>;
+    constexpr int W = PV * K::VEC;
+    if constexpr (P * PV < K::NV) {
+      float xp[W];
+#pragma unroll
+      for (int e = 0; e < W; ++e) xp[e] = xs[P * W + e];
+      float S[9][W];
+      init_layer<SZ, JD>(S, xp);
+      if (live) RegionLayer<0, JD, SZ, CIN, false, PV, P>::run(S, c, rin, bsum, choff);
+#pragma unroll
+      for (int k = 0; k < 9; ++k)
+#pragma unroll
+        for (int i = 0; i < PV; ++i) {
+          typename K::Vec v;
+          if constexpr (K::VEC == 1) v = S[k][i];
+          else {
+#pragma unroll
+            for (int e = 0; e < K::VEC; ++e) v[e] = S[k][K::VEC * i + e];
+          }
+          *reinterpret_cast<typename K::Vec*>(sl + k * CIN + K::VSTRIDE * (P * PV + i) + choff) = v;
+        }
+      __builtin_amdgcn_sched_barrier(0);
+      LayerSumsLds<CIN, SZ, JD, PV, P + 1>::run(c, xs, live, rin, bsum, choff, sl);
+    }
+  }
+};
+
+template <int CIN, int SZ, int MT>
+__global__ void __launch_bounds__(192) k_wgrad_cellr(
+    int64_t n_leaves, const int32_t* __restrict__ brow, const int64_t* __restrict__ meta, int kind,
+    const int32_t* __restrict__ codes, const float* __restrict__ bsum, int64_t ccap,
+    const float* __restrict__ in, uint32_t in_bytes, const float* __restrict__ dy,
+    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
+  using K = CellCfg<CIN, 1>;
+  constexpr int NT = CIN > 16 ? 2 : 1;
+  constexpr int PV = OC_CELLR_PV < K::NV ? OC_CELLR_PV : K::NV;
+  __shared__ float lds[3][16 * 9 * CIN];
+  const int lane = lane_id();
+  const int jd = (int)(threadIdx.x >> 6);
+  float* sw = lds[jd];
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
+  int64_t lbeg, lcnt;
+  kind_range(meta, kind, n_leaves, lbeg, lcnt);
+  const int m = lane % 16, g = lane / 16;
+  const int choff = K::VEC * g;
+  const int q = lane >> 4, c16 = lane & 15;
+  const float inv = 1.f / (float)(SZ * SZ * SZ);
+  wg_f4 acc[9][MT][NT];
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
+  const int64_t n_tiles = (lcnt + 15) / 16;
+  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const int64_t idx = tile * 16 + m;
+    int row = idx < lcnt ? brow[lbeg + idx] : -1;
+    if (row >= n_leaves || lbeg + idx >= ccap) row = -1;  // only a non-canonical structure
+    const int32_t* col = codes + (lbeg + idx);
+    float xs[K::CH];
+    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), xs);
+    int32_t c[27];
+    float* sl = sw + m * 9 * CIN;
+    if (jd == 0) {
+      if (row >= 0) RegionLayer<0, 0, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
+      LayerSumsLds<CIN, SZ, 0, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
+    } else if (jd == 1) {
+      if (row >= 0) RegionLayer<0, 1, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
+      LayerSumsLds<CIN, SZ, 1, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
+    } else {
+      if (row >= 0) RegionLayer<0, 2, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
+      LayerSumsLds<CIN, SZ, 2, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) {
+      const int cc = 4 * i4 + q;  // the cell of this lane's k-slot
+      const int rc = __shfl(row, cc, 64);
+      float A[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int co = 16 * mt + c16;
+        const uint32_t off = (rc >= 0 && co < cout) ? (uint32_t)rc * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
+                                                    : kOutside;
+        A[mt] = gather<1>(rdy, off) * inv;
+      }
+#pragma unroll
+      for (int t = 0; t < 9; ++t)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          const int ci = 16 * nt + c16;
+          const float b = ci < CIN ? sw[(cc * 9 + t) * CIN + ci] : 0.f;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+            acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], b, acc[t][mt][nt], 0, 0, 0);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();  // the next tile rewrites the LDS
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  }
+  wgrad_store<MT, NT>(acc, jd - 1, CIN, cout, partial + (int64_t)blockIdx.x * 27 * CIN * cout);
+}
+
+// Column sums of dy over row chunks (bias gradient), then over chunks in
+// order.  A block takes one chunk: thread t sums column t % c of every
+// (256 / c)-th row (coalesced loads), and the row lanes of a column are
+// added in a fixed order in LDS.
+__global__ void __launch_bounds__(256) k_colsum_partial(const float* __restrict__ dy, int64_t n_rows,
+                                                        int c, float* __restrict__ partial) {
+  __shared__ float red[256];
   const int64_t per = (n_rows + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = (int64_t)blockIdx.x * per, hi = min(n_rows, lo + per);
-  for (int co = threadIdx.x; co < c; co += blockDim.x) {
+  const int64_t lo = min(n_rows, (int64_t)blockIdx.x * per), hi = min(n_rows, lo + per);
+  const int t = threadIdx.x;
+  const int R = c < 256 ? 256 / c : 1;  // row lanes per column
+  for (int c0 = 0; c0 < c; c0 += 256) {
+    const int col = c0 + (R > 1 ? t % c : t);
+    const int rsub = R > 1 ? t / c : 0;
     float a = 0.f;
-    for (int64_t r = lo; r < hi; ++r) a += dy[r * c + co];
-    partial[(int64_t)blockIdx.x * c + co] = a;
+    if (rsub < R && col < c)
+      for (int64_t r = lo + rsub; r < hi; r += R) a += dy[r * c + col];
+    red[t] = a;
+    __syncthreads();
+    if (t < 256 && rsub == 0 && col < c) {
+      float v = red[t];
+      for (int k = 1; k < R; ++k) v += red[t + k * c];
+      partial[(int64_t)blockIdx.x * c + col] = v;
+    }
+    __syncthreads();
   }
 }
 
@@ -2557,7 +2694,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
 // and bias partials.
 // ---------------------------------------------------------------------------
 namespace {
-constexpr int kBiasChunks = 256;  // row chunks of the bias gradient
+constexpr int kBiasChunks = 1024;  // row chunks of the bias gradient
 
 // Leaf chunks of the weight gradient: one per compute unit, fewer when the
 // partials ([chunks][27 cin cout] floats) would pass 64 MB.
@@ -2579,9 +2716,48 @@ bool wgrad_mfma_ok(int cin, int cout) {
   return cin <= 32 && cout <= 32 && find_variant(cout, cin) != nullptr;
 }
 
+constexpr int kWgCellrGroups = 512;  // workgroups of each edge-4/8 window-sum kernel
+
+// The edge-4/8 window-sum kernel is instantiated for these input widths;
+// other widths take those cells through the generic window sums.
+bool wgrad_cellr_ok(int cin) { return cin == 8 || cin == 16 || cin == 32; }
+
 // Partial sets of the weight gradient, each [27 cin cout].
 int wgrad_sets(int cin, int cout) {
-  return wgrad_chunks(cin, cout) + (wgrad_mfma_ok(cin, cout) ? kWgBlockGroups + kWgCellGroups : 0);
+  if (!wgrad_mfma_ok(cin, cout)) return wgrad_chunks(cin, cout);
+  return kWgBlockGroups + kWgCellGroups +
+         (wgrad_cellr_ok(cin) ? 2 * kWgCellrGroups : wgrad_chunks(cin, cout));
+}
+
+typedef void (*WgCellrFn)(int64_t, const int32_t*, const int64_t*, int, const int32_t*, const float*,
+                          int64_t, const float*, uint32_t, const float*, uint32_t, int, float*);
+
+WgCellrFn wg_cellr_fn(int cin, int sz, int mt) {
+#define OC_WG_CELLR(C)                                                              \
+  if (cin == C)                                                                     \
+    return sz == 8 ? (mt == 1 ? &k_wgrad_cellr<C, 8, 1> : &k_wgrad_cellr<C, 8, 2>)  \
+                   : (mt == 1 ? &k_wgrad_cellr<C, 4, 1> : &k_wgrad_cellr<C, 4, 2>);
+  OC_WG_CELLR(8)
+  OC_WG_CELLR(16)
+  OC_WG_CELLR(32)
+#undef OC_WG_CELLR
+  return nullptr;
+}
+
+typedef void (*WgSumsFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
+                         const int64_t*, int64_t, int64_t, const float*, uint32_t, float*,
+                         const int64_t*, const int64_t*, int64_t, int64_t, const uint32_t*);
+
+WgSumsFn wg_sums_fn(int cin) {
+  if (cin == 8) return &k_boundary_sums<8>;
+  if (cin == 16) return &k_boundary_sums<16>;
+  if (cin == 32) return &k_boundary_sums<32>;
+  return nullptr;
+}
+
+// Boundary-sum slots of a structure with n_leaves leaves (as the forward's).
+int64_t slot_cap(int64_t n_trees, int64_t n_leaves) {
+  return n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1;
 }
 
 typedef void (*WgBlocksFn)(const int32_t*, const int64_t*, int64_t, const uint32_t*, const int64_t*,
@@ -2600,12 +2776,26 @@ WgCellsFn wg_cells_fn(int mt, int nt) {
   return nt == 1 ? &k_wgrad_cells8t<2, 1> : &k_wgrad_cells8t<2, 2>;
 }
 
+hipError_t scale_rows(const float* src, float* dst, const uint64_t* info, int64_t n_leaves, int c,
+                      int mul, hipStream_t s) {
+  const bool v4 = c % 4 == 0 && ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
+  const int64_t n = n_leaves * (v4 ? c / 4 : c);
+  if (v4)
+    hipLaunchKernelGGL(k_scale_rows<4>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst,
+                       info, n_leaves, c, mul);
+  else
+    hipLaunchKernelGGL(k_scale_rows<1>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst,
+                       info, n_leaves, c, mul);
+  return hipGetLastError();
+}
+
 struct BwdWs {
   uint64_t* info;
   float* wt;
   float* g;
   float* wpart;
   float* bpart;
+  float* bsum;  // boundary sums of the forward input (cin channels)
   void* fws;
   size_t fws_bytes;
   size_t total;
@@ -2626,6 +2816,9 @@ BwdWs carve_bwd(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout
   w.wpart = reinterpret_cast<float*>(
       take(sizeof(float) * (size_t)wgrad_sets(cin, cout) * 27 * (size_t)cin * cout));
   w.bpart = reinterpret_cast<float*>(take(sizeof(float) * (size_t)kBiasChunks * cout));
+  const bool cellr = wgrad_mfma_ok(cin, cout) && wgrad_cellr_ok(cin);
+  w.bsum = reinterpret_cast<float*>(
+      take(cellr ? sizeof(float) * kSets * (size_t)cin * (size_t)slot_cap(n_trees, n_leaves) : 0));
   w.fws_bytes = oci::conv_workspace(n_trees, n_leaves, cout, cin);
   w.fws = take(w.fws_bytes);
   w.total = off + 256;
@@ -2681,7 +2874,6 @@ hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
   const BwdWs w = carve_bwd(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
   e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
   if (e != hipSuccess) return e;
-  const int64_t nyc = a.n_leaves * a.cout, nxc = a.n_leaves * a.cin;
   const uint64_t x_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cin * 4u;
   const uint64_t y_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cout * 4u;
   const bool mfma_wg = a.dweight && a.in && wgrad_mfma_ok(a.cin, a.cout) && x_bytes < kOutside &&
@@ -2704,59 +2896,85 @@ hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
   }
   if (a.dx) {
     // |l'| * conv_{W'}(dy / |l|).
-    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nyc + 255) / 256)), dim3(256), 0, s, a.dy,
-                       w.g, (const uint64_t*)w.info, a.n_leaves, a.cout, 0);
+    e = scale_rows(a.dy, w.g, w.info, a.n_leaves, a.cout, 0, s);
+    if (e != hipSuccess) return e;
     e = launch_conv_execute(f, w.fws, conv_mfma_supported(a.cout, a.cin) ? 2 : 1, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_scale_rows, dim3((unsigned)((nxc + 255) / 256)), dim3(256), 0, s,
-                       (const float*)a.dx, a.dx, (const uint64_t*)w.info, a.n_leaves, a.cin, 1);
+    e = scale_rows(a.dx, a.dx, w.info, a.n_leaves, a.cin, 1, s);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (a.dweight) {
     e = device_limits();
     if (e != hipSuccess) return e;
-    const WgradPlan pl = wgrad_plan(a.cin, a.cout, g_max_smem);
-    if (pl.tm < 1) return hipErrorInvalidConfiguration;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_wgrad),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.smem);
-    if (e != hipSuccess) return e;
     const int chunks = wgrad_chunks(a.cin, a.cout);
     const int64_t n_ent = 27LL * a.cin * a.cout;
-    int sets = chunks;
-    const int32_t* rows = nullptr;
+    // Partial sets, in reduction order: [2^3 blocks][edge-8 with unsplit
+    // neighbours][the other edge-8 and the edge-4 cells], or only window-sum
+    // chunks when the matrix-core path does not apply.
+    float* part = w.wpart;
+    int sets = 0;
+    const int32_t* rows = nullptr;  // window sums over a list (else every leaf)
     const int64_t* meta = nullptr;
+    bool generic = true;
     if (mfma_wg) {
-      // Unit voxels, edge-2 cells and edge-8 cells with unsplit neighbours
-      // on the matrix cores; the other edge-8 and the edge-4 cells by
-      // window sums.
       const ConvWs fw = carve(w.fws, a.n_trees, a.n_leaves, a.cout, a.cin);
       const int mt = a.cout > 16 ? 2 : 1, nt = a.cin > 16 ? 2 : 1;
-      float* pb = w.wpart + (int64_t)chunks * n_ent;
-      float* pc = pb + (int64_t)kWgBlockGroups * n_ent;
       hipLaunchKernelGGL(wg_blocks_fn(mt, nt), dim3(kWgBlockGroups), dim3(192), 0, s,
                          (const int32_t*)fw.nbt, (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves,
                          a.trees, a.prefix, a.gd, a.gh, a.gw, (const uint64_t*)w.info,
                          (const int32_t*)fw.brow, (const int64_t*)fw.meta, a.in, (uint32_t)x_bytes,
-                         a.cin, a.dy, (uint32_t)y_bytes, a.cout, pb);
+                         a.cin, a.dy, (uint32_t)y_bytes, a.cout, part);
+      part += (int64_t)kWgBlockGroups * n_ent;
       hipLaunchKernelGGL(wg_cells_fn(mt, nt), dim3(kWgCellGroups), dim3(192), 0, s,
                          (const int32_t*)fw.brow, (const int64_t*)fw.meta, (const int32_t*)fw.codes,
                          fw.ccap, a.n_leaves, a.in, (uint32_t)x_bytes, a.cin, a.dy, (uint32_t)y_bytes,
-                         a.cout, pc);
-      sets += kWgBlockGroups + kWgCellGroups;
+                         a.cout, part);
+      part += (int64_t)kWgCellGroups * n_ent;
+      sets = kWgBlockGroups + kWgCellGroups;
       rows = fw.brow;
       meta = fw.meta;
+      if (wgrad_cellr_ok(a.cin)) {
+        // Boundary sums of the input for the split neighbours, then the
+        // edge-8 (kind 1) and edge-4 (kind 2) cells that read them.
+        const int64_t per_block = 4 * (64 / a.cin);
+        int64_t blocks = (a.n_trees + per_block - 1) / per_block;
+        if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
+        hipLaunchKernelGGL(wg_sums_fn(a.cin), dim3((unsigned)blocks), dim3(256), 0, s, a.trees,
+                           a.prefix, (const int32_t*)fw.stl, (const int64_t*)fw.meta,
+                           (const int64_t*)fw.pre[kSlotScan], a.n_trees, fw.cap, a.in,
+                           (uint32_t)x_bytes, w.bsum, (const int64_t*)fw.pre[1],
+                           (const int64_t*)fw.pre[2], (int64_t)0, a.n_trees,
+                           (const uint32_t*)fw.smask);
+        for (int kind = 1; kind <= 2; ++kind) {
+          hipLaunchKernelGGL(wg_cellr_fn(a.cin, kind == 1 ? 8 : 4, mt), dim3(kWgCellrGroups), dim3(192),
+                             0, s, a.n_leaves, (const int32_t*)fw.brow, (const int64_t*)fw.meta, kind,
+                             (const int32_t*)fw.codes, (const float*)w.bsum, fw.ccap, a.in,
+                             (uint32_t)x_bytes, a.dy, (uint32_t)y_bytes, a.cout, part);
+          part += (int64_t)kWgCellrGroups * n_ent;
+        }
+        sets += 2 * kWgCellrGroups;
+        generic = false;
+      }
     }
-    hipLaunchKernelGGL(k_conv_wgrad, dim3(chunks, pl.slices), dim3(kThreads), pl.smem, s, a.trees,
-                       a.prefix, (const uint64_t*)w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin,
-                       a.dy, a.cout, pl.tm, pl.slice, w.wpart, rows, meta);
+    if (generic) {
+      const WgradPlan pl = wgrad_plan(a.cin, a.cout, g_max_smem);
+      if (pl.tm < 1) return hipErrorInvalidConfiguration;
+      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_wgrad),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.smem);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL(k_conv_wgrad, dim3(chunks, pl.slices), dim3(kThreads), pl.smem, s, a.trees,
+                         a.prefix, (const uint64_t*)w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin,
+                         a.dy, a.cout, pl.tm, pl.slice, part, rows, meta);
+      sets += chunks;
+    }
     hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((n_ent + 255) / 256)), dim3(256), 0, s,
                        (const float*)w.wpart, sets, a.cin, a.cout, a.dweight);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (a.dbias) {
-    hipLaunchKernelGGL(k_colsum_partial, dim3(kBiasChunks), dim3(64), 0, s, a.dy, a.n_leaves,
+    hipLaunchKernelGGL(k_colsum_partial, dim3(kBiasChunks), dim3(256), 0, s, a.dy, a.n_leaves,
                        a.cout, w.bpart);
     hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)((a.cout + 63) / 64)), dim3(64), 0, s,
                        (const float*)w.bpart, kBiasChunks, a.cout, a.dbias);
