@@ -594,6 +594,17 @@ __device__ __forceinline__ WaveTiles wave_tiles(int64_t n_tiles) {
   return t;
 }
 
+// The same schedule for workgroups whose waves all work on one tile.
+__device__ __forceinline__ WaveTiles group_tiles(int64_t n_tiles) {
+  const int xcd = blockIdx.x % 8, slot = blockIdx.x / 8, xblocks = gridDim.x / 8;
+  const int64_t per = (n_tiles + 7) / 8;
+  WaveTiles t;
+  t.end = min(n_tiles, (int64_t)(xcd + 1) * per);
+  t.first = (int64_t)xcd * per + slot;
+  t.stride = xblocks;
+  return t;
+}
+
 // Gathers of input rows use raw buffer loads: one resource covers the input
 // (in_bytes valid bytes), offsets are 32-bit, and an offset past the end
 // reads as zero, which is the zero padding outside the grid.
@@ -2006,87 +2017,323 @@ __device__ __forceinline__ void wgrad_store(const wg_f4 (&acc)[9][MT][NT], int d
   }
 }
 
+// Neighbourhood table of the edge-2 cells, as the unit groups' (a cell is a
+// 2^3 block at its depth-2 node): nbt2[64 k + u] for the k < meta[3] cells
+// of the list.  Grid-stride, the count being on the device.
+__global__ void k_edge2_table(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
+                              int gd, int gh, int gw, int64_t n_leaves,
+                              const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
+                              const int64_t* __restrict__ meta, int64_t cap2,
+                              int32_t* __restrict__ nbt2) {
+  const int64_t off2 = meta[0] + meta[1] + meta[2];
+  const int64_t n2 = min(min(meta[3], n_leaves - off2), cap2);
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < 64 * n2; i += stride) {
+    const int32_t row = brow[off2 + (i >> 6)];
+    const uint64_t inf = info[row];
+    const int64_t key = ((int64_t)(inf >> 10) << 6) | (int64_t)((int)(inf & 1023u) - 9);
+    const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, key, (int)(i & 63));
+    nbt2[i] = r < n_leaves ? r : -1;
+  }
+}
+
+// Nine waves per workgroup, wave w taking the offsets delta_d = w / 3 - 1,
+// delta_h = w % 3 - 1 and the three delta_w; all nine read the same block's
+// rows, so they meet in the compute unit's cache.  Software pipeline: the
+// gathers of block i + 1 and the table row of block i + 2 are issued before
+// the MFMAs of block i, so a wave keeps two blocks of loads in flight.
 template <int MT, int NT>
-__global__ void __launch_bounds__(192) k_wgrad_blocks(
+struct BlockOps {
+  float A[2][MT];
+  float B[3][2][NT];
+};
+
+template <int MT, int NT>
+__device__ __forceinline__ void block_gather(BlockOps<MT, NT>& o, int nbv, const int (&uc)[2],
+                                             int dd, int dh, int c16, __amdgpu_buffer_rsrc_t rin,
+                                             int cin, __amdgpu_buffer_rsrc_t rdy, int cout) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int rv = __shfl(nbv, uc[j], 64);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const int co = 16 * mt + c16;
+      const uint32_t off = (rv >= 0 && co < cout) ? (uint32_t)rv * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
+                                                  : kOutside;
+      o.A[j][mt] = gather<1>(rdy, off);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int row = __shfl(nbv, uc[j] + dd * 16 + dh * 4 + (t - 1), 64);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int ci = 16 * nt + c16;
+        const uint32_t off = (row < 0 || ci >= cin) ? kOutside
+                                                    : (uint32_t)row * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
+        o.B[t][j][nt] = gather<1>(rin, off);
+      }
+    }
+}
+
+template <int MT, int NT>
+__global__ void __launch_bounds__(576) k_wgrad_blocks(
     const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups, int64_t n_leaves,
-    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
-    const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, const float* __restrict__ in, uint32_t in_bytes, int cin,
-    const float* __restrict__ dy, uint32_t dy_bytes, int cout, float* __restrict__ partial) {
+    const int32_t* __restrict__ nbt2, const int64_t* __restrict__ meta, int64_t cap2,
+    const float* __restrict__ in, uint32_t in_bytes, int cin, const float* __restrict__ dy,
+    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
   const int lane = lane_id();
-  const int dd = (int)(threadIdx.x >> 6) - 1;
+  const int wv = (int)(threadIdx.x >> 6);
+  const int dd = wv / 3 - 1, dh = wv % 3 - 1;
   const int q = lane >> 4, c16 = lane & 15;
   const int64_t ng = min(*n_groups, n_leaves / 8);
   const int64_t off2 = meta[0] + meta[1] + meta[2];
-  const int64_t nblk = ng + min(meta[3], n_leaves - off2);
+  const int64_t nblk = ng + min(min(meta[3], n_leaves - off2), cap2);
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
-  // Position in the 4^3 neighbourhood of the voxel of item slot q in each
-  // half of the block (voxels 4j + q, octant order).
   int uc[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int v = 4 * j + q;
     uc[j] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
   }
-  wg_f4 acc[9][MT][NT];
+  wg_f4 acc[3][MT][NT];
 #pragma unroll
-  for (int t = 0; t < 9; ++t)
+  for (int t = 0; t < 3; ++t)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  for (int64_t b = blockIdx.x; b < nblk; b += gridDim.x) {
-    int nbv;
-    float sc;
-    if (b < ng) {
-      nbv = nbt[64 * b + lane];
-      sc = 1.f;
-    } else {
-      // An edge-2 cell: its depth-2 node fixes the block's position.
-      const int32_t row = brow[off2 + (b - ng)];
-      const uint64_t inf = info[row];
-      const int64_t key = ((int64_t)(inf >> 10) << 6) | (int64_t)((int)(inf & 1023u) - 9);
-      nbv = neighbour_row(trees, prefix, gd, gh, gw, key, lane);
-      sc = 0.125f;
+  // Table row of block b (clamped into range: a block past the end is
+  // loaded, never used, so the loads need no branch).
+  auto table = [&](int64_t b) {
+    b = b < nblk ? b : nblk - 1;
+    const int32_t* p = b < ng ? nbt + 64 * b : nbt2 + 64 * (b - ng);
+    return p[lane];
+  };
+  const WaveTiles gt = group_tiles(nblk);
+  if (gt.first < gt.end) {
+    BlockOps<MT, NT> cur;
+    block_gather<MT, NT>(cur, table(gt.first), uc, dd, dh, c16, rin, cin, rdy, cout);
+    int nbv_next = table(gt.first + gt.stride);
+    for (int64_t b = gt.first; b < gt.end; b += gt.stride) {
+      BlockOps<MT, NT> nxt;
+      block_gather<MT, NT>(nxt, nbv_next, uc, dd, dh, c16, rin, cin, rdy, cout);
+      nbv_next = table(b + 2 * gt.stride);
+      __builtin_amdgcn_sched_barrier(0);
+      const float sc = b < ng ? 1.f : 0.125f;  // edge-2 cells: g = dy / 8 on each voxel
+#pragma unroll
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+              acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.A[j][mt] * sc, cur.B[t][j][nt],
+                                                                    acc[t][mt][nt], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      cur = nxt;
     }
-    float A[2][MT];
+  }
+  // Offsets (dd, dh, dw) of this wave: dl = 9 (dd + 1) + 3 (dh + 1) + dw + 1.
+  float* dst = partial + (int64_t)blockIdx.x * 27 * cin * cout;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int rv = __shfl(nbv, uc[j], 64);
+  for (int t = 0; t < 3; ++t) {
+    const int dl = 9 * (dd + 1) + 3 * (dh + 1) + t;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int co = 16 * mt + c16;
-        const uint32_t off = co < cout ? (uint32_t)rv * (uint32_t)(cout * 4) + (uint32_t)(co * 4) : kOutside;
-        A[j][mt] = gather<1>(rdy, off) * sc;
-      }
-    }
-    float B[9][2][NT];
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int t = 0; t < 9; ++t)
+      for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int u = uc[j] + dd * 16 + (t / 3 - 1) * 4 + (t % 3 - 1);
-        const int row = __shfl(nbv, u, 64);
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int ci = 16 * nt + c16;
-          const uint32_t off = (row < 0 || ci >= cin) ? kOutside
-                                                      : (uint32_t)row * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
-          B[t][j][nt] = gather<1>(rin, off);
+        for (int r = 0; r < 4; ++r) {
+          const int co = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + (lane & 15);
+          if (co < cout && ci < cin) dst[((int64_t)dl * cin + ci) * cout + co] = acc[t][mt][nt][r];
         }
-      }
+  }
+}
+
+// The same contraction with the block's rows staged through LDS: the
+// workgroup loads a block's 64 neighbourhood rows and its 8 dy rows once
+// (16-byte vectors spread over the threads): at iteration i the rows of
+// blocks i + 2 and i + 3 are in flight in registers, block i + 1 is written
+// to LDS and block i runs on the matrix cores.  Wave w takes the offsets
+// delta_d = w / 3 - 1, delta_h = w % 3 - 1 and the three delta_w, for every
+// output tile.  Channel counts divisible by 4.
+template <int CIN, int COUT>
+struct BlockLds {
+  static constexpr int MT = (COUT + 15) / 16, NT = (CIN + 15) / 16;
+  static constexpr int NW = 9;                                     // waves
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int XS = (CIN / 16) % 2 == 1 ? CIN : CIN + 16;  // row stride (banks)
+  static constexpr int STAGE = 64 * XS + 8 * COUT;                 // floats per stage
+  static constexpr int XT = 16 * CIN;                              // row vectors
+  static constexpr int GT = 2 * COUT;                              // dy vectors
+  static constexpr int V = (XT + GT + THREADS - 1) / THREADS;      // vectors per thread
+  static_assert(CIN % 4 == 0 && COUT % 4 == 0, "16-byte rows");
+  static_assert(XT % 64 == 0, "row and dy vectors in different waves");
+};
+
+template <int CIN, int COUT>
+__global__ void __launch_bounds__((BlockLds<CIN, COUT>::THREADS)) k_wgrad_blocks_lds(
+    const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups, int64_t n_leaves,
+    const int32_t* __restrict__ nbt2, const int64_t* __restrict__ meta, int64_t cap2,
+    const float* __restrict__ in, uint32_t in_bytes, const float* __restrict__ dy,
+    uint32_t dy_bytes, float* __restrict__ partial) {
+  using L = BlockLds<CIN, COUT>;
+  using F4 = typename VecT<4>::type;
+  constexpr int V = L::V;
+  __shared__ float lds[3 * L::STAGE];
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wv = tid >> 6;
+  constexpr int MT = L::MT, NT = L::NT;
+  const int dd = wv / 3 - 1, dh = wv % 3 - 1;
+  const int q = lane >> 4, c16 = lane & 15;
+  const int64_t ng = min(*n_groups, n_leaves / 8);
+  const int64_t off2 = meta[0] + meta[1] + meta[2];
+  const int64_t nblk = ng + min(min(meta[3], n_leaves - off2), cap2);
+  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
+  // Vector i of this thread: id = tid + i THREADS; row u's channels 4k ..
+  // 4k + 3 (id < XT), or the dy row of voxel v (XT <= id < XT + GT).
+  int u_ld[V], k_ld[V], lds_off[V], kind[V];  // kind: 0 row, 1 dy, 2 none
 #pragma unroll
-    for (int t = 0; t < 9; ++t)
+  for (int i = 0; i < V; ++i) {
+    const int id = tid + i * L::THREADS;
+    if (id < L::XT) {
+      kind[i] = 0;
+      u_ld[i] = id / (CIN / 4);
+      k_ld[i] = id % (CIN / 4);
+      lds_off[i] = u_ld[i] * L::XS + 4 * k_ld[i];
+    } else if (id < L::XT + L::GT) {
+      const int t = id - L::XT;
+      const int v = t / (COUT / 4);
+      kind[i] = 1;
+      k_ld[i] = t % (COUT / 4);
+      u_ld[i] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
+      lds_off[i] = 64 * L::XS + v * COUT + 4 * k_ld[i];
+    } else {
+      kind[i] = 2;
+      u_ld[i] = 0;
+      k_ld[i] = 0;
+      lds_off[i] = 0;
+    }
+  }
+  auto table = [&](int64_t b, int (&nb)[V]) {
+    b = b < nblk ? b : nblk - 1;
+    const int32_t* p = b < ng ? nbt + 64 * b : nbt2 + 64 * (b - ng);
+#pragma unroll
+    for (int i = 0; i < V; ++i) nb[i] = p[u_ld[i]];
+  };
+  auto fetch = [&](const int (&nb)[V], F4 (&r)[V]) {
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+      uint32_t off = kOutside;
+      if (kind[i] == 0 && nb[i] >= 0) off = (uint32_t)nb[i] * (uint32_t)(CIN * 4) + (uint32_t)(16 * k_ld[i]);
+      if (kind[i] == 1 && nb[i] >= 0) off = (uint32_t)nb[i] * (uint32_t)(COUT * 4) + (uint32_t)(16 * k_ld[i]);
+      // Row and dy vectors never share a wave (XT is a multiple of 64), so
+      // the resource is chosen per wave.
+      const int first = __builtin_amdgcn_readfirstlane(tid - lane + i * L::THREADS);
+      r[i] = gather<4>(first >= L::XT ? rdy : rin, off);
+    }
+  };
+  auto put = [&](float* stage_base, const F4 (&r)[V]) {
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+      if (kind[i] != 2) *reinterpret_cast<F4*>(stage_base + lds_off[i]) = r[i];
+  };
+  int uc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int v = 4 * j + q;
+    uc[j] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
+  }
+  wg_f4 acc[3][MT][NT];
+#pragma unroll
+  for (int t = 0; t < 3; ++t)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
+  const WaveTiles gt = group_tiles(nblk);
+  if (gt.first < gt.end) {
+    const int64_t st = gt.stride;
+    // Prologue: block 0 to LDS stage 0, blocks 1 and 2 in flight, the table
+    // rows of blocks 3 and 4 loaded.
+    int nb3[V], nb4[V];
+    F4 r1[V], r2[V];
+    table(gt.first, nb3);
+    fetch(nb3, r1);
+    put(lds, r1);
+    table(gt.first + st, nb3);
+    fetch(nb3, r1);
+    table(gt.first + 2 * st, nb4);
+    fetch(nb4, r2);
+    table(gt.first + 3 * st, nb3);
+    table(gt.first + 4 * st, nb4);
+    __syncthreads();
+    int stage = 0;
+    for (int64_t b = gt.first; b < gt.end; b += st) {
+      // Loads of block i + 3, table row of block i + 5, block i + 1 to LDS.
+      F4 rn[V];
+      fetch(nb3, rn);
+#pragma unroll
+      for (int i = 0; i < V; ++i) nb3[i] = nb4[i];
+      table(b + 5 * st, nb4);
+      const int s1 = stage == 2 ? 0 : stage + 1;
+      put(lds + s1 * L::STAGE, r1);
+#pragma unroll
+      for (int i = 0; i < V; ++i) {
+        r1[i] = r2[i];
+        r2[i] = rn[i];
+      }
+      // Block i from stage `stage`.
+      const float* X = lds + stage * L::STAGE;
+      const float* G = X + 64 * L::XS;
+      const float sc = b < ng ? 1.f : 0.125f;  // edge-2 cells: g = dy / 8 on each voxel
+      float A[2][MT];
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+        for (int mt = 0; mt < MT; ++mt) {
+          const int co = 16 * mt + c16;
+          A[j][mt] = co < COUT ? G[(4 * j + q) * COUT + co] * sc : 0.f;
+        }
 #pragma unroll
-          for (int nt = 0; nt < NT; ++nt)
-            acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[j][mt], B[t][j][nt], acc[t][mt][nt], 0, 0, 0);
+      for (int t = 0; t < 3; ++t)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int u = uc[j] + dd * 16 + dh * 4 + (t - 1);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            const int ci = 16 * nt + c16;
+            const float bv = ci < CIN ? X[u * L::XS + ci] : 0.f;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[j][mt], bv, acc[t][mt][nt], 0, 0, 0);
+          }
+        }
+      stage = s1;
+      __syncthreads();  // stage s1 complete; the stage read above is free again
+    }
   }
-  wgrad_store<MT, NT>(acc, dd, cin, cout, partial + (int64_t)blockIdx.x * 27 * cin * cout);
+  float* dst = partial + (int64_t)blockIdx.x * 27 * CIN * COUT;
+#pragma unroll
+  for (int t = 0; t < 3; ++t) {
+    const int dl = 9 * (dd + 1) + 3 * (dh + 1) + t;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int o = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + c16;
+          if (o < COUT && ci < CIN) dst[((int64_t)dl * CIN + ci) * COUT + o] = acc[t][mt][nt][r];
+        }
+  }
 }
 
 // Edge-8 cells whose face and edge neighbours are unsplit trees: each of the
@@ -2117,7 +2364,8 @@ __global__ void __launch_bounds__(192) k_wgrad_cells8t(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  for (int64_t b = blockIdx.x; b < ngrp; b += gridDim.x) {
+  const WaveTiles gt = group_tiles(ngrp);
+  for (int64_t b = gt.first; b < gt.end; b += gt.stride) {
     const int64_t j = 4 * b + q;
     const bool ok = j < n8;
     const int row = ok ? brow[j] : -1;
@@ -2249,8 +2497,8 @@ __global__ void __launch_bounds__(192) k_wgrad_cellr(
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  const int64_t n_tiles = (lcnt + 15) / 16;
-  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+  const WaveTiles gt = group_tiles((lcnt + 15) / 16);
+  for (int64_t tile = gt.first; tile < gt.end; tile += gt.stride) {
     const int64_t idx = tile * 16 + m;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
     if (row >= n_leaves || lbeg + idx >= ccap) row = -1;  // only a non-canonical structure
@@ -2709,7 +2957,7 @@ int wgrad_chunks(int cin, int cout) {
 // The matrix-core weight gradient: input and output channels up to 32, and
 // the neighbourhood tables of the (cout -> cin) forward preparation (built
 // where that direction has an MFMA variant).
-constexpr int kWgBlockGroups = 1024;  // workgroups of the 2^3-block kernel
+constexpr int kWgBlockGroups = 512;   // workgroups of the 2^3-block kernel
 constexpr int kWgCellGroups = 256;    // workgroups of the edge-8 kernel
 
 bool wgrad_mfma_ok(int cin, int cout) {
@@ -2760,11 +3008,31 @@ int64_t slot_cap(int64_t n_trees, int64_t n_leaves) {
   return n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1;
 }
 
-typedef void (*WgBlocksFn)(const int32_t*, const int64_t*, int64_t, const uint32_t*, const int64_t*,
-                           int, int, int, const uint64_t*, const int32_t*, const int64_t*,
-                           const float*, uint32_t, int, const float*, uint32_t, int, float*);
+typedef void (*WgBlocksFn)(const int32_t*, const int64_t*, int64_t, const int32_t*, const int64_t*,
+                           int64_t, const float*, uint32_t, int, const float*, uint32_t, int, float*);
 typedef void (*WgCellsFn)(const int32_t*, const int64_t*, const int32_t*, int64_t, int64_t,
                           const float*, uint32_t, int, const float*, uint32_t, int, float*);
+
+typedef void (*WgBlocksLdsFn)(const int32_t*, const int64_t*, int64_t, const int32_t*, const int64_t*,
+                              int64_t, const float*, uint32_t, const float*, uint32_t, float*);
+
+// The LDS-staged block kernel for (cin, cout), or null.
+WgBlocksLdsFn wg_blocks_lds_fn(int cin, int cout) {
+#define OC_WG_BL(C)                                                     \
+  if (cin == C) {                                                       \
+    if (cout == 4) return &k_wgrad_blocks_lds<C, 4>;                    \
+    if (cout == 8) return &k_wgrad_blocks_lds<C, 8>;                    \
+    if (cout == 16) return &k_wgrad_blocks_lds<C, 16>;                  \
+    if (cout == 32) return &k_wgrad_blocks_lds<C, 32>;                  \
+  }
+  OC_WG_BL(8)
+  OC_WG_BL(16)
+  OC_WG_BL(32)
+#undef OC_WG_BL
+  return nullptr;
+}
+
+int wg_blocks_lds_threads(int, int) { return 576; }
 
 WgBlocksFn wg_blocks_fn(int mt, int nt) {
   if (mt == 1) return nt == 1 ? &k_wgrad_blocks<1, 1> : &k_wgrad_blocks<1, 2>;
@@ -2795,7 +3063,8 @@ struct BwdWs {
   float* g;
   float* wpart;
   float* bpart;
-  float* bsum;  // boundary sums of the forward input (cin channels)
+  float* bsum;    // boundary sums of the forward input (cin channels)
+  int32_t* nbt2;  // neighbourhood rows of the edge-2 cells
   void* fws;
   size_t fws_bytes;
   size_t total;
@@ -2817,6 +3086,9 @@ BwdWs carve_bwd(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout
       take(sizeof(float) * (size_t)wgrad_sets(cin, cout) * 27 * (size_t)cin * cout));
   w.bpart = reinterpret_cast<float*>(take(sizeof(float) * (size_t)kBiasChunks * cout));
   const bool cellr = wgrad_mfma_ok(cin, cout) && wgrad_cellr_ok(cin);
+  // An edge-2 cell is a leaf: at most n_leaves of them.
+  w.nbt2 = reinterpret_cast<int32_t*>(
+      take(wgrad_mfma_ok(cin, cout) ? sizeof(int32_t) * 64 * (size_t)n_leaves : 0));
   w.bsum = reinterpret_cast<float*>(
       take(cellr ? sizeof(float) * kSets * (size_t)cin * (size_t)slot_cap(n_trees, n_leaves) : 0));
   w.fws_bytes = oci::conv_workspace(n_trees, n_leaves, cout, cin);
@@ -2920,11 +3192,21 @@ hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
     if (mfma_wg) {
       const ConvWs fw = carve(w.fws, a.n_trees, a.n_leaves, a.cout, a.cin);
       const int mt = a.cout > 16 ? 2 : 1, nt = a.cin > 16 ? 2 : 1;
-      hipLaunchKernelGGL(wg_blocks_fn(mt, nt), dim3(kWgBlockGroups), dim3(192), 0, s,
-                         (const int32_t*)fw.nbt, (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves,
-                         a.trees, a.prefix, a.gd, a.gh, a.gw, (const uint64_t*)w.info,
-                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, a.in, (uint32_t)x_bytes,
-                         a.cin, a.dy, (uint32_t)y_bytes, a.cout, part);
+      hipLaunchKernelGGL(k_edge2_table, dim3((unsigned)(8 * g_num_cus)), dim3(256), 0, s, a.trees,
+                         a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
+                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, a.n_leaves, w.nbt2);
+      const WgBlocksLdsFn bl = wg_blocks_lds_fn(a.cin, a.cout);
+      if (bl)
+        hipLaunchKernelGGL(bl, dim3(kWgBlockGroups), dim3(wg_blocks_lds_threads(a.cin, a.cout)), 0, s,
+                           (const int32_t*)fw.nbt,
+                           (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves, (const int32_t*)w.nbt2,
+                           (const int64_t*)fw.meta, a.n_leaves, a.in, (uint32_t)x_bytes, a.dy,
+                           (uint32_t)y_bytes, part);
+      else
+        hipLaunchKernelGGL(wg_blocks_fn(mt, nt), dim3(kWgBlockGroups), dim3(576), 0, s,
+                           (const int32_t*)fw.nbt, (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves,
+                           (const int32_t*)w.nbt2, (const int64_t*)fw.meta, a.n_leaves, a.in,
+                           (uint32_t)x_bytes, a.cin, a.dy, (uint32_t)y_bytes, a.cout, part);
       part += (int64_t)kWgBlockGroups * n_ent;
       hipLaunchKernelGGL(wg_cells_fn(mt, nt), dim3(kWgCellGroups), dim3(192), 0, s,
                          (const int32_t*)fw.brow, (const int64_t*)fw.meta, (const int32_t*)fw.codes,
