@@ -1866,726 +1866,6 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 }
 
 // ---------------------------------------------------------------------------
-// Gradients of the convolution (bias and ReLU excluded).
-//
-// Input gradient.  The forward output of leaf l is (1/|l|) sum over l's
-// voxels v of sum_delta W[1-delta] x(v + delta), so input voxel u receives
-// sum_delta W[1-delta]^T g(u - delta) with g = dy / |l| spread over every
-// voxel of leaf l, and input leaf l' sums that over its |l'| voxels.  With
-// delta' = -delta that is |l'| times the forward convolution, with the
-// flipped and transposed kernel W'[tap] = W[2 - tap]^T, of the leaf features
-// g: the forward kernels compute it between two per-row scalings.
-//
-// Weight gradient.  dW[co][ci][1-delta] = sum over leaves l of
-// (dy_l[co] / |l|) S_delta(l)[ci], S the forward window sums of the input.
-// ---------------------------------------------------------------------------
-
-// w' [cin][cout][27] from w [cout][cin][27]: swap the channel roles, flip the taps.
-__global__ void k_flip_transpose(const float* __restrict__ w, int cin, int cout,
-                                 float* __restrict__ wt) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = 27LL * cin * cout;
-  if (i >= total) return;
-  const int tap = (int)(i % 27);
-  const int64_t r = i / 27;
-  const int co = (int)(r % cout), ci = (int)(r / cout);  // wt[ci][co][tap]
-  wt[i] = w[((int64_t)co * cin + ci) * 27 + (26 - tap)];
-}
-
-// dst[row][k] = src[row][k] * |leaf|^(+1 or -1) (edge^3 is a power of two,
-// so both are exact).  In place allowed.  V channels per thread (c % V == 0).
-template <int V>
-__global__ void k_scale_rows(const float* src, float* dst, const uint64_t* __restrict__ info,
-                             int64_t n_leaves, int c, int mul) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int cv = c / V;
-  if (i >= n_leaves * cv) return;
-  const int64_t row = i / cv;
-  const int sz = cell_of((int)(info[row] & 1023u)).size;
-  const float f = mul ? (float)(sz * sz * sz) : 1.f / (float)(sz * sz * sz);
-  typedef typename VecT<V>::type T;
-  T v = reinterpret_cast<const T*>(src)[i];
-  v *= f;
-  reinterpret_cast<T*>(dst)[i] = v;
-}
-
-// Weight-gradient partials.  Block (x, y) takes leaf chunk x and entry slice
-// y (`slice` entries) of the flattened (delta, ci, co) index: window sums of
-// a tile of tm leaves go to LDS (as in the generic forward kernel), dy / |l|
-// beside them, and each thread accumulates its entries of the slice in LDS
-// over the chunk, in leaf order.  partial: [chunks][27 * cin * cout].
-__global__ void __launch_bounds__(kThreads) k_conv_wgrad(
-    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
-    const uint64_t* __restrict__ info, int64_t n_leaves, int gd, int gh, int gw,
-    const float* __restrict__ in, int cin, const float* __restrict__ dy, int cout, int tm,
-    int slice, float* __restrict__ partial, const int32_t* __restrict__ rows,
-    const int64_t* __restrict__ meta) {
-  extern __shared__ float smem[];
-  Entry* slots_all = reinterpret_cast<Entry*>(smem);
-  int* counts_all = reinterpret_cast<int*>(slots_all + 4 * kSlots);
-  float* acc = reinterpret_cast<float*>(counts_all + 4 * 32);
-  float* sums = acc + slice;
-  float* gs = sums + (int64_t)tm * 27 * cin;
-  const int wv = threadIdx.x >> 6;
-  const int K = 27 * cin;
-  const int64_t n_ent = (int64_t)K * cout;
-  const int64_t e0 = (int64_t)blockIdx.y * slice;
-  const int ne = (int)min((int64_t)slice, n_ent - e0);
-  for (int e = threadIdx.x; e < ne; e += kThreads) acc[e] = 0.f;
-  // With a list: the edge-8 cells with a split neighbour and the edge-4
-  // cells (rows[meta[0] ..), meta[1] + meta[2] of them); else every leaf.
-  const int64_t n_items = rows ? min(meta[1] + meta[2], n_leaves - meta[0]) : n_leaves;
-  const int32_t* list = rows ? rows + meta[0] : nullptr;
-  const int64_t per = (n_items + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = min(n_items, (int64_t)blockIdx.x * per), hi = min(n_items, lo + per);
-  __syncthreads();
-  for (int64_t base = lo; base < hi; base += tm) {
-    const int mt = (int)min((int64_t)tm, hi - base);
-    for (int m = wv; m < mt; m += 4) {
-      const int64_t row = list ? (int64_t)list[base + m] : base + m;
-      const LeafGeo g = leaf_geo(info[row], row, gd, gh, gw);
-      window_sums(g, trees, prefix, gd, gh, gw, in, cin, slots_all + wv * kSlots,
-                  counts_all + wv * 32, sums + (int64_t)m * K);
-      const float inv = 1.f / (float)(g.s * g.s * g.s);
-      for (int co = lane_id(); co < cout; co += 64) gs[m * cout + co] = dy[row * cout + co] * inv;
-      __builtin_amdgcn_wave_barrier();
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < ne; e += kThreads) {
-      const int64_t f = e0 + e;  // (dl, ci, co) flattened, co fastest
-      const int co = (int)(f % cout);
-      const int k = (int)(f / cout);  // dl * cin + ci
-      float a = acc[e];
-      for (int m = 0; m < mt; ++m) a = fmaf(sums[(int64_t)m * K + k], gs[m * cout + co], a);
-      acc[e] = a;
-    }
-    __syncthreads();  // the next tile reuses the LDS
-  }
-  float* dst = partial + (int64_t)blockIdx.x * n_ent + e0;
-  for (int e = threadIdx.x; e < ne; e += kThreads) dst[e] = acc[e];
-}
-
-// dw[co][ci][26 - dl] = sum over chunks, in chunk order, of the partials.
-__global__ void k_wgrad_reduce(const float* __restrict__ partial, int chunks, int cin, int cout,
-                               float* __restrict__ dw) {
-  const int64_t f = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t n_ent = 27LL * cin * cout;
-  if (f >= n_ent) return;
-  float a = 0.f;
-  for (int x = 0; x < chunks; ++x) a += partial[(int64_t)x * n_ent + f];
-  const int co = (int)(f % cout);
-  const int k = (int)(f / cout);
-  const int dl = k / cin, ci = k % cin;
-  dw[((int64_t)co * cin + ci) * 27 + (26 - dl)] = a;
-}
-
-// ---------------------------------------------------------------------------
-// Weight gradient on the matrix cores.  dW_delta = sum over items of
-// g_item (x) B_item,delta, the item sum being the K dimension of
-// v_mfma_f32_16x16x4_f32 (4 items per instruction): lane l supplies g of
-// item l/16 at output channel 16 mt + l%16 (A) and B of item l/16 at input
-// channel 16 nt + l%16 (B), and holds D[co = 16 mt + 4 (l/16) + r][ci = 16 nt
-// + l%16] in register r.  The three waves of a workgroup take one layer dd
-// of the offsets each (9 offsets, MT x NT tiles); every workgroup leaves its
-// sums in a partial set [(delta, ci, co)], the layout of the window-sum
-// kernel above, reduced afterwards in a fixed order.
-//
-// Items: the unit voxels and, as 8 voxels sharing one g = dy / 8, the
-// edge-2 cells, both taken as 2^3 blocks whose 4^3 neighbourhood rows give
-// B = x(v + delta) directly; and the edge-8 cells whose 26 neighbouring
-// regions are single leaves, whose window sums are weighted sums of those
-// 27 rows.
-// ---------------------------------------------------------------------------
-typedef float __attribute__((ext_vector_type(4))) wg_f4;
-
-template <int MT, int NT>
-__device__ __forceinline__ void wgrad_store(const wg_f4 (&acc)[9][MT][NT], int dd, int cin,
-                                            int cout, float* __restrict__ dst) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int t = 0; t < 9; ++t) {
-    const int dl = (dd + 1) * 9 + t;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int co = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + (lane & 15);
-          if (co < cout && ci < cin) dst[((int64_t)dl * cin + ci) * cout + co] = acc[t][mt][nt][r];
-        }
-  }
-}
-
-// Neighbourhood table of the edge-2 cells, as the unit groups' (a cell is a
-// 2^3 block at its depth-2 node): nbt2[64 k + u] for the k < meta[3] cells
-// of the list.  Grid-stride, the count being on the device.
-__global__ void k_edge2_table(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
-                              int gd, int gh, int gw, int64_t n_leaves,
-                              const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-                              const int64_t* __restrict__ meta, int64_t cap2,
-                              int32_t* __restrict__ nbt2) {
-  const int64_t off2 = meta[0] + meta[1] + meta[2];
-  const int64_t n2 = min(min(meta[3], n_leaves - off2), cap2);
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < 64 * n2; i += stride) {
-    const int32_t row = brow[off2 + (i >> 6)];
-    const uint64_t inf = info[row];
-    const int64_t key = ((int64_t)(inf >> 10) << 6) | (int64_t)((int)(inf & 1023u) - 9);
-    const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, key, (int)(i & 63));
-    nbt2[i] = r < n_leaves ? r : -1;
-  }
-}
-
-// Nine waves per workgroup, wave w taking the offsets delta_d = w / 3 - 1,
-// delta_h = w % 3 - 1 and the three delta_w; all nine read the same block's
-// rows, so they meet in the compute unit's cache.  Software pipeline: the
-// gathers of block i + 1 and the table row of block i + 2 are issued before
-// the MFMAs of block i, so a wave keeps two blocks of loads in flight.
-template <int MT, int NT>
-struct BlockOps {
-  float A[2][MT];
-  float B[3][2][NT];
-};
-
-template <int MT, int NT>
-__device__ __forceinline__ void block_gather(BlockOps<MT, NT>& o, int nbv, const int (&uc)[2],
-                                             int dd, int dh, int c16, __amdgpu_buffer_rsrc_t rin,
-                                             int cin, __amdgpu_buffer_rsrc_t rdy, int cout) {
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int rv = __shfl(nbv, uc[j], 64);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int co = 16 * mt + c16;
-      const uint32_t off = (rv >= 0 && co < cout) ? (uint32_t)rv * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
-                                                  : kOutside;
-      o.A[j][mt] = gather<1>(rdy, off);
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < 3; ++t)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int row = __shfl(nbv, uc[j] + dd * 16 + dh * 4 + (t - 1), 64);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int ci = 16 * nt + c16;
-        const uint32_t off = (row < 0 || ci >= cin) ? kOutside
-                                                    : (uint32_t)row * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
-        o.B[t][j][nt] = gather<1>(rin, off);
-      }
-    }
-}
-
-template <int MT, int NT>
-__global__ void __launch_bounds__(576) k_wgrad_blocks(
-    const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups, int64_t n_leaves,
-    const int32_t* __restrict__ nbt2, const int64_t* __restrict__ meta, int64_t cap2,
-    const float* __restrict__ in, uint32_t in_bytes, int cin, const float* __restrict__ dy,
-    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
-  const int lane = lane_id();
-  const int wv = (int)(threadIdx.x >> 6);
-  const int dd = wv / 3 - 1, dh = wv % 3 - 1;
-  const int q = lane >> 4, c16 = lane & 15;
-  const int64_t ng = min(*n_groups, n_leaves / 8);
-  const int64_t off2 = meta[0] + meta[1] + meta[2];
-  const int64_t nblk = ng + min(min(meta[3], n_leaves - off2), cap2);
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
-  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
-  int uc[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int v = 4 * j + q;
-    uc[j] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
-  }
-  wg_f4 acc[3][MT][NT];
-#pragma unroll
-  for (int t = 0; t < 3; ++t)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  // Table row of block b (clamped into range: a block past the end is
-  // loaded, never used, so the loads need no branch).
-  auto table = [&](int64_t b) {
-    b = b < nblk ? b : nblk - 1;
-    const int32_t* p = b < ng ? nbt + 64 * b : nbt2 + 64 * (b - ng);
-    return p[lane];
-  };
-  const WaveTiles gt = group_tiles(nblk);
-  if (gt.first < gt.end) {
-    BlockOps<MT, NT> cur;
-    block_gather<MT, NT>(cur, table(gt.first), uc, dd, dh, c16, rin, cin, rdy, cout);
-    int nbv_next = table(gt.first + gt.stride);
-    for (int64_t b = gt.first; b < gt.end; b += gt.stride) {
-      BlockOps<MT, NT> nxt;
-      block_gather<MT, NT>(nxt, nbv_next, uc, dd, dh, c16, rin, cin, rdy, cout);
-      nbv_next = table(b + 2 * gt.stride);
-      __builtin_amdgcn_sched_barrier(0);
-      const float sc = b < ng ? 1.f : 0.125f;  // edge-2 cells: g = dy / 8 on each voxel
-#pragma unroll
-      for (int t = 0; t < 3; ++t)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-              acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.A[j][mt] * sc, cur.B[t][j][nt],
-                                                                    acc[t][mt][nt], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      cur = nxt;
-    }
-  }
-  // Offsets (dd, dh, dw) of this wave: dl = 9 (dd + 1) + 3 (dh + 1) + dw + 1.
-  float* dst = partial + (int64_t)blockIdx.x * 27 * cin * cout;
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int dl = 9 * (dd + 1) + 3 * (dh + 1) + t;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int co = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + (lane & 15);
-          if (co < cout && ci < cin) dst[((int64_t)dl * cin + ci) * cout + co] = acc[t][mt][nt][r];
-        }
-  }
-}
-
-// The same contraction with the block's rows staged through LDS: the
-// workgroup loads a block's 64 neighbourhood rows and its 8 dy rows once
-// (16-byte vectors spread over the threads): at iteration i the rows of
-// blocks i + 2 and i + 3 are in flight in registers, block i + 1 is written
-// to LDS and block i runs on the matrix cores.  Wave w takes the offsets
-// delta_d = w / 3 - 1, delta_h = w % 3 - 1 and the three delta_w, for every
-// output tile.  Channel counts divisible by 4.
-template <int CIN, int COUT>
-struct BlockLds {
-  static constexpr int MT = (COUT + 15) / 16, NT = (CIN + 15) / 16;
-  static constexpr int NW = 9;                                     // waves
-  static constexpr int THREADS = 64 * NW;
-  static constexpr int XS = (CIN / 16) % 2 == 1 ? CIN : CIN + 16;  // row stride (banks)
-  static constexpr int STAGE = 64 * XS + 8 * COUT;                 // floats per stage
-  static constexpr int XT = 16 * CIN;                              // row vectors
-  static constexpr int GT = 2 * COUT;                              // dy vectors
-  static constexpr int V = (XT + GT + THREADS - 1) / THREADS;      // vectors per thread
-  static_assert(CIN % 4 == 0 && COUT % 4 == 0, "16-byte rows");
-  static_assert(XT % 64 == 0, "row and dy vectors in different waves");
-};
-
-template <int CIN, int COUT>
-__global__ void __launch_bounds__((BlockLds<CIN, COUT>::THREADS)) k_wgrad_blocks_lds(
-    const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups, int64_t n_leaves,
-    const int32_t* __restrict__ nbt2, const int64_t* __restrict__ meta, int64_t cap2,
-    const float* __restrict__ in, uint32_t in_bytes, const float* __restrict__ dy,
-    uint32_t dy_bytes, float* __restrict__ partial) {
-  using L = BlockLds<CIN, COUT>;
-  using F4 = typename VecT<4>::type;
-  constexpr int V = L::V;
-  __shared__ float lds[3 * L::STAGE];
-  const int tid = threadIdx.x;
-  const int lane = lane_id();
-  const int wv = tid >> 6;
-  constexpr int MT = L::MT, NT = L::NT;
-  const int dd = wv / 3 - 1, dh = wv % 3 - 1;
-  const int q = lane >> 4, c16 = lane & 15;
-  const int64_t ng = min(*n_groups, n_leaves / 8);
-  const int64_t off2 = meta[0] + meta[1] + meta[2];
-  const int64_t nblk = ng + min(min(meta[3], n_leaves - off2), cap2);
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
-  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
-  // Vector i of this thread: id = tid + i THREADS; row u's channels 4k ..
-  // 4k + 3 (id < XT), or the dy row of voxel v (XT <= id < XT + GT).
-  int u_ld[V], k_ld[V], lds_off[V], kind[V];  // kind: 0 row, 1 dy, 2 none
-#pragma unroll
-  for (int i = 0; i < V; ++i) {
-    const int id = tid + i * L::THREADS;
-    if (id < L::XT) {
-      kind[i] = 0;
-      u_ld[i] = id / (CIN / 4);
-      k_ld[i] = id % (CIN / 4);
-      lds_off[i] = u_ld[i] * L::XS + 4 * k_ld[i];
-    } else if (id < L::XT + L::GT) {
-      const int t = id - L::XT;
-      const int v = t / (COUT / 4);
-      kind[i] = 1;
-      k_ld[i] = t % (COUT / 4);
-      u_ld[i] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
-      lds_off[i] = 64 * L::XS + v * COUT + 4 * k_ld[i];
-    } else {
-      kind[i] = 2;
-      u_ld[i] = 0;
-      k_ld[i] = 0;
-      lds_off[i] = 0;
-    }
-  }
-  auto table = [&](int64_t b, int (&nb)[V]) {
-    b = b < nblk ? b : nblk - 1;
-    const int32_t* p = b < ng ? nbt + 64 * b : nbt2 + 64 * (b - ng);
-#pragma unroll
-    for (int i = 0; i < V; ++i) nb[i] = p[u_ld[i]];
-  };
-  auto fetch = [&](const int (&nb)[V], F4 (&r)[V]) {
-#pragma unroll
-    for (int i = 0; i < V; ++i) {
-      uint32_t off = kOutside;
-      if (kind[i] == 0 && nb[i] >= 0) off = (uint32_t)nb[i] * (uint32_t)(CIN * 4) + (uint32_t)(16 * k_ld[i]);
-      if (kind[i] == 1 && nb[i] >= 0) off = (uint32_t)nb[i] * (uint32_t)(COUT * 4) + (uint32_t)(16 * k_ld[i]);
-      // Row and dy vectors never share a wave (XT is a multiple of 64), so
-      // the resource is chosen per wave.
-      const int first = __builtin_amdgcn_readfirstlane(tid - lane + i * L::THREADS);
-      r[i] = gather<4>(first >= L::XT ? rdy : rin, off);
-    }
-  };
-  auto put = [&](float* stage_base, const F4 (&r)[V]) {
-#pragma unroll
-    for (int i = 0; i < V; ++i)
-      if (kind[i] != 2) *reinterpret_cast<F4*>(stage_base + lds_off[i]) = r[i];
-  };
-  int uc[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int v = 4 * j + q;
-    uc[j] = (1 + (v >> 2)) * 16 + (1 + ((v >> 1) & 1)) * 4 + (1 + (v & 1));
-  }
-  wg_f4 acc[3][MT][NT];
-#pragma unroll
-  for (int t = 0; t < 3; ++t)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  const WaveTiles gt = group_tiles(nblk);
-  if (gt.first < gt.end) {
-    const int64_t st = gt.stride;
-    // Prologue: block 0 to LDS stage 0, blocks 1 and 2 in flight, the table
-    // rows of blocks 3 and 4 loaded.
-    int nb3[V], nb4[V];
-    F4 r1[V], r2[V];
-    table(gt.first, nb3);
-    fetch(nb3, r1);
-    put(lds, r1);
-    table(gt.first + st, nb3);
-    fetch(nb3, r1);
-    table(gt.first + 2 * st, nb4);
-    fetch(nb4, r2);
-    table(gt.first + 3 * st, nb3);
-    table(gt.first + 4 * st, nb4);
-    __syncthreads();
-    int stage = 0;
-    for (int64_t b = gt.first; b < gt.end; b += st) {
-      // Loads of block i + 3, table row of block i + 5, block i + 1 to LDS.
-      F4 rn[V];
-      fetch(nb3, rn);
-#pragma unroll
-      for (int i = 0; i < V; ++i) nb3[i] = nb4[i];
-      table(b + 5 * st, nb4);
-      const int s1 = stage == 2 ? 0 : stage + 1;
-      put(lds + s1 * L::STAGE, r1);
-#pragma unroll
-      for (int i = 0; i < V; ++i) {
-        r1[i] = r2[i];
-        r2[i] = rn[i];
-      }
-      // Block i from stage `stage`.
-      const float* X = lds + stage * L::STAGE;
-      const float* G = X + 64 * L::XS;
-      const float sc = b < ng ? 1.f : 0.125f;  // edge-2 cells: g = dy / 8 on each voxel
-      float A[2][MT];
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const int co = 16 * mt + c16;
-          A[j][mt] = co < COUT ? G[(4 * j + q) * COUT + co] * sc : 0.f;
-        }
-#pragma unroll
-      for (int t = 0; t < 3; ++t)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int u = uc[j] + dd * 16 + dh * 4 + (t - 1);
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const int ci = 16 * nt + c16;
-            const float bv = ci < CIN ? X[u * L::XS + ci] : 0.f;
-#pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[j][mt], bv, acc[t][mt][nt], 0, 0, 0);
-          }
-        }
-      stage = s1;
-      __syncthreads();  // stage s1 complete; the stage read above is free again
-    }
-  }
-  float* dst = partial + (int64_t)blockIdx.x * 27 * CIN * COUT;
-#pragma unroll
-  for (int t = 0; t < 3; ++t) {
-    const int dl = 9 * (dd + 1) + 3 * (dh + 1) + t;
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int o = 16 * mt + 4 * (lane >> 4) + r, ci = 16 * nt + c16;
-          if (o < COUT && ci < CIN) dst[((int64_t)dl * CIN + ci) * COUT + o] = acc[t][mt][nt][r];
-        }
-  }
-}
-
-// Edge-8 cells whose face and edge neighbours are unsplit trees: each of the
-// 27 regions around the cell (itself included) is one leaf, so along each
-// axis the window shifted by delta_a overlaps the cell's own span by
-// 8 - |delta_a| voxels and the neighbour on side delta_a by one voxel, and
-// S_delta = sum over regions of the product of those overlaps times the
-// region's row, evaluated axis by axis.
-template <int MT, int NT>
-__global__ void __launch_bounds__(192) k_wgrad_cells8t(
-    const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
-    const int32_t* __restrict__ codes, int64_t ccap, int64_t n_leaves,
-    const float* __restrict__ in, uint32_t in_bytes, int cin, const float* __restrict__ dy,
-    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
-  const int lane = lane_id();
-  const int dd = (int)(threadIdx.x >> 6) - 1;
-  const int q = lane >> 4, c16 = lane & 15;
-  const int64_t n8 = min(min(meta[0], ccap), n_leaves);
-  const int64_t ngrp = (n8 + 3) / 4;
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
-  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
-  constexpr float kInv = 1.f / 512.f;
-  const float wd0 = dd == 0 ? 8.f : 7.f;  // overlap with the cell's own span along d
-  wg_f4 acc[9][MT][NT];
-#pragma unroll
-  for (int t = 0; t < 9; ++t)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  const WaveTiles gt = group_tiles(ngrp);
-  for (int64_t b = gt.first; b < gt.end; b += gt.stride) {
-    const int64_t j = 4 * b + q;
-    const bool ok = j < n8;
-    const int row = ok ? brow[j] : -1;
-    float A[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      const int co = 16 * mt + c16;
-      const uint32_t off = (row >= 0 && co < cout) ? (uint32_t)row * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
-                                                   : kOutside;
-      A[mt] = gather<1>(rdy, off) * kInv;
-    }
-    // Rows of the regions in layer 0 (the cell's d span) and layer dd.
-    float X[2][3][3][NT];
-#pragma unroll
-    for (int L = 0; L < 2; ++L)
-#pragma unroll
-      for (int rh = 0; rh < 3; ++rh)
-#pragma unroll
-        for (int rw = 0; rw < 3; ++rw) {
-          const int rd = L == 0 ? 0 : dd;
-          const int r = (rd + 1) * 9 + rh * 3 + rw;
-          int code = -1;
-          if (ok && (L == 0 || dd != 0))
-            code = r == 13 ? row : codes[(int64_t)(r - (r > 13)) * ccap + j];
-#pragma unroll
-          for (int nt = 0; nt < NT; ++nt) {
-            const int ci = 16 * nt + c16;
-            const uint32_t off = (code < 0 || ci >= cin)
-                                     ? kOutside
-                                     : (uint32_t)code * (uint32_t)(cin * 4) + (uint32_t)(ci * 4);
-            X[L][rh][rw][nt] = gather<1>(rin, off);
-          }
-        }
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      // d: the cell's layer weighted by its overlap plus the dd layer.
-      float Y[3][3];
-#pragma unroll
-      for (int rh = 0; rh < 3; ++rh)
-#pragma unroll
-        for (int rw = 0; rw < 3; ++rw) Y[rh][rw] = wd0 * X[0][rh][rw][nt] + X[1][rh][rw][nt];
-      // w: for each offset dw, the own column weighted 8 - |dw| plus column dw.
-      float Z[3][3];  // [rh][dw]
-#pragma unroll
-      for (int rh = 0; rh < 3; ++rh) {
-        Z[rh][0] = 7.f * Y[rh][1] + Y[rh][0];
-        Z[rh][1] = 8.f * Y[rh][1];
-        Z[rh][2] = 7.f * Y[rh][1] + Y[rh][2];
-      }
-#pragma unroll
-      for (int dw = 0; dw < 3; ++dw) {
-        const float s_m = 7.f * Z[1][dw] + Z[0][dw];
-        const float s_0 = 8.f * Z[1][dw];
-        const float s_p = 7.f * Z[1][dw] + Z[2][dw];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          acc[0 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_m, acc[0 + dw][mt][nt], 0, 0, 0);
-          acc[3 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_0, acc[3 + dw][mt][nt], 0, 0, 0);
-          acc[6 + dw][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], s_p, acc[6 + dw][mt][nt], 0, 0, 0);
-        }
-      }
-    }
-  }
-  wgrad_store<MT, NT>(acc, dd, cin, cout, partial + (int64_t)blockIdx.x * 27 * cin * cout);
-}
-
-// Edge-8 cells with a split neighbour and edge-4 cells: the window sums of
-// the forward cell kernel (the cell's own row, region rows and boundary
-// sums of split neighbours, layer by layer), written to LDS per tile of 16
-// cells and read back in the B-operand layout.  Wave jd of a workgroup
-// computes layer jd (offsets delta_d = jd - 1) of every cell of the tile.
-template <int CIN, int SZ, int JD, int PV, int P>
-struct LayerSumsLds {
-  __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
-                                             bool live, __amdgpu_buffer_rsrc_t rin,
-                                             const float* bsum, int choff, float* sl) {
-    using K = CellCfg<CIN, 1>;
-    constexpr int W = PV * K::VEC;
-    if constexpr (P * PV < K::NV) {
-      float xp[W];
-#pragma unroll
-      for (int e = 0; e < W; ++e) xp[e] = xs[P * W + e];
-      float S[9][W];
-      init_layer<SZ, JD>(S, xp);
-      if (live) RegionLayer<0, JD, SZ, CIN, false, PV, P>::run(S, c, rin, bsum, choff);
-#pragma unroll
-      for (int k = 0; k < 9; ++k)
-#pragma unroll
-        for (int i = 0; i < PV; ++i) {
-          typename K::Vec v;
-          if constexpr (K::VEC == 1) v = S[k][i];
-          else {
-#pragma unroll
-            for (int e = 0; e < K::VEC; ++e) v[e] = S[k][K::VEC * i + e];
-          }
-          *reinterpret_cast<typename K::Vec*>(sl + k * CIN + K::VSTRIDE * (P * PV + i) + choff) = v;
-        }
-      __builtin_amdgcn_sched_barrier(0);
-      LayerSumsLds<CIN, SZ, JD, PV, P + 1>::run(c, xs, live, rin, bsum, choff, sl);
-    }
-  }
-};
-
-template <int CIN, int SZ, int MT>
-__global__ void __launch_bounds__(192) k_wgrad_cellr(
-    int64_t n_leaves, const int32_t* __restrict__ brow, const int64_t* __restrict__ meta, int kind,
-    const int32_t* __restrict__ codes, const float* __restrict__ bsum, int64_t ccap,
-    const float* __restrict__ in, uint32_t in_bytes, const float* __restrict__ dy,
-    uint32_t dy_bytes, int cout, float* __restrict__ partial) {
-  using K = CellCfg<CIN, 1>;
-  constexpr int NT = CIN > 16 ? 2 : 1;
-  constexpr int PV = OC_CELLR_PV < K::NV ? OC_CELLR_PV : K::NV;
-  __shared__ float lds[3][16 * 9 * CIN];
-  const int lane = lane_id();
-  const int jd = (int)(threadIdx.x >> 6);
-  float* sw = lds[jd];
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
-  const __amdgpu_buffer_rsrc_t rdy = input_rsrc(dy, dy_bytes);
-  int64_t lbeg, lcnt;
-  kind_range(meta, kind, n_leaves, lbeg, lcnt);
-  const int m = lane % 16, g = lane / 16;
-  const int choff = K::VEC * g;
-  const int q = lane >> 4, c16 = lane & 15;
-  const float inv = 1.f / (float)(SZ * SZ * SZ);
-  wg_f4 acc[9][MT][NT];
-#pragma unroll
-  for (int t = 0; t < 9; ++t)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) acc[t][mt][nt] = wg_f4{0.f, 0.f, 0.f, 0.f};
-  const WaveTiles gt = group_tiles((lcnt + 15) / 16);
-  for (int64_t tile = gt.first; tile < gt.end; tile += gt.stride) {
-    const int64_t idx = tile * 16 + m;
-    int row = idx < lcnt ? brow[lbeg + idx] : -1;
-    if (row >= n_leaves || lbeg + idx >= ccap) row = -1;  // only a non-canonical structure
-    const int32_t* col = codes + (lbeg + idx);
-    float xs[K::CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), xs);
-    int32_t c[27];
-    float* sl = sw + m * 9 * CIN;
-    if (jd == 0) {
-      if (row >= 0) RegionLayer<0, 0, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
-      LayerSumsLds<CIN, SZ, 0, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
-    } else if (jd == 1) {
-      if (row >= 0) RegionLayer<0, 1, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
-      LayerSumsLds<CIN, SZ, 1, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
-    } else {
-      if (row >= 0) RegionLayer<0, 2, SZ, CIN, false, 1, 0>::codes(c, col, ccap);
-      LayerSumsLds<CIN, SZ, 2, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, sl);
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-#pragma unroll
-    for (int i4 = 0; i4 < 4; ++i4) {
-      const int cc = 4 * i4 + q;  // the cell of this lane's k-slot
-      const int rc = __shfl(row, cc, 64);
-      float A[MT];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int co = 16 * mt + c16;
-        const uint32_t off = (rc >= 0 && co < cout) ? (uint32_t)rc * (uint32_t)(cout * 4) + (uint32_t)(co * 4)
-                                                    : kOutside;
-        A[mt] = gather<1>(rdy, off) * inv;
-      }
-#pragma unroll
-      for (int t = 0; t < 9; ++t)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt) {
-          const int ci = 16 * nt + c16;
-          const float b = ci < CIN ? sw[(cc * 9 + t) * CIN + ci] : 0.f;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-            acc[t][mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(A[mt], b, acc[t][mt][nt], 0, 0, 0);
-        }
-    }
-    __builtin_amdgcn_wave_barrier();  // the next tile rewrites the LDS
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  }
-  wgrad_store<MT, NT>(acc, jd - 1, CIN, cout, partial + (int64_t)blockIdx.x * 27 * CIN * cout);
-}
-
-// Column sums of dy over row chunks (bias gradient), then over chunks in
-// order.  A block takes one chunk: thread t sums column t % c of every
-// (256 / c)-th row (coalesced loads), and the row lanes of a column are
-// added in a fixed order in LDS.
-__global__ void __launch_bounds__(256) k_colsum_partial(const float* __restrict__ dy, int64_t n_rows,
-                                                        int c, float* __restrict__ partial) {
-  __shared__ float red[256];
-  const int64_t per = (n_rows + gridDim.x - 1) / gridDim.x;
-  const int64_t lo = min(n_rows, (int64_t)blockIdx.x * per), hi = min(n_rows, lo + per);
-  const int t = threadIdx.x;
-  const int R = c < 256 ? 256 / c : 1;  // row lanes per column
-  for (int c0 = 0; c0 < c; c0 += 256) {
-    const int col = c0 + (R > 1 ? t % c : t);
-    const int rsub = R > 1 ? t / c : 0;
-    float a = 0.f;
-    if (rsub < R && col < c)
-      for (int64_t r = lo + rsub; r < hi; r += R) a += dy[r * c + col];
-    red[t] = a;
-    __syncthreads();
-    if (t < 256 && rsub == 0 && col < c) {
-      float v = red[t];
-      for (int k = 1; k < R; ++k) v += red[t + k * c];
-      partial[(int64_t)blockIdx.x * c + col] = v;
-    }
-    __syncthreads();
-  }
-}
-
-__global__ void k_colsum_reduce(const float* __restrict__ partial, int chunks, int c,
-                                float* __restrict__ out) {
-  const int co = blockIdx.x * blockDim.x + threadIdx.x;
-  if (co >= c) return;
-  float a = 0.f;
-  for (int x = 0; x < chunks; ++x) a += partial[(int64_t)x * c + co];
-  out[co] = a;
-}
-
-// ---------------------------------------------------------------------------
 // Instantiated channel pairs.
 // ---------------------------------------------------------------------------
 typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, const float*,
@@ -2936,332 +2216,6 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
 
 }  // namespace oci
 
-// ---------------------------------------------------------------------------
-// Convolution gradients.  Workspace: leaf_info, w', the rows g = dy / |l|,
-// the forward workspace of the (cout -> cin) convolution, weight-gradient
-// and bias partials.
-// ---------------------------------------------------------------------------
-namespace {
-constexpr int kBiasChunks = 1024;  // row chunks of the bias gradient
-
-// Leaf chunks of the weight gradient: one per compute unit, fewer when the
-// partials ([chunks][27 cin cout] floats) would pass 64 MB.
-int wgrad_chunks(int cin, int cout) {
-  const int64_t n_ent = 27LL * cin * cout;
-  int64_t c = (16LL << 20) / n_ent;
-  if (c > 256) c = 256;
-  if (c < 8) c = 8;
-  return (int)c;
-}
-
-// The matrix-core weight gradient: input and output channels up to 32, and
-// the neighbourhood tables of the (cout -> cin) forward preparation (built
-// where that direction has an MFMA variant).
-constexpr int kWgBlockGroups = 512;   // workgroups of the 2^3-block kernel
-constexpr int kWgCellGroups = 256;    // workgroups of the edge-8 kernel
-
-bool wgrad_mfma_ok(int cin, int cout) {
-  return cin <= 32 && cout <= 32 && find_variant(cout, cin) != nullptr;
-}
-
-constexpr int kWgCellrGroups = 512;  // workgroups of each edge-4/8 window-sum kernel
-
-// The edge-4/8 window-sum kernel is instantiated for these input widths;
-// other widths take those cells through the generic window sums.
-bool wgrad_cellr_ok(int cin) { return cin == 8 || cin == 16 || cin == 32; }
-
-// Partial sets of the weight gradient, each [27 cin cout].
-int wgrad_sets(int cin, int cout) {
-  if (!wgrad_mfma_ok(cin, cout)) return wgrad_chunks(cin, cout);
-  return kWgBlockGroups + kWgCellGroups +
-         (wgrad_cellr_ok(cin) ? 2 * kWgCellrGroups : wgrad_chunks(cin, cout));
-}
-
-typedef void (*WgCellrFn)(int64_t, const int32_t*, const int64_t*, int, const int32_t*, const float*,
-                          int64_t, const float*, uint32_t, const float*, uint32_t, int, float*);
-
-WgCellrFn wg_cellr_fn(int cin, int sz, int mt) {
-#define OC_WG_CELLR(C)                                                              \
-  if (cin == C)                                                                     \
-    return sz == 8 ? (mt == 1 ? &k_wgrad_cellr<C, 8, 1> : &k_wgrad_cellr<C, 8, 2>)  \
-                   : (mt == 1 ? &k_wgrad_cellr<C, 4, 1> : &k_wgrad_cellr<C, 4, 2>);
-  OC_WG_CELLR(8)
-  OC_WG_CELLR(16)
-  OC_WG_CELLR(32)
-#undef OC_WG_CELLR
-  return nullptr;
-}
-
-typedef void (*WgSumsFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
-                         const int64_t*, int64_t, int64_t, const float*, uint32_t, float*,
-                         const int64_t*, const int64_t*, int64_t, int64_t, const uint32_t*);
-
-WgSumsFn wg_sums_fn(int cin) {
-  if (cin == 8) return &k_boundary_sums<8>;
-  if (cin == 16) return &k_boundary_sums<16>;
-  if (cin == 32) return &k_boundary_sums<32>;
-  return nullptr;
-}
-
-// Boundary-sum slots of a structure with n_leaves leaves (as the forward's).
-int64_t slot_cap(int64_t n_trees, int64_t n_leaves) {
-  return n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1;
-}
-
-typedef void (*WgBlocksFn)(const int32_t*, const int64_t*, int64_t, const int32_t*, const int64_t*,
-                           int64_t, const float*, uint32_t, int, const float*, uint32_t, int, float*);
-typedef void (*WgCellsFn)(const int32_t*, const int64_t*, const int32_t*, int64_t, int64_t,
-                          const float*, uint32_t, int, const float*, uint32_t, int, float*);
-
-typedef void (*WgBlocksLdsFn)(const int32_t*, const int64_t*, int64_t, const int32_t*, const int64_t*,
-                              int64_t, const float*, uint32_t, const float*, uint32_t, float*);
-
-// The LDS-staged block kernel for (cin, cout), or null.
-WgBlocksLdsFn wg_blocks_lds_fn(int cin, int cout) {
-#define OC_WG_BL(C)                                                     \
-  if (cin == C) {                                                       \
-    if (cout == 4) return &k_wgrad_blocks_lds<C, 4>;                    \
-    if (cout == 8) return &k_wgrad_blocks_lds<C, 8>;                    \
-    if (cout == 16) return &k_wgrad_blocks_lds<C, 16>;                  \
-    if (cout == 32) return &k_wgrad_blocks_lds<C, 32>;                  \
-  }
-  OC_WG_BL(8)
-  OC_WG_BL(16)
-  OC_WG_BL(32)
-#undef OC_WG_BL
-  return nullptr;
-}
-
-int wg_blocks_lds_threads(int, int) { return 576; }
-
-WgBlocksFn wg_blocks_fn(int mt, int nt) {
-  if (mt == 1) return nt == 1 ? &k_wgrad_blocks<1, 1> : &k_wgrad_blocks<1, 2>;
-  return nt == 1 ? &k_wgrad_blocks<2, 1> : &k_wgrad_blocks<2, 2>;
-}
-
-WgCellsFn wg_cells_fn(int mt, int nt) {
-  if (mt == 1) return nt == 1 ? &k_wgrad_cells8t<1, 1> : &k_wgrad_cells8t<1, 2>;
-  return nt == 1 ? &k_wgrad_cells8t<2, 1> : &k_wgrad_cells8t<2, 2>;
-}
-
-hipError_t scale_rows(const float* src, float* dst, const uint64_t* info, int64_t n_leaves, int c,
-                      int mul, hipStream_t s) {
-  const bool v4 = c % 4 == 0 && ((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15) == 0;
-  const int64_t n = n_leaves * (v4 ? c / 4 : c);
-  if (v4)
-    hipLaunchKernelGGL(k_scale_rows<4>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst,
-                       info, n_leaves, c, mul);
-  else
-    hipLaunchKernelGGL(k_scale_rows<1>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, dst,
-                       info, n_leaves, c, mul);
-  return hipGetLastError();
-}
-
-struct BwdWs {
-  uint64_t* info;
-  float* wt;
-  float* g;
-  float* wpart;
-  float* bpart;
-  float* bsum;    // boundary sums of the forward input (cin channels)
-  int32_t* nbt2;  // neighbourhood rows of the edge-2 cells
-  void* fws;
-  size_t fws_bytes;
-  size_t total;
-};
-
-BwdWs carve_bwd(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
-  char* p = static_cast<char*>(base);
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    char* q = p ? p + off : nullptr;
-    off += oci::align256(bytes);
-    return q;
-  };
-  BwdWs w;
-  w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
-  w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
-  w.g = reinterpret_cast<float*>(take(sizeof(float) * (size_t)n_leaves * cout));
-  w.wpart = reinterpret_cast<float*>(
-      take(sizeof(float) * (size_t)wgrad_sets(cin, cout) * 27 * (size_t)cin * cout));
-  w.bpart = reinterpret_cast<float*>(take(sizeof(float) * (size_t)kBiasChunks * cout));
-  const bool cellr = wgrad_mfma_ok(cin, cout) && wgrad_cellr_ok(cin);
-  // An edge-2 cell is a leaf: at most n_leaves of them.
-  w.nbt2 = reinterpret_cast<int32_t*>(
-      take(wgrad_mfma_ok(cin, cout) ? sizeof(int32_t) * 64 * (size_t)n_leaves : 0));
-  w.bsum = reinterpret_cast<float*>(
-      take(cellr ? sizeof(float) * kSets * (size_t)cin * (size_t)slot_cap(n_trees, n_leaves) : 0));
-  w.fws_bytes = oci::conv_workspace(n_trees, n_leaves, cout, cin);
-  w.fws = take(w.fws_bytes);
-  w.total = off + 256;
-  return w;
-}
-
-// LDS plan of k_conv_wgrad: shell entries, the accumulator slice, and tm
-// rows of window sums and scaled dy.  The slice takes what leaves at least
-// 8 rows (or the whole entry range when that fits); tm then takes the rest.
-struct WgradPlan {
-  int tm, slice, slices;
-  size_t smem;
-};
-
-WgradPlan wgrad_plan(int cin, int cout, size_t budget) {
-  WgradPlan pl{0, 0, 0, 0};
-  const size_t fixed = sizeof(Entry) * 4 * kSlots + sizeof(int) * 4 * 32;
-  const size_t per = sizeof(float) * (27 * (size_t)cin + cout);
-  const int64_t n_ent = 27LL * cin * cout;
-  if (budget < fixed + per + sizeof(float) * kThreads) return pl;
-  int64_t room = (int64_t)((budget - fixed) / sizeof(float));
-  int64_t want = room - 8 * (int64_t)(per / sizeof(float));
-  if (want < kThreads) want = kThreads;
-  int64_t slice = n_ent < want ? n_ent : want;
-  const int64_t slices = (n_ent + slice - 1) / slice;
-  slice = (n_ent + slices - 1) / slices;
-  const int64_t left = room - slice;
-  int64_t tm = left / (int64_t)(per / sizeof(float));
-  if (tm > 32) tm = 32;
-  if (tm < 1) return pl;
-  pl.tm = (int)tm;
-  pl.slice = (int)slice;
-  pl.slices = (int)slices;
-  pl.smem = fixed + sizeof(float) * ((size_t)slice + (size_t)tm * (27 * (size_t)cin + cout));
-  return pl;
-}
-}  // namespace
-
-namespace oci {
-
-size_t conv_backward_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout) {
-  return carve_bwd(nullptr, n_trees, n_leaves, cin, cout).total;
-}
-
-bool conv_backward_supported(int cin, int cout) {
-  const size_t limit = device_limits() == hipSuccess ? g_max_smem : 160 * 1024;
-  return wgrad_plan(cin, cout, limit).tm >= 1;
-}
-
-hipError_t launch_conv_backward(const ConvBwdArgs& a, void* ws, hipStream_t s) {
-  hipError_t e = init_slots();
-  if (e != hipSuccess) return e;
-  const BwdWs w = carve_bwd(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
-  e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
-  if (e != hipSuccess) return e;
-  const uint64_t x_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cin * 4u;
-  const uint64_t y_bytes = (uint64_t)a.n_leaves * (uint64_t)a.cout * 4u;
-  const bool mfma_wg = a.dweight && a.in && wgrad_mfma_ok(a.cin, a.cout) && x_bytes < kOutside &&
-                       y_bytes < kOutside;
-  // The (cout -> cin) forward convolution with the flipped, transposed
-  // kernel: its preparation also builds the structure tables (unit-group
-  // neighbourhoods, cell lists, region codes) the weight gradient reads.
-  ConvArgs f;
-  f.trees = a.trees; f.prefix = a.prefix;
-  f.n = a.n; f.gd = a.gd; f.gh = a.gh; f.gw = a.gw;
-  f.n_trees = a.n_trees; f.n_leaves = a.n_leaves;
-  f.in = w.g; f.cin = a.cout; f.weight = w.wt; f.bias = nullptr; f.cout = a.cin;
-  f.relu = 0; f.out = a.dx;
-  if (a.dx || mfma_wg) {
-    const int64_t nw = 27LL * a.cin * a.cout;
-    hipLaunchKernelGGL(k_flip_transpose, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
-                       a.weight, a.cin, a.cout, w.wt);
-    e = launch_conv_prepare(f, w.fws, s);
-    if (e != hipSuccess) return e;
-  }
-  if (a.dx) {
-    // |l'| * conv_{W'}(dy / |l|).
-    e = scale_rows(a.dy, w.g, w.info, a.n_leaves, a.cout, 0, s);
-    if (e != hipSuccess) return e;
-    e = launch_conv_execute(f, w.fws, conv_mfma_supported(a.cout, a.cin) ? 2 : 1, s);
-    if (e != hipSuccess) return e;
-    e = scale_rows(a.dx, a.dx, w.info, a.n_leaves, a.cin, 1, s);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (a.dweight) {
-    e = device_limits();
-    if (e != hipSuccess) return e;
-    const int chunks = wgrad_chunks(a.cin, a.cout);
-    const int64_t n_ent = 27LL * a.cin * a.cout;
-    // Partial sets, in reduction order: [2^3 blocks][edge-8 with unsplit
-    // neighbours][the other edge-8 and the edge-4 cells], or only window-sum
-    // chunks when the matrix-core path does not apply.
-    float* part = w.wpart;
-    int sets = 0;
-    const int32_t* rows = nullptr;  // window sums over a list (else every leaf)
-    const int64_t* meta = nullptr;
-    bool generic = true;
-    if (mfma_wg) {
-      const ConvWs fw = carve(w.fws, a.n_trees, a.n_leaves, a.cout, a.cin);
-      const int mt = a.cout > 16 ? 2 : 1, nt = a.cin > 16 ? 2 : 1;
-      hipLaunchKernelGGL(k_edge2_table, dim3((unsigned)(8 * g_num_cus)), dim3(256), 0, s, a.trees,
-                         a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
-                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, a.n_leaves, w.nbt2);
-      const WgBlocksLdsFn bl = wg_blocks_lds_fn(a.cin, a.cout);
-      if (bl)
-        hipLaunchKernelGGL(bl, dim3(kWgBlockGroups), dim3(wg_blocks_lds_threads(a.cin, a.cout)), 0, s,
-                           (const int32_t*)fw.nbt,
-                           (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves, (const int32_t*)w.nbt2,
-                           (const int64_t*)fw.meta, a.n_leaves, a.in, (uint32_t)x_bytes, a.dy,
-                           (uint32_t)y_bytes, part);
-      else
-        hipLaunchKernelGGL(wg_blocks_fn(mt, nt), dim3(kWgBlockGroups), dim3(576), 0, s,
-                           (const int32_t*)fw.nbt, (const int64_t*)(fw.pre[0] + a.n_trees), a.n_leaves,
-                           (const int32_t*)w.nbt2, (const int64_t*)fw.meta, a.n_leaves, a.in,
-                           (uint32_t)x_bytes, a.cin, a.dy, (uint32_t)y_bytes, a.cout, part);
-      part += (int64_t)kWgBlockGroups * n_ent;
-      hipLaunchKernelGGL(wg_cells_fn(mt, nt), dim3(kWgCellGroups), dim3(192), 0, s,
-                         (const int32_t*)fw.brow, (const int64_t*)fw.meta, (const int32_t*)fw.codes,
-                         fw.ccap, a.n_leaves, a.in, (uint32_t)x_bytes, a.cin, a.dy, (uint32_t)y_bytes,
-                         a.cout, part);
-      part += (int64_t)kWgCellGroups * n_ent;
-      sets = kWgBlockGroups + kWgCellGroups;
-      rows = fw.brow;
-      meta = fw.meta;
-      if (wgrad_cellr_ok(a.cin)) {
-        // Boundary sums of the input for the split neighbours, then the
-        // edge-8 (kind 1) and edge-4 (kind 2) cells that read them.
-        const int64_t per_block = 4 * (64 / a.cin);
-        int64_t blocks = (a.n_trees + per_block - 1) / per_block;
-        if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
-        hipLaunchKernelGGL(wg_sums_fn(a.cin), dim3((unsigned)blocks), dim3(256), 0, s, a.trees,
-                           a.prefix, (const int32_t*)fw.stl, (const int64_t*)fw.meta,
-                           (const int64_t*)fw.pre[kSlotScan], a.n_trees, fw.cap, a.in,
-                           (uint32_t)x_bytes, w.bsum, (const int64_t*)fw.pre[1],
-                           (const int64_t*)fw.pre[2], (int64_t)0, a.n_trees,
-                           (const uint32_t*)fw.smask);
-        for (int kind = 1; kind <= 2; ++kind) {
-          hipLaunchKernelGGL(wg_cellr_fn(a.cin, kind == 1 ? 8 : 4, mt), dim3(kWgCellrGroups), dim3(192),
-                             0, s, a.n_leaves, (const int32_t*)fw.brow, (const int64_t*)fw.meta, kind,
-                             (const int32_t*)fw.codes, (const float*)w.bsum, fw.ccap, a.in,
-                             (uint32_t)x_bytes, a.dy, (uint32_t)y_bytes, a.cout, part);
-          part += (int64_t)kWgCellrGroups * n_ent;
-        }
-        sets += 2 * kWgCellrGroups;
-        generic = false;
-      }
-    }
-    if (generic) {
-      const WgradPlan pl = wgrad_plan(a.cin, a.cout, g_max_smem);
-      if (pl.tm < 1) return hipErrorInvalidConfiguration;
-      e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_conv_wgrad),
-                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.smem);
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(k_conv_wgrad, dim3(chunks, pl.slices), dim3(kThreads), pl.smem, s, a.trees,
-                         a.prefix, (const uint64_t*)w.info, a.n_leaves, a.gd, a.gh, a.gw, a.in, a.cin,
-                         a.dy, a.cout, pl.tm, pl.slice, part, rows, meta);
-      sets += chunks;
-    }
-    hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((n_ent + 255) / 256)), dim3(256), 0, s,
-                       (const float*)w.wpart, sets, a.cin, a.cout, a.dweight);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  if (a.dbias) {
-    hipLaunchKernelGGL(k_colsum_partial, dim3(kBiasChunks), dim3(256), 0, s, a.dy, a.n_leaves,
-                       a.cout, w.bpart);
-    hipLaunchKernelGGL(k_colsum_reduce, dim3((unsigned)((a.cout + 63) / 64)), dim3(64), 0, s,
-                       (const float*)w.bpart, kBiasChunks, a.cout, a.dbias);
-  }
-  return hipGetLastError();
-}
-
-}  // namespace oci
+// The gradients, in one translation unit with the forward kernels whose
+// helpers and preparation they use.
+#include "oc_conv_bwd.inc"
