@@ -59,9 +59,10 @@ extern "C" {
 #define OC_POOL_MAX 1
 
 /* Convolution implementations (oc_conv3x3x3_ex). */
-#define OC_CONV_AUTO 0    /* fastest available for the channel counts */
+#define OC_CONV_AUTO 0    /* OC_CONV_MFMA where supported, else OC_CONV_GEMM */
 #define OC_CONV_GENERIC 1 /* any channel counts: window sums + VALU contraction */
 #define OC_CONV_MFMA 2    /* fp32 MFMA contraction; OC_EINVAL if unsupported */
+#define OC_CONV_GEMM 3    /* any channel counts: window sums of row chunks, then an fp32 MFMA GEMM */
 
 /* Static text for a return code. */
 const char* oc_error_string(int code);
@@ -261,6 +262,29 @@ int oc_unpool2_backward(const uint32_t* in_trees, const int64_t* in_prefix, int 
 /* Gradient of oc_relu given its output: din = dout where out > 0, else 0.
  * din may alias dout; count 0 does nothing (the pointers may then be NULL). */
 int oc_relu_backward(const float* out, const float* dout, float* din, int64_t count, void* stream);
+
+/*
+ * Channel concatenation of two leaf arrays on one structure: out[row] =
+ * [a[row] (ca channels), b[row] (cb channels)], the skip connections of the
+ * encoder-decoder network (Sec. 5 and the segmentation architecture table:
+ * concat of an encoder output and the unpooled decoder features at the
+ * same resolution, i.e. on the same structure).
+ *   a: float [n_rows][ca], b: float [n_rows][cb], out: float [n_rows][ca+cb].
+ * n_rows 0 does nothing (pointers may then be NULL).
+ */
+int oc_concat(const float* a, int ca, const float* b, int cb, int64_t n_rows, float* out,
+              void* stream);
+
+/* Gradient of oc_concat: da[row] = dout[row][0..ca), db[row] = dout[row][ca..ca+cb).
+ * da or db may be NULL (that part is not written). */
+int oc_concat_backward(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
+                       void* stream);
+
+/* y += x elementwise on leaf data (pointwise, Sec. 3.2): the gradient of a
+ * layer output that feeds two layers (an encoder output used by the next
+ * level and by a concat) is the sum of both.  x must not alias y partially;
+ * count 0 does nothing. */
+int oc_add(float* y, const float* x, int64_t count, void* stream);
 
 #ifdef __cplusplus
 }

@@ -456,6 +456,21 @@ def unpool2_bwd(g: Grid, dy: np.ndarray, out_g: Grid) -> np.ndarray:
     return dx
 
 
+def concat(a: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """Skip connection of the segmentation network (architecture table):
+    the channels of a followed by those of b, row by row (one structure)."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    assert a.shape[0] == b.shape[0]
+    return np.concatenate([a, b], axis=1)
+
+
+def concat_bwd(d: np.ndarray, ca: int) -> tuple[np.ndarray, np.ndarray]:
+    """Gradient of concat: the first ca channels of d, and the rest."""
+    d = np.asarray(d, dtype=np.float64)
+    return d[:, :ca].copy(), d[:, ca:].copy()
+
+
 def relu_bwd(y: np.ndarray, dy: np.ndarray) -> np.ndarray:
     """Gradient of max(0, .) given its output y: dy where y > 0, else 0."""
     y = np.asarray(y, dtype=np.float64)

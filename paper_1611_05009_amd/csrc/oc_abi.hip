@@ -208,12 +208,12 @@ int conv_args(const char* who, const uint32_t* trees, const int64_t* prefix, int
 }
 
 int conv_impl(const char* who, int impl, int cin, int cout, int* use) {
-  if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA)
+  if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA && impl != OC_CONV_GEMM)
     return fail(OC_EINVAL, "%s: bad impl %d", who, impl);
   const bool mfma_ok = oci::conv_mfma_supported(cin, cout);
   if (impl == OC_CONV_MFMA && !mfma_ok)
     return fail(OC_EINVAL, "%s: no MFMA kernel for (%d, %d)", who, cin, cout);
-  *use = impl == OC_CONV_AUTO ? (mfma_ok ? OC_CONV_MFMA : OC_CONV_GENERIC) : impl;
+  *use = impl == OC_CONV_AUTO ? (mfma_ok ? OC_CONV_MFMA : OC_CONV_GEMM) : impl;
   return OC_OK;
 }
 
@@ -437,6 +437,35 @@ int oc_relu_backward(const float* out, const float* dout, float* din, int64_t co
   if (count == 0) return OC_OK;
   if (!out || !dout || !din) return fail(OC_EINVAL, "oc_relu_backward: null pointer");
   OC_CHECK_HIP(oci::launch_relu_bwd(out, dout, din, count, as_stream(stream)), "oc_relu_backward");
+  return OC_OK;
+}
+
+int oc_concat(const float* a, int ca, const float* b, int cb, int64_t n_rows, float* out, void* stream) {
+  g_last_error.clear();
+  if (ca <= 0 || cb <= 0 || n_rows < 0) return fail(OC_EINVAL, "oc_concat: non-positive size");
+  if (n_rows == 0) return OC_OK;
+  if (!a || !b || !out) return fail(OC_EINVAL, "oc_concat: null pointer");
+  if ((double)n_rows * (ca + cb) >= 9.0e18) return fail(OC_EOVERFLOW, "oc_concat: too large");
+  OC_CHECK_HIP(oci::launch_concat(a, ca, b, cb, n_rows, out, as_stream(stream)), "oc_concat");
+  return OC_OK;
+}
+
+int oc_concat_backward(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
+                       void* stream) {
+  g_last_error.clear();
+  if (ca <= 0 || cb <= 0 || n_rows < 0) return fail(OC_EINVAL, "oc_concat_backward: non-positive size");
+  if (n_rows == 0 || (!da && !db)) return OC_OK;
+  if (!dout) return fail(OC_EINVAL, "oc_concat_backward: null pointer");
+  OC_CHECK_HIP(oci::launch_split(dout, ca, cb, n_rows, da, db, as_stream(stream)), "oc_concat_backward");
+  return OC_OK;
+}
+
+int oc_add(float* y, const float* x, int64_t count, void* stream) {
+  g_last_error.clear();
+  if (count < 0) return fail(OC_EINVAL, "oc_add: negative count");
+  if (count == 0) return OC_OK;
+  if (!y || !x) return fail(OC_EINVAL, "oc_add: null pointer");
+  OC_CHECK_HIP(oci::launch_add(y, x, count, as_stream(stream)), "oc_add");
   return OC_OK;
 }
 

@@ -2009,6 +2009,7 @@ struct ConvWs {
   int32_t* codes;
   int64_t ccap;
   uint32_t* smask;
+  float* sgemm;  // window sums of one row chunk (GEMM path)
   size_t total;
 };
 
@@ -2043,6 +2044,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.nbt = reinterpret_cast<int32_t*>(take(v ? sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1) : 0));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
+  w.sgemm = reinterpret_cast<float*>(take(oci::conv_gemm_buffer(n_leaves, cin)));
   w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.total = off + 256;
   return w;
@@ -2129,6 +2131,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
   const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
+  if (impl == 3) return launch_conv_gemm(a, w.info, w.wt, w.sgemm, s);
   if (impl != 2) {
     const unsigned blocks = (unsigned)(all_tiles < 65536 ? all_tiles : 65536);
     hipLaunchKernelGGL(k_conv_generic, dim3(blocks), dim3(kThreads), gsmem, s, a.trees, a.prefix,
@@ -2216,6 +2219,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
 
 }  // namespace oci
 
-// The gradients, in one translation unit with the forward kernels whose
+// The window-sum GEMM path for channel counts without a fused variant, and
+// the gradients, in one translation unit with the forward kernels whose
 // helpers and preparation they use.
+#include "oc_conv_gemm.inc"
 #include "oc_conv_bwd.inc"

@@ -6,6 +6,10 @@ using namespace ocd;
 
 namespace {
 
+template <int V> struct VecF;
+template <> struct VecF<1> { typedef float type; };
+template <> struct VecF<4> { typedef float4 type; };
+
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 // Eq. 4: one thread per voxel copies the c features of the leaf holding it.
@@ -387,6 +391,51 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
   }
 }
 
+// Channel concatenation of two leaf arrays on one structure (the skip
+// connections of the encoder-decoder): out[row] = [a[row], b[row]], and its
+// gradient, the split of dout into da and db (either may be null).  V floats
+// per thread (ca, cb divisible by V).
+template <int V>
+__global__ void k_concat(const float* __restrict__ a, int ca, const float* __restrict__ b, int cb,
+                         int64_t n_rows, float* __restrict__ out) {
+  typedef typename VecF<V>::type T;
+  const int va = ca / V, vc = (ca + cb) / V;
+  const int64_t n = n_rows * vc;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t row = i / vc;
+    const int k = (int)(i - row * vc);
+    reinterpret_cast<T*>(out)[i] = k < va ? reinterpret_cast<const T*>(a)[row * va + k]
+                                          : reinterpret_cast<const T*>(b)[row * (vc - va) + (k - va)];
+  }
+}
+
+template <int V>
+__global__ void k_split(const float* __restrict__ dout, int ca, int cb, int64_t n_rows,
+                        float* __restrict__ da, float* __restrict__ db) {
+  typedef typename VecF<V>::type T;
+  const int va = ca / V, vc = (ca + cb) / V;
+  const int64_t n = n_rows * vc;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const int64_t row = i / vc;
+    const int k = (int)(i - row * vc);
+    const T v = reinterpret_cast<const T*>(dout)[i];
+    if (k < va) {
+      if (da) reinterpret_cast<T*>(da)[row * va + k] = v;
+    } else if (db) {
+      reinterpret_cast<T*>(db)[row * (vc - va) + (k - va)] = v;
+    }
+  }
+}
+
+// y += x on leaf data (gradient accumulation where a layer output feeds two
+// layers, as an encoder output feeding both the next level and a concat).
+__global__ void k_add(float* y, const float* x, int64_t count) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) y[i] += x[i];
+}
+
 __global__ void k_fill_zero(float* __restrict__ x, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) x[i] = 0.f;
@@ -487,6 +536,46 @@ hipError_t launch_relu_bwd(const float* y, const float* dy, float* din, int64_t 
   int64_t blocks = (count + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(k_relu_bwd, dim3((unsigned)blocks), dim3(256), 0, s, y, dy, din, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_concat(const float* a, int ca, const float* b, int cb, int64_t n_rows, float* out,
+                         hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  const uintptr_t al = reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+                       reinterpret_cast<uintptr_t>(out);
+  const bool v4 = ca % 4 == 0 && cb % 4 == 0 && (al & 15) == 0;
+  const int64_t n = n_rows * (int64_t)(ca + cb) / (v4 ? 4 : 1);
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  if (v4)
+    hipLaunchKernelGGL(k_concat<4>, dim3((unsigned)blocks), dim3(256), 0, s, a, ca, b, cb, n_rows, out);
+  else
+    hipLaunchKernelGGL(k_concat<1>, dim3((unsigned)blocks), dim3(256), 0, s, a, ca, b, cb, n_rows, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_split(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
+                        hipStream_t s) {
+  if (n_rows <= 0) return hipSuccess;
+  const uintptr_t al = reinterpret_cast<uintptr_t>(dout) | reinterpret_cast<uintptr_t>(da) |
+                       reinterpret_cast<uintptr_t>(db);
+  const bool v4 = ca % 4 == 0 && cb % 4 == 0 && (al & 15) == 0;
+  const int64_t n = n_rows * (int64_t)(ca + cb) / (v4 ? 4 : 1);
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  if (v4)
+    hipLaunchKernelGGL(k_split<4>, dim3((unsigned)blocks), dim3(256), 0, s, dout, ca, cb, n_rows, da, db);
+  else
+    hipLaunchKernelGGL(k_split<1>, dim3((unsigned)blocks), dim3(256), 0, s, dout, ca, cb, n_rows, da, db);
+  return hipGetLastError();
+}
+
+hipError_t launch_add(float* y, const float* x, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  int64_t blocks = (count + 255) / 256;
+  if (blocks > 16384) blocks = 16384;
+  hipLaunchKernelGGL(k_add, dim3((unsigned)blocks), dim3(256), 0, s, y, x, count);
   return hipGetLastError();
 }
 

@@ -57,6 +57,13 @@ hipError_t launch_unpool_bwd(const uint32_t* in_trees, const int64_t* in_prefix,
                              hipStream_t s);
 hipError_t launch_relu_bwd(const float* y, const float* dy, float* din, int64_t count,
                            hipStream_t s);
+// Channel concatenation of two leaf arrays and its gradient (da, db may be null).
+hipError_t launch_concat(const float* a, int ca, const float* b, int cb, int64_t n_rows, float* out,
+                         hipStream_t s);
+hipError_t launch_split(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
+                        hipStream_t s);
+// y += x.
+hipError_t launch_add(float* y, const float* x, int64_t count, hipStream_t s);
 
 // Convolution.
 struct ConvArgs {
@@ -77,8 +84,13 @@ bool conv_mfma_supported(int cin, int cout);
 // Structure- and weight-dependent preparation into the workspace (the
 // weight pointer of `a` is read, the features are not).
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
-// The convolution proper; impl: 1 generic, 2 mfma (caller checked support).
+// The convolution proper; impl: 1 generic, 2 mfma (caller checked support),
+// 3 window-sum GEMM.
 hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s);
+// Bytes of the window-sum buffer of the GEMM path (one row chunk).
+size_t conv_gemm_buffer(int64_t n_leaves, int cin);
+hipError_t launch_conv_gemm(const ConvArgs& a, const uint64_t* info, const float* wt, float* sbuf,
+                            hipStream_t s);
 
 // Convolution gradients (bias and ReLU excluded): any of dx, dweight, dbias
 // may be null.

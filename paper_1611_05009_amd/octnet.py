@@ -21,9 +21,9 @@ LIB_PATH = os.path.join(_HERE, "liboctnet_hip.so")
 OC_OK = 0
 OC_SPLIT_MIXED, OC_SPLIT_ANY = 0, 1
 OC_POOL_AVG, OC_POOL_MAX = 0, 1
-OC_CONV_AUTO, OC_CONV_GENERIC, OC_CONV_MFMA = 0, 1, 2
+OC_CONV_AUTO, OC_CONV_GENERIC, OC_CONV_MFMA, OC_CONV_GEMM = 0, 1, 2, 3
 
-_IMPL = {"auto": OC_CONV_AUTO, "generic": OC_CONV_GENERIC, "mfma": OC_CONV_MFMA}
+_IMPL = {"auto": OC_CONV_AUTO, "generic": OC_CONV_GENERIC, "mfma": OC_CONV_MFMA, "gemm": OC_CONV_GEMM}
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int
@@ -60,6 +60,9 @@ SIGNATURES = {
     "oc_pool2_max_backward": (_I, [_P, _P, _I, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
     "oc_unpool2_backward": (_I, [_P, _P, _I, _I, _I, _I, _L, _I, _P, _P, _P, _P, _P]),
     "oc_relu_backward": (_I, [_P, _P, _P, _L, _P]),
+    "oc_concat": (_I, [_P, _I, _P, _I, _L, _P, _P]),
+    "oc_concat_backward": (_I, [_P, _I, _I, _L, _P, _P, _P]),
+    "oc_add": (_I, [_P, _P, _L, _P]),
 }
 
 _lib = None
@@ -394,3 +397,31 @@ def relu_backward(out: torch.Tensor, dout: torch.Tensor, din: torch.Tensor | Non
     _check(lib().oc_relu_backward(_ptr(out), _ptr(dout), _ptr(din), dout.numel(), _stream()),
            "oc_relu_backward")
     return din
+
+
+def concat(a: torch.Tensor, b: torch.Tensor) -> torch.Tensor:
+    """[a, b] along the channels of two leaf arrays on one structure."""
+    if a.shape[0] != b.shape[0]:
+        raise OctNetError("concat needs the same row count")
+    out = torch.empty((a.shape[0], a.shape[1] + b.shape[1]), dtype=torch.float32, device=a.device)
+    _check(lib().oc_concat(_ptr(a), a.shape[1], _ptr(b), b.shape[1], a.shape[0], _ptr(out), _stream()),
+           "oc_concat")
+    return out
+
+
+def concat_backward(dout: torch.Tensor, ca: int):
+    """Gradient of concat: (da [rows, ca], db [rows, C - ca])."""
+    cb = dout.shape[1] - ca
+    da = torch.empty((dout.shape[0], ca), dtype=torch.float32, device=dout.device)
+    db = torch.empty((dout.shape[0], cb), dtype=torch.float32, device=dout.device)
+    _check(lib().oc_concat_backward(_ptr(dout), ca, cb, dout.shape[0], _ptr(da), _ptr(db), _stream()),
+           "oc_concat_backward")
+    return da, db
+
+
+def add_(y: torch.Tensor, x: torch.Tensor) -> torch.Tensor:
+    """y += x (same shape), in place."""
+    if y.shape != x.shape:
+        raise OctNetError("add_ needs one shape")
+    _check(lib().oc_add(_ptr(y), _ptr(x), y.numel(), _stream()), "oc_add")
+    return y

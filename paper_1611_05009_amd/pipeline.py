@@ -96,9 +96,14 @@ def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: st
     if records is not None:
         records.append(OpRecord("input", g, x, g, x))
     guides = []
+    skips = []
     for op, p in W.layers:
         g_in, x_in = g, x
-        if op == "conv":
+        if op == "save":
+            skips.append(x)
+        elif op == "concat":
+            x = timed("concat", lambda: oc.concat(skips.pop(), x_in))
+        elif op == "conv":
             if prep_timer is not None:
                 ps, pe = prep_timer()
                 ps.record()
@@ -131,8 +136,8 @@ def run_backward(W: Workload, records: list, dy: torch.Tensor, op_timer=None, tr
     back through the layer stack recorded by run_step(W, records).  Returns
     (gradient of the input leaf features, {conv index: (dweight, dbias)}).
     op_timer(name), as in run_step, brackets each call: "unpool_bwd",
-    "pool_bwd", "relu_bwd", "conv_bwd_input" and "conv_bwd_weight" (the
-    weight and bias gradients).  trace, when given, receives (record,
+    "pool_bwd", "relu_bwd", "conv_bwd_input", "conv_bwd_weight" (the
+    weight and bias gradients), "concat_bwd" and "add" (skip connections).  trace, when given, receives (record,
     gradient in, gradients out) for each op: out is the input gradient, or
     (relu-masked gradient, input gradient, dweight, dbias) for a conv."""
     def timed(name, fn):
@@ -145,11 +150,22 @@ def run_backward(W: Workload, records: list, dy: torch.Tensor, op_timer=None, tr
         return r
 
     grads = {}
+    skip_grads = []
     for rec in reversed(records):
         if rec.op == "input":
             break
         dy_in = dy
-        if rec.op in ("unpool", "unpool_guided"):
+        if rec.op == "concat":
+            # The concat took [saved encoder output, decoder features].
+            ca = rec.x_out.shape[1] - rec.x_in.shape[1]
+            d_enc, dy = timed("concat_bwd", lambda: oc.concat_backward(dy_in, ca))
+            skip_grads.append(d_enc)
+            out = (d_enc, dy)
+        elif rec.op == "save":
+            # The saved output also fed the concat: its gradients add up.
+            dy = timed("add", lambda: oc.add_(dy_in, skip_grads.pop()))
+            out = dy
+        elif rec.op in ("unpool", "unpool_guided"):
             dy = timed("unpool_bwd", lambda: oc.unpool2_backward(rec.g_in, rec.g_out, dy))
             out = dy
         elif rec.op == "pool":

@@ -198,7 +198,7 @@ def facade_sample(rng: np.random.Generator, res: int = 256, noise: float = 0.02)
 
 @dataclass
 class Layer:
-    op: str              # "conv" | "relu" | "pool" | "unpool" | "unpool_guided"
+    op: str              # "conv" | "relu" | "pool" | "unpool" | "unpool_guided" | "save" | "concat"
     cin: int = 0
     cout: int = 0
 
@@ -237,11 +237,38 @@ WORKLOADS = {
                    " ReLU, guided unpool, conv 32->8"),
 }
 
+def _unet_layers():
+    """The segmentation encoder-decoder of the paper's architecture table:
+    four (conv, conv, max-pool) encoder levels, three convs at the coarsest
+    level, and four (guided unpool, concat with the encoder output of that
+    level, conv, conv) decoder levels; ReLU after every conv but the last.
+    "save" keeps an encoder output for the matching "concat"."""
+    L = []
+    enc = [(8, 8, 16), (16, 16, 32), (32, 32, 64), (64, 64, 128)]
+    for a, b, c in enc:
+        L += [Layer("conv", a, b), Layer("relu"), Layer("conv", b, c), Layer("relu"), Layer("save"),
+              Layer("pool")]
+    for _ in range(3):
+        L += [Layer("conv", 128, 128), Layer("relu")]
+    dec = [(256, 128, 64), (128, 64, 32), (64, 32, 16), (32, 32, 8)]
+    for i, (a, b, c) in enumerate(dec):
+        L += [Layer("unpool_guided"), Layer("concat"), Layer("conv", a, b), Layer("relu"),
+              Layer("conv", b, c)]
+        if i < 3:
+            L += [Layer("relu")]
+    return L
+
+
+WORKLOADS["unet"] = Workload(
+    "unet", 6, 256, 1, 8, _unet_layers(), False,
+    "256^3 facade scene, batch 1, 8 channels; the segmentation U-Net (4 levels, skip concats, guided"
+    " unpooling)")
+
 SIZE_RANGE = {2: (8.0, 40.0), 3: (16.0, 100.0), 4: (32.0, 220.0)}
 
 
 def occupancy(wl: Workload, batch: int | None = None, samples=None) -> np.ndarray:
-    """uint8 [N, res, res, res] occupancy for the workload (c1-c4)."""
+    """uint8 [N, res, res, res] occupancy for the workload (c1-c4, the U-Net's facades)."""
     idx = list(range(wl.batch if batch is None else batch)) if samples is None else list(samples)
     out = np.zeros((len(idx), wl.res, wl.res, wl.res), dtype=np.uint8)
     for j, s in enumerate(idx):
@@ -259,6 +286,8 @@ def occupancy(wl: Workload, batch: int | None = None, samples=None) -> np.ndarra
                 if 0.01 <= frac <= 0.03:
                     break
             out[j] = occ
+        elif wl.index == 6:
+            out[j] = facade_sample(rng, wl.res)[0]
         else:
             raise ValueError("workload %s has a dense colour input; use facade_input" % wl.key)
     return out

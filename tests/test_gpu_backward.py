@@ -69,7 +69,8 @@ def structure(case):
     return rng, ref, g
 
 
-@pytest.mark.parametrize("cin,cout", [(32, 32), (16, 32), (8, 16), (4, 16), (32, 8), (3, 5)])
+@pytest.mark.parametrize("cin,cout", [(32, 32), (16, 32), (8, 16), (4, 16), (32, 8), (3, 5), (64, 64),
+                                      (128, 64)])
 @pytest.mark.parametrize("case", CASES)
 def test_conv_backward(case, cin, cout):
     rng, ref, g = structure(case)
@@ -195,3 +196,20 @@ def test_relu_backward(count):
     d = dev(dy)
     oc.relu_backward(dev(y), d, din=d)  # in place
     assert np.array_equal(d.cpu().numpy(), O.relu_bwd(y, dy).astype(np.float32))
+
+
+@pytest.mark.parametrize("ca,cb,rows", [(16, 16, 1000), (3, 5, 777), (128, 128, 300), (8, 4, 0)])
+def test_concat_split_add(ca, cb, rows):
+    rng = np.random.default_rng(ca * 1000 + cb)
+    a = rng.standard_normal((rows, ca)).astype(np.float32)
+    b = rng.standard_normal((rows, cb)).astype(np.float32)
+    got = oc.concat(dev(a), dev(b)).cpu().numpy()
+    assert np.array_equal(got, O.concat(a, b).astype(np.float32))
+    d = rng.standard_normal((rows, ca + cb)).astype(np.float32)
+    da, db = oc.concat_backward(dev(d), ca)
+    wa, wb = O.concat_bwd(d, ca)
+    assert np.array_equal(da.cpu().numpy(), wa.astype(np.float32))
+    assert np.array_equal(db.cpu().numpy(), wb.astype(np.float32))
+    y = dev(a.copy())
+    oc.add_(y, dev(a))
+    assert np.array_equal(y.cpu().numpy(), a + a)

@@ -147,7 +147,7 @@ def conv_case(seed, cin, cout, shape=(2, 3, 2, 3)):
     return occ, ref, x, w, b
 
 
-@pytest.mark.parametrize("impl", ["generic", "mfma"])
+@pytest.mark.parametrize("impl", ["generic", "mfma", "gemm"])
 @pytest.mark.parametrize("cin,cout", CHANNELS)
 def test_conv_small(cin, cout, impl):
     if impl == "mfma" and not oc.mfma_supported(cin, cout):
@@ -161,7 +161,7 @@ def test_conv_small(cin, cout, impl):
     assert_close(got_r, np.maximum(O.conv3(ref, x, w, None), 0), "conv relu")
 
 
-@pytest.mark.parametrize("impl", ["generic", "mfma"])
+@pytest.mark.parametrize("impl", ["generic", "mfma", "gemm"])
 def test_conv_degenerate_structures(impl):
     cin, cout = 32, 32
     if impl == "mfma" and not oc.mfma_supported(cin, cout):
@@ -185,6 +185,17 @@ def test_conv_degenerate_structures(impl):
         w = (rng.standard_normal((cout, cin, 3, 3, 3)) / np.sqrt(27 * cin)).astype(np.float32)
         got = host(oc.conv3x3x3(g, dev(x), dev(w), impl=impl))
         assert_close(got, O.conv3(ref, x, w), "conv %s %s" % (impl, name))
+
+
+@pytest.mark.parametrize("cin,cout", [(64, 64), (128, 64), (256, 128), (64, 130)])
+def test_conv_wide_channels(cin, cout):
+    """Widths of the encoder-decoder's coarse levels (no fused variant: the
+    window-sum GEMM path under auto)."""
+    occ, ref, x, w, b = conv_case(5000 + cin + cout, cin, cout, shape=(2, 2, 3, 2))
+    g = oc.build(dev(occ))
+    want = O.conv3(ref, x, w, b)
+    got = host(oc.conv3x3x3(g, dev(x), dev(w), dev(b)))
+    assert_close(got, want, "conv auto %dx%d" % (cin, cout))
 
 
 def test_conv_closed_form_single_cell():

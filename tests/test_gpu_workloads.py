@@ -36,7 +36,7 @@ def check_structure(g, ref):
     assert np.array_equal(host(g.prefix), ref.prefix)
 
 
-@pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5", "unet"])
 def test_workload_chain(key):
     from paper_1611_05009_amd import pipeline
     log("workload %s: generating inputs" % key)
@@ -54,8 +54,15 @@ def test_workload_chain(key):
                 want = O.ten2oc(ref, W.dense.cpu().numpy(), "avg")
                 assert_close(host(r.x_out), want, "%s ten2oc" % key)
             continue
+        if r.op == "save":
+            continue
         gi = ref_grid(r.g_in)
         xi = host(r.x_in)
+        if r.op == "concat":
+            skip = host(r.x_out)[:, :r.x_out.shape[1] - xi.shape[1]]
+            assert np.array_equal(host(r.x_out), O.concat(skip, xi).astype(np.float32))
+            assert np.array_equal(host(r.g_out.trees), host(r.g_in.trees))
+            continue
         if r.op == "conv":
             info = O.leaf_info(gi)
             rows = sample_rows(gi.n_leaves, info, 1500, seed=k)
@@ -100,7 +107,7 @@ def close_sum(got, want, absum, what):
     assert not bad.any(), "%s: %d/%d out of tolerance" % (what, int(bad.sum()), bad.size)
 
 
-@pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5"])
+@pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5", "unet"])
 def test_workload_backward_chain(key):
     """The gradients of a full-size pass, op by op in reverse, each checked
     against the oracle fed the GPU's own gradient into that op: ReLU and pool
@@ -121,8 +128,16 @@ def test_workload_backward_chain(key):
     log("workload %s backward: %d ops" % (key, len(trace)))
     for k, (r, d_in, out) in enumerate(trace):
         log("  bwd op %d %s" % (k, r.op))
-        gi = ref_grid(r.g_in)
         di = host(d_in)
+        if r.op == "concat":
+            d_enc, d_dec = out
+            wa, wb = O.concat_bwd(di, r.x_out.shape[1] - r.x_in.shape[1])
+            assert np.array_equal(host(d_enc), wa.astype(np.float32))
+            assert np.array_equal(host(d_dec), wb.astype(np.float32))
+            continue
+        if r.op == "save":
+            continue  # the sum of two gradients; its parts are checked where they are made
+        gi = ref_grid(r.g_in)
         if r.op == "pool":
             want = O.pool2_max_bwd(gi, host(r.x_in), di, ref_grid(r.g_out))
             assert np.array_equal(host(out), want.astype(np.float32))

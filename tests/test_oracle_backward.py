@@ -167,3 +167,19 @@ def test_input_gradient_is_the_flipped_convolution(case):
     rows = np.array([0, g.n_leaves // 2, g.n_leaves - 1])
     samp = vol[rows, None] * O.conv3_sampled(g, dy / vol[:, None], flipped_kernel(w), None, False, rows)
     np.testing.assert_allclose(samp, O.conv3_bwd_data(g, dy, w)[rows], rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("case", STRUCTS)
+def test_concat_is_the_dense_channel_concatenation(case):
+    """Concatenating leaf features equals concatenating the dense feature
+    maps (oc2ten) along channels, the layer's definition on dense grids; its
+    gradient satisfies the adjoint identity."""
+    rng, g = grid_of(case)
+    a = rng.standard_normal((g.n_leaves, 3))
+    b = rng.standard_normal((g.n_leaves, 2))
+    y = O.concat(a, b)
+    dense = np.concatenate([O.oc2ten(g, a), O.oc2ten(g, b)], axis=-1)
+    np.testing.assert_array_equal(O.oc2ten(g, y), dense)
+    d = rng.standard_normal(y.shape)
+    da, db = O.concat_bwd(d, 3)
+    assert rel(float((y * d).sum()), float((a * da).sum() + (b * db).sum())) < 1e-12
