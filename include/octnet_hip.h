@@ -280,11 +280,11 @@ int oc_concat(const float* a, int ca, const float* b, int cb, int64_t n_rows, fl
 int oc_concat_backward(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
                        void* stream);
 
-/* y += x elementwise on leaf data (pointwise, Sec. 3.2): the gradient of a
- * layer output that feeds two layers (an encoder output used by the next
- * level and by a concat) is the sum of both.  x must not alias y partially;
- * count 0 does nothing. */
-int oc_add(float* y, const float* x, int64_t count, void* stream);
+/* out = a + b elementwise on leaf data (pointwise, Sec. 3.2): the gradient
+ * of a layer output that feeds two layers (an encoder output used by the
+ * next level and by a concat) is the sum of both.  out may alias a or b
+ * (entirely, not in part); count 0 does nothing. */
+int oc_add(const float* a, const float* b, float* out, int64_t count, void* stream);
 
 #ifdef __cplusplus
 }

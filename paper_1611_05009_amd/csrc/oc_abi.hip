@@ -460,12 +460,12 @@ int oc_concat_backward(const float* dout, int ca, int cb, int64_t n_rows, float*
   return OC_OK;
 }
 
-int oc_add(float* y, const float* x, int64_t count, void* stream) {
+int oc_add(const float* a, const float* b, float* out, int64_t count, void* stream) {
   g_last_error.clear();
   if (count < 0) return fail(OC_EINVAL, "oc_add: negative count");
   if (count == 0) return OC_OK;
-  if (!y || !x) return fail(OC_EINVAL, "oc_add: null pointer");
-  OC_CHECK_HIP(oci::launch_add(y, x, count, as_stream(stream)), "oc_add");
+  if (!a || !b || !out) return fail(OC_EINVAL, "oc_add: null pointer");
+  OC_CHECK_HIP(oci::launch_add(a, b, out, count, as_stream(stream)), "oc_add");
   return OC_OK;
 }
 

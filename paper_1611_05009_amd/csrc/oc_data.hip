@@ -429,11 +429,13 @@ __global__ void k_split(const float* __restrict__ dout, int ca, int cb, int64_t 
   }
 }
 
-// y += x on leaf data (gradient accumulation where a layer output feeds two
-// layers, as an encoder output feeding both the next level and a concat).
-__global__ void k_add(float* y, const float* x, int64_t count) {
+// out = a + b on leaf data (gradient accumulation where a layer output
+// feeds two layers, as an encoder output feeding both the next level and a
+// concat).  out may alias a or b.
+__global__ void k_add(const float* a, const float* b, float* out, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) y[i] += x[i];
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    out[i] = a[i] + b[i];
 }
 
 __global__ void k_fill_zero(float* __restrict__ x, int64_t count) {
@@ -571,11 +573,11 @@ hipError_t launch_split(const float* dout, int ca, int cb, int64_t n_rows, float
   return hipGetLastError();
 }
 
-hipError_t launch_add(float* y, const float* x, int64_t count, hipStream_t s) {
+hipError_t launch_add(const float* a, const float* b, float* out, int64_t count, hipStream_t s) {
   if (count <= 0) return hipSuccess;
   int64_t blocks = (count + 255) / 256;
   if (blocks > 16384) blocks = 16384;
-  hipLaunchKernelGGL(k_add, dim3((unsigned)blocks), dim3(256), 0, s, y, x, count);
+  hipLaunchKernelGGL(k_add, dim3((unsigned)blocks), dim3(256), 0, s, a, b, out, count);
   return hipGetLastError();
 }
 

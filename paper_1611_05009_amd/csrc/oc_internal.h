@@ -62,8 +62,8 @@ hipError_t launch_concat(const float* a, int ca, const float* b, int cb, int64_t
                          hipStream_t s);
 hipError_t launch_split(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
                         hipStream_t s);
-// y += x.
-hipError_t launch_add(float* y, const float* x, int64_t count, hipStream_t s);
+// out = a + b (out may alias a or b).
+hipError_t launch_add(const float* a, const float* b, float* out, int64_t count, hipStream_t s);
 
 // Convolution.
 struct ConvArgs {

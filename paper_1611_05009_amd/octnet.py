@@ -62,7 +62,7 @@ SIGNATURES = {
     "oc_relu_backward": (_I, [_P, _P, _P, _L, _P]),
     "oc_concat": (_I, [_P, _I, _P, _I, _L, _P, _P]),
     "oc_concat_backward": (_I, [_P, _I, _I, _L, _P, _P, _P]),
-    "oc_add": (_I, [_P, _P, _L, _P]),
+    "oc_add": (_I, [_P, _P, _P, _L, _P]),
 }
 
 _lib = None
@@ -419,9 +419,11 @@ def concat_backward(dout: torch.Tensor, ca: int):
     return da, db
 
 
-def add_(y: torch.Tensor, x: torch.Tensor) -> torch.Tensor:
-    """y += x (same shape), in place."""
-    if y.shape != x.shape:
-        raise OctNetError("add_ needs one shape")
-    _check(lib().oc_add(_ptr(y), _ptr(x), y.numel(), _stream()), "oc_add")
-    return y
+def add(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """a + b (same shape); out may be a or b."""
+    if a.shape != b.shape:
+        raise OctNetError("add needs one shape")
+    if out is None:
+        out = torch.empty_like(a)
+    _check(lib().oc_add(_ptr(a), _ptr(b), _ptr(out), a.numel(), _stream()), "oc_add")
+    return out

@@ -163,7 +163,7 @@ def run_backward(W: Workload, records: list, dy: torch.Tensor, op_timer=None, tr
             out = (d_enc, dy)
         elif rec.op == "save":
             # The saved output also fed the concat: its gradients add up.
-            dy = timed("add", lambda: oc.add_(dy_in, skip_grads.pop()))
+            dy = timed("add", lambda: oc.add(dy_in, skip_grads.pop()))
             out = dy
         elif rec.op in ("unpool", "unpool_guided"):
             dy = timed("unpool_bwd", lambda: oc.unpool2_backward(rec.g_in, rec.g_out, dy))

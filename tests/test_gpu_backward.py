@@ -211,5 +211,6 @@ def test_concat_split_add(ca, cb, rows):
     assert np.array_equal(da.cpu().numpy(), wa.astype(np.float32))
     assert np.array_equal(db.cpu().numpy(), wb.astype(np.float32))
     y = dev(a.copy())
-    oc.add_(y, dev(a))
+    assert np.array_equal(oc.add(y, dev(a)).cpu().numpy(), a + a)
+    oc.add(y, dev(a), out=y)  # in place
     assert np.array_equal(y.cpu().numpy(), a + a)
