@@ -35,7 +35,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "unet"])
     ap.add_argument("--impl", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--bwd-steps", type=int, default=3,
@@ -229,12 +229,17 @@ def main():
     op_ms = {}
     for name, s, e in op_events:
         op_ms[name] = op_ms.get(name, 0.0) + s.elapsed_time(e) / args.steps
-    # Dominant kernel: the first conv layer (the only one in the 256^3 workload).
-    p0 = convs[0][1]
-    gd = W.occ_np.shape[1] // 8
-    n_trees = W.batch * gd ** 3
-    flops, nbytes = conv_flops_bytes(W.n_leaves, n_trees, p0["cin"], p0["cout"])
-    t_conv = per_layer_ms[0] * 1e-3
+    # Dominant kernel: the conv layer with the longest execute (the only one
+    # in the 256^3 workload); its leaf count from one recorded pass.
+    recs = []
+    pipeline.run_step(W, recs)
+    conv_recs = [r for r in recs if r.op == "conv"]
+    kd = max(range(n_conv), key=lambda k: per_layer_ms[k])
+    p0 = convs[kd][1]
+    g0 = conv_recs[kd].g_in
+    n_trees = g0.n_trees
+    flops, nbytes = conv_flops_bytes(g0.n_leaves, n_trees, p0["cin"], p0["cout"])
+    t_conv = per_layer_ms[kd] * 1e-3
     achieved = flops / t_conv / 1e12
     out = {
         "metric": "octree conv3x3x3 leaf-cells/s + effective dense voxels/s at 256^3; % roofline",
@@ -262,8 +267,8 @@ def main():
         "conv_ms": per_layer_ms,
         "conv_prepare_ms": prep_ms,
         "op_ms": op_ms,
-        "conv_leaf_cells_per_s": W.n_leaves / t_conv,
-        "dense_voxels_per_s": W.dense_voxels / t_conv,
+        "conv_leaf_cells_per_s": g0.n_leaves / t_conv,
+        "dense_voxels_per_s": 512.0 * n_trees / t_conv,
         "roofline": {
             "bound": "mfma",
             "achieved": achieved,
@@ -271,7 +276,7 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_FP32_TFLOPS,
             "traffic": measured_traffic(args.config),
-            "kernel": "conv3x3x3 execute, layer 0 (%dx%d): the unit-voxel MFMA kernel, the boundary sums and the four cell kernels, one HIP-event pair around all of them (prepare, which depends on the structure and weights only, is timed apart as conv_prepare_ms and is part of every step)" % (p0["cin"], p0["cout"]),
+            "kernel": "conv3x3x3 execute, layer %d (%dx%d, %d leaves): one HIP-event pair around all its launches (for a fused MFMA variant: the unit-voxel kernel, the boundary sums and the four cell kernels; otherwise window sums of row chunks and the MFMA GEMM); prepare, which depends on the structure and weights only, is timed apart as conv_prepare_ms and is part of every step" % (kd, p0["cin"], p0["cout"], g0.n_leaves),
             "alg_flops": flops,
             "alg_bytes": nbytes,
             "hbm_frac": nbytes / t_conv / 1e9 / PEAK_HBM_GBS,
