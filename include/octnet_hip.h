@@ -286,6 +286,43 @@ int oc_concat_backward(const float* dout, int ca, int cb, int64_t n_rows, float*
  * (entirely, not in part); count 0 does nothing. */
 int oc_add(const float* a, const float* b, float* out, int64_t count, void* stream);
 
+/*
+ * Point clouds (Sec. 5, the facade segmentation input: the points are mapped
+ * into the grid-octree; a leaf holding points takes the mean of their
+ * features and the majority of their labels).
+ *   pts:   float [n_pts][3], coordinates in voxels along (d, h, w) of the
+ *          8gd x 8gh x 8gw grid; a point lies in voxel floor(coordinate).
+ *   batch: int32 [n_pts], the sample of each point, or NULL (all sample 0).
+ * Points outside the grid (or of a sample outside [0, n)) are ignored.
+ */
+
+/* occ [n][8gd][8gh][8gw] (uint8): 1 where a point lies, else 0 (cleared by
+ * the call).  Build the structure from occ with oc_build. */
+int oc_points_voxelize(const float* pts, const int32_t* batch, int64_t n_pts, int n, int gd, int gh,
+                       int gw, uint8_t* occ, void* stream);
+
+/* rows [n_pts] (int32): the row of the leaf holding each point (Eq. 3 on the
+ * bit index of its cell), -1 for an ignored point.  Requires n_leaves < 2^31. */
+int oc_points_leaf_rows(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                        const float* pts, const int32_t* batch, int64_t n_pts, int32_t* rows,
+                        void* stream);
+
+/* Bytes of scratch for oc_points_average (n_labels = 1) and oc_points_vote. */
+size_t oc_points_workspace(int64_t n_leaves, int n_labels);
+
+/* out [n_leaves][c + 1]: channel 0 = 1 where at least one point fell into the
+ * leaf, else 0 (the binary occupancy feature); channels 1..c = the mean of
+ * the points' features feat [n_pts][c] (0 without points).  The sums run in
+ * atomic order, so the means may differ in the last bits between runs. */
+int oc_points_average(const int32_t* rows, int64_t n_pts, const float* feat, int c, int64_t n_leaves,
+                      float* out, void* ws, size_t ws_bytes, void* stream);
+
+/* out [n_leaves] (int32): the most frequent label in [0, n_labels) among the
+ * leaf's points, the smallest of tied labels, -1 without labelled points.
+ * Exact (integer counts). */
+int oc_points_vote(const int32_t* rows, int64_t n_pts, const int32_t* labels, int n_labels,
+                   int64_t n_leaves, int32_t* out, void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

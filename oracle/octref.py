@@ -471,6 +471,66 @@ def concat_bwd(d: np.ndarray, ca: int) -> tuple[np.ndarray, np.ndarray]:
     return d[:, :ca].copy(), d[:, ca:].copy()
 
 
+def points_voxelize(pts: np.ndarray, batch, n: int, gd: int, gh: int, gw: int) -> np.ndarray:
+    """Sec. 5: a point cloud mapped into the voxel grid; a point lies in voxel
+    floor(coordinate); points outside the grid (or the batch) are dropped."""
+    pts = np.asarray(pts, dtype=np.float32)
+    b = np.zeros(len(pts), np.int64) if batch is None else np.asarray(batch, np.int64)
+    D, H, W = 8 * gd, 8 * gh, 8 * gw
+    occ = np.zeros((n, D, H, W), dtype=np.uint8)
+    ok = point_inside(pts, b, n, D, H, W)
+    v = np.floor(pts[ok]).astype(np.int64)
+    occ[b[ok], v[:, 0], v[:, 1], v[:, 2]] = 1
+    return occ
+
+
+def point_inside(pts, b, n, D, H, W):
+    lim = np.array([D, H, W], dtype=np.float32)
+    return np.all(pts >= 0, axis=1) & np.all(pts < lim, axis=1) & (b >= 0) & (b < n)
+
+
+def points_leaf_rows(g: Grid, pts: np.ndarray, batch) -> np.ndarray:
+    """The row of the leaf whose cell holds each point (-1 if dropped), read
+    from the dense row map of the structure."""
+    pts = np.asarray(pts, dtype=np.float32)
+    b = np.zeros(len(pts), np.int64) if batch is None else np.asarray(batch, np.int64)
+    ok = point_inside(pts, b, g.n, 8 * g.gd, 8 * g.gh, 8 * g.gw)
+    rows = np.full(len(pts), -1, dtype=np.int64)
+    v = np.floor(pts[ok]).astype(np.int64)
+    rm = rowmap(g)
+    rows[ok] = rm[b[ok], v[:, 0], v[:, 1], v[:, 2]]
+    return rows
+
+
+def points_average(n_leaves: int, rows: np.ndarray, feat: np.ndarray) -> np.ndarray:
+    """Sec. 5: a leaf holding points takes the mean of their features; channel
+    0 is the binary occupancy (1 where a point fell in the leaf)."""
+    rows = np.asarray(rows, np.int64)
+    feat = np.asarray(feat, np.float64)
+    c = feat.shape[1]
+    out = np.zeros((n_leaves, c + 1), dtype=np.float64)
+    cnt = np.zeros(n_leaves, dtype=np.int64)
+    ok = rows >= 0
+    np.add.at(out[:, 1:], rows[ok], feat[ok])
+    np.add.at(cnt, rows[ok], 1)
+    has = cnt > 0
+    out[has, 1:] /= cnt[has, None]
+    out[has, 0] = 1.0
+    return out
+
+
+def points_vote(n_leaves: int, rows: np.ndarray, labels: np.ndarray, n_labels: int) -> np.ndarray:
+    """Sec. 5: the majority label of a leaf's points (the smallest of tied
+    labels; -1 without labelled points)."""
+    rows = np.asarray(rows, np.int64)
+    labels = np.asarray(labels, np.int64)
+    hist = np.zeros((n_leaves, n_labels), dtype=np.int64)
+    ok = (rows >= 0) & (labels >= 0) & (labels < n_labels)
+    np.add.at(hist, (rows[ok], labels[ok]), 1)
+    out = np.where(hist.max(axis=1) > 0, hist.argmax(axis=1), -1)
+    return out.astype(np.int64)
+
+
 def relu_bwd(y: np.ndarray, dy: np.ndarray) -> np.ndarray:
     """Gradient of max(0, .) given its output y: dy where y > 0, else 0."""
     y = np.asarray(y, dtype=np.float64)

@@ -469,4 +469,61 @@ int oc_add(const float* a, const float* b, float* out, int64_t count, void* stre
   return OC_OK;
 }
 
+int oc_points_voxelize(const float* pts, const int32_t* batch, int64_t n_pts, int n, int gd, int gh,
+                       int gw, uint8_t* occ, void* stream) {
+  g_last_error.clear();
+  if (!occ || (n_pts > 0 && !pts)) return fail(OC_EINVAL, "oc_points_voxelize: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || n_pts < 0) return fail(OC_EINVAL, "oc_points_voxelize: non-positive dims");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_points_voxelize: grid too large");
+  OC_CHECK_HIP(oci::launch_voxelize(pts, batch, n_pts, n, gd, gh, gw, occ, as_stream(stream)),
+               "oc_points_voxelize");
+  return OC_OK;
+}
+
+int oc_points_leaf_rows(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                        const float* pts, const int32_t* batch, int64_t n_pts, int32_t* rows,
+                        void* stream) {
+  g_last_error.clear();
+  if (n_pts < 0 || !dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_points_leaf_rows: bad size");
+  if (n_pts == 0) return OC_OK;
+  if (!trees || !prefix || !pts || !rows) return fail(OC_EINVAL, "oc_points_leaf_rows: null pointer");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_points_leaf_rows: grid too large");
+  OC_CHECK_HIP(oci::launch_point_rows(trees, prefix, n, gd, gh, gw, pts, batch, n_pts, rows,
+                                      as_stream(stream)),
+               "oc_points_leaf_rows");
+  return OC_OK;
+}
+
+size_t oc_points_workspace(int64_t n_leaves, int n_labels) {
+  const int64_t per = n_labels > 1 ? n_labels : 1;
+  return (size_t)(n_leaves > 0 ? n_leaves : 0) * (size_t)per * sizeof(uint32_t) + 256;
+}
+
+int oc_points_average(const int32_t* rows, int64_t n_pts, const float* feat, int c, int64_t n_leaves,
+                      float* out, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (n_pts < 0 || c < 0 || n_leaves <= 0) return fail(OC_EINVAL, "oc_points_average: bad size");
+  if (!out || !ws || (n_pts > 0 && (!rows || (c > 0 && !feat))))
+    return fail(OC_EINVAL, "oc_points_average: null pointer");
+  if (ws_bytes < oc_points_workspace(n_leaves, 1))
+    return fail(OC_EWORKSPACE, "oc_points_average: workspace too small");
+  OC_CHECK_HIP(oci::launch_point_means(rows, n_pts, feat, c, n_leaves, out, static_cast<uint32_t*>(ws),
+                                       as_stream(stream)),
+               "oc_points_average");
+  return OC_OK;
+}
+
+int oc_points_vote(const int32_t* rows, int64_t n_pts, const int32_t* labels, int n_labels,
+                   int64_t n_leaves, int32_t* out, void* ws, size_t ws_bytes, void* stream) {
+  g_last_error.clear();
+  if (n_pts < 0 || n_labels <= 0 || n_leaves <= 0) return fail(OC_EINVAL, "oc_points_vote: bad size");
+  if (!out || !ws || (n_pts > 0 && (!rows || !labels))) return fail(OC_EINVAL, "oc_points_vote: null pointer");
+  if (ws_bytes < oc_points_workspace(n_leaves, n_labels))
+    return fail(OC_EWORKSPACE, "oc_points_vote: workspace too small");
+  OC_CHECK_HIP(oci::launch_label_vote(rows, n_pts, labels, n_labels, n_leaves, out,
+                                      static_cast<uint32_t*>(ws), as_stream(stream)),
+               "oc_points_vote");
+  return OC_OK;
+}
+
 }  // extern "C"

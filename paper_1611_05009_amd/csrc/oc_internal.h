@@ -62,6 +62,18 @@ hipError_t launch_concat(const float* a, int ca, const float* b, int cb, int64_t
                          hipStream_t s);
 hipError_t launch_split(const float* dout, int ca, int cb, int64_t n_rows, float* da, float* db,
                         hipStream_t s);
+// Point clouds: voxelise (clears occ first), the leaf row of each point,
+// per-leaf feature means (out [n_leaves][c + 1]; count: n_leaves words of
+// scratch) and label majority votes (hist: n_leaves * L words of scratch).
+hipError_t launch_voxelize(const float* pts, const int32_t* batch, int64_t n_pts, int n, int gd, int gh,
+                           int gw, uint8_t* occ, hipStream_t s);
+hipError_t launch_point_rows(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
+                             const float* pts, const int32_t* batch, int64_t n_pts, int32_t* rows,
+                             hipStream_t s);
+hipError_t launch_point_means(const int32_t* rows, int64_t n_pts, const float* feat, int c,
+                              int64_t n_leaves, float* out, uint32_t* count, hipStream_t s);
+hipError_t launch_label_vote(const int32_t* rows, int64_t n_pts, const int32_t* labels, int L,
+                             int64_t n_leaves, int32_t* out, uint32_t* hist, hipStream_t s);
 // out = a + b (out may alias a or b).
 hipError_t launch_add(const float* a, const float* b, float* out, int64_t count, hipStream_t s);
 

@@ -63,6 +63,11 @@ SIGNATURES = {
     "oc_concat": (_I, [_P, _I, _P, _I, _L, _P, _P]),
     "oc_concat_backward": (_I, [_P, _I, _I, _L, _P, _P, _P]),
     "oc_add": (_I, [_P, _P, _P, _L, _P]),
+    "oc_points_voxelize": (_I, [_P, _P, _L, _I, _I, _I, _I, _P, _P]),
+    "oc_points_leaf_rows": (_I, [_P, _P, _I, _I, _I, _I, _P, _P, _L, _P, _P]),
+    "oc_points_workspace": (_S, [_L, _I]),
+    "oc_points_average": (_I, [_P, _L, _P, _I, _L, _P, _P, _S, _P]),
+    "oc_points_vote": (_I, [_P, _L, _P, _I, _L, _P, _P, _S, _P]),
 }
 
 _lib = None
@@ -426,4 +431,39 @@ def add(a: torch.Tensor, b: torch.Tensor, out: torch.Tensor | None = None) -> to
     if out is None:
         out = torch.empty_like(a)
     _check(lib().oc_add(_ptr(a), _ptr(b), _ptr(out), a.numel(), _stream()), "oc_add")
+    return out
+
+
+def points_voxelize(pts: torch.Tensor, n: int, gd: int, gh: int, gw: int,
+                    batch: torch.Tensor | None = None) -> torch.Tensor:
+    """uint8 occupancy [n, 8gd, 8gh, 8gw] of a point cloud (pts [P, 3] in voxels)."""
+    occ = torch.empty((n, 8 * gd, 8 * gh, 8 * gw), dtype=torch.uint8, device=pts.device)
+    _check(lib().oc_points_voxelize(_ptr(pts), _ptr(batch), pts.shape[0], n, gd, gh, gw, _ptr(occ),
+                                    _stream()), "oc_points_voxelize")
+    return occ
+
+
+def points_leaf_rows(g: Octree, pts: torch.Tensor, batch: torch.Tensor | None = None) -> torch.Tensor:
+    rows = torch.empty(pts.shape[0], dtype=torch.int32, device=pts.device)
+    _check(lib().oc_points_leaf_rows(_ptr(g.trees), _ptr(g.prefix), *g.dims(), _ptr(pts), _ptr(batch),
+                                     pts.shape[0], _ptr(rows), _stream()), "oc_points_leaf_rows")
+    return rows
+
+
+def points_average(g: Octree, rows: torch.Tensor, feat: torch.Tensor) -> torch.Tensor:
+    """[n_leaves, 1 + C]: occupancy flag and the mean point features per leaf."""
+    c = feat.shape[1]
+    out = torch.empty((g.n_leaves, c + 1), dtype=torch.float32, device=rows.device)
+    ws = torch.empty(lib().oc_points_workspace(g.n_leaves, 1), dtype=torch.uint8, device=rows.device)
+    _check(lib().oc_points_average(_ptr(rows), rows.shape[0], _ptr(feat), c, g.n_leaves, _ptr(out),
+                                   _ptr(ws), ws.numel(), _stream()), "oc_points_average")
+    return out
+
+
+def points_vote(g: Octree, rows: torch.Tensor, labels: torch.Tensor, n_labels: int) -> torch.Tensor:
+    """[n_leaves] majority label per leaf (-1 without points)."""
+    out = torch.empty(g.n_leaves, dtype=torch.int32, device=rows.device)
+    ws = torch.empty(lib().oc_points_workspace(g.n_leaves, n_labels), dtype=torch.uint8, device=rows.device)
+    _check(lib().oc_points_vote(_ptr(rows), rows.shape[0], _ptr(labels), n_labels, g.n_leaves, _ptr(out),
+                                _ptr(ws), ws.numel(), _stream()), "oc_points_vote")
     return out

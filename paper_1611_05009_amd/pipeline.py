@@ -35,7 +35,15 @@ class Workload:
         self.batch = self.wl.batch if batch is None else batch
         self.device = torch.device(device)
         wl = self.wl
-        if wl.dense_features:
+        self.points = None
+        if wl.points:
+            pts, bidx, feat, labels = synth.point_cloud(wl, batch=self.batch)
+            self.points = (torch.from_numpy(pts).to(self.device), torch.from_numpy(bidx).to(self.device),
+                           torch.from_numpy(feat).to(self.device), torch.from_numpy(labels).to(self.device))
+            self.points_np = (pts, bidx, feat, labels)
+            occ = None  # voxelised on the GPU by every step
+            self.dense = None
+        elif wl.dense_features:
             if key == "c1":
                 occ = synth.occupancy(wl, batch=self.batch)
                 dense = occ[..., None].astype(np.float32)
@@ -46,11 +54,15 @@ class Workload:
             occ = synth.occupancy(wl, batch=self.batch)
             self.dense = None
         self.occ_np = occ
-        self.occ = torch.from_numpy(occ).to(self.device)
+        if occ is None:
+            self.occ = oc.points_voxelize(self.points[0], self.batch, wl.grid, wl.grid, wl.grid,
+                                          batch=self.points[1])
+        else:
+            self.occ = torch.from_numpy(occ).to(self.device)
         g = oc.build(self.occ)
         self.n_leaves = g.n_leaves
         self.features = None
-        if not wl.dense_features:
+        if not wl.dense_features and not wl.points:
             self.features = torch.from_numpy(synth.leaf_features(wl, g.n_leaves, wl.cin)).to(self.device)
         # Conv layers with their fused ReLU flags.
         self.layers = []
@@ -71,7 +83,7 @@ class Workload:
 
     @property
     def dense_voxels(self) -> int:
-        return int(np.prod(self.occ_np.shape))
+        return int(np.prod(self.occ.shape))
 
 
 def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: str = "auto",
@@ -91,8 +103,22 @@ def run_step(W: Workload, records: list | None = None, conv_timer=None, impl: st
         e.record()
         return r
 
-    g = timed("build", lambda: oc.build(W.occ))
-    x = oc.ten2oc(g, W.dense, "avg") if W.dense is not None else W.features
+    if W.points is not None:
+        # Point cloud: voxelise, build, then the per-leaf occupancy flag and
+        # mean point features.
+        pts, bidx, feat, _ = W.points
+        n, gdim = W.batch, W.wl.grid
+
+        def from_points():
+            occ = oc.points_voxelize(pts, n, gdim, gdim, gdim, batch=bidx)
+            gg = oc.build(occ)
+            rows = oc.points_leaf_rows(gg, pts, bidx)
+            return gg, oc.points_average(gg, rows, feat)
+
+        g, x = timed("build", from_points)
+    else:
+        g = timed("build", lambda: oc.build(W.occ))
+        x = oc.ten2oc(g, W.dense, "avg") if W.dense is not None else W.features
     if records is not None:
         records.append(OpRecord("input", g, x, g, x))
     guides = []

@@ -191,6 +191,26 @@ def facade_sample(rng: np.random.Generator, res: int = 256, noise: float = 0.02)
     return occ, colour
 
 
+def facade_points(rng: np.random.Generator, res: int = 256, noise: float = 0.002):
+    """A coloured facade point cloud: 1 + Poisson(0.5) points per occupied
+    voxel of a facade scene (uniform within the voxel).  Returns
+    (points float32 [P, 3] in voxels along (d, h, w), features float32
+    [P, 7] = RGB, a unit normal, height d / res, labels int32 [P] in 0..6,
+    constant over 32^3 blocks of the scene)."""
+    occ, colour = facade_sample(rng, res, noise)
+    vox = np.argwhere(occ > 0)
+    k = 1 + rng.poisson(0.5, size=len(vox))
+    vox = np.repeat(vox, k, axis=0)
+    pts = (vox + rng.random((len(vox), 3), dtype=np.float32)).astype(np.float32)
+    rgb = colour[vox[:, 0], vox[:, 1], vox[:, 2]] + 0.05 * rng.standard_normal((len(vox), 3), dtype=np.float32)
+    nrm = rng.standard_normal((len(vox), 3), dtype=np.float32)
+    nrm /= np.maximum(np.linalg.norm(nrm, axis=1, keepdims=True), 1e-6)
+    height = (pts[:, :1] / res).astype(np.float32)
+    feat = np.concatenate([rgb, nrm, height], axis=1).astype(np.float32)
+    labels = ((vox[:, 0] // 32) * 3 + (vox[:, 1] // 32) + 2 * (vox[:, 2] // 32)) % 7
+    return pts, feat, labels.astype(np.int32)
+
+
 # ----------------------------------------------------------------------------
 # Workloads
 # ----------------------------------------------------------------------------
@@ -213,6 +233,7 @@ class Workload:
     layers: list
     dense_features: bool  # True: leaf features = ten2oc(avg) of a dense input
     description: str
+    points: bool = False  # True: the input is a point cloud (occupancy + mean features per leaf)
 
     @property
     def grid(self) -> int:
@@ -261,8 +282,22 @@ def _unet_layers():
 
 WORKLOADS["unet"] = Workload(
     "unet", 6, 256, 1, 8, _unet_layers(), False,
-    "256^3 facade scene, batch 1, 8 channels; the segmentation U-Net (4 levels, skip concats, guided"
-    " unpooling)")
+    "256^3 facade point cloud, batch 1, 8 input channels (occupancy, RGB, normal, height averaged per"
+    " leaf); the segmentation U-Net (4 levels, skip concats, guided unpooling)", points=True)
+
+
+def point_cloud(wl: Workload, batch: int | None = None):
+    """(points [P, 3], batch index [P], features [P, 7], labels [P]) of the
+    workload's samples, concatenated."""
+    n = wl.batch if batch is None else batch
+    P, B, F, L = [], [], [], []
+    for s in range(n):
+        p, f, l = facade_points(rng_for(wl.index, s, 0), wl.res)
+        P.append(p)
+        F.append(f)
+        L.append(l)
+        B.append(np.full(len(p), s, dtype=np.int32))
+    return np.concatenate(P), np.concatenate(B), np.concatenate(F), np.concatenate(L)
 
 SIZE_RANGE = {2: (8.0, 40.0), 3: (16.0, 100.0), 4: (32.0, 220.0)}
 

@@ -47,6 +47,14 @@ def test_workload_chain(key):
     log("workload %s: %d leaves, %d ops" % (key, W.n_leaves, len(recs)))
     for k, r in enumerate(recs):
         log("  op %d %s" % (k, r.op))
+        if r.op == "input" and W.points is not None:
+            pts, bidx, feat, _ = W.points_np
+            gd = W.wl.grid
+            ref = O.build(O.points_voxelize(pts, bidx, W.batch, gd, gd, gd))
+            check_structure(r.g_out, ref)
+            rows = O.points_leaf_rows(ref, pts, bidx)
+            assert_close(host(r.x_out), O.points_average(ref.n_leaves, rows, feat), "%s point means" % key)
+            continue
         if r.op == "input":
             ref = O.build(W.occ_np)
             check_structure(r.g_out, ref)

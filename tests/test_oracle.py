@@ -435,3 +435,69 @@ def test_guided_unpool_restores_guide_structure():
         bg = O.words_to_bits(tg)
         bg[9:] = 0
         assert np.array_equal(O.words_to_bits(tp), bg)
+
+
+# ---------------------------------------------------------------------------
+# Point clouds (Sec. 5): voxelise, build, per-leaf mean features and votes.
+# ---------------------------------------------------------------------------
+
+def test_points_voxelize_floor_and_drop():
+    pts = np.array([[0.0, 0.0, 0.0], [7.99, 0.5, 15.999], [8.0, 8.0, 8.0], [-0.01, 1, 1],
+                    [16.0, 1, 1], [1, 1, 1]], np.float32)
+    batch = np.array([0, 0, 0, 0, 0, 1])
+    occ = O.points_voxelize(pts, batch, 1, 2, 1, 2)
+    assert occ.shape == (1, 16, 8, 16)
+    assert occ.sum() == 2  # the last four are outside the grid or the batch
+    assert occ[0, 0, 0, 0] == 1 and occ[0, 7, 0, 15] == 1
+    # (8, 8, 8) is outside the 8-voxel-high grid along h
+    assert occ[0, 8, :, 8].sum() == 0
+
+
+def test_points_average_and_vote_by_hand():
+    # One empty 8^3 tree with no points but a point block in the corner: the
+    # build splits down to that voxel; a second point in the same voxel and
+    # a third in a coarse empty leaf far away.
+    pts = np.array([[0.5, 0.5, 0.5], [0.25, 0.75, 0.5], [6.5, 6.5, 6.5]], np.float32)
+    feat = np.array([[1.0, 10.0], [3.0, 20.0], [5.0, 7.0]], np.float32)
+    labels = np.array([2, 1, 4])
+    occ = O.points_voxelize(pts, None, 1, 1, 1, 1)
+    g = O.build(occ)
+    rows = O.points_leaf_rows(g, pts, None)
+    assert rows[0] == rows[1] != rows[2]
+    avg = O.points_average(g.n_leaves, rows, feat)
+    np.testing.assert_allclose(avg[rows[0]], [1.0, 2.0, 15.0])
+    np.testing.assert_allclose(avg[rows[2]], [1.0, 5.0, 7.0])
+    others = np.setdiff1d(np.arange(g.n_leaves), rows)
+    assert np.all(avg[others] == 0)
+    vote = O.points_vote(g.n_leaves, rows, labels, 5)
+    assert vote[rows[0]] == 1  # tie 1 vs 2: the smaller label
+    assert vote[rows[2]] == 4
+    assert np.all(vote[others] == -1)
+
+
+def test_points_leaf_contains_point():
+    """Every point's leaf cell contains the point's voxel, for a random cloud."""
+    rng = np.random.default_rng(8)
+    pts = (rng.random((400, 3)) * np.array([16, 24, 16])).astype(np.float32)
+    occ = O.points_voxelize(pts, None, 1, 2, 3, 2)
+    g = O.build(occ)
+    rows = O.points_leaf_rows(g, pts, None)
+    info = O.leaf_info(g)
+    def cell(bit):
+        # Origin and edge of the cell of bit index `bit` (octant o covers
+        # offset ((o>>2)&1, (o>>1)&1, o&1) times the child edge).
+        size = 8 if bit == 0 else (4 if bit < 9 else (2 if bit < 73 else 1))
+        o, i, edge = np.zeros(3, int), bit, size
+        while i > 0:
+            oc_ = (i - 1) % 8
+            o += np.array([(oc_ >> 2) & 1, (oc_ >> 1) & 1, oc_ & 1]) * edge
+            i, edge = (i - 1) // 8, edge * 2
+        return o, size
+
+    for p, r in zip(pts, rows):
+        t, bit = int(info[r] >> np.uint64(10)), int(info[r] & np.uint64(1023))
+        td, th, tw = t // 6, (t // 2) % 3, t % 2
+        (d, h, w), s = cell(bit)
+        v = np.floor(p).astype(int)
+        o = np.array([8 * td + d, 8 * th + h, 8 * tw + w])
+        assert np.all(v >= o) and np.all(v < o + s)
