@@ -258,7 +258,7 @@ def main():
             "workload": W.wl.description,
             "key": args.config,
             "batch": W.batch,
-            "grid": list(W.occ_np.shape[1:]),
+            "grid": list(W.occ.shape[1:]),
             "n_leaves": W.n_leaves,
             "n_trees": n_trees,
             "layers": [L.op if L.op != "conv" else "conv%dx%d" % (L.cin, L.cout) for L in W.wl.layers],
