@@ -38,6 +38,8 @@ def parse():
     ap.add_argument("--config", default="c4", choices=["c1", "c2", "c3", "c4", "c5", "unet"])
     ap.add_argument("--impl", default="auto", choices=["auto", "generic", "mfma"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--report", choices=["memory", "truncated"], default=None,
+                    help="print a report table instead of the bench line")
     ap.add_argument("--bwd-steps", type=int, default=3,
                     help="backward passes timed after the forward steps (0: none)")
     ap.add_argument("--cpu-rows", type=int, default=6000,
@@ -155,8 +157,77 @@ def backward_times(W, steps):
     return ms
 
 
+def memory_report():
+    """Grid-octree vs dense bytes (1 and 8 features) of synthetic surface
+    shapes at 8^3 .. 256^3, structures built on the GPU."""
+    import torch
+    from paper_1611_05009_amd import octnet as oc
+    from paper_1611_05009_amd import reports as R
+    from paper_1611_05009_amd import synth
+
+    oc.lib()
+    print("| grid | shape size (voxels) | occupancy % | leaves | dense MB (c=1) | octree MB (c=1) | dense MB (c=8) | octree MB (c=8) |")
+    print("|---|---|---|---|---|---|---|---|")
+    rng = np.random.default_rng(2017)
+    for res in (8, 16, 32, 64, 128, 256):
+        for frac in (0.3, 0.6, 0.95):
+            size = max(2.0, frac * res)
+            occ = synth.surface_sample(rng, res, size * 0.9, size)
+            g = oc.build(torch.from_numpy(occ[None]).cuda())
+            n_trees = (res // 8) ** 3
+            vox = res ** 3
+            print("| %d^3 | %.0f | %.2f | %d | %.3f | %.3f | %.3f | %.3f |" % (
+                res, size, 100.0 * occ.mean(), g.n_leaves,
+                R.dense_bytes(vox, 1) / 1e6, R.octree_bytes(n_trees, g.n_leaves, 1) / 1e6,
+                R.dense_bytes(vox, 8) / 1e6, R.octree_bytes(n_trees, g.n_leaves, 8) / 1e6), flush=True)
+
+
+def truncated_report(config):
+    """Products per channel pair of the three schemes over the workload's
+    first conv layer, and the measured time of the truncated kernel (the
+    paper's scheme) beside the default path on that layer."""
+    import torch
+    from paper_1611_05009_amd import octnet as oc
+    from paper_1611_05009_amd import pipeline
+    from paper_1611_05009_amd import reports as R
+
+    oc.lib()
+    W = pipeline.Workload(config)
+    recs = []
+    pipeline.run_step(W, recs)
+    conv = next(r for r in recs if r.op == "conv")
+    g, x, p = conv.g_in, conv.x_in, conv.params
+    info = oc.leaf_index(g).cpu().numpy()
+    bits = info & 1023
+    hist = {8: int((bits == 0).sum()), 4: int(((bits >= 1) & (bits < 9)).sum()),
+            2: int(((bits >= 9) & (bits < 73)).sum()), 1: int((bits >= 73).sum())}
+    prods = R.workload_products(hist, p["cin"], p["cout"])
+    times = {}
+    for impl in ("auto", "truncated"):
+        oc.conv3x3x3(g, x, p["w"], p["b"], impl=impl)
+        torch.cuda.synchronize()
+        s = torch.cuda.Event(enable_timing=True)
+        e = torch.cuda.Event(enable_timing=True)
+        s.record()
+        oc.conv3x3x3(g, x, p["w"], p["b"], impl=impl)
+        e.record()
+        torch.cuda.synchronize()
+        times[impl] = s.elapsed_time(e)
+    print("| workload | conv | leaves (edge 8/4/2/1) | naive products | truncated products | window-sum products | truncated kernel ms | default path ms |")
+    print("|---|---|---|---|---|---|---|---|")
+    print("| %s | %dx%d | %d / %d / %d / %d | %.4g | %.4g | %.4g | %.2f | %.2f |" % (
+        config, p["cin"], p["cout"], hist[8], hist[4], hist[2], hist[1], prods["naive"],
+        prods["truncated"], prods["window_sums"], times["truncated"], times["auto"]))
+
+
 def main():
     args = parse()
+    if args.report == "memory":
+        memory_report()
+        return
+    if args.report == "truncated":
+        truncated_report(args.config)
+        return
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return

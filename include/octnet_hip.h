@@ -63,6 +63,8 @@ extern "C" {
 #define OC_CONV_GENERIC 1 /* any channel counts: window sums + VALU contraction */
 #define OC_CONV_MFMA 2    /* fp32 MFMA contraction; OC_EINVAL if unsupported */
 #define OC_CONV_GEMM 3    /* any channel counts: window sums of row chunks, then an fp32 MFMA GEMM */
+#define OC_CONV_TRUNCATED 4 /* the supplement's efficient convolution (constant part + truncated
+                              kernels at boundary voxels), VALU; oc_conv3x3x3_ex only */
 
 /* Static text for a return code. */
 const char* oc_error_string(int code);

@@ -208,7 +208,8 @@ int conv_args(const char* who, const uint32_t* trees, const int64_t* prefix, int
 }
 
 int conv_impl(const char* who, int impl, int cin, int cout, int* use) {
-  if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA && impl != OC_CONV_GEMM)
+  if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA && impl != OC_CONV_GEMM &&
+      impl != OC_CONV_TRUNCATED)
     return fail(OC_EINVAL, "%s: bad impl %d", who, impl);
   const bool mfma_ok = oci::conv_mfma_supported(cin, cout);
   if (impl == OC_CONV_MFMA && !mfma_ok)
@@ -246,6 +247,8 @@ int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, in
   int use = 0;
   rc = conv_impl("oc_conv3x3x3_execute", impl, cin, cout, &use);
   if (rc != OC_OK) return rc;
+  if (use == OC_CONV_TRUNCATED)
+    return fail(OC_EINVAL, "oc_conv3x3x3_execute: OC_CONV_TRUNCATED runs through oc_conv3x3x3_ex");
   a.in = in; a.bias = bias; a.relu = relu ? 1 : 0; a.out = out;
   OC_CHECK_HIP(oci::launch_conv_execute(a, ws, use, as_stream(stream)), "oc_conv3x3x3_execute");
   return OC_OK;
@@ -266,6 +269,11 @@ int oc_conv3x3x3_ex(const uint32_t* trees, const int64_t* prefix, int n, int gd,
   if (rc != OC_OK) return rc;
   a.in = in; a.weight = weight; a.bias = bias; a.relu = relu ? 1 : 0; a.out = out;
   hipStream_t s = as_stream(stream);
+  if (use == OC_CONV_TRUNCATED) {
+    // Needs only the leaf index, at the start of the workspace.
+    OC_CHECK_HIP(oci::launch_conv_truncated(a, static_cast<uint64_t*>(ws), s), "oc_conv3x3x3");
+    return OC_OK;
+  }
   OC_CHECK_HIP(oci::launch_conv_prepare(a, ws, s), "oc_conv3x3x3");
   OC_CHECK_HIP(oci::launch_conv_execute(a, ws, use, s), "oc_conv3x3x3");
   return OC_OK;

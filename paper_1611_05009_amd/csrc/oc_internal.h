@@ -99,6 +99,9 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
 // The convolution proper; impl: 1 generic, 2 mfma (caller checked support),
 // 3 window-sum GEMM.
 hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s);
+// The paper's efficient convolution (constant part plus truncated kernels
+// at boundary voxels), VALU; info: n_leaves words of scratch.
+hipError_t launch_conv_truncated(const ConvArgs& a, uint64_t* info, hipStream_t s);
 // Bytes of the window-sum buffer of the GEMM path (one row chunk).
 size_t conv_gemm_buffer(int64_t n_leaves, int cin);
 hipError_t launch_conv_gemm(const ConvArgs& a, const uint64_t* info, const float* wt, float* sbuf,

@@ -21,9 +21,10 @@ LIB_PATH = os.path.join(_HERE, "liboctnet_hip.so")
 OC_OK = 0
 OC_SPLIT_MIXED, OC_SPLIT_ANY = 0, 1
 OC_POOL_AVG, OC_POOL_MAX = 0, 1
-OC_CONV_AUTO, OC_CONV_GENERIC, OC_CONV_MFMA, OC_CONV_GEMM = 0, 1, 2, 3
+OC_CONV_AUTO, OC_CONV_GENERIC, OC_CONV_MFMA, OC_CONV_GEMM, OC_CONV_TRUNCATED = 0, 1, 2, 3, 4
 
-_IMPL = {"auto": OC_CONV_AUTO, "generic": OC_CONV_GENERIC, "mfma": OC_CONV_MFMA, "gemm": OC_CONV_GEMM}
+_IMPL = {"auto": OC_CONV_AUTO, "generic": OC_CONV_GENERIC, "mfma": OC_CONV_MFMA, "gemm": OC_CONV_GEMM,
+         "truncated": OC_CONV_TRUNCATED}
 
 _P = ctypes.c_void_p
 _I = ctypes.c_int

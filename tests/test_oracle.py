@@ -501,3 +501,32 @@ def test_points_leaf_contains_point():
         v = np.floor(p).astype(int)
         o = np.array([8 * td + d, 8 * th + h, 8 * tw + w])
         assert np.all(v >= o) and np.all(v < o + s)
+
+
+# ---------------------------------------------------------------------------
+# The supplement's efficient convolution: operation counts.
+# ---------------------------------------------------------------------------
+
+def test_truncated_kernel_counts_match_the_paper():
+    from paper_1611_05009_amd import reports as R
+    # The supplement's figures for an 8^3 cell and a 3^3 kernel.
+    assert R.conv_products(8, "naive") == 13824
+    assert R.conv_products(8, "truncated") == 3203
+    assert round(100.0 * 3203 / 13824, 2) == 23.17
+
+
+@pytest.mark.parametrize("s", [1, 2, 3, 4, 5, 8])
+def test_truncated_kernel_counts_by_enumeration(s):
+    """The closed form equals a brute-force count of (voxel, tap) pairs whose
+    tap leaves the cell."""
+    from paper_1611_05009_amd import reports as R
+    n = 0
+    for d in range(s):
+        for h in range(s):
+            for w in range(s):
+                for dd in (-1, 0, 1):
+                    for dh in (-1, 0, 1):
+                        for dw in (-1, 0, 1):
+                            q = (d + dd, h + dh, w + dw)
+                            n += any(c < 0 or c >= s for c in q)
+    assert R.outside_taps(s) == n
