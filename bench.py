@@ -354,7 +354,17 @@ def main():
         },
     }
     if args.bwd_steps > 0:
-        out["backward_ms"] = backward_times(W, args.bwd_steps)
+        bms = backward_times(W, args.bwd_steps)
+        out["backward_ms"] = bms
+        # Matrix-core rates of the conv gradients over all conv layers: each
+        # gradient is 2 * 27 * Cin * Cout flops per leaf, like the forward.
+        fl = sum(2.0 * 27 * r.params["cin"] * r.params["cout"] * r.g_in.n_leaves for r in conv_recs)
+        rates = {}
+        for name in ("conv_bwd_input", "conv_bwd_weight"):
+            if bms.get(name):
+                tf = fl / (bms[name] * 1e-3) / 1e12
+                rates[name] = {"achieved_tflops": tf, "frac_of_fp32_mfma_peak": tf / PEAK_FP32_TFLOPS}
+        out["backward_roofline"] = rates
     if not args.no_cpu_baseline:
         print("timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_rows)

@@ -2041,7 +2041,9 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   // 0 (and discard it) when no cell of a wave needs boundary sums.
   w.cap = v ? (n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1) : 0;
   w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)cin * (size_t)w.cap));
-  w.nbt = reinterpret_cast<int32_t*>(take(v ? sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1) : 0));
+  // Also without a variant: the GEMM path gathers unit voxels' window sums
+  // through it.
+  w.nbt = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1)));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
   w.sgemm = reinterpret_cast<float*>(take(oci::conv_gemm_buffer(n_leaves, cin)));
@@ -2077,13 +2079,14 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
                      a.weight, a.cin, a.cout, w.wt);
   const MfmaVariant* v = find_variant(a.cin, a.cout);
-  if (v == nullptr) return hipGetLastError();
-  hipLaunchKernelGGL(v->weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
-                     a.weight, a.cout, w.wm);
-  hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256)), dim3(256), 0,
-                     s, a.weight, a.cout, w.wc);
-  hipLaunchKernelGGL(v->eff_weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
-                     a.weight, a.cout, 8, w.w8);
+  if (v != nullptr) {
+    hipLaunchKernelGGL(v->weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
+                       a.weight, a.cout, w.wm);
+    hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256)), dim3(256), 0,
+                       s, a.weight, a.cout, w.wc);
+    hipLaunchKernelGGL(v->eff_weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
+                       a.weight, a.cout, 8, w.w8);
+  }
   const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
@@ -2131,7 +2134,9 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
   const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
-  if (impl == 3) return launch_conv_gemm(a, w.info, w.wt, w.sgemm, s);
+  if (impl == 3)
+    return launch_conv_gemm(a, w.info, w.wt, w.sgemm, w.nbt, w.pre[0], (const int64_t*)(w.pre[0] + a.n_trees),
+                            s);
   if (impl != 2) {
     const unsigned blocks = (unsigned)(all_tiles < 65536 ? all_tiles : 65536);
     hipLaunchKernelGGL(k_conv_generic, dim3(blocks), dim3(kThreads), gsmem, s, a.trees, a.prefix,

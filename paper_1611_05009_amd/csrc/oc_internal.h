@@ -104,7 +104,11 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
 hipError_t launch_conv_truncated(const ConvArgs& a, uint64_t* info, hipStream_t s);
 // Bytes of the window-sum buffer of the GEMM path (one row chunk).
 size_t conv_gemm_buffer(int64_t n_leaves, int cin);
+// nbt, gpre, n_groups: the unit-group neighbourhood table, the per-tree
+// group prefix and the group count of the preparation (unit voxels' window
+// sums are gathered through them).
 hipError_t launch_conv_gemm(const ConvArgs& a, const uint64_t* info, const float* wt, float* sbuf,
+                            const int32_t* nbt, const int64_t* gpre, const int64_t* n_groups,
                             hipStream_t s);
 
 // Convolution gradients (bias and ReLU excluded): any of dx, dweight, dbias
