@@ -44,7 +44,9 @@ __global__ void __launch_bounds__(256) k_ten2oc(const uint32_t* __restrict__ tre
   const int64_t W = 8LL * gw, H = 8LL * gh, D = 8LL * gd;
   const int64_t row0 = prefix[t];
   int base = 0;
-  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+  // No split depth-2 node: no leaf past position 72.
+  const int nend = (((b.lo >> 9) != 0ull) || b.hi) ? kNodes : 73;
+  for (int c0 = 0; c0 < nend; c0 += 64) {
     const int i = c0 + lane_id();
     const bool leaf = i < kNodes && is_leaf(b, i);
     const uint64_t m = __ballot(leaf);
@@ -106,7 +108,9 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
   const Bits ob = load_bits(out_trees, t);
   const int64_t row0 = out_prefix[t];
   int base = 0;
-  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+  // No split depth-2 node: no leaf past position 72.
+  const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
+  for (int c0 = 0; c0 < nend; c0 += 64) {
     const int i = c0 + lane_id();
     const bool leaf = i < kNodes && is_leaf(ob, i);
     const uint64_t m = __ballot(leaf);
@@ -223,7 +227,9 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
     const Bits ob = load_bits(out_trees, t);
     const int64_t row0 = out_prefix[t];
     int base = 0;
-    for (int c0 = 1; c0 < kNodes; c0 += 64) {
+    // No split depth-2 node: no leaf past position 72.
+    const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
+    for (int c0 = 1; c0 < nend; c0 += 64) {
       const int i = c0 + lane;
       const bool leaf = i < kNodes && is_leaf(ob, i);
       const uint64_t m = __ballot(leaf);
@@ -282,7 +288,9 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
   const Bits ob = load_bits(out_trees, t);
   const int64_t row0 = out_prefix[t];
   int base = 0;
-  for (int c0 = 0; c0 < kNodes; c0 += 64) {
+  // No split depth-2 node: no leaf past position 72.
+  const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
+  for (int c0 = 0; c0 < nend; c0 += 64) {
     const int i = c0 + lane_id();
     const bool leaf = i < kNodes && is_leaf(ob, i);
     uint64_t m = __ballot(leaf);
@@ -371,7 +379,9 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
       continue;
     }
     int base = 0;
-    for (int c0 = 1; c0 < kNodes; c0 += 64) {
+    // No split depth-2 node: no leaf past position 72.
+    const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
+    for (int c0 = 1; c0 < nend; c0 += 64) {
       const int i = c0 + lane;
       const bool leaf = i < kNodes && is_leaf(ob, i);
       const uint64_t m = __ballot(leaf);
