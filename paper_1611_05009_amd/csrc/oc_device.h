@@ -119,6 +119,16 @@ struct TreePos {
 
 __device__ __forceinline__ TreePos tree_pos(int64_t t, int gd, int gh, int gw) {
   TreePos p;
+  if ((uint64_t)t < (1ull << 32)) {
+    // 32-bit divisions (every grid here has fewer than 2^32 trees; the
+    // 64-bit ones cost several times more).
+    uint32_t u = (uint32_t)t;
+    p.w = (int)(u % (uint32_t)gw); u /= (uint32_t)gw;
+    p.h = (int)(u % (uint32_t)gh); u /= (uint32_t)gh;
+    p.d = (int)(u % (uint32_t)gd); u /= (uint32_t)gd;
+    p.n = (int64_t)u;
+    return p;
+  }
   p.w = (int)(t % gw); t /= gw;
   p.h = (int)(t % gh); t /= gh;
   p.d = (int)(t % gd); t /= gd;
