@@ -74,34 +74,64 @@ __global__ void __launch_bounds__(256) k_ten2oc(const uint32_t* __restrict__ tre
   }
 }
 
-// Copy (or max over 8 consecutive rows) of leaf rows, lanes over channels.
-// Each lane first resolves one output leaf of the current 64-position chunk;
-// the wave then walks those leaves one by one.
-__device__ __forceinline__ void copy_rows(uint64_t m, int64_t out_row, int64_t src_row, int nmax,
-                                          const float* __restrict__ in, int c,
-                                          float* __restrict__ out) {
-  while (m) {
-    const int j = __ffsll((unsigned long long)m) - 1;
-    m &= m - 1;
-    const int64_t orow = __shfl(out_row, j, 64);
-    const int64_t srow = __shfl(src_row, j, 64);
-    const int nm = __shfl(nmax, j, 64);
-    for (int k = lane_id(); k < c; k += 64) {
-      const float* s = in + srow * c + k;
-      float v = s[0];
-      for (int r = 1; r < nm; ++r) v = fmaxf(v, s[(int64_t)r * c]);
-      out[orow * c + k] = v;
+// Copy (or max over 8 consecutive rows) of the leaf rows marked in m (lane
+// j of m holds out_row, src_row, nmax): the leaves are compacted into the
+// wave's LDS slots, then handled W floats per lane with several leaves side
+// by side (16 leaves per instruction for 16 channels and W = 4).
+template <int W>
+__device__ __forceinline__ void pool_leaf_rows(uint64_t m, int64_t out_row, int64_t src_row, int nmax,
+                                               const float* __restrict__ in, int c,
+                                               float* __restrict__ out, int64_t* slots) {
+  const int nl = __popcll(m);
+  if (nl == 0) return;
+  const int lane = lane_id();
+  if ((m >> lane) & 1ull) {
+    const int k = __popcll(m & lanemask_lt());
+    slots[3 * k] = out_row;
+    slots[3 * k + 1] = src_row;
+    slots[3 * k + 2] = nmax;
+  }
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  const int ne = c / W;
+  const int lpr = ne < 64 ? ne : 64;
+  const int rpi = 64 / lpr;
+  const int q0 = lane % lpr, rsub = lane / lpr;
+  typedef typename VecF<W>::type T;
+  for (int r0 = 0; r0 < nl; r0 += rpi) {
+    const int r = r0 + rsub;
+    if (rsub < rpi && r < nl) {
+      const int64_t o = slots[3 * r], sr = slots[3 * r + 1];
+      const int nm = (int)slots[3 * r + 2];
+      for (int q = q0; q < ne; q += lpr) {
+        const T* src = reinterpret_cast<const T*>(in + sr * c) + q;
+        T v = src[0];
+        for (int k = 1; k < nm; ++k) {
+          const T x = src[(int64_t)k * ne];
+          if constexpr (W == 4) {
+            v.x = fmaxf(v.x, x.x); v.y = fmaxf(v.y, x.y); v.z = fmaxf(v.z, x.z); v.w = fmaxf(v.w, x.w);
+          } else {
+            v = fmaxf(v, x);
+          }
+        }
+        reinterpret_cast<T*>(out + o * c)[q] = v;
+      }
     }
   }
+  __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next call
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 }
 
 // Eq. 10 data: one wave per output tree.
+template <int W>
 __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ in_trees,
                                                   const int64_t* __restrict__ in_prefix, int64_t n_out,
                                                   int gd, int gh, int gw, const float* __restrict__ in,
                                                   int c, const uint32_t* __restrict__ out_trees,
                                                   const int64_t* __restrict__ out_prefix,
                                                   float* __restrict__ out) {
+  __shared__ int64_t slots_all[4][3 * 64];
+  int64_t* slots = slots_all[threadIdx.x >> 6];
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= n_out) return;
   const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
@@ -135,7 +165,7 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    copy_rows(m, orow, srow, nmax, in, c, out);
+    pool_leaf_rows<W>(m, orow, srow, nmax, in, c, out, slots);
     base += __popcll(m);
   }
 }
@@ -282,6 +312,8 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
     int gd, int gh, int gw, const float* __restrict__ in, int c,
     const uint32_t* __restrict__ out_trees, const int64_t* __restrict__ out_prefix,
     const float* __restrict__ dy, float* __restrict__ din) {
+  __shared__ int64_t slots_all[4][3 * 64];
+  int64_t* slots = slots_all[threadIdx.x >> 6];
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= n_out) return;
   const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
@@ -316,13 +348,24 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    while (m) {
-      const int j = __ffsll((unsigned long long)m) - 1;
-      m &= m - 1;
-      const int64_t orj = __shfl(orow, j, 64);
-      const int64_t srj = __shfl(srow, j, 64);
-      const int nm = __shfl(nmax, j, 64);
-      for (int k = lane_id(); k < c; k += 64) {
+    // The leaves of this chunk, compacted into LDS, several side by side
+    // (as the forward): lanes over (leaf, channel).
+    if ((m >> lane_id()) & 1ull) {
+      const int k = __popcll(m & lanemask_lt());
+      slots[3 * k] = orow;
+      slots[3 * k + 1] = srow;
+      slots[3 * k + 2] = nmax;
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int lpr = c < 64 ? c : 64, rpi = 64 / lpr;
+    const int q0 = lane_id() % lpr, rsub = lane_id() / lpr;
+    for (int r0 = 0; r0 < nleaf; r0 += rpi) {
+      const int rl = r0 + rsub;
+      if (rsub >= rpi || rl >= nleaf) continue;
+      const int64_t orj = slots[3 * rl], srj = slots[3 * rl + 1];
+      const int nm = (int)slots[3 * rl + 2];
+      for (int k = q0; k < c; k += lpr) {
         const float g = dy[orj * c + k];
         if (nm == 1) {
           din[srj * c + k] = g;
@@ -338,6 +381,8 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
         }
       }
     }
+    __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next chunk
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     base += nleaf;
   }
 }
@@ -484,8 +529,14 @@ hipError_t launch_pool_max(const uint32_t* in_trees, const int64_t* in_prefix, i
                            int gh, int gw, const float* in, int c, const uint32_t* out_trees,
                            const int64_t* out_prefix, float* out, hipStream_t s) {
   const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
-  hipLaunchKernelGGL(k_pool_max, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
-                     gd, gh, gw, in, c, out_trees, out_prefix, out);
+  const bool vec = c % 4 == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(out) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_pool_max<4>, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
+                       gd, gh, gw, in, c, out_trees, out_prefix, out);
+  else
+    hipLaunchKernelGGL(k_pool_max<1>, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix, no,
+                       gd, gh, gw, in, c, out_trees, out_prefix, out);
   return hipGetLastError();
 }
 
