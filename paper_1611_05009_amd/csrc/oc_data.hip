@@ -74,22 +74,54 @@ __global__ void __launch_bounds__(256) k_ten2oc(const uint32_t* __restrict__ tre
   }
 }
 
-// Copy (or max over 8 consecutive rows) of the leaf rows marked in m (lane
-// j of m holds out_row, src_row, nmax): the leaves are compacted into the
-// wave's LDS slots, then handled W floats per lane with several leaves side
-// by side (16 leaves per instruction for 16 channels and W = 4).
+// W consecutive floats of a row, held as an array so that each component can
+// be handled on its own.
+template <int W> struct Vec { float v[W]; };
+
 template <int W>
-__device__ __forceinline__ void pool_leaf_rows(uint64_t m, int64_t out_row, int64_t src_row, int nmax,
-                                               const float* __restrict__ in, int c,
-                                               float* __restrict__ out, int64_t* slots) {
+__device__ __forceinline__ Vec<W> vload(const float* __restrict__ p) {
+  Vec<W> r;
+  if constexpr (W == 4) {
+    const float4 x = *reinterpret_cast<const float4*>(p);
+    r.v[0] = x.x; r.v[1] = x.y; r.v[2] = x.z; r.v[3] = x.w;
+  } else {
+    r.v[0] = *p;
+  }
+  return r;
+}
+
+template <int W>
+__device__ __forceinline__ void vstore(float* __restrict__ p, const Vec<W>& r) {
+  if constexpr (W == 4) *reinterpret_cast<float4*>(p) = make_float4(r.v[0], r.v[1], r.v[2], r.v[3]);
+  else *p = r.v[0];
+}
+
+// What leaf_rows does with one leaf (dst, src, nm), nm being 1 or 8:
+//   kRowMax:    out[dst] = max over k < nm of in[src + k] (pooling; nm = 1 copies)
+//   kRowSum:    out[dst] = in[src] + in[src + 1] + ... in that order (unpooling
+//               gradient; nm = 1 copies)
+//   kRowCopy:   out[dst] = in[src] (nm must be 1)
+//   kRowArgmax: dst is an output row and src the first of its nm input rows:
+//               out[src + k] = in[dst] where x[src + k] is the first maximum
+//               of x[src .. src + nm - 1] (per channel), else 0 (pooling gradient)
+enum RowOp { kRowMax, kRowSum, kRowCopy, kRowArgmax };
+
+// The row operation on the leaves marked in m (lane j of m holds dst, src,
+// nm): the leaves are compacted into the wave's LDS slots, then handled W
+// floats per lane with several leaves side by side (16 leaves per
+// instruction for 16 channels and W = 4).
+template <int W, int OP>
+__device__ __forceinline__ void leaf_rows(uint64_t m, int64_t dst, int64_t src, int nm,
+                                          const float* __restrict__ in, const float* __restrict__ x,
+                                          int c, float* __restrict__ out, int64_t* slots) {
   const int nl = __popcll(m);
   if (nl == 0) return;
   const int lane = lane_id();
   if ((m >> lane) & 1ull) {
     const int k = __popcll(m & lanemask_lt());
-    slots[3 * k] = out_row;
-    slots[3 * k + 1] = src_row;
-    slots[3 * k + 2] = nmax;
+    slots[3 * k] = dst;
+    slots[3 * k + 1] = src;
+    slots[3 * k + 2] = nm;
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -97,24 +129,58 @@ __device__ __forceinline__ void pool_leaf_rows(uint64_t m, int64_t out_row, int6
   const int lpr = ne < 64 ? ne : 64;
   const int rpi = 64 / lpr;
   const int q0 = lane % lpr, rsub = lane / lpr;
-  typedef typename VecF<W>::type T;
   for (int r0 = 0; r0 < nl; r0 += rpi) {
     const int r = r0 + rsub;
     if (rsub < rpi && r < nl) {
-      const int64_t o = slots[3 * r], sr = slots[3 * r + 1];
-      const int nm = (int)slots[3 * r + 2];
+      const int64_t d = slots[3 * r], sr = slots[3 * r + 1];
+      const bool one = slots[3 * r + 2] == 1;
       for (int q = q0; q < ne; q += lpr) {
-        const T* src = reinterpret_cast<const T*>(in + sr * c) + q;
-        T v = src[0];
-        for (int k = 1; k < nm; ++k) {
-          const T x = src[(int64_t)k * ne];
-          if constexpr (W == 4) {
-            v.x = fmaxf(v.x, x.x); v.y = fmaxf(v.y, x.y); v.z = fmaxf(v.z, x.z); v.w = fmaxf(v.w, x.w);
-          } else {
-            v = fmaxf(v, x);
+        const int64_t e = (int64_t)q * W;
+        if constexpr (OP == kRowArgmax) {
+          const Vec<W> g = vload<W>(in + d * c + e);
+          if (one) {
+            vstore<W>(out + sr * c + e, g);
+            continue;
           }
+          Vec<W> xs[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) xs[k] = vload<W>(x + (sr + k) * c + e);
+          int arg[W];
+          float best[W];
+#pragma unroll
+          for (int j = 0; j < W; ++j) {
+            best[j] = xs[0].v[j];
+            arg[j] = 0;
+          }
+#pragma unroll
+          for (int k = 1; k < 8; ++k)
+#pragma unroll
+            for (int j = 0; j < W; ++j)
+              if (xs[k].v[j] > best[j]) {
+                best[j] = xs[k].v[j];
+                arg[j] = k;
+              }
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            Vec<W> o;
+#pragma unroll
+            for (int j = 0; j < W; ++j) o.v[j] = arg[j] == k ? g.v[j] : 0.f;
+            vstore<W>(out + (sr + k) * c + e, o);
+          }
+        } else {
+          Vec<W> v = vload<W>(in + sr * c + e);
+          if (OP != kRowCopy && !one) {
+            Vec<W> u[7];
+#pragma unroll
+            for (int k = 0; k < 7; ++k) u[k] = vload<W>(in + (sr + 1 + k) * c + e);
+#pragma unroll
+            for (int k = 0; k < 7; ++k)
+#pragma unroll
+              for (int j = 0; j < W; ++j)
+                v.v[j] = OP == kRowMax ? fmaxf(v.v[j], u[k].v[j]) : v.v[j] + u[k].v[j];
+          }
+          vstore<W>(out + d * c + e, v);
         }
-        reinterpret_cast<T*>(out + o * c)[q] = v;
       }
     }
   }
@@ -165,47 +231,9 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    pool_leaf_rows<W>(m, orow, srow, nmax, in, c, out, slots);
+    leaf_rows<W, kRowMax>(m, orow, srow, nmax, in, nullptr, c, out, slots);
     base += __popcll(m);
   }
-}
-
-// Row copies for the leaves marked in m (lane j of m holds out_row, src_row):
-// the leaves are compacted into the wave's LDS slots, then copied W floats
-// per lane with several rows side by side (8 rows per instruction for 32
-// channels and W = 4).
-template <int W>
-__device__ __forceinline__ void copy_leaf_rows(uint64_t m, int64_t out_row, int64_t src_row,
-                                               const float* __restrict__ in, int c,
-                                               float* __restrict__ out, int64_t* slots) {
-  const int nl = __popcll(m);
-  if (nl == 0) return;
-  const int lane = lane_id();
-  if ((m >> lane) & 1ull) {
-    const int k = __popcll(m & lanemask_lt());
-    slots[2 * k] = out_row;
-    slots[2 * k + 1] = src_row;
-  }
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-  const int ne = c / W;  // W-float elements per row
-  const int lpr = ne < 64 ? ne : 64;
-  const int rpi = 64 / lpr;
-  const int q0 = lane % lpr, rsub = lane / lpr;
-  for (int r0 = 0; r0 < nl; r0 += rpi) {
-    const int r = r0 + rsub;
-    if (rsub < rpi && r < nl) {
-      const int64_t o = slots[2 * r], sr = slots[2 * r + 1];
-      for (int q = q0; q < ne; q += lpr) {
-        if constexpr (W == 4)
-          reinterpret_cast<float4*>(out + o * c)[q] = reinterpret_cast<const float4*>(in + sr * c)[q];
-        else
-          out[o * c + q] = in[sr * c + q];
-      }
-    }
-  }
-  __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next call
-  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 }
 
 // Eq. 12 data (plain or guided): one wave per input tree and its 8 output
@@ -220,7 +248,7 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
                                                 int c, const uint32_t* __restrict__ out_trees,
                                                 const int64_t* __restrict__ out_prefix,
                                                 float* __restrict__ out) {
-  __shared__ int64_t slots_all[4][128];
+  __shared__ int64_t slots_all[4][3 * 64];
   const int wave = threadIdx.x >> 6;
   const int64_t ti = (int64_t)blockIdx.x * 4 + wave;
   if (ti >= n_in) return;  // whole wave exits together
@@ -249,7 +277,7 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
   }
   const uint64_t singles = __ballot(single);
   const uint64_t split = __ballot(lane < 8 && !single);
-  copy_leaf_rows<W>(singles, orow, srow, in, c, out, slots);
+  leaf_rows<W, kRowCopy>(singles, orow, srow, 1, in, nullptr, c, out, slots);
   // Split output trees.
   for (uint32_t sm = (uint32_t)split; sm; sm &= sm - 1) {
     const int o = __ffs(sm) - 1;
@@ -273,7 +301,7 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
         else node = 73 + 64 * o + ((i - 73) >> 3);     // guided depth 3 <- same voxel
         ls = in_row0 + data_idx(ib, node);
       }
-      copy_leaf_rows<W>(m, lo, ls, in, c, out, slots);
+      leaf_rows<W, kRowCopy>(m, lo, ls, 1, in, nullptr, c, out, slots);
       base += __popcll(m);
     }
   }
@@ -307,6 +335,7 @@ __global__ void k_relu_scalar(float* __restrict__ x, int64_t count) {
 // the first voxel (in child order) holding the maximum and 0 to the others.
 // Every input leaf has exactly one output leaf, so every row of din is
 // written once.  One wave per output tree, as the forward kernel.
+template <int W>
 __global__ void __launch_bounds__(256) k_pool_max_bwd(
     const uint32_t* __restrict__ in_trees, const int64_t* __restrict__ in_prefix, int64_t n_out,
     int gd, int gh, int gw, const float* __restrict__ in, int c,
@@ -325,8 +354,7 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
   for (int c0 = 0; c0 < nend; c0 += 64) {
     const int i = c0 + lane_id();
     const bool leaf = i < kNodes && is_leaf(ob, i);
-    uint64_t m = __ballot(leaf);
-    const int nleaf = __popcll(m);
+    const uint64_t m = __ballot(leaf);
     int64_t orow = 0, srow = 0;
     int nmax = 1;
     if (leaf) {
@@ -348,81 +376,79 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    // The leaves of this chunk, compacted into LDS, several side by side
-    // (as the forward): lanes over (leaf, channel).
-    if ((m >> lane_id()) & 1ull) {
-      const int k = __popcll(m & lanemask_lt());
-      slots[3 * k] = orow;
-      slots[3 * k + 1] = srow;
-      slots[3 * k + 2] = nmax;
-    }
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    const int lpr = c < 64 ? c : 64, rpi = 64 / lpr;
-    const int q0 = lane_id() % lpr, rsub = lane_id() / lpr;
-    for (int r0 = 0; r0 < nleaf; r0 += rpi) {
-      const int rl = r0 + rsub;
-      if (rsub >= rpi || rl >= nleaf) continue;
-      const int64_t orj = slots[3 * rl], srj = slots[3 * rl + 1];
-      const int nm = (int)slots[3 * rl + 2];
-      for (int k = q0; k < c; k += lpr) {
-        const float g = dy[orj * c + k];
-        if (nm == 1) {
-          din[srj * c + k] = g;
-        } else {
-          const float* sx = in + srj * c + k;
-          float v = sx[0];
-          int arg = 0;
-          for (int r = 1; r < 8; ++r) {
-            const float x = sx[(int64_t)r * c];
-            if (x > v) { v = x; arg = r; }
-          }
-          for (int r = 0; r < 8; ++r) din[(srj + r) * c + k] = r == arg ? g : 0.f;
-        }
-      }
-    }
-    __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next chunk
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    base += nleaf;
+    leaf_rows<W, kRowArgmax>(m, orow, srow, nmax, dy, in, c, din, slots);
+    base += __popcll(m);
   }
 }
 
 // Gradient of Eq. 12 (plain or guided): every input leaf receives the sum of
-// dy over the output leaves that copy it.  One wave per input tree walks its
-// 8 output trees in row order, as the forward kernel, and adds each output
-// row into its source row; the wave owns every source row it touches, so the
-// sums need no atomics and come out in the same order on every run.  din
-// must be zero on entry.
+// dy over the output leaves that copy it, in output row order.  One wave per
+// input tree, as the forward kernel; each input leaf is written once, from
+// what it gathers:
+//   - an unsplit input root: the 8 single-leaf output trees it spawned;
+//   - an output tree with a single leaf: that row (input node 1 + o);
+//   - in a split output tree, a leaf above depth 3: its own row (input leaf
+//     one level deeper); the 8 depth-3 leaves of a split depth-2 node (guided
+//     only): their 8 consecutive rows, summed into the input voxel that
+//     pooled them.
+// The output structure is the plain unpooling of the input or a guide that
+// pools to it, so every input leaf is covered.
+template <int W>
 __global__ void __launch_bounds__(256) k_unpool_bwd(
     const uint32_t* __restrict__ in_trees, const int64_t* __restrict__ in_prefix, int64_t n_in,
     int gd, int gh, int gw, int c, const uint32_t* __restrict__ out_trees,
     const int64_t* __restrict__ out_prefix, const float* __restrict__ dy, float* __restrict__ din) {
-  const int64_t ti = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (ti >= n_in) return;
+  __shared__ int64_t slots_all[4][3 * 64];
+  const int wave = threadIdx.x >> 6;
+  const int64_t ti = (int64_t)blockIdx.x * 4 + wave;
+  if (ti >= n_in) return;  // whole wave exits together
+  int64_t* slots = slots_all[wave];
   const int lane = lane_id();
   const TreePos p = tree_pos(ti, gd, gh, gw);
   const Bits ib = load_bits(in_trees, ti);
   const int64_t in_row0 = in_prefix[ti];
   const bool in_split = (ib.lo & 1ull) != 0;
   const int Gh = 2 * gh, Gw = 2 * gw, Gd = 2 * gd;
-  auto add_rows = [&](uint64_t m, int64_t lo, int64_t ls) {
-    while (m) {
-      const int j = __ffsll((unsigned long long)m) - 1;
-      m &= m - 1;
-      const int64_t orj = __shfl(lo, j, 64);
-      const int64_t srj = __shfl(ls, j, 64);
-      for (int k = lane; k < c; k += 64) din[srj * c + k] += dy[orj * c + k];
-    }
+  auto out_tree = [&](int o) {
+    return ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw + 2 * p.w +
+           (o & 1);
   };
-  for (int o = 0; o < 8; ++o) {
-    const int64_t t = ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw +
-                      2 * p.w + (o & 1);
+  bool single = false;
+  int64_t orow = 0, irow = 0;
+  if (lane < 8) {
+    const int64_t t = out_tree(lane);
+    const Bits ob = load_bits(out_trees, t);
+    single = !(ob.lo & 1ull);
+    orow = out_prefix[t];
+    irow = in_row0 + (in_split ? data_idx(ib, 1 + lane) : 0);
+  }
+  if (!in_split) {
+    int64_t r[8];
+#pragma unroll
+    for (int o = 0; o < 8; ++o) r[o] = __shfl(orow, o, 64);
+    const int ne = c / W;
+    for (int q = lane; q < ne; q += 64) {
+      const int64_t e = (int64_t)q * W;
+      Vec<W> v = vload<W>(dy + r[0] * c + e);
+      Vec<W> u[7];
+#pragma unroll
+      for (int o = 0; o < 7; ++o) u[o] = vload<W>(dy + r[o + 1] * c + e);
+#pragma unroll
+      for (int o = 0; o < 7; ++o)
+#pragma unroll
+        for (int j = 0; j < W; ++j) v.v[j] += u[o].v[j];
+      vstore<W>(din + in_row0 * c + e, v);
+    }
+    return;
+  }
+  const uint64_t singles = __ballot(lane < 8 && single);
+  const uint64_t split = __ballot(lane < 8 && !single);
+  leaf_rows<W, kRowCopy>(singles, irow, orow, 1, dy, nullptr, c, din, slots);
+  for (uint32_t sm = (uint32_t)split; sm; sm &= sm - 1) {
+    const int o = __ffs(sm) - 1;
+    const int64_t t = out_tree(o);
     const Bits ob = load_bits(out_trees, t);
     const int64_t row0 = out_prefix[t];
-    if (!(ob.lo & 1ull)) {  // a single output leaf
-      add_rows(1ull, row0, in_row0 + data_idx(ib, in_split ? 1 + o : 0));
-      continue;
-    }
     int base = 0;
     // No split depth-2 node: no leaf past position 72.
     const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
@@ -430,17 +456,27 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
       const int i = c0 + lane;
       const bool leaf = i < kNodes && is_leaf(ob, i);
       const uint64_t m = __ballot(leaf);
-      int64_t lo = 0, ls = 0;
-      if (leaf) {
-        lo = row0 + base + __popcll(m & lanemask_lt());
+      // Depth-3 leaves come as 8 siblings in consecutive rows (inside one
+      // 64-position chunk, as 73 + 8k and the chunk starts are 8-aligned
+      // relative to each other); the first one stands for all 8.
+      const bool head = leaf && (i < 73 || ((i - 73) & 7) == 0);
+      const uint64_t h = __ballot(head);
+      int64_t dst = 0, src = 0;
+      int nm = 1;
+      if (head) {
+        src = row0 + base + __popcll(m & lanemask_lt());
         int node;
-        if (!in_split) node = 0;
-        else if (i < 9) node = 9 + 8 * o + (i - 1);
-        else if (i < 73) node = 73 + 64 * o + (i - 9);
-        else node = 73 + 64 * o + ((i - 73) >> 3);
-        ls = in_row0 + data_idx(ib, node);
+        if (i < 9) {
+          node = 9 + 8 * o + (i - 1);        // depth 1 <- depth 2
+        } else if (i < 73) {
+          node = 73 + 64 * o + (i - 9);      // depth 2 <- depth-3 voxel
+        } else {
+          node = 73 + 64 * o + ((i - 73) >> 3);  // guided depth 3 <- same voxel
+          nm = 8;
+        }
+        dst = in_row0 + data_idx(ib, node);
       }
-      add_rows(m, lo, ls);
+      leaf_rows<W, kRowSum>(h, dst, src, nm, dy, nullptr, c, din, slots);
       base += __popcll(m);
     }
   }
@@ -491,11 +527,6 @@ __global__ void k_add(const float* a, const float* b, float* out, int64_t count)
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
     out[i] = a[i] + b[i];
-}
-
-__global__ void k_fill_zero(float* __restrict__ x, int64_t count) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) x[i] = 0.f;
 }
 
 // din = dy where the ReLU output y is positive, else 0.  din may alias dy.
@@ -573,8 +604,15 @@ hipError_t launch_pool_max_bwd(const uint32_t* in_trees, const int64_t* in_prefi
                                const int64_t* out_prefix, const float* dy, float* din,
                                hipStream_t s) {
   const int64_t no = (int64_t)n * (gd / 2) * (gh / 2) * (gw / 2);
-  hipLaunchKernelGGL(k_pool_max_bwd, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix,
-                     no, gd, gh, gw, in, c, out_trees, out_prefix, dy, din);
+  const bool vec = c % 4 == 0 && (reinterpret_cast<uintptr_t>(in) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(din) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_pool_max_bwd<4>, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix,
+                       no, gd, gh, gw, in, c, out_trees, out_prefix, dy, din);
+  else
+    hipLaunchKernelGGL(k_pool_max_bwd<1>, dim3(blocks_for(no, 4)), dim3(256), 0, s, in_trees, in_prefix,
+                       no, gd, gh, gw, in, c, out_trees, out_prefix, dy, din);
   return hipGetLastError();
 }
 
@@ -582,14 +620,16 @@ hipError_t launch_unpool_bwd(const uint32_t* in_trees, const int64_t* in_prefix,
                              int gh, int gw, int64_t in_n_leaves, int c, const uint32_t* out_trees,
                              const int64_t* out_prefix, const float* dy, float* din,
                              hipStream_t s) {
+  (void)in_n_leaves;  // every input row is written by the gather
   const int64_t ni = (int64_t)n * gd * gh * gw;
-  const int64_t count = in_n_leaves * c;
-  int64_t zb = (count + 255) / 256;
-  if (zb > 8192) zb = 8192;
-  if (zb < 1) zb = 1;
-  hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)zb), dim3(256), 0, s, din, count);
-  hipLaunchKernelGGL(k_unpool_bwd, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
-                     gd, gh, gw, c, out_trees, out_prefix, dy, din);
+  const bool vec = c % 4 == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(din) & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(k_unpool_bwd<4>, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
+                       gd, gh, gw, c, out_trees, out_prefix, dy, din);
+  else
+    hipLaunchKernelGGL(k_unpool_bwd<1>, dim3(blocks_for(ni, 4)), dim3(256), 0, s, in_trees, in_prefix, ni,
+                       gd, gh, gw, c, out_trees, out_prefix, dy, din);
   return hipGetLastError();
 }
 
