@@ -59,9 +59,9 @@ extern "C" {
 #define OC_POOL_MAX 1
 
 /* Convolution implementations (oc_conv3x3x3_ex). */
-#define OC_CONV_AUTO 0    /* OC_CONV_MFMA where supported, else OC_CONV_GEMM */
+#define OC_CONV_AUTO 0    /* OC_CONV_MFMA where a fused variant exists, or in channel blocks on >= 65536 leaves; else OC_CONV_GEMM */
 #define OC_CONV_GENERIC 1 /* any channel counts: window sums + VALU contraction */
-#define OC_CONV_MFMA 2    /* fp32 MFMA contraction; OC_EINVAL if unsupported */
+#define OC_CONV_MFMA 2    /* fused fp32 MFMA kernels; OC_EINVAL if unsupported */
 #define OC_CONV_GEMM 3    /* any channel counts: window sums of row chunks, then an fp32 MFMA GEMM */
 #define OC_CONV_TRUNCATED 4 /* the supplement's efficient convolution (constant part + truncated
                               kernels at boundary voxels), VALU; oc_conv3x3x3_ex only */
@@ -162,7 +162,13 @@ int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, in
                          int relu, float* out, const void* ws, size_t ws_bytes, int impl,
                          void* stream);
 
-/* Does OC_CONV_MFMA support (cin, cout)?  1 yes, 0 no. */
+/* Does OC_CONV_MFMA support (cin, cout)?  1 yes, 0 no.  Fused variants exist
+ * for cin in {4, 8, 16, 32} and cout in [5, 32].  Wider layers with cin a
+ * multiple of 32 and cout a multiple of 32 up to 256 (or a fused width below
+ * 32) run in channel blocks: Eq. 7 is a sum over input channels, so the
+ * layer is computed as (cin/32) x (cout/cb) fused 32 -> cb convolutions into
+ * partial outputs in the workspace, whose sums over input blocks (in block
+ * order), bias and ReLU one more kernel writes. */
 int oc_conv3x3x3_mfma_supported(int cin, int cout);
 
 /*

@@ -207,14 +207,14 @@ int conv_args(const char* who, const uint32_t* trees, const int64_t* prefix, int
   return OC_OK;
 }
 
-int conv_impl(const char* who, int impl, int cin, int cout, int* use) {
+int conv_impl(const char* who, int impl, int64_t n_leaves, int cin, int cout, int* use) {
   if (impl != OC_CONV_AUTO && impl != OC_CONV_GENERIC && impl != OC_CONV_MFMA && impl != OC_CONV_GEMM &&
       impl != OC_CONV_TRUNCATED)
     return fail(OC_EINVAL, "%s: bad impl %d", who, impl);
   const bool mfma_ok = oci::conv_mfma_supported(cin, cout);
   if (impl == OC_CONV_MFMA && !mfma_ok)
     return fail(OC_EINVAL, "%s: no MFMA kernel for (%d, %d)", who, cin, cout);
-  *use = impl == OC_CONV_AUTO ? (mfma_ok ? OC_CONV_MFMA : OC_CONV_GEMM) : impl;
+  *use = impl == OC_CONV_AUTO ? oci::conv_auto_impl(n_leaves, cin, cout) : impl;
   return OC_OK;
 }
 
@@ -245,7 +245,7 @@ int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, in
   if (rc != OC_OK) return rc;
   if (!in || !out) return fail(OC_EINVAL, "oc_conv3x3x3_execute: null pointer");
   int use = 0;
-  rc = conv_impl("oc_conv3x3x3_execute", impl, cin, cout, &use);
+  rc = conv_impl("oc_conv3x3x3_execute", impl, n_leaves, cin, cout, &use);
   if (rc != OC_OK) return rc;
   if (use == OC_CONV_TRUNCATED)
     return fail(OC_EINVAL, "oc_conv3x3x3_execute: OC_CONV_TRUNCATED runs through oc_conv3x3x3_ex");
@@ -265,7 +265,7 @@ int oc_conv3x3x3_ex(const uint32_t* trees, const int64_t* prefix, int n, int gd,
   if (rc != OC_OK) return rc;
   if (!in || !weight || !out) return fail(OC_EINVAL, "oc_conv3x3x3: null pointer");
   int use = 0;
-  rc = conv_impl("oc_conv3x3x3", impl, cin, cout, &use);
+  rc = conv_impl("oc_conv3x3x3", impl, n_leaves, cin, cout, &use);
   if (rc != OC_OK) return rc;
   a.in = in; a.weight = weight; a.bias = bias; a.relu = relu ? 1 : 0; a.out = out;
   hipStream_t s = as_stream(stream);

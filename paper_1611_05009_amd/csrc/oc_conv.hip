@@ -1820,6 +1820,9 @@ __global__ void k_eff_weights(const float* __restrict__ w, int cout, int sz,
   using C = MfmaCfg<CIN, NT, MS>;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= C::WFLOATS) return;
+  // Channel blocks: blockIdx.y selects a [cout][CIN][27] weight block.
+  w += (int64_t)blockIdx.y * cout * CIN * 27;
+  wm += (int64_t)blockIdx.y * C::WFLOATS;
   int q = idx;
   const int e = q % C::VEC; q /= C::VEC;
   const int lane = q % 64; q /= 64;
@@ -1854,6 +1857,9 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
   using C = MfmaCfg<CIN, NT, MS>;
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= C::WFLOATS) return;
+  // Channel blocks: blockIdx.y selects a [cout][CIN][27] weight block.
+  w += (int64_t)blockIdx.y * cout * CIN * 27;
+  wm += (int64_t)blockIdx.y * C::WFLOATS;
   int r = idx;
   const int e = r % C::VEC; r /= C::VEC;
   const int lane = r % 64; r /= 64;
@@ -1938,6 +1944,76 @@ const MfmaVariant* find_variant(int cin, int cout) {
   return nullptr;
 }
 
+// Channel blocks for layers without a fused variant: cin a multiple of 32 and
+// cout a multiple of 32 up to 256 (or below 32 with a variant of its own).
+// Eq. 7 sums over input channels, so the layer is the sum over j of the
+// convolutions of input channels [32j, 32j + 32) with the matching weight
+// columns: it runs as J x K fused 32 -> cb convolutions into partial outputs
+// [J][K][n_leaves][cb], and one kernel adds each output block's J partials in
+// order, then the bias and the ReLU.
+struct Blocks {
+  const MfmaVariant* v;  // the 32 -> cb variant; null when not blocked
+  int J, K, cb;
+};
+
+Blocks conv_blocks(int cin, int cout) {
+  Blocks b{nullptr, 0, 0, 0};
+  if (find_variant(cin, cout) != nullptr || cin % 32 != 0 || cin > 256 || cout > 256) return b;
+  const int cb = cout % 32 == 0 ? 32 : cout;
+  if (cb != 32 && cout > 32) return b;
+  b.v = find_variant(32, cb);
+  if (b.v == nullptr) return b;
+  b.J = cin / 32;
+  b.K = cout / cb;
+  b.cb = cb;
+  return b;
+}
+
+// Weight blocks: wb[(j K + k)][co][ci][t] = w[cb k + co][32 j + ci][t].
+__global__ void k_weight_blocks(const float* __restrict__ w, int cin, int cout, int cb,
+                                float* __restrict__ wb) {
+  const int64_t n = 27LL * cin * cout;
+  const int K = cout / cb;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    int64_t r = i;
+    const int t = (int)(r % 27); r /= 27;
+    const int ci = (int)(r % 32); r /= 32;
+    const int co = (int)(r % cb); r /= cb;
+    const int k = (int)(r % K);
+    const int j = (int)(r / K);
+    wb[i] = w[((int64_t)(cb * k + co) * cin + 32 * j + ci) * 27 + t];
+  }
+}
+
+// xb[row][0..32) = x[row][32 j .. 32 j + 32): one float4 per thread (x and
+// xb 16-byte aligned, cin a multiple of 32).
+__global__ void k_channel_block(const float* __restrict__ x, int cin, int j, int64_t n_rows,
+                                float* __restrict__ xb) {
+  const int64_t n = n_rows * 8;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i >> 3;
+    const int q = (int)(i & 7);
+    reinterpret_cast<float4*>(xb)[i] = reinterpret_cast<const float4*>(x + row * cin + 32 * j)[q];
+  }
+}
+
+// out[row][cb k + c] = act(bias + sum over j (in order) of part[j][k][row][c]).
+__global__ void k_block_reduce(const float* __restrict__ part, int J, int K, int cb, int64_t n_rows,
+                               const float* __restrict__ bias, int relu, float* __restrict__ out) {
+  const int cout = K * cb;
+  const int64_t n = n_rows * cout;
+  const int64_t pstride = n_rows * cout;  // one j
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t row = i / cout;
+    const int co = (int)(i - row * cout);
+    const int k = co / cb, c = co - k * cb;
+    const int64_t pi = ((int64_t)k * n_rows + row) * cb + c;
+    float v = bias ? bias[co] : 0.f;
+    for (int j = 0; j < J; ++j) v += part[(int64_t)j * pstride + pi];
+    out[i] = relu ? fmaxf(v, 0.f) : v;
+  }
+}
+
 constexpr int kMfmaThreads = 512;
 
 // Chunks of trees for the boundary sums and the cells that read them (one:
@@ -2010,6 +2086,9 @@ struct ConvWs {
   int64_t ccap;
   uint32_t* smask;
   float* sgemm;  // window sums of one row chunk (GEMM path)
+  float* wblk;   // channel blocks: weight blocks, one input block, partial outputs
+  float* xblk;
+  float* part;
   size_t total;
 };
 
@@ -2023,12 +2102,18 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
     off += align256(bytes);
     return q;
   };
+  // The fused kernels' variant: the layer's own, or the 32 -> cb one of its
+  // channel blocks (one weight layout per block, 32-channel boundary sums).
+  const Blocks bl = conv_blocks(cin, cout);
   const MfmaVariant* v = find_variant(cin, cout);
+  const size_t nwl = v ? 1 : (bl.v ? (size_t)bl.J * bl.K : 0);
+  const int kcin = v ? cin : 32;
+  if (!v) v = bl.v;
   w.info = reinterpret_cast<uint64_t*>(take(sizeof(uint64_t) * (size_t)n_leaves));
   w.wt = reinterpret_cast<float*>(take(sizeof(float) * 27 * (size_t)cin * cout));
-  w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
-  w.wc = reinterpret_cast<float*>(take(v ? sizeof(float) * v->cell_wfloats : 0));
-  w.w8 = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats : 0));
+  w.wm = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats * nwl : 0));
+  w.wc = reinterpret_cast<float*>(take(v ? sizeof(float) * v->cell_wfloats * nwl : 0));
+  w.w8 = reinterpret_cast<float*>(take(v ? sizeof(float) * v->wfloats * nwl : 0));
   for (int k = 0; k < kScans; ++k) {
     w.scan[k] = take(oci::scan_workspace(n_trees));
     w.pre[k] = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)(n_trees + 1)));
@@ -2040,7 +2125,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   // At least one slot where a variant exists: the cell kernels may read slot
   // 0 (and discard it) when no cell of a wave needs boundary sums.
   w.cap = v ? (n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1) : 0;
-  w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)cin * (size_t)w.cap));
+  w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)kcin * (size_t)w.cap));
   // Also without a variant: the GEMM path gathers unit voxels' window sums
   // through it.
   w.nbt = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1)));
@@ -2048,8 +2133,113 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
   w.sgemm = reinterpret_cast<float*>(take(oci::conv_gemm_buffer(n_leaves, cin)));
   w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
+  w.wblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 27 * (size_t)cin * cout : 0));
+  w.xblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 32 * (size_t)n_leaves : 0));
+  w.part = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * (size_t)bl.J * n_leaves * cout : 0));
   w.total = off + 256;
   return w;
+}
+
+// Output side of one fused pass: weight layouts, bias, width, ReLU and the
+// [n_leaves][cout] destination.
+struct FusedOut {
+  const float* wm;
+  const float* wc;
+  const float* w8;
+  const float* bias;
+  int cout, relu;
+  float* out;
+};
+
+constexpr int kMaxOutBlocks = 8;
+#ifndef OC_BLOCKED_MIN_LEAVES
+#define OC_BLOCKED_MIN_LEAVES 65536
+#endif
+constexpr int64_t kBlockedMinLeaves = OC_BLOCKED_MIN_LEAVES;
+
+// The fused kernels of variant v on input `in` (v->cin channels; in_bytes its
+// size) for each of the n_outs outputs: unit voxels, edge-8 cells with
+// unsplit neighbours and edge-2 cells, then the boundary sums of split nodes
+// (once, they depend on the input only) and the edge-8 and edge-4 cells that
+// read them.
+hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant* v, const float* in,
+                      uint32_t in_bytes, const FusedOut* outs, int n_outs, hipStream_t s) {
+  const size_t wsmem = sizeof(float) * v->cell_wfloats;
+  const size_t msmem = mfma_smem(*v);
+  if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
+  const int nblk = ((g_num_cus + 7) / 8) * 8;
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
+  if (e != hipSuccess) return e;
+  // Edge-8 cells with unsplit face and edge neighbours: the gather-GEMM with
+  // effective weights (same LDS footprint as the unit kernel, no tables).
+  const size_t gsm = sizeof(float) * v->wfloats;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g),
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
+  if (e != hipSuccess) return e;
+  auto launch_cells = [&](int k, int64_t t0, int64_t t1, const FusedOut& o) -> hipError_t {
+    // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
+    const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
+    if (smem > g_max_smem) return hipErrorInvalidConfiguration;
+    const CellFn f = k == 1 || k == 0 ? v->cell8 : (k == 2 ? v->cell4 : v->cell2);
+    hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (r != hipSuccess) return r;
+    hipLaunchKernelGGL(f, dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
+                       a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
+                       (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
+                       (const float*)w.bsum, w.ccap, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out,
+                       (const int64_t*)w.pre[1 + k], t0, t1);
+    return hipGetLastError();
+  };
+  for (int i = 0; i < n_outs; ++i) {
+    const FusedOut& o = outs[i];
+    hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.n_leaves,
+                       (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), in, o.wm,
+                       in_bytes, o.bias, o.cout, o.relu, o.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(v->cell8g, dim3(nblk), dim3(kUnitThreads), gsm, s, a.n_leaves,
+                       (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes, w.ccap,
+                       in, o.w8, in_bytes, o.bias, o.cout, o.relu, o.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // Edge-2 cells (no boundary sums).
+    e = launch_cells(3, 0, a.n_trees, o);
+    if (e != hipSuccess) return e;
+  }
+  // Boundary sums and the cells that read them (other edge-8, edge-4), in
+  // chunks of trees: the sums of the trees up to a chunk's end plus one tree
+  // plane (every neighbour of its cells), then the chunk's cells, so that the
+  // sums they read were written moments before and are still cached.
+  const int64_t plane = (int64_t)a.gh * a.gw + a.gw + 1;
+  const int64_t per_block = 4 * (64 / v->cin);  // trees per pass of a 256-thread block
+  int64_t done = 0;
+  for (int c = 0; c < kSumChunks; ++c) {
+    const int64_t t0 = a.n_trees * c / kSumChunks, t1 = a.n_trees * (c + 1) / kSumChunks;
+    const int64_t need = c + 1 == kSumChunks ? a.n_trees : min(a.n_trees, t1 + plane);
+    if (need > done) {
+      int64_t blocks = (need - done + per_block - 1) / per_block;
+      if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
+      hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
+                         (const int32_t*)w.stl, (const int64_t*)w.meta,
+                         (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, in, in_bytes, w.bsum,
+                         (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need,
+                         (const uint32_t*)w.smask);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      done = need;
+    }
+    if (t1 > t0) {
+      for (int i = 0; i < n_outs; ++i) {
+        e = launch_cells(1, t0, t1, outs[i]);
+        if (e != hipSuccess) return e;
+        e = launch_cells(2, t0, t1, outs[i]);
+        if (e != hipSuccess) return e;
+      }
+    }
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -2062,11 +2252,20 @@ size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout) {
 
 bool conv_mfma_supported(int cin, int cout) {
   const MfmaVariant* v = find_variant(cin, cout);
+  if (!v) v = conv_blocks(cin, cout).v;
   if (!v) return false;
   // LDS: the whole weight set plus the neighbourhood rows of every wave must
   // fit one workgroup (160 KB on gfx950; the device is asked when present).
   const size_t limit = device_limits() == hipSuccess ? g_max_smem : 160 * 1024;
   return mfma_smem(*v) <= limit;
+}
+
+int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
+  if (!conv_mfma_supported(cin, cout)) return 3;
+  if (find_variant(cin, cout) != nullptr) return 2;
+  // Channel blocks pay J x K passes of about six launches each: on small
+  // structures the window-sum GEMM is faster.
+  return n_leaves >= kBlockedMinLeaves ? 2 : 3;
 }
 
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
@@ -2079,13 +2278,26 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
                      a.weight, a.cin, a.cout, w.wt);
   const MfmaVariant* v = find_variant(a.cin, a.cout);
-  if (v != nullptr) {
-    hipLaunchKernelGGL(v->weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
-                       a.weight, a.cout, w.wm);
-    hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256)), dim3(256), 0,
-                       s, a.weight, a.cout, w.wc);
-    hipLaunchKernelGGL(v->eff_weights, dim3((unsigned)((v->wfloats + 255) / 256)), dim3(256), 0, s,
-                       a.weight, a.cout, 8, w.w8);
+  const Blocks bl = conv_blocks(a.cin, a.cout);
+  if (v != nullptr || bl.v != nullptr) {
+    // Channel blocks: the layouts of every weight block, one grid row each.
+    const float* wsrc = a.weight;
+    int wcout = a.cout;
+    unsigned nb = 1;
+    if (v == nullptr) {
+      v = bl.v;
+      hipLaunchKernelGGL(k_weight_blocks, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s, a.weight,
+                         a.cin, a.cout, bl.cb, w.wblk);
+      wsrc = w.wblk;
+      wcout = bl.cb;
+      nb = (unsigned)(bl.J * bl.K);
+    }
+    hipLaunchKernelGGL(v->weights, dim3((unsigned)((v->wfloats + 255) / 256), nb), dim3(256), 0, s,
+                       wsrc, wcout, w.wm);
+    hipLaunchKernelGGL(v->cell_weights, dim3((unsigned)((v->cell_wfloats + 255) / 256), nb), dim3(256), 0,
+                       s, wsrc, wcout, w.wc);
+    hipLaunchKernelGGL(v->eff_weights, dim3((unsigned)((v->wfloats + 255) / 256), nb), dim3(256), 0, s,
+                       wsrc, wcout, 8, w.w8);
   }
   const unsigned tb = (unsigned)((a.n_trees + 255) / 256);
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
@@ -2127,9 +2339,12 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   if (e != hipSuccess) return e;
   const ConvWs w = carve(const_cast<void*>(ws), a.n_trees, a.n_leaves, a.cin, a.cout);
   // The MFMA kernels gather input rows with 16-byte buffer loads at 32-bit
-  // offsets below kOutside; otherwise the generic kernel runs.
-  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)a.cin * 4u;
-  if (impl == 2 && ((reinterpret_cast<uintptr_t>(a.in) & 15) != 0 || in_bytes64 >= kOutside)) impl = 1;
+  // offsets below kOutside; otherwise the generic kernel (or, for channel
+  // blocks, the GEMM path) runs.
+  const MfmaVariant* v = find_variant(a.cin, a.cout);
+  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)(v ? a.cin : 32) * 4u;
+  if (impl == 2 && ((reinterpret_cast<uintptr_t>(a.in) & 15) != 0 || in_bytes64 >= kOutside))
+    impl = v ? 1 : 3;
   const uint32_t in_bytes = (uint32_t)(in_bytes64 < kOutside ? in_bytes64 : 0);
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
@@ -2146,79 +2361,37 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   }
   e = device_limits();
   if (e != hipSuccess) return e;
-  const MfmaVariant* v = find_variant(a.cin, a.cout);
-  const size_t wsmem = sizeof(float) * v->cell_wfloats;
-  const size_t msmem = mfma_smem(*v);
-  if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
-  const int nblk = ((g_num_cus + 7) / 8) * 8;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.n_leaves,
-                     (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), a.in,
-                     (const float*)w.wm, in_bytes, a.bias, a.cout, a.relu, a.out);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // Edge-8 cells with unsplit face and edge neighbours: the gather-GEMM with
-  // effective weights (same LDS footprint as the unit kernel, no tables).
-  {
-    const size_t gsm = sizeof(float) * v->wfloats;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(v->cell8g, dim3(nblk), dim3(kUnitThreads), gsm, s, a.n_leaves,
-                       (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes,
-                       w.ccap, a.in, (const float*)w.w8, in_bytes, a.bias, a.cout, a.relu, a.out);
-    e = hipGetLastError();
+  if (v != nullptr) {
+    const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu, a.out};
+    return fused_pass(a, w, v, a.in, in_bytes, &o, 1, s);
+  }
+  // Channel blocks: per input block j (copied to a dense [n_leaves][32]
+  // array unless it is the whole input), the boundary sums once and the K
+  // output blocks' kernels into their partials; then the ordered sums.
+  const Blocks bl = conv_blocks(a.cin, a.cout);
+  if (bl.v == nullptr || bl.K > kMaxOutBlocks) return hipErrorInvalidValue;
+  const int64_t n = a.n_leaves;
+  for (int j = 0; j < bl.J; ++j) {
+    const float* xin = a.in;
+    if (bl.J > 1) {
+      int64_t nb = (n * 8 + 255) / 256;
+      if (nb > 8LL * g_num_cus * 8) nb = 8LL * g_num_cus * 8;
+      hipLaunchKernelGGL(k_channel_block, dim3((unsigned)nb), dim3(256), 0, s, a.in, a.cin, j, n, w.xblk);
+      xin = w.xblk;
+    }
+    FusedOut outs[kMaxOutBlocks];
+    for (int k = 0; k < bl.K; ++k) {
+      const size_t b = (size_t)j * bl.K + k;
+      outs[k] = FusedOut{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
+                         nullptr, bl.cb, 0, w.part + b * (size_t)n * bl.cb};
+    }
+    e = fused_pass(a, w, bl.v, xin, in_bytes, outs, bl.K, s);
     if (e != hipSuccess) return e;
   }
-  auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
-    // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
-    const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
-    if (smem > g_max_smem) return hipErrorInvalidConfiguration;
-    const CellFn f = k == 1 || k == 0 ? v->cell8 : (k == 2 ? v->cell4 : v->cell2);
-    hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
-    if (r != hipSuccess) return r;
-    hipLaunchKernelGGL(f, dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
-                       a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
-                       (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
-                       (const float*)w.bsum, w.ccap, a.in, (const float*)w.wc, in_bytes, a.bias,
-                       a.cout, a.relu, a.out, (const int64_t*)w.pre[1 + k], t0, t1);
-    return hipGetLastError();
-  };
-  // Edge-2 cells (no boundary sums).
-  e = launch_cells(3, 0, a.n_trees);
-  if (e != hipSuccess) return e;
-  // Boundary sums and the cells that read them (other edge-8, edge-4), in
-  // chunks of trees: the sums of the trees up to a chunk's end plus one tree
-  // plane (every neighbour of its cells), then the chunk's cells, so that the
-  // sums they read were written moments before and are still cached.
-  const int64_t plane = (int64_t)a.gh * a.gw + a.gw + 1;
-  const int64_t per_block = 4 * (64 / a.cin);  // trees per pass of a 256-thread block
-  int64_t done = 0;
-  for (int c = 0; c < kSumChunks; ++c) {
-    const int64_t t0 = a.n_trees * c / kSumChunks, t1 = a.n_trees * (c + 1) / kSumChunks;
-    const int64_t need = c + 1 == kSumChunks ? a.n_trees : min(a.n_trees, t1 + plane);
-    if (need > done) {
-      int64_t blocks = (need - done + per_block - 1) / per_block;
-      if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
-      hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
-                         (const int32_t*)w.stl, (const int64_t*)w.meta,
-                         (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, a.in, in_bytes,
-                         w.bsum, (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need,
-                         (const uint32_t*)w.smask);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-      done = need;
-    }
-    if (t1 > t0) {
-      e = launch_cells(1, t0, t1);
-      if (e != hipSuccess) return e;
-      e = launch_cells(2, t0, t1);
-      if (e != hipSuccess) return e;
-    }
-  }
+  int64_t rb = (n * a.cout + 255) / 256;
+  if (rb > 8LL * g_num_cus * 8) rb = 8LL * g_num_cus * 8;
+  hipLaunchKernelGGL(k_block_reduce, dim3((unsigned)rb), dim3(256), 0, s, (const float*)w.part, bl.J, bl.K,
+                     bl.cb, n, a.bias, a.relu, a.out);
   return hipGetLastError();
 }
 

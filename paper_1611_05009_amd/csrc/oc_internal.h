@@ -93,6 +93,9 @@ struct ConvArgs {
 };
 size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout);
 bool conv_mfma_supported(int cin, int cout);
+// The implementation OC_CONV_AUTO runs: 2 (fused MFMA kernels, in channel
+// blocks for wide layers on large structures) or 3 (window-sum GEMM).
+int conv_auto_impl(int64_t n_leaves, int cin, int cout);
 // Structure- and weight-dependent preparation into the workspace (the
 // weight pointer of `a` is read, the features are not).
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);

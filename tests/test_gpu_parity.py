@@ -206,15 +206,22 @@ def test_conv_degenerate_structures(impl):
             assert_close(got, O.conv3(ref, x, w), "conv %s %s" % (impl, name))
 
 
-@pytest.mark.parametrize("cin,cout", [(64, 64), (128, 64), (256, 128), (64, 130)])
-def test_conv_wide_channels(cin, cout):
-    """Widths of the encoder-decoder's coarse levels (no fused variant: the
-    window-sum GEMM path under auto)."""
+@pytest.mark.parametrize("impl", ["auto", "mfma", "gemm"])
+@pytest.mark.parametrize("cin,cout", [(64, 64), (128, 64), (256, 128), (64, 130), (32, 64), (64, 8),
+                                      (96, 16), (64, 32)])
+def test_conv_wide_channels(cin, cout, impl):
+    """Widths of the encoder-decoder's coarse levels, which have no fused
+    variant: the window-sum GEMM path, and the fused kernels run in 32-channel
+    blocks ("mfma"; auto takes it on large structures only)."""
+    if impl == "mfma" and not oc.mfma_supported(cin, cout):
+        pytest.skip("no channel blocks for (%d, %d)" % (cin, cout))
     occ, ref, x, w, b = conv_case(5000 + cin + cout, cin, cout, shape=(2, 2, 3, 2))
     g = oc.build(dev(occ))
     want = O.conv3(ref, x, w, b)
-    got = host(oc.conv3x3x3(g, dev(x), dev(w), dev(b)))
-    assert_close(got, want, "conv auto %dx%d" % (cin, cout))
+    got = host(oc.conv3x3x3(g, dev(x), dev(w), dev(b), impl=impl))
+    assert_close(got, want, "conv %s %dx%d" % (impl, cin, cout))
+    got_r = host(oc.conv3x3x3(g, dev(x), dev(w), None, relu=True, impl=impl))
+    assert_close(got_r, np.maximum(O.conv3(ref, x, w, None), 0), "conv %s relu %dx%d" % (impl, cin, cout))
 
 
 def test_conv_closed_form_single_cell():
