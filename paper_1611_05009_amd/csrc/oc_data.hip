@@ -96,7 +96,7 @@ __device__ __forceinline__ void vstore(float* __restrict__ p, const Vec<W>& r) {
   else *p = r.v[0];
 }
 
-// What leaf_rows does with one leaf (dst, src, nm), nm being 1 or 8:
+// What slots_flush does with one leaf (dst, src, nm), nm being 1 or 8:
 //   kRowMax:    out[dst] = max over k < nm of in[src + k] (pooling; nm = 1 copies)
 //   kRowSum:    out[dst] = in[src] + in[src + 1] + ... in that order (unpooling
 //               gradient; nm = 1 copies)
@@ -106,23 +106,38 @@ __device__ __forceinline__ void vstore(float* __restrict__ p, const Vec<W>& r) {
 //               of x[src .. src + nm - 1] (per channel), else 0 (pooling gradient)
 enum RowOp { kRowMax, kRowSum, kRowCopy, kRowArgmax };
 
-// The row operation on the leaves marked in m (lane j of m holds dst, src,
-// nm): the leaves are compacted into the wave's LDS slots, then handled W
-// floats per lane with several leaves side by side (16 leaves per
-// instruction for 16 channels and W = 4).
-template <int W, int OP>
-__device__ __forceinline__ void leaf_rows(uint64_t m, int64_t dst, int64_t src, int nm,
-                                          const float* __restrict__ in, const float* __restrict__ x,
-                                          int c, float* __restrict__ out, int64_t* slots) {
-  const int nl = __popcll(m);
-  if (nl == 0) return;
+// Pending leaves of a wave in LDS: up to kSlotCap (dst, src, nm) triples.
+// Leaves are added a 64-position chunk at a time and handled once 64 or
+// more are pending (and at the end), so that a copy phase covers the leaves
+// of several chunks and trees.
+constexpr int kSlotCap = 128;
+
+struct Slots {
+  int64_t* s;
+  int count;  // wave-uniform
+};
+
+// Adds the leaves marked in m (lane j of m holds dst, src, nm).
+__device__ __forceinline__ void slots_add(Slots& sl, uint64_t m, int64_t dst, int64_t src, int nm) {
   const int lane = lane_id();
   if ((m >> lane) & 1ull) {
-    const int k = __popcll(m & lanemask_lt());
-    slots[3 * k] = dst;
-    slots[3 * k + 1] = src;
-    slots[3 * k + 2] = nm;
+    const int k = sl.count + __popcll(m & lanemask_lt());
+    sl.s[3 * k] = dst;
+    sl.s[3 * k + 1] = src;
+    sl.s[3 * k + 2] = nm;
   }
+  sl.count += __popcll(m);
+}
+
+// The row operation on every pending leaf, W floats per lane with several
+// leaves side by side (16 leaves per instruction for 16 channels and W = 4).
+template <int W, int OP>
+__device__ __forceinline__ void slots_flush(Slots& sl, const float* __restrict__ in,
+                                            const float* __restrict__ x, int c, float* __restrict__ out) {
+  const int nl = sl.count;
+  if (nl == 0) return;
+  const int64_t* slots = sl.s;
+  const int lane = lane_id();
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   const int ne = c / W;
@@ -184,8 +199,19 @@ __device__ __forceinline__ void leaf_rows(uint64_t m, int64_t dst, int64_t src, 
       }
     }
   }
-  __builtin_amdgcn_wave_barrier();  // the slots are rewritten by the next call
+  __builtin_amdgcn_wave_barrier();  // the slots are rewritten after this
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  sl.count = 0;
+}
+
+// Adds the leaves marked in m and runs the pending ones once 64 or more wait
+// (at most 63 + 64 < kSlotCap are then held).
+template <int W, int OP>
+__device__ __forceinline__ void slots_push(Slots& sl, uint64_t m, int64_t dst, int64_t src, int nm,
+                                           const float* __restrict__ in, const float* __restrict__ x,
+                                           int c, float* __restrict__ out) {
+  slots_add(sl, m, dst, src, nm);
+  if (sl.count >= 64) slots_flush<W, OP>(sl, in, x, c, out);
 }
 
 // Eq. 10 data: one wave per output tree.
@@ -196,8 +222,8 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
                                                   int c, const uint32_t* __restrict__ out_trees,
                                                   const int64_t* __restrict__ out_prefix,
                                                   float* __restrict__ out) {
-  __shared__ int64_t slots_all[4][3 * 64];
-  int64_t* slots = slots_all[threadIdx.x >> 6];
+  __shared__ int64_t slots_all[4][3 * kSlotCap];
+  Slots sl{slots_all[threadIdx.x >> 6], 0};
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= n_out) return;
   const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
@@ -231,9 +257,10 @@ __global__ void __launch_bounds__(256) k_pool_max(const uint32_t* __restrict__ i
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    leaf_rows<W, kRowMax>(m, orow, srow, nmax, in, nullptr, c, out, slots);
+    slots_push<W, kRowMax>(sl, m, orow, srow, nmax, in, nullptr, c, out);
     base += __popcll(m);
   }
+  slots_flush<W, kRowMax>(sl, in, nullptr, c, out);
 }
 
 // Eq. 12 data (plain or guided): one wave per input tree and its 8 output
@@ -248,42 +275,42 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
                                                 int c, const uint32_t* __restrict__ out_trees,
                                                 const int64_t* __restrict__ out_prefix,
                                                 float* __restrict__ out) {
-  __shared__ int64_t slots_all[4][3 * 64];
+  __shared__ int64_t slots_all[4][3 * kSlotCap];
   const int wave = threadIdx.x >> 6;
   const int64_t ti = (int64_t)blockIdx.x * 4 + wave;
   if (ti >= n_in) return;  // whole wave exits together
-  int64_t* slots = slots_all[wave];
+  Slots sl{slots_all[wave], 0};
   const int lane = lane_id();
   const TreePos p = tree_pos(ti, gd, gh, gw);
   const Bits ib = load_bits(in_trees, ti);
   const int64_t in_row0 = in_prefix[ti];
   const bool in_split = (ib.lo & 1ull) != 0;
   const int Gh = 2 * gh, Gw = 2 * gw, Gd = 2 * gd;
-  auto out_tree = [&](int o) {
-    return ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw + 2 * p.w +
-           (o & 1);
-  };
-  // Output trees with a single leaf.
+  // Lane o < 8 loads output tree o's bits and first row; split trees take
+  // them from that lane.
   bool single = false;
+  Bits obl{0ull, 0u};
   int64_t orow = 0, srow = 0;
   if (lane < 8) {
-    const int64_t t = out_tree(lane);
-    const Bits ob = load_bits(out_trees, t);
-    single = !(ob.lo & 1ull);
-    if (single) {
-      orow = out_prefix[t];
-      srow = in_row0 + data_idx(ib, in_split ? 1 + lane : 0);
-    }
+    const int o = lane;
+    const int64_t t = ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw +
+                      2 * p.w + (o & 1);
+    obl = load_bits(out_trees, t);
+    single = !(obl.lo & 1ull);
+    orow = out_prefix[t];
+    srow = in_row0 + data_idx(ib, in_split ? 1 + lane : 0);
   }
   const uint64_t singles = __ballot(single);
   const uint64_t split = __ballot(lane < 8 && !single);
-  leaf_rows<W, kRowCopy>(singles, orow, srow, 1, in, nullptr, c, out, slots);
+  // Output trees with a single leaf.
+  slots_add(sl, singles, orow, srow, 1);
   // Split output trees.
   for (uint32_t sm = (uint32_t)split; sm; sm &= sm - 1) {
     const int o = __ffs(sm) - 1;
-    const int64_t t = out_tree(o);
-    const Bits ob = load_bits(out_trees, t);
-    const int64_t row0 = out_prefix[t];
+    Bits ob;
+    ob.lo = __shfl(obl.lo, o, 64);
+    ob.hi = __shfl(obl.hi, o, 64);
+    const int64_t row0 = __shfl(orow, o, 64);
     int base = 0;
     // No split depth-2 node: no leaf past position 72.
     const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
@@ -301,10 +328,11 @@ __global__ void __launch_bounds__(256) k_unpool(const uint32_t* __restrict__ in_
         else node = 73 + 64 * o + ((i - 73) >> 3);     // guided depth 3 <- same voxel
         ls = in_row0 + data_idx(ib, node);
       }
-      leaf_rows<W, kRowCopy>(m, lo, ls, 1, in, nullptr, c, out, slots);
+      slots_push<W, kRowCopy>(sl, m, lo, ls, 1, in, nullptr, c, out);
       base += __popcll(m);
     }
   }
+  slots_flush<W, kRowCopy>(sl, in, nullptr, c, out);
 }
 
 __global__ void k_relu(float* __restrict__ x, int64_t count) {
@@ -341,8 +369,8 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
     int gd, int gh, int gw, const float* __restrict__ in, int c,
     const uint32_t* __restrict__ out_trees, const int64_t* __restrict__ out_prefix,
     const float* __restrict__ dy, float* __restrict__ din) {
-  __shared__ int64_t slots_all[4][3 * 64];
-  int64_t* slots = slots_all[threadIdx.x >> 6];
+  __shared__ int64_t slots_all[4][3 * kSlotCap];
+  Slots sl{slots_all[threadIdx.x >> 6], 0};
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= n_out) return;
   const TreePos p = tree_pos(t, gd / 2, gh / 2, gw / 2);
@@ -376,9 +404,10 @@ __global__ void __launch_bounds__(256) k_pool_max_bwd(
       }
       srow = in_prefix[ti] + data_idx(ib, node);
     }
-    leaf_rows<W, kRowArgmax>(m, orow, srow, nmax, dy, in, c, din, slots);
+    slots_push<W, kRowArgmax>(sl, m, orow, srow, nmax, dy, in, c, din);
     base += __popcll(m);
   }
+  slots_flush<W, kRowArgmax>(sl, dy, in, c, din);
 }
 
 // Gradient of Eq. 12 (plain or guided): every input leaf receives the sum of
@@ -398,27 +427,27 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
     const uint32_t* __restrict__ in_trees, const int64_t* __restrict__ in_prefix, int64_t n_in,
     int gd, int gh, int gw, int c, const uint32_t* __restrict__ out_trees,
     const int64_t* __restrict__ out_prefix, const float* __restrict__ dy, float* __restrict__ din) {
-  __shared__ int64_t slots_all[4][3 * 64];
+  __shared__ int64_t slots_all[4][3 * kSlotCap];
   const int wave = threadIdx.x >> 6;
   const int64_t ti = (int64_t)blockIdx.x * 4 + wave;
   if (ti >= n_in) return;  // whole wave exits together
-  int64_t* slots = slots_all[wave];
+  Slots sl{slots_all[wave], 0};
   const int lane = lane_id();
   const TreePos p = tree_pos(ti, gd, gh, gw);
   const Bits ib = load_bits(in_trees, ti);
   const int64_t in_row0 = in_prefix[ti];
   const bool in_split = (ib.lo & 1ull) != 0;
   const int Gh = 2 * gh, Gw = 2 * gw, Gd = 2 * gd;
-  auto out_tree = [&](int o) {
-    return ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw + 2 * p.w +
-           (o & 1);
-  };
+  // Lane o < 8 loads output tree o's bits and first row.
   bool single = false;
+  Bits obl{0ull, 0u};
   int64_t orow = 0, irow = 0;
   if (lane < 8) {
-    const int64_t t = out_tree(lane);
-    const Bits ob = load_bits(out_trees, t);
-    single = !(ob.lo & 1ull);
+    const int o = lane;
+    const int64_t t = ((p.n * Gd + 2 * p.d + ((o >> 2) & 1)) * Gh + 2 * p.h + ((o >> 1) & 1)) * Gw +
+                      2 * p.w + (o & 1);
+    obl = load_bits(out_trees, t);
+    single = !(obl.lo & 1ull);
     orow = out_prefix[t];
     irow = in_row0 + (in_split ? data_idx(ib, 1 + lane) : 0);
   }
@@ -443,12 +472,13 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
   }
   const uint64_t singles = __ballot(lane < 8 && single);
   const uint64_t split = __ballot(lane < 8 && !single);
-  leaf_rows<W, kRowCopy>(singles, irow, orow, 1, dy, nullptr, c, din, slots);
+  slots_add(sl, singles, irow, orow, 1);
   for (uint32_t sm = (uint32_t)split; sm; sm &= sm - 1) {
     const int o = __ffs(sm) - 1;
-    const int64_t t = out_tree(o);
-    const Bits ob = load_bits(out_trees, t);
-    const int64_t row0 = out_prefix[t];
+    Bits ob;
+    ob.lo = __shfl(obl.lo, o, 64);
+    ob.hi = __shfl(obl.hi, o, 64);
+    const int64_t row0 = __shfl(orow, o, 64);
     int base = 0;
     // No split depth-2 node: no leaf past position 72.
     const int nend = (((ob.lo >> 9) != 0ull) || ob.hi) ? kNodes : 73;
@@ -476,10 +506,11 @@ __global__ void __launch_bounds__(256) k_unpool_bwd(
         }
         dst = in_row0 + data_idx(ib, node);
       }
-      leaf_rows<W, kRowSum>(h, dst, src, nm, dy, nullptr, c, din, slots);
+      slots_push<W, kRowSum>(sl, h, dst, src, nm, dy, nullptr, c, din);
       base += __popcll(m);
     }
   }
+  slots_flush<W, kRowSum>(sl, dy, nullptr, c, din);
 }
 
 // Channel concatenation of two leaf arrays on one structure (the skip
