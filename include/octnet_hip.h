@@ -121,9 +121,11 @@ int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int g
 
 /* Bytes of workspace for oc_conv3x3x3 on a structure with n_trees trees and
  * n_leaves leaves.  *bytes [host].  The size is a bound that holds for every
- * canonical structure of that size; on the MFMA path it is dominated by the
- * per-call boundary sums of split nodes, 26*cin*4*(n_leaves - n_trees)/7
- * bytes. */
+ * canonical structure of that size and covers every implementation; on the
+ * fused MFMA path it is dominated by the per-call boundary sums of split
+ * nodes, 26*cin*4*(n_leaves - n_trees)/7 bytes, in channel blocks by the
+ * partial outputs, (cin/32)*n_leaves*cout*4 bytes, and on the GEMM path by
+ * one chunk of window sums (about 256 MB). */
 int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes);
 
 /*
