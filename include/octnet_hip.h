@@ -59,7 +59,7 @@ extern "C" {
 #define OC_POOL_MAX 1
 
 /* Convolution implementations (oc_conv3x3x3_ex). */
-#define OC_CONV_AUTO 0    /* OC_CONV_MFMA where a fused variant exists, or in channel blocks on >= 65536 leaves; else OC_CONV_GEMM */
+#define OC_CONV_AUTO 0    /* OC_CONV_MFMA where a fused variant exists, or in channel blocks on >= 65536 leaves (>= 16384 for cin >= 128); else OC_CONV_GEMM */
 #define OC_CONV_GENERIC 1 /* any channel counts: window sums + VALU contraction */
 #define OC_CONV_MFMA 2    /* fused fp32 MFMA kernels; OC_EINVAL if unsupported */
 #define OC_CONV_GEMM 3    /* any channel counts: window sums of row chunks, then an fp32 MFMA GEMM */

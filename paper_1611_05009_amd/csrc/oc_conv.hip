@@ -641,6 +641,11 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
     int64_t n_leaves, const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups,
     const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
     const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
+  // Channel blocks: blockIdx.y selects an output block (its weight layout
+  // and its [n_leaves][cout] destination).
+  wm += (int64_t)blockIdx.y * MfmaCfg<CIN, NT, MS>::WFLOATS;
+  out += (int64_t)blockIdx.y * n_leaves * cout;
+  if (bias != nullptr) bias += (int64_t)blockIdx.y * cout;
   using C = MfmaCfg<CIN, NT, MS>;
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   using Vec = typename VecT<C::VEC>::type;
@@ -1098,6 +1103,11 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const float* __restrict__, int64_t, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out, const int64_t* __restrict__, int64_t, int64_t) {
+  // Channel blocks: blockIdx.y selects an output block (its weight layout
+  // and its [n_leaves][cout] destination).
+  wm += (int64_t)blockIdx.y * MfmaCfg<CIN, NT, 16>::WFLOATS;
+  out += (int64_t)blockIdx.y * n_leaves * cout;
+  if (bias != nullptr) bias += (int64_t)blockIdx.y * cout;
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
   extern __shared__ float smem[];
@@ -1626,6 +1636,11 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const float* __restrict__ bsum, int64_t ccap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out, const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
+  // Channel blocks: blockIdx.y selects an output block (its weight layout
+  // and its [n_leaves][cout] destination).
+  wm += (int64_t)blockIdx.y * MfmaCfg<CIN, NT, 16>::WFLOATS;
+  out += (int64_t)blockIdx.y * n_leaves * cout;
+  if (bias != nullptr) bias += (int64_t)blockIdx.y * cout;
   using K = CellCfg<CIN, NT>;
   constexpr int CH = K::CH;
   // Channel vectors per window-sum pass.
@@ -1693,6 +1708,11 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
     const int32_t* __restrict__ codes, int64_t ccap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
+  // Channel blocks: blockIdx.y selects an output block (its weight layout
+  // and its [n_leaves][cout] destination).
+  wm += (int64_t)blockIdx.y * MfmaCfg<CIN, NT, MS>::WFLOATS;
+  out += (int64_t)blockIdx.y * n_leaves * cout;
+  if (bias != nullptr) bias += (int64_t)blockIdx.y * cout;
   using C = MfmaCfg<CIN, NT, MS>;
   using Vec = typename VecT<C::VEC>::type;
   using Acc = typename AccT<MS>::type;
@@ -2158,12 +2178,13 @@ constexpr int kMaxOutBlocks = 8;
 constexpr int64_t kBlockedMinLeaves = OC_BLOCKED_MIN_LEAVES;
 
 // The fused kernels of variant v on input `in` (v->cin channels; in_bytes its
-// size) for each of the n_outs outputs: unit voxels, edge-8 cells with
-// unsplit neighbours and edge-2 cells, then the boundary sums of split nodes
-// (once, they depend on the input only) and the edge-8 and edge-4 cells that
-// read them.
+// size) for nk output blocks (grid rows; block k's weight layouts and
+// destination follow block k - 1's, as the kernels expect): unit voxels,
+// edge-8 cells with unsplit neighbours and edge-2 cells, then the boundary
+// sums of split nodes (once, they depend on the input only) and the edge-8
+// and edge-4 cells that read them.
 hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant* v, const float* in,
-                      uint32_t in_bytes, const FusedOut* outs, int n_outs, hipStream_t s) {
+                      uint32_t in_bytes, const FusedOut& o, int nk, hipStream_t s) {
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
@@ -2177,7 +2198,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
   if (e != hipSuccess) return e;
-  auto launch_cells = [&](int k, int64_t t0, int64_t t1, const FusedOut& o) -> hipError_t {
+  auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
     const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
     if (smem > g_max_smem) return hipErrorInvalidConfiguration;
@@ -2185,29 +2206,26 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (r != hipSuccess) return r;
-    hipLaunchKernelGGL(f, dim3(nblk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
+    hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
                        a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
                        (const float*)w.bsum, w.ccap, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out,
                        (const int64_t*)w.pre[1 + k], t0, t1);
     return hipGetLastError();
   };
-  for (int i = 0; i < n_outs; ++i) {
-    const FusedOut& o = outs[i];
-    hipLaunchKernelGGL(v->kernel, dim3(nblk), dim3(kUnitThreads), msmem, s, a.n_leaves,
-                       (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), in, o.wm,
-                       in_bytes, o.bias, o.cout, o.relu, o.out);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(v->cell8g, dim3(nblk), dim3(kUnitThreads), gsm, s, a.n_leaves,
-                       (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes, w.ccap,
-                       in, o.w8, in_bytes, o.bias, o.cout, o.relu, o.out);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // Edge-2 cells (no boundary sums).
-    e = launch_cells(3, 0, a.n_trees, o);
-    if (e != hipSuccess) return e;
-  }
+  hipLaunchKernelGGL(v->kernel, dim3(nblk, nk), dim3(kUnitThreads), msmem, s, a.n_leaves,
+                     (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), in, o.wm, in_bytes,
+                     o.bias, o.cout, o.relu, o.out);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(v->cell8g, dim3(nblk, nk), dim3(kUnitThreads), gsm, s, a.n_leaves,
+                     (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes, w.ccap, in,
+                     o.w8, in_bytes, o.bias, o.cout, o.relu, o.out);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // Edge-2 cells (no boundary sums).
+  e = launch_cells(3, 0, a.n_trees);
+  if (e != hipSuccess) return e;
   // Boundary sums and the cells that read them (other edge-8, edge-4), in
   // chunks of trees: the sums of the trees up to a chunk's end plus one tree
   // plane (every neighbour of its cells), then the chunk's cells, so that the
@@ -2231,12 +2249,10 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
       done = need;
     }
     if (t1 > t0) {
-      for (int i = 0; i < n_outs; ++i) {
-        e = launch_cells(1, t0, t1, outs[i]);
-        if (e != hipSuccess) return e;
-        e = launch_cells(2, t0, t1, outs[i]);
-        if (e != hipSuccess) return e;
-      }
+      e = launch_cells(1, t0, t1);
+      if (e != hipSuccess) return e;
+      e = launch_cells(2, t0, t1);
+      if (e != hipSuccess) return e;
     }
   }
   return hipGetLastError();
@@ -2263,9 +2279,13 @@ bool conv_mfma_supported(int cin, int cout) {
 int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
   if (!conv_mfma_supported(cin, cout)) return 3;
   if (find_variant(cin, cout) != nullptr) return 2;
-  // Channel blocks pay J x K passes of about six launches each: on small
-  // structures the window-sum GEMM is faster.
-  return n_leaves >= kBlockedMinLeaves ? 2 : 3;
+  // Channel blocks pay Cin/32 passes of six launches each, while the
+  // window-sum GEMM writes and re-reads 27 Cin floats per leaf: the GEMM is
+  // faster on small structures unless the input is wide (measured on
+  // 32768 leaves: 64->64 and 64->128 favour the GEMM, 128->64 and 256->128
+  // the blocks; on 4096 leaves the GEMM throughout).
+  if (n_leaves >= kBlockedMinLeaves) return 2;
+  return cin >= 128 && n_leaves >= kBlockedMinLeaves / 4 ? 2 : 3;
 }
 
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
@@ -2363,7 +2383,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   if (e != hipSuccess) return e;
   if (v != nullptr) {
     const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu, a.out};
-    return fused_pass(a, w, v, a.in, in_bytes, &o, 1, s);
+    return fused_pass(a, w, v, a.in, in_bytes, o, 1, s);
   }
   // Channel blocks: per input block j (copied to a dense [n_leaves][32]
   // array unless it is the whole input), the boundary sums once and the K
@@ -2379,13 +2399,11 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
       hipLaunchKernelGGL(k_channel_block, dim3((unsigned)nb), dim3(256), 0, s, a.in, a.cin, j, n, w.xblk);
       xin = w.xblk;
     }
-    FusedOut outs[kMaxOutBlocks];
-    for (int k = 0; k < bl.K; ++k) {
-      const size_t b = (size_t)j * bl.K + k;
-      outs[k] = FusedOut{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
-                         nullptr, bl.cb, 0, w.part + b * (size_t)n * bl.cb};
-    }
-    e = fused_pass(a, w, bl.v, xin, in_bytes, outs, bl.K, s);
+    // The K output blocks of input block j in one grid (rows k).
+    const size_t b = (size_t)j * bl.K;
+    const FusedOut o{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
+                     nullptr, bl.cb, 0, w.part + b * (size_t)n * bl.cb};
+    e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, s);
     if (e != hipSuccess) return e;
   }
   int64_t rb = (n * a.cout + 255) / 256;
