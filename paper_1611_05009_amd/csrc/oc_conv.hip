@@ -498,22 +498,35 @@ __device__ __forceinline__ int32_t neighbour_row(const uint32_t* __restrict__ tr
 
 // Neighbourhood table of the unit-voxel groups (structure only, built once
 // per structure): nbt[64 k + u] = neighbour_row(group k, u), -1 outside the
-// grid, for the G = min(n_groups, n_leaves / 8) groups.
+// grid, for the G = min(n_groups, n_leaves / 8) groups.  One wave takes
+// kTableGroups groups, lane u entry u of each, so that the lookups of the
+// groups (tree bits, then prefix) are in flight together.
+constexpr int kTableGroups = 4;
+
 __global__ void k_unit_table(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
                              int gd, int gh, int gw, int64_t n_leaves,
                              const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
                              int32_t* __restrict__ nbt) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+  const int u = (int)(threadIdx.x & 63);
   const int64_t G = min(*n_groups, n_leaves / 8);
-  if (i >= G * 64) return;  // G * 64 is a multiple of 64: whole waves exit
-  // One group per wave: its key is wave-uniform, so the tree position is
-  // derived once per wave on the scalar unit.
-  const uint64_t k64 = (uint64_t)gkey[i >> 6];
-  const uint32_t klo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)k64);
-  const uint32_t khi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(k64 >> 32));
-  const int64_t key = (int64_t)(((uint64_t)khi << 32) | klo);
-  const int32_t r = neighbour_row(trees, prefix, gd, gh, gw, key, (int)(i & 63));
-  nbt[i] = r < n_leaves ? r : -1;  // only a non-canonical structure exceeds
+  const int64_t g0 = wv * kTableGroups;
+  if (g0 >= G) return;  // wave-uniform
+  // The keys are wave-uniform: tree positions are derived on the scalar unit.
+  int64_t key[kTableGroups];
+#pragma unroll
+  for (int q = 0; q < kTableGroups; ++q) {
+    const uint64_t k64 = (uint64_t)gkey[min(g0 + q, G - 1)];
+    const uint32_t klo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)k64);
+    const uint32_t khi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(k64 >> 32));
+    key[q] = (int64_t)(((uint64_t)khi << 32) | klo);
+  }
+  int32_t r[kTableGroups];
+#pragma unroll
+  for (int q = 0; q < kTableGroups; ++q) r[q] = neighbour_row(trees, prefix, gd, gh, gw, key[q], u);
+#pragma unroll
+  for (int q = 0; q < kTableGroups; ++q)
+    if (g0 + q < G) nbt[(g0 + q) * 64 + u] = r[q] < n_leaves ? r[q] : -1;  // only a non-canonical structure exceeds
 }
 
 // ---------------------------------------------------------------------------
@@ -2338,7 +2351,7 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                      w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
                      a.n_leaves, w.stl, w.meta);
   // Neighbourhood tables of the MFMA kernels.
-  const int64_t nt_threads = 64 * (a.n_leaves / 8);
+  const int64_t nt_threads = 64 * ((a.n_leaves / 8 + kTableGroups - 1) / kTableGroups);
   if (nt_threads > 0)
     hipLaunchKernelGGL(k_unit_table, dim3((unsigned)((nt_threads + 255) / 256)), dim3(256), 0, s,
                        a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
