@@ -1392,8 +1392,11 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
   int o[3];
   cell_origin(info, row, gd, gh, gw, n, o);
   const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
-  for (int r = 0; r < 27; ++r) {
-    if (r == 13) continue;
+  // Grid row y takes regions y, y + gridDim.y, ... (indices without the
+  // centre): on small structures one region per thread, so that a cell's
+  // lookups run side by side; on large ones one thread per cell.
+  for (int rs = (int)blockIdx.y; rs < kSets; rs += (int)gridDim.y) {
+    const int r = rs + (rs >= 13 ? 1 : 0);
     const int dir[3] = {r / 9 - 1, (r / 3) % 3 - 1, r % 3 - 1};
     int lo[3];
     bool inside = row >= 0;
@@ -2360,7 +2363,8 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((w.cap + 255) / 256)), dim3(256), 0, s, w.smask,
                        w.cap);
   if (w.ccap > 0)
-    hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256)), dim3(256), 0, s,
+    hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256), w.ccap < 65536 ? kSets : 1),
+                       dim3(256), 0, s,
                        a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta,
                        (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes, w.smask);
