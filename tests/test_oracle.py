@@ -314,6 +314,22 @@ def test_conv_linearity():
                                O.conv3(g, x1, w1) + 3 * O.conv3(g, x1, w2), rtol=1e-10, atol=1e-10)
 
 
+def test_conv_is_a_sum_over_input_channel_blocks():
+    """Eq. 7 sums over input channels: the convolution of all channels is
+    the sum of the convolutions of channel blocks with the matching weight
+    columns, and output channels are independent (the identity the wide
+    layers' channel blocks rest on)."""
+    rng = np.random.default_rng(14)
+    g = O.build(synth.random_occupancy(rng, 1, 2, 2, 2))
+    cin, cout = 6, 4
+    x = rng.standard_normal((g.n_leaves, cin))
+    w = rng.standard_normal((cout, cin, 3, 3, 3))
+    full = O.conv3(g, x, w)
+    parts = sum(O.conv3(g, x[:, j:j + 2], w[:, j:j + 2]) for j in range(0, cin, 2))
+    np.testing.assert_allclose(parts, full, rtol=1e-10, atol=1e-10)
+    np.testing.assert_allclose(O.conv3(g, x, w[1:3]), full[:, 1:3], rtol=1e-12, atol=1e-12)
+
+
 def test_conv_axis_permutation_equivariance():
     rng = np.random.default_rng(13)
     occ = synth.random_occupancy(rng, 1, 1, 2, 3)
