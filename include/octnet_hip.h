@@ -124,7 +124,7 @@ int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int g
  * canonical structure of that size and covers every implementation; on the
  * fused MFMA path it is dominated by the per-call boundary sums of split
  * nodes, 26*cin*4*(n_leaves - n_trees)/7 bytes, in channel blocks by the
- * partial outputs, (cin/32)*n_leaves*cout*4 bytes, and on the GEMM path by
+ * partial outputs of one input block, n_leaves*cout*4 bytes, and on the GEMM path by
  * one chunk of window sums (about 256 MB). */
 int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes);
 
@@ -168,9 +168,9 @@ int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, in
  * for cin in {4, 8, 16, 32} and cout in [5, 32].  Wider layers with cin a
  * multiple of 32 and cout a multiple of 32 up to 256 (or a fused width below
  * 32) run in channel blocks: Eq. 7 is a sum over input channels, so the
- * layer is computed as (cin/32) x (cout/cb) fused 32 -> cb convolutions into
- * partial outputs in the workspace, whose sums over input blocks (in block
- * order), bias and ReLU one more kernel writes. */
+ * layer is computed as (cin/32) x (cout/cb) fused 32 -> cb convolutions; the
+ * partial outputs of each input block go to the workspace and are added to
+ * the output in block order (after the bias; the ReLU after the last). */
 int oc_conv3x3x3_mfma_supported(int cin, int cout);
 
 /*

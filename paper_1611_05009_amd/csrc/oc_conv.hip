@@ -1984,9 +1984,9 @@ const MfmaVariant* find_variant(int cin, int cout) {
 // cout a multiple of 32 up to 256 (or below 32 with a variant of its own).
 // Eq. 7 sums over input channels, so the layer is the sum over j of the
 // convolutions of input channels [32j, 32j + 32) with the matching weight
-// columns: it runs as J x K fused 32 -> cb convolutions into partial outputs
-// [J][K][n_leaves][cb], and one kernel adds each output block's J partials in
-// order, then the bias and the ReLU.
+// columns: it runs as J x K fused 32 -> cb convolutions; those of input
+// block j write partial outputs [K][n_leaves][cb], which one kernel adds to
+// the output (after the bias, before the ReLU) in block order.
 struct Blocks {
   const MfmaVariant* v;  // the 32 -> cb variant; null when not blocked
   int J, K, cb;
@@ -2033,20 +2033,22 @@ __global__ void k_channel_block(const float* __restrict__ x, int cin, int j, int
   }
 }
 
-// out[row][cb k + c] = act(bias + sum over j (in order) of part[j][k][row][c]).
-__global__ void k_block_reduce(const float* __restrict__ part, int J, int K, int cb, int64_t n_rows,
-                               const float* __restrict__ bias, int relu, float* __restrict__ out) {
+// One input block's share of the output: out[row][cb k + c] = (first ? bias
+// : out[row][cb k + c]) + part[k][row][c], then max(0, .) after the last
+// block when relu is set.  Called for j = 0 .. J - 1 in order, it leaves
+// act(bias + P_0 + P_1 + ...) summed in block order.
+__global__ void k_block_accum(const float* __restrict__ part, int K, int cb, int64_t n_rows,
+                              const float* __restrict__ bias, int first, int last, int relu,
+                              float* __restrict__ out) {
   const int cout = K * cb;
   const int64_t n = n_rows * cout;
-  const int64_t pstride = n_rows * cout;  // one j
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const int64_t row = i / cout;
     const int co = (int)(i - row * cout);
     const int k = co / cb, c = co - k * cb;
-    const int64_t pi = ((int64_t)k * n_rows + row) * cb + c;
-    float v = bias ? bias[co] : 0.f;
-    for (int j = 0; j < J; ++j) v += part[(int64_t)j * pstride + pi];
-    out[i] = relu ? fmaxf(v, 0.f) : v;
+    float v = first ? (bias ? bias[co] : 0.f) : out[i];
+    v += part[((int64_t)k * n_rows + row) * cb + c];
+    out[i] = (last && relu) ? fmaxf(v, 0.f) : v;
   }
 }
 
@@ -2171,7 +2173,7 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.wblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 27 * (size_t)cin * cout : 0));
   w.xblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 32 * (size_t)n_leaves : 0));
-  w.part = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * (size_t)bl.J * n_leaves * cout : 0));
+  w.part = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * (size_t)n_leaves * cout : 0));
   w.total = off + 256;
   return w;
 }
@@ -2403,8 +2405,8 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     return fused_pass(a, w, v, a.in, in_bytes, o, 1, s);
   }
   // Channel blocks: per input block j (copied to a dense [n_leaves][32]
-  // array unless it is the whole input), the boundary sums once and the K
-  // output blocks' kernels into their partials; then the ordered sums.
+  // array unless it is the whole input), the boundary sums once, the K
+  // output blocks' kernels into the partials, and their sum into the output.
   const Blocks bl = conv_blocks(a.cin, a.cout);
   if (bl.v == nullptr || bl.K > kMaxOutBlocks) return hipErrorInvalidValue;
   const int64_t n = a.n_leaves;
@@ -2419,15 +2421,17 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     // The K output blocks of input block j in one grid (rows k).
     const size_t b = (size_t)j * bl.K;
     const FusedOut o{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
-                     nullptr, bl.cb, 0, w.part + b * (size_t)n * bl.cb};
+                     nullptr, bl.cb, 0, w.part};
     e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, s);
     if (e != hipSuccess) return e;
+    int64_t rb = (n * a.cout + 255) / 256;
+    if (rb > 8LL * g_num_cus * 8) rb = 8LL * g_num_cus * 8;
+    hipLaunchKernelGGL(k_block_accum, dim3((unsigned)rb), dim3(256), 0, s, (const float*)w.part, bl.K, bl.cb, n,
+                       a.bias, j == 0 ? 1 : 0, j + 1 == bl.J ? 1 : 0, a.relu, a.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
-  int64_t rb = (n * a.cout + 255) / 256;
-  if (rb > 8LL * g_num_cus * 8) rb = 8LL * g_num_cus * 8;
-  hipLaunchKernelGGL(k_block_reduce, dim3((unsigned)rb), dim3(256), 0, s, (const float*)w.part, bl.J, bl.K,
-                     bl.cb, n, a.bias, a.relu, a.out);
-  return hipGetLastError();
+  return hipSuccess;
 }
 
 }  // namespace oci
