@@ -42,7 +42,7 @@ def parse():
                     help="print a report table instead of the bench line")
     ap.add_argument("--bwd-steps", type=int, default=3,
                     help="backward passes timed after the forward steps (0: none)")
-    ap.add_argument("--cpu-rows", type=int, default=6000,
+    ap.add_argument("--cpu-rows", type=int, default=500000,
                     help="leaves in the oracle's timed sample")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times (a plain copy of "
