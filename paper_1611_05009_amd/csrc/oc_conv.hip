@@ -723,7 +723,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
         const int row0 = tnb[(i >> 3) * 64 + 21];  // voxel (1,1,1): first row of the group
         if (row0 < 0 || row0 + 8 > n_leaves || co >= cout) continue;
         float v = res[nt][r] + bv;
-        if (relu) v = fmaxf(v, 0.f);
+        if (relu & 1) v = fmaxf(v, 0.f);
         out[(int64_t)(row0 + (i & 7)) * cout + co] = v;
       }
     }
@@ -945,7 +945,7 @@ __device__ __forceinline__ void store_tile16(const typename AccT<16>::type (&acc
       const int rowi = __shfl(row, 4 * g + r, 64);
       if (rowi < 0 || co >= cout) continue;
       float v = fmaf(acc[nt][r], inv, bv);
-      if (relu) v = fmaxf(v, 0.f);
+      if (relu & 1) v = fmaxf(v, 0.f);
       out[(int64_t)rowi * cout + co] = v;
     }
   }
@@ -1213,7 +1213,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     __builtin_amdgcn_wave_barrier();  // offm is rewritten by the next tile
     // The row of cell m, for the store's MFMA layout.
     const int row_m = __builtin_amdgcn_ds_bpermute(perm, row);
-    store_tile16<NT>(acc, row_m, 0.125f, lane, bvals, cout, relu, out);
+    store_tile16<NT>(acc, row_m, (relu & 2) ? 1.f : 0.125f, lane, bvals, cout, relu, out);
   }
 }
 
@@ -1705,7 +1705,8 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
       if (jd == 2) LayerPasses<CIN, NT, SZ, TRIV, 2, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
       __builtin_amdgcn_sched_barrier(0);  // keeps the next layer's loads out of this one
     }
-    store_tile16<NT>(acc, row, 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu, out);
+    store_tile16<NT>(acc, row, (relu & 2) ? 1.f : 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu,
+                     out);
   }
 }
 
@@ -1769,8 +1770,8 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
         const int i = MS == 32 ? 8 * (r / 4) + 4 * g + (r % 4) : 4 * g + r;
         const int rowi = __shfl(srow, i, 64);
         if (rowi < 0 || co >= cout) continue;
-        float v = res[nt][r] + bvals[nt];
-        if (relu) v = fmaxf(v, 0.f);
+        float v = fmaf(res[nt][r], (relu & 2) ? 512.f : 1.f, bvals[nt]);
+        if (relu & 1) v = fmaxf(v, 0.f);
         out[(int64_t)rowi * cout + co] = v;
       }
     }
@@ -2178,8 +2179,10 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   return w;
 }
 
-// Output side of one fused pass: weight layouts, bias, width, ReLU and the
-// [n_leaves][cout] destination.
+// Output side of one fused pass: weight layouts, bias, width, epilogue mode
+// and the [n_leaves][cout] destination.  relu: bit 0 applies max(0, .),
+// bit 1 writes each cell's sum over its voxels instead of their mean (the
+// bias still added once).
 struct FusedOut {
   const float* wm;
   const float* wc;
@@ -2373,17 +2376,27 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   return hipGetLastError();
 }
 
+bool conv_runs_fused(const ConvArgs& a, int impl) {
+  if (impl != 2) return false;
+  const MfmaVariant* v = find_variant(a.cin, a.cout);
+  if (v == nullptr && conv_blocks(a.cin, a.cout).v == nullptr) return false;
+  // The MFMA kernels gather input rows with 16-byte buffer loads at 32-bit
+  // offsets below kOutside.
+  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)(v ? a.cin : 32) * 4u;
+  return (reinterpret_cast<uintptr_t>(a.in) & 15) == 0 && in_bytes64 < kOutside;
+}
+
 hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s) {
   hipError_t e = init_slots();
   if (e != hipSuccess) return e;
   const ConvWs w = carve(const_cast<void*>(ws), a.n_trees, a.n_leaves, a.cin, a.cout);
-  // The MFMA kernels gather input rows with 16-byte buffer loads at 32-bit
-  // offsets below kOutside; otherwise the generic kernel (or, for channel
-  // blocks, the GEMM path) runs.
+  // Where the MFMA kernels cannot gather the input, the generic kernel (or,
+  // for channel blocks, the GEMM path) runs.
   const MfmaVariant* v = find_variant(a.cin, a.cout);
   const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)(v ? a.cin : 32) * 4u;
-  if (impl == 2 && ((reinterpret_cast<uintptr_t>(a.in) & 15) != 0 || in_bytes64 >= kOutside))
-    impl = v ? 1 : 3;
+  if (impl == 2 && !conv_runs_fused(a, impl)) impl = v ? 1 : 3;
+  // Cell sums come from the fused kernels' epilogues only.
+  if (a.sum_cells && impl != 2) return hipErrorInvalidValue;
   const uint32_t in_bytes = (uint32_t)(in_bytes64 < kOutside ? in_bytes64 : 0);
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
@@ -2401,7 +2414,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
   e = device_limits();
   if (e != hipSuccess) return e;
   if (v != nullptr) {
-    const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu, a.out};
+    const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu | (a.sum_cells ? 2 : 0), a.out};
     return fused_pass(a, w, v, a.in, in_bytes, o, 1, s);
   }
   // Channel blocks: per input block j (copied to a dense [n_leaves][32]
@@ -2421,7 +2434,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     // The K output blocks of input block j in one grid (rows k).
     const size_t b = (size_t)j * bl.K;
     const FusedOut o{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
-                     nullptr, bl.cb, 0, w.part};
+                     nullptr, bl.cb, a.sum_cells ? 2 : 0, w.part};
     e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, s);
     if (e != hipSuccess) return e;
     int64_t rb = (n * a.cout + 255) / 256;

@@ -46,7 +46,7 @@ hipError_t launch_unpool(const uint32_t* in_trees, const int64_t* in_prefix, int
                          const int64_t* out_prefix, float* out, hipStream_t s);
 hipError_t launch_relu(float* x, int64_t count, hipStream_t s);
 // Gradients (the arguments mirror the forward calls; dy/din are the output
-// and input gradients).  din of the unpool gradient is cleared first.
+// and input gradients).  Every din row is written (no clearing needed).
 hipError_t launch_pool_max_bwd(const uint32_t* in_trees, const int64_t* in_prefix, int n, int gd,
                                int gh, int gw, const float* in, int c, const uint32_t* out_trees,
                                const int64_t* out_prefix, const float* dy, float* din,
@@ -90,12 +90,18 @@ struct ConvArgs {
   int cout;
   int relu;
   float* out;
+  // Internal: the fused kernels write each cell's sum (|l| times Eq. 8's
+  // mean) instead of its mean; only where conv_runs_fused holds.
+  int sum_cells = 0;
 };
 size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout);
 bool conv_mfma_supported(int cin, int cout);
 // The implementation OC_CONV_AUTO runs: 2 (fused MFMA kernels, in channel
 // blocks for wide layers on large structures) or 3 (window-sum GEMM).
 int conv_auto_impl(int64_t n_leaves, int cin, int cout);
+// Whether launch_conv_execute with impl runs the fused MFMA kernels (directly
+// or in channel blocks) for these arguments.
+bool conv_runs_fused(const ConvArgs& a, int impl);
 // Structure- and weight-dependent preparation into the workspace (the
 // weight pointer of `a` is read, the features are not).
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
