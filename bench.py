@@ -44,6 +44,10 @@ def parse():
                     help="backward passes timed after the forward steps (0: none)")
     ap.add_argument("--cpu-rows", type=int, default=500000,
                     help="leaves in the oracle's timed sample")
+    ap.add_argument("--cpu-threads", type=int, default=0,
+                    help="host threads of the oracle's timed run (0: all)")
+    ap.add_argument("--print-hash", action="store_true",
+                    help="print the conv translation unit's source hash and exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times (a plain copy of "
                          "known size, to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -67,14 +71,12 @@ def measured_traffic(config):
     """HBM bytes per conv call from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE summary (copy-calibrated), or None when the summary is for
     another workload or the convolution source has changed since."""
-    import hashlib
     if config != "c4":
         return None
     path = os.path.join(ROOT, "profiles", "traffic_conv_surf256_b16.md")
-    src = os.path.join(ROOT, "paper_1611_05009_amd", "csrc", "oc_conv.hip")
     try:
         text = open(path).read()
-        h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        h = conv_source_hash()
     except OSError:
         return None
     fields = dict(line.split(": ", 1) for line in text.splitlines() if ": " in line and
@@ -82,6 +84,21 @@ def measured_traffic(config):
     if fields.get("conv_source_sha256_16") != h:
         return None
     return float(fields["traffic_bytes_per_conv"])
+
+
+# Every file of the convolution's translation unit: a change to any of them
+# can change the kernels the traffic counters were taken on.
+CONV_TU = ("oc_conv.hip", "oc_conv_gemm.inc", "oc_conv_bwd.inc", "oc_internal.h", "oc_device.h")
+
+
+def conv_source_hash():
+    """sha256 (first 16 hex digits) over the conv translation unit's files."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in CONV_TU:
+        h.update(name.encode())
+        h.update(open(os.path.join(ROOT, "paper_1611_05009_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def conv_flops_bytes(n_leaves, n_trees, cin, cout):
@@ -93,11 +110,56 @@ def conv_flops_bytes(n_leaves, n_trees, cin, cout):
     return flops, nbytes
 
 
-def cpu_baseline(W, rows_wanted):
+def per_op_rooflines(W, recs, conv_ms, prep_ms, op_ms):
+    """Per op of one step: time, leaf-cells/s, dense voxels/s and the
+    fraction of the roofline that binds it (conv: max of the fp32 MFMA time
+    and the HBM time of its algorithmic work; build, pool, unpool: HBM bytes
+    of rows, bit strings and prefixes read and written)."""
+    rows = []
+    k = 0
+    per_name = {}
+    for r in recs:
+        if r.op in ("input", "save"):
+            if r.op == "input":
+                nb = W.dense_voxels + 24.0 * r.g_out.n_trees
+                per_name.setdefault("build", []).append(nb)
+            continue
+        if r.op == "conv":
+            p = r.params
+            t = conv_ms[k] * 1e-3
+            fl, nb = conv_flops_bytes(r.g_in.n_leaves, r.g_in.n_trees, p["cin"], p["cout"])
+            t_roof = max(fl / (PEAK_FP32_TFLOPS * 1e12), nb / (PEAK_HBM_GBS * 1e9))
+            rows.append({"op": "conv%dx%d" % (p["cin"], p["cout"]), "ms": conv_ms[k],
+                         "prepare_ms": prep_ms[k], "leaves": r.g_in.n_leaves,
+                         "leaf_cells_per_s": r.g_in.n_leaves / t,
+                         "dense_voxels_per_s": 512.0 * r.g_in.n_trees / t,
+                         "bound": "mfma" if fl / (PEAK_FP32_TFLOPS * 1e12) >= nb / (PEAK_HBM_GBS * 1e9) else "hbm",
+                         "frac": t_roof / t, "frac_with_prepare": t_roof / (t + prep_ms[k] * 1e-3)})
+            k += 1
+            continue
+        c = r.x_in.shape[1]
+        nb = 4.0 * c * (r.g_in.n_leaves + r.g_out.n_leaves) + 24.0 * (r.g_in.n_trees + r.g_out.n_trees)
+        per_name.setdefault(r.op, []).append(nb)
+    for name, nbs in per_name.items():
+        ms = op_ms.get(name)
+        if not ms:
+            continue
+        nb = sum(nbs)
+        rows.append({"op": name, "calls": len(nbs), "ms": ms, "alg_bytes": nb, "bound": "hbm",
+                     "frac": nb / (PEAK_HBM_GBS * 1e9) / (ms * 1e-3),
+                     "note": "structure call included (it synchronizes to return the leaf count)"
+                     if name != "concat" else ""})
+    return rows
+
+
+def cpu_baseline(W, rows_wanted, threads=0):
     """The oracle (never tuned) on a random sample of the workload's leaves,
-    for the first conv layer: leaf-cells per second on the host cores."""
+    for the first conv layer: leaf-cells per second on the host cores
+    (threads > 0: on that many)."""
     sys.path.insert(0, os.path.join(ROOT, "oracle"))
     import octref as O
+    if threads > 0:
+        O.set_num_threads(threads)
     import torch
     from paper_1611_05009_amd import pipeline
 
@@ -231,6 +293,9 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
+    if args.print_hash:
+        print(conv_source_hash())
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(see DESIGN.md for how the work would shard)", file=sys.stderr)
@@ -351,7 +416,12 @@ def main():
             "alg_flops": flops,
             "alg_bytes": nbytes,
             "hbm_frac": nbytes / t_conv / 1e9 / PEAK_HBM_GBS,
+            # The prepare call (structure and weight tables) runs once per
+            # conv in every step: the fraction with it counted.
+            "frac_with_prepare": flops / (t_conv + prep_ms[kd] * 1e-3) / 1e12 / PEAK_FP32_TFLOPS,
+            "prepare_ms": prep_ms[kd],
         },
+        "per_op": per_op_rooflines(W, recs, per_layer_ms, prep_ms, op_ms),
     }
     if args.bwd_steps > 0:
         bms = backward_times(W, args.bwd_steps)
@@ -367,7 +437,7 @@ def main():
         out["backward_roofline"] = rates
     if not args.no_cpu_baseline:
         print("timing the oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(W, args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(W, args.cpu_rows, args.cpu_threads)
     print(json.dumps(out), flush=True)
 
 

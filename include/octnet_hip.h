@@ -17,7 +17,11 @@
  *     (Eq. 1-2).  The child with octant o covers the sub-cube offset by
  *     ((o>>2)&1, (o>>1)&1, o&1) times the child size along (d, h, w).
  *   - A tree is canonical when no bit is set below an unsplit node.  Every
- *     call below assumes canonical trees (oc_validate checks it).
+ *     call below assumes canonical trees.  oc_build and the pooling and
+ *     unpooling structure calls only produce canonical trees; oc_prefix,
+ *     where trees made elsewhere enter, rejects non-canonical ones with
+ *     OC_ESTRUCT; oc_validate (device) and oc_validate_host (host, header
+ *     only) check explicitly.
  *   - prefix: int64 [n_trees + 1], prefix[t] = leaves in trees 0..t-1.  The
  *     leaves of tree t occupy rows prefix[t] .. prefix[t+1]-1 in ascending
  *     bit-index order, i.e. row = prefix[t] + data_idx(i) with data_idx from
@@ -65,6 +69,95 @@ extern "C" {
 #define OC_CONV_GEMM 3    /* any channel counts: window sums of row chunks, then an fp32 MFMA GEMM */
 #define OC_CONV_TRUNCATED 4 /* the supplement's efficient convolution (constant part + truncated
                               kernels at boundary voxels), VALU; oc_conv3x3x3_ex only */
+
+/*
+ * Header-only helpers on one shallow octree's bit string t[4] (layout
+ * above).  They compile as plain C on the host and, inside a HIP
+ * translation unit, as host + device functions.  Nothing is exported from
+ * the library for them.
+ */
+#ifdef __HIP__
+#define OC_INLINE static inline __attribute__((host, device))
+#else
+#define OC_INLINE static inline
+#endif
+
+/* Eq. 1: parent of node i >= 1 is floor((i - 1) / 8); the root (i = 0) has
+ * none and gets -1. */
+OC_INLINE int oc_parent(int i) { return i <= 0 ? -1 : (i - 1) / 8; }
+
+/* Eq. 2: the first child of node i is 8i + 1; its children are
+ * 8i + 1 + o for octants o = 0..7. */
+OC_INLINE int oc_child(int i) { return 8 * i + 1; }
+
+/* Split bit i (Sec. 3.1: bit j of the 73-bit string, stored LSB first in
+ * t[j >> 5]).  Indices outside [0, 73) read 0: the implicit depth-3 voxels
+ * are never split. */
+OC_INLINE int oc_bit(const uint32_t t[4], int i) {
+  if (i < 0 || i >= 73) return 0;
+  return (int)((t[i >> 5] >> (i & 31)) & 1u);
+}
+
+/* Set bits among indices [0, n), n clamped to [0, 73]. */
+OC_INLINE int oc_popc_below(const uint32_t t[4], int n) {
+  int c = 0, k;
+  if (n > 73) n = 73;
+  for (k = 0; n > 0; ++k, n -= 32) {
+    const uint32_t w = t[k];
+    c += __builtin_popcount(n >= 32 ? w : (w & ((1u << n) - 1u)));
+  }
+  return c;
+}
+
+/* Eq. 3 (the "Data Index" of the supplement): offset of leaf i in its tree's
+ * block of rows, counting with popcount.  For i >= 1:
+ *   8 * popc(bits [0, pa(i))) + 1 - popc(bits [0, i)) + ((i - 1) mod 8).
+ * An unsplit root is the tree's only leaf: oc_data_idx(t, 0) = 0.  The
+ * result is meaningful only when node i is a leaf of a canonical tree. */
+OC_INLINE int oc_data_idx(const uint32_t t[4], int i) {
+  if (i <= 0) return 0;
+  return 8 * oc_popc_below(t, (i - 1) / 8) + 1 - oc_popc_below(t, i) + (i - 1) % 8;
+}
+
+/* Leaves of a canonical tree: every split adds 7, so 1 + 7 * (set bits). */
+OC_INLINE int oc_n_leaves(const uint32_t t[4]) { return 1 + 7 * oc_popc_below(t, 73); }
+
+/* Bit index of the leaf holding local voxel (ld, lh, lw), each in [0, 8)
+ * (the voxel addressing of Sec. 3.2: descend from the root while the node
+ * is split; at depth k the child's octant takes bit 2 - k of each of d, h,
+ * w).  *depth (if not NULL) receives the leaf's depth 0..3; its cell has
+ * edge 8 >> depth.  Returns -1 for a voxel outside [0, 8)^3. */
+OC_INLINE int oc_leaf_at(const uint32_t t[4], int ld, int lh, int lw, int* depth) {
+  int i = 0, d;
+  if (ld < 0 || lh < 0 || lw < 0 || ld > 7 || lh > 7 || lw > 7) return -1;
+  for (d = 0; d < 3 && oc_bit(t, i); ++d) {
+    const int sh = 2 - d;
+    i = oc_child(i) + (((ld >> sh) & 1) << 2) + (((lh >> sh) & 1) << 1) + ((lw >> sh) & 1);
+  }
+  if (depth) *depth = d;
+  return i;
+}
+
+/* Is the tree canonical (no set bit below an unsplit node, bits 73..127
+ * zero)?  1 yes, 0 no. */
+OC_INLINE int oc_tree_canonical(const uint32_t t[4]) {
+  int i;
+  if ((t[2] >> 9) != 0u || t[3] != 0u) return 0;
+  for (i = 1; i < 73; ++i)
+    if (oc_bit(t, i) && !oc_bit(t, oc_parent(i))) return 0;
+  return 1;
+}
+
+/* Host check of n_trees trees in host memory: OC_OK if every tree is
+ * canonical, OC_ESTRUCT at the first that is not, OC_EINVAL for a null
+ * pointer or a negative count.  The device form is oc_validate. */
+OC_INLINE int oc_validate_host(const uint32_t* trees_host, int64_t n_trees) {
+  int64_t k;
+  if (!trees_host || n_trees < 0) return OC_EINVAL;
+  for (k = 0; k < n_trees; ++k)
+    if (!oc_tree_canonical(trees_host + 4 * k)) return OC_ESTRUCT;
+  return OC_OK;
+}
 
 /* Static text for a return code. */
 const char* oc_error_string(int code);
@@ -155,13 +248,18 @@ int oc_conv3x3x3_ex(const uint32_t* trees, const int64_t* prefix, int n, int gd,
  * time the convolution proper.  prepare writes everything that depends on
  * the structure and the weights into ws (it reads weight, not the features);
  * execute runs the convolution from that workspace and must get the same
- * structure, channel counts and ws as the prepare call before it. */
+ * structure, channel counts and ws as the prepare call before it.  execute
+ * also writes per-call scratch into ws (boundary sums of the input,
+ * window-sum chunks, channel-block partials) but leaves what prepare wrote
+ * intact, so one prepared ws serves any number of executes in stream order;
+ * two executes that share one ws and may overlap (different streams) race:
+ * give each its own prepared ws. */
 int oc_conv3x3x3_prepare(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
                          int64_t n_leaves, const float* weight, int cin, int cout, void* ws,
                          size_t ws_bytes, void* stream);
 int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
                          int64_t n_leaves, const float* in, int cin, const float* bias, int cout,
-                         int relu, float* out, const void* ws, size_t ws_bytes, int impl,
+                         int relu, float* out, void* ws, size_t ws_bytes, int impl,
                          void* stream);
 
 /* Does OC_CONV_MFMA support (cin, cout)?  1 yes, 0 no.  Fused variants exist

@@ -105,8 +105,19 @@ int oc_prefix(const uint32_t* trees, int64_t n_trees, int64_t* prefix, int64_t* 
   if (n_trees <= 0) return fail(OC_EINVAL, "oc_prefix: n_trees <= 0");
   if (ws_bytes < oc_structure_workspace(n_trees)) return fail(OC_EWORKSPACE, "oc_prefix: workspace too small");
   hipStream_t s = as_stream(stream);
+  // Trees made outside the library enter here: count the non-canonical ones
+  // (the counter sits in the workspace's last 256 bytes) with the leaves.
+  int32_t* counter = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + oc_structure_workspace(n_trees) - 256);
+  OC_CHECK_HIP(hipMemsetAsync(counter, 0, sizeof(int32_t), s), "oc_prefix");
+  OC_CHECK_HIP(oci::launch_validate(trees, n_trees, counter, s), "oc_prefix");
   OC_CHECK_HIP(oci::launch_count(trees, n_trees, oci::scan_counts_buffer(ws), s), "oc_prefix");
-  return finish_prefix(n_trees, prefix, n_leaves, ws, s, "oc_prefix");
+  int rc = finish_prefix(n_trees, prefix, n_leaves, ws, s, "oc_prefix");
+  if (rc != OC_OK) return rc;
+  int32_t bad = 0;
+  OC_CHECK_HIP(hipMemcpyAsync(&bad, counter, sizeof(int32_t), hipMemcpyDeviceToHost, s), "oc_prefix");
+  OC_CHECK_HIP(hipStreamSynchronize(s), "oc_prefix");
+  if (bad) return fail(OC_ESTRUCT, "oc_prefix: %d non-canonical trees", bad);
+  return OC_OK;
 }
 
 int oc_validate(const uint32_t* trees, int64_t n_trees, int64_t* n_bad, void* ws, size_t ws_bytes,
@@ -236,7 +247,7 @@ int oc_conv3x3x3_prepare(const uint32_t* trees, const int64_t* prefix, int n, in
 
 int oc_conv3x3x3_execute(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
                          int64_t n_leaves, const float* in, int cin, const float* bias, int cout,
-                         int relu, float* out, const void* ws, size_t ws_bytes, int impl,
+                         int relu, float* out, void* ws, size_t ws_bytes, int impl,
                          void* stream) {
   g_last_error.clear();
   oci::ConvArgs a;

@@ -11,6 +11,8 @@
 // observation that the response inside a cell is constant up to its boundary
 // (Sec. 3.2 and the supplement's "Efficient Convolution"), turned into 27
 // window sums followed by one (27*Cin) x Cout contraction per leaf.
+#include <mutex>
+
 #include "oc_internal.h"
 
 // Tuning knobs (compile-time): deltas of gathered A rows in flight in the
@@ -62,7 +64,21 @@ struct Entry {
 // Slot capacity of region r for the largest cell (s = 8): the number of unit
 // voxels in the region.  Offsets are the running sums; the self entry uses
 // slot kSelfSlot.
-__constant__ int c_slot_off[27];
+struct SlotTable {
+  int off[27];
+};
+constexpr SlotTable make_slot_table() {
+  SlotTable t{};
+  int acc = 0;
+  for (int r = 0; r < 27; ++r) {
+    t.off[r] = acc;
+    if (r == 13) continue;
+    const int dd = r / 9 - 1, dh = (r / 3) % 3 - 1, dw = r % 3 - 1;
+    acc += (dd == 0 ? 8 : 1) * (dh == 0 ? 8 : 1) * (dw == 0 ? 8 : 1);
+  }
+  return t;
+}
+__constant__ SlotTable c_slots = make_slot_table();
 
 // Edge-2 cells.  The shell is the 56 voxels u of the 4^3 block [o-1, o+3)
 // outside [o, o+2) (u in [0,4)^3 minus [1,2]^3); voxel u lies in the window
@@ -86,7 +102,15 @@ constexpr int shell2_q(int u) {
   return -1;
 }
 
-__constant__ uint8_t c_shell2[56];
+struct Shell2Table {
+  uint8_t u[56];
+};
+constexpr Shell2Table make_shell2_table() {
+  Shell2Table t{};
+  for (int q = 0; q < 56; ++q) t.u[q] = (uint8_t)shell2_u(q);
+  return t;
+}
+__constant__ Shell2Table c_shell2 = make_shell2_table();
 constexpr int kSlots = 6 * 64 + 12 * 8 + 8 + 1;  // 489
 constexpr int kSelfSlot = kSlots - 1;
 
@@ -212,7 +236,7 @@ __device__ void window_sums(const LeafGeo& g, const uint32_t* __restrict__ trees
       slots[kSelfSlot] = e;
       cnt = 1;
     } else {
-      cnt = enumerate_region(g, r, trees, prefix, gd, gh, gw, slots + c_slot_off[r]);
+      cnt = enumerate_region(g, r, trees, prefix, gd, gh, gw, slots + c_slots.off[r]);
     }
     counts[r] = cnt;
   }
@@ -225,7 +249,7 @@ __device__ void window_sums(const LeafGeo& g, const uint32_t* __restrict__ trees
     for (int k = 0; k < 27; ++k) S[k] = 0.f;
     for (int r = 0; r < 27; ++r) {
       const int cnt = counts[r];
-      const Entry* es = slots + (r == 13 ? kSelfSlot : c_slot_off[r]);
+      const Entry* es = slots + (r == 13 ? kSelfSlot : c_slots.off[r]);
       for (int e = 0; e < cnt; ++e) {
         const Entry en = es[e];
         const float x = ci < cin ? in[(int64_t)en.row * cin + ci] : 0.f;
@@ -325,27 +349,6 @@ int generic_tile(int cin) {
 size_t generic_smem(int cin, int tm) {
   return sizeof(Entry) * 4 * kSlots + sizeof(int) * 4 * 32 + sizeof(int64_t) * 32 +
          sizeof(float) * (size_t)tm * 27 * cin + sizeof(float) * tm;
-}
-
-bool g_slots_ready = false;
-
-hipError_t init_slots() {
-  if (g_slots_ready) return hipSuccess;
-  int off[27];
-  int acc = 0;
-  for (int r = 0; r < 27; ++r) {
-    off[r] = acc;
-    if (r == 13) continue;
-    const int dd = r / 9 - 1, dh = (r / 3) % 3 - 1, dw = r % 3 - 1;
-    acc += (dd == 0 ? 8 : 1) * (dh == 0 ? 8 : 1) * (dw == 0 ? 8 : 1);
-  }
-  hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(c_slot_off), off, sizeof(off));
-  if (e != hipSuccess) return e;
-  uint8_t sh2[56];
-  for (int q = 0; q < 56; ++q) sh2[q] = (uint8_t)shell2_u(q);
-  e = hipMemcpyToSymbol(HIP_SYMBOL(c_shell2), sh2, sizeof(sh2));
-  if (e == hipSuccess) g_slots_ready = true;
-  return e;
 }
 
 // ---------------------------------------------------------------------------
@@ -1154,7 +1157,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
       int mine[14];
 #pragma unroll
       for (int j = 0; j < 14; ++j) {
-        const int u = c_shell2[4 * j + q];
+        const int u = c_shell2.u[4 * j + q];
         const int vd = o[0] - 1 + (u >> 4), vh = o[1] - 1 + ((u >> 2) & 3), vw = o[2] - 1 + (u & 3);
         int r = -1;
         if (row >= 0 && vd >= 0 && vh >= 0 && vw >= 0 && vd < 8 * gd && vh < 8 * gh && vw < 8 * gw) {
@@ -2067,19 +2070,47 @@ size_t mfma_smem(const MfmaVariant& v) {
   return sizeof(float) * v.wfloats + sizeof(int32_t) * (kUnitThreads / 64) * 2 * (v.ms / 8) * 64;
 }
 
-int g_num_cus = 0;
-size_t g_max_smem = 0;
+// Compute units and LDS bytes per workgroup of the current device, queried
+// once per device (std::call_once: calls from several threads are safe).
+struct DevLimits {
+  int num_cus = 0;
+  size_t max_smem = 0;
+};
 
-hipError_t device_limits() {
-  if (g_num_cus > 0) return hipSuccess;
-  int dev = 0, cus = 0, smem = 0;
+constexpr int kMaxDevices = 64;
+
+struct DevSlot {
+  std::once_flag once;
+  hipError_t err = hipSuccess;
+  DevLimits lim;
+};
+
+DevSlot g_devices[kMaxDevices];
+
+hipError_t device_limits(DevLimits* out) {
+  int dev = 0;
   hipError_t e = hipGetDevice(&dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-  if (e == hipSuccess) e = hipDeviceGetAttribute(&smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
   if (e != hipSuccess) return e;
-  g_num_cus = cus;
-  g_max_smem = (size_t)smem;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  DevSlot& d = g_devices[dev];
+  std::call_once(d.once, [&d, dev]() {
+    int cus = 0, smem = 0;
+    hipError_t r = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (r == hipSuccess) r = hipDeviceGetAttribute(&smem, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    d.err = r;
+    d.lim.num_cus = cus;
+    d.lim.max_smem = (size_t)smem;
+  });
+  if (d.err != hipSuccess) return d.err;
+  *out = d.lim;
   return hipSuccess;
+}
+
+// LDS bytes per workgroup for the support queries: the device's, or gfx950's
+// 160 KB where none can be asked.
+size_t smem_limit() {
+  DevLimits L;
+  return device_limits(&L) == hipSuccess ? L.max_smem : 160 * 1024;
 }
 
 // Workspace layout (each part 256-byte aligned):
@@ -2205,11 +2236,13 @@ constexpr int64_t kBlockedMinLeaves = OC_BLOCKED_MIN_LEAVES;
 // sums of split nodes (once, they depend on the input only) and the edge-8
 // and edge-4 cells that read them.
 hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant* v, const float* in,
-                      uint32_t in_bytes, const FusedOut& o, int nk, hipStream_t s) {
+                      uint32_t in_bytes, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
+  const int num_cus = L.num_cus;
+  const size_t max_smem = L.max_smem;
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
-  if (msmem > g_max_smem) return hipErrorInvalidConfiguration;
-  const int nblk = ((g_num_cus + 7) / 8) * 8;
+  if (msmem > max_smem) return hipErrorInvalidConfiguration;
+  const int nblk = ((num_cus + 7) / 8) * 8;
   hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
   if (e != hipSuccess) return e;
@@ -2222,7 +2255,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
     const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
-    if (smem > g_max_smem) return hipErrorInvalidConfiguration;
+    if (smem > max_smem) return hipErrorInvalidConfiguration;
     const CellFn f = k == 1 || k == 0 ? v->cell8 : (k == 2 ? v->cell4 : v->cell2);
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
@@ -2259,7 +2292,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
     const int64_t need = c + 1 == kSumChunks ? a.n_trees : min(a.n_trees, t1 + plane);
     if (need > done) {
       int64_t blocks = (need - done + per_block - 1) / per_block;
-      if (blocks > 8LL * g_num_cus) blocks = 8LL * g_num_cus;
+      if (blocks > 8LL * num_cus) blocks = 8LL * num_cus;
       hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
                          (const int32_t*)w.stl, (const int64_t*)w.meta,
                          (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, in, in_bytes, w.bsum,
@@ -2293,8 +2326,7 @@ bool conv_mfma_supported(int cin, int cout) {
   if (!v) return false;
   // LDS: the whole weight set plus the neighbourhood rows of every wave must
   // fit one workgroup (160 KB on gfx950; the device is asked when present).
-  const size_t limit = device_limits() == hipSuccess ? g_max_smem : 160 * 1024;
-  return mfma_smem(*v) <= limit;
+  return mfma_smem(*v) <= smem_limit();
 }
 
 int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
@@ -2310,10 +2342,8 @@ int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
 }
 
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
-  hipError_t e = init_slots();
-  if (e != hipSuccess) return e;
   const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
-  e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
+  hipError_t e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
   if (e != hipSuccess) return e;
   const int64_t nw = 27LL * a.cin * a.cout;
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
@@ -2386,10 +2416,8 @@ bool conv_runs_fused(const ConvArgs& a, int impl) {
   return (reinterpret_cast<uintptr_t>(a.in) & 15) == 0 && in_bytes64 < kOutside;
 }
 
-hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s) {
-  hipError_t e = init_slots();
-  if (e != hipSuccess) return e;
-  const ConvWs w = carve(const_cast<void*>(ws), a.n_trees, a.n_leaves, a.cin, a.cout);
+hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_t s) {
+  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
   // Where the MFMA kernels cannot gather the input, the generic kernel (or,
   // for channel blocks, the GEMM path) runs.
   const MfmaVariant* v = find_variant(a.cin, a.cout);
@@ -2411,11 +2439,13 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
                        a.relu, a.out, tm, (const int32_t*)nullptr, (const int64_t*)nullptr);
     return hipGetLastError();
   }
-  e = device_limits();
+  DevLimits L;
+  hipError_t e = device_limits(&L);
   if (e != hipSuccess) return e;
+  const int num_cus = L.num_cus;
   if (v != nullptr) {
     const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu | (a.sum_cells ? 2 : 0), a.out};
-    return fused_pass(a, w, v, a.in, in_bytes, o, 1, s);
+    return fused_pass(a, w, v, a.in, in_bytes, o, 1, L, s);
   }
   // Channel blocks: per input block j (copied to a dense [n_leaves][32]
   // array unless it is the whole input), the boundary sums once, the K
@@ -2427,7 +2457,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     const float* xin = a.in;
     if (bl.J > 1) {
       int64_t nb = (n * 8 + 255) / 256;
-      if (nb > 8LL * g_num_cus * 8) nb = 8LL * g_num_cus * 8;
+      if (nb > 8LL * num_cus * 8) nb = 8LL * num_cus * 8;
       hipLaunchKernelGGL(k_channel_block, dim3((unsigned)nb), dim3(256), 0, s, a.in, a.cin, j, n, w.xblk);
       xin = w.xblk;
     }
@@ -2435,10 +2465,10 @@ hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipS
     const size_t b = (size_t)j * bl.K;
     const FusedOut o{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
                      nullptr, bl.cb, a.sum_cells ? 2 : 0, w.part};
-    e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, s);
+    e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, L, s);
     if (e != hipSuccess) return e;
     int64_t rb = (n * a.cout + 255) / 256;
-    if (rb > 8LL * g_num_cus * 8) rb = 8LL * g_num_cus * 8;
+    if (rb > 8LL * num_cus * 8) rb = 8LL * num_cus * 8;
     hipLaunchKernelGGL(k_block_accum, dim3((unsigned)rb), dim3(256), 0, s, (const float*)w.part, bl.K, bl.cb, n,
                        a.bias, j == 0 ? 1 : 0, j + 1 == bl.J ? 1 : 0, a.relu, a.out);
     e = hipGetLastError();

@@ -107,7 +107,7 @@ bool conv_runs_fused(const ConvArgs& a, int impl);
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s);
 // The convolution proper; impl: 1 generic, 2 mfma (caller checked support),
 // 3 window-sum GEMM.
-hipError_t launch_conv_execute(const ConvArgs& a, const void* ws, int impl, hipStream_t s);
+hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_t s);
 // The paper's efficient convolution (constant part plus truncated kernels
 // at boundary voxels), VALU; info: n_leaves words of scratch.
 hipError_t launch_conv_truncated(const ConvArgs& a, uint64_t* info, hipStream_t s);

@@ -11,10 +11,20 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "octnet_hip.h")
 
 
+def _header_text():
+    return re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+
+
+def inline_helpers():
+    """Header-only helpers (static inline, not exported by the library)."""
+    return sorted(set(re.findall(r"OC_INLINE\s+\w+\s+(oc_\w+)\s*\(", _header_text())))
+
+
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(oc_\w+)\s*\(", text)))
+    """Functions the library exports: every oc_* the header names, minus the
+    header-only helpers."""
+    names = set(re.findall(r"\b(oc_\w+)\s*\(", _header_text()))
+    return sorted(names - set(inline_helpers()))
 
 
 @pytest.fixture(scope="module")
@@ -34,6 +44,12 @@ def test_header_declares_the_binding_surface():
 def test_library_exports_every_declared_symbol(L):
     for name in declared_functions():
         assert hasattr(L, name), name
+
+
+def test_header_only_helpers_are_present():
+    assert inline_helpers() == sorted([
+        "oc_parent", "oc_child", "oc_bit", "oc_popc_below", "oc_data_idx", "oc_n_leaves",
+        "oc_leaf_at", "oc_tree_canonical", "oc_validate_host"])
 
 
 def test_error_strings_and_version(L):

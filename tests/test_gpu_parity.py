@@ -96,8 +96,15 @@ def test_validate_flags_noncanonical_trees():
     t[0] = [0, 0, 0, 0]
     t[0][0] = 1 << 9     # depth-2 bit under an unsplit root
     t[1][2] |= 1 << 12   # bit 76: beyond the 73-bit string
-    bad = oc.from_trees(dev(t.view(np.int32)), *g.dims())
+    # oc_prefix, where trees made elsewhere enter, rejects them...
+    with pytest.raises(oc.OctNetError, match="non-canonical"):
+        oc.from_trees(dev(t.view(np.int32)), *g.dims())
+    # ...and oc_validate counts them (it needs no prefix).
+    bad = oc.Octree(*g.dims(), dev(t.view(np.int32)), g.prefix, g.n_leaves)
     assert oc.validate(bad) == 2
+    # The host form agrees tree by tree (header-only oc_validate_host is
+    # pinned against the oracle in test_header_helpers.py).
+    assert [O.tree_valid(w) for w in t[:3]] == [False, False, True]
 
 
 @pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5"])

@@ -45,6 +45,7 @@ def test_workload_chain(key):
     pipeline.run_step(W, recs)
     torch.cuda.synchronize()
     log("workload %s: %d leaves, %d ops" % (key, W.n_leaves, len(recs)))
+    pre_pool = []  # the oracle's grid of each pool's input, for the guided unpools
     for k, r in enumerate(recs):
         log("  op %d %s" % (k, r.op))
         if r.op == "input" and W.points is not None:
@@ -78,6 +79,7 @@ def test_workload_chain(key):
             want = O.conv3_sampled(gi, xi, host(p["w"]), host(p["b"]), p["relu"], rows, info=info)
             assert_close(host(r.x_out)[rows], want, "%s op %d conv" % (key, k))
         elif r.op == "pool":
+            pre_pool.append(gi)
             go = O.pool2_structure(gi)
             check_structure(r.g_out, go)
             out = host(r.x_out)
@@ -88,7 +90,9 @@ def test_workload_chain(key):
             if r.op == "unpool":
                 go = O.unpool2_structure(gi)
             else:
-                go = ref_grid(r.g_out)  # the guide; its pooling must be the input
+                # The guide is the structure recorded at the matching pool
+                # (checked against the oracle there); it pools to this input.
+                go = pre_pool.pop()
                 assert np.array_equal(O.pool2_structure(go).trees, gi.trees)
             check_structure(r.g_out, go)
             rows = sample_rows(go.n_leaves, O.leaf_info(go), 20000, seed=k)
@@ -198,3 +202,58 @@ def test_conv_backward_full_size_adjoint():
     assert abs(wdw - yy) <= 1e-4 * yy
     s = y.double().sum(0)
     assert bool(((db.double() - s).abs() <= 1e-4 * (s.abs() + y.double().abs().sum(0))).all())
+
+
+def _sample0(octree, x):
+    """Oracle grid of sample 0 of a batch, its row range and rows of x."""
+    per = octree.gd * octree.gh * octree.gw
+    pre = host(octree.prefix)
+    b = int(pre[per])
+    g0 = O.make_grid(np.ascontiguousarray(trees_np(octree.trees)[:per]), 1, octree.gd, octree.gh, octree.gw)
+    return g0, b, host(x)[:b]
+
+
+def test_c4_conv_every_leaf_of_one_sample():
+    """Every leaf of sample 0 of the 256^3 batch-16 conv 32->32, computed in
+    the benchmark's launch configuration (the whole batch in one call), within
+    1e-5 + 1e-4 |oracle| element by element: all tile positions, schedule
+    slots and cell kinds of that sample, not a row sample."""
+    from paper_1611_05009_amd import pipeline
+    W = pipeline.Workload("c4")
+    recs = []
+    pipeline.run_step(W, recs)
+    torch.cuda.synchronize()
+    conv = next(r for r in recs if r.op == "conv")
+    g0, b, x0 = _sample0(conv.g_in, conv.x_in)
+    p = conv.params
+    log("c4 sample 0: %d leaves" % b)
+    want = O.conv3(g0, x0, host(p["w"]), host(p["b"]), p["relu"])
+    assert_close(host(conv.x_out)[:b], want, "c4 conv, every leaf of sample 0")
+
+
+def test_c4_weight_gradient_element_wise():
+    """The weight and bias gradients of the 256^3 conv 32->32 on sample 0
+    alone (627 k leaves, every cell kind), each of the 27 648 dW entries
+    within 1e-5 + 1e-4 |oracle| of the oracle's voxel-by-voxel sum."""
+    from paper_1611_05009_amd import octnet as oc
+    from paper_1611_05009_amd import pipeline
+    W = pipeline.Workload("c4")
+    recs = []
+    pipeline.run_step(W, recs)
+    conv = next(r for r in recs if r.op == "conv")
+    per = conv.g_in.gd * conv.g_in.gh * conv.g_in.gw
+    g0, b, x0 = _sample0(conv.g_in, conv.x_in)
+    gpu0 = oc.from_trees(conv.g_in.trees[:per].contiguous(), 1, conv.g_in.gd, conv.g_in.gh, conv.g_in.gw)
+    assert gpu0.n_leaves == b
+    dy = np.random.default_rng(21).standard_normal((b, 32)).astype(np.float32)
+    w = conv.params["w"]
+    _, dw, db = oc.conv3x3x3_backward(gpu0, conv.x_in[:b].contiguous(), w,
+                                      torch.from_numpy(dy).cuda(), need_input=False)
+    torch.cuda.synchronize()
+    log("c4 sample 0 weight gradient: %d leaves" % b)
+    want_w, want_b = O.conv3_bwd_weight(g0, x0, dy)
+    got_w = host(dw).astype(np.float64)
+    lim = 1e-5 + 1e-4 * np.abs(want_w)
+    log("  dW: max |err| / bar = %.3g" % float((np.abs(got_w - want_w) / lim).max()))
+    assert_close(got_w, want_w, "c4 dW, sample 0")
+    assert_close(host(db), want_b, "c4 db, sample 0")
