@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import octref as O
-from common import assert_close, log, sample_rows, trees_np
+from common import assert_close, assert_close_sum, log, sample_rows, trees_np
 
 pytestmark = pytest.mark.gpu
 
@@ -111,14 +111,6 @@ def flipped_kernel(w):
     return np.ascontiguousarray(np.flip(w, axis=(2, 3, 4)).transpose(1, 0, 2, 3, 4))
 
 
-def close_sum(got, want, absum, what):
-    got = np.asarray(got, dtype=np.float64)
-    want = np.asarray(want, dtype=np.float64)
-    lim = 1e-5 + 1e-4 * (np.abs(want) + absum)
-    bad = np.abs(got - want) > lim
-    assert not bad.any(), "%s: %d/%d out of tolerance" % (what, int(bad.sum()), bad.size)
-
-
 @pytest.mark.parametrize("key", ["c1", "c2", "c3", "c4", "c5", "unet"])
 def test_workload_backward_chain(key):
     """The gradients of a full-size pass, op by op in reverse, each checked
@@ -126,8 +118,10 @@ def test_workload_backward_chain(key):
     routing exact, unpool sums in full, the conv input gradient on sampled
     rows (as |l| times the oracle's forward convolution with the flipped
     kernel of dy / |l|, an identity pinned on the CPU), the bias gradient as
-    fp64 column sums.  The weight gradient at full size is checked by
-    test_conv_backward_full_size_adjoint."""
+    fp64 column sums, the weight gradient in full at 32^3 and 64^3.  At
+    256^3 the weight gradient is checked element-wise on one sample by
+    test_c4_weight_gradient_element_wise and through the adjoint identity
+    by test_conv_backward_full_size_adjoint."""
     from paper_1611_05009_amd import pipeline
     W = pipeline.Workload(key)
     recs = []
@@ -156,7 +150,7 @@ def test_workload_backward_chain(key):
         elif r.op in ("unpool", "unpool_guided"):
             go = ref_grid(r.g_out)
             want = O.unpool2_bwd(gi, di, go)
-            close_sum(host(out), want, O.unpool2_bwd(gi, np.abs(di), go), "%s unpool bwd" % key)
+            assert_close(host(out), want, "%s unpool bwd" % key)
         elif r.op == "conv":
             dyc, dx, dw, db = out
             dyc_h = host(dyc)
@@ -168,12 +162,18 @@ def test_workload_backward_chain(key):
             w = host(r.params["w"])
             gsc = dyc_h.astype(np.float64) / vol[:, None]
             want = vol[rows, None] * O.conv3_sampled(gi, gsc, flipped_kernel(w), None, False, rows, info=info)
-            absum = vol[rows, None] * O.conv3_sampled(gi, np.abs(gsc), np.abs(flipped_kernel(w)), None,
-                                                      False, rows, info=info)
-            close_sum(host(dx)[rows], want, absum, "%s conv input gradient" % key)
-            close_sum(host(db), dyc_h.astype(np.float64).sum(0), np.abs(dyc_h).astype(np.float64).sum(0),
-                      "%s bias gradient" % key)
-            assert np.isfinite(host(dw)).all()
+            assert_close(host(dx)[rows], want, "%s conv input gradient" % key)
+            assert_close_sum(host(db), dyc_h.astype(np.float64).sum(0), np.abs(dyc_h).astype(np.float64).sum(0),
+                             "%s bias gradient" % key)
+            if key in ("c1", "c2"):
+                # The weight gradient of the whole batch (the oracle's
+                # voxel-by-voxel sum is cheap at 32^3 and 64^3).
+                xi = host(r.x_in)
+                want_w, _ = O.conv3_bwd_weight(gi, xi, dyc_h)
+                abs_w, _ = O.conv3_bwd_weight(gi, np.abs(xi), np.abs(dyc_h))
+                assert_close_sum(host(dw), want_w, abs_w, "%s weight gradient" % key)
+            else:
+                assert np.isfinite(host(dw)).all()
         else:
             raise AssertionError(r.op)
 
@@ -234,7 +234,9 @@ def test_c4_conv_every_leaf_of_one_sample():
 def test_c4_weight_gradient_element_wise():
     """The weight and bias gradients of the 256^3 conv 32->32 on sample 0
     alone (627 k leaves, every cell kind), each of the 27 648 dW entries
-    within 1e-5 + 1e-4 |oracle| of the oracle's voxel-by-voxel sum."""
+    compared with the oracle's voxel-by-voxel fp64 sum at the summed-result
+    bar (1e-5 + 1e-4 |oracle| + 2^-24 sum |terms|); the entries where the
+    plain bar alone fails are logged (they are the sums that cancel)."""
     from paper_1611_05009_amd import octnet as oc
     from paper_1611_05009_amd import pipeline
     W = pipeline.Workload("c4")
@@ -252,8 +254,6 @@ def test_c4_weight_gradient_element_wise():
     torch.cuda.synchronize()
     log("c4 sample 0 weight gradient: %d leaves" % b)
     want_w, want_b = O.conv3_bwd_weight(g0, x0, dy)
-    got_w = host(dw).astype(np.float64)
-    lim = 1e-5 + 1e-4 * np.abs(want_w)
-    log("  dW: max |err| / bar = %.3g" % float((np.abs(got_w - want_w) / lim).max()))
-    assert_close(got_w, want_w, "c4 dW, sample 0")
-    assert_close(host(db), want_b, "c4 db, sample 0")
+    abs_w, abs_b = O.conv3_bwd_weight(g0, np.abs(x0), np.abs(dy))
+    assert_close_sum(host(dw), want_w, abs_w, "c4 dW, sample 0")
+    assert_close_sum(host(db), want_b, abs_b, "c4 db, sample 0")
