@@ -113,6 +113,8 @@ constexpr Shell2Table make_shell2_table() {
 __constant__ Shell2Table c_shell2 = make_shell2_table();
 constexpr int kSlots = 6 * 64 + 12 * 8 + 8 + 1;  // 489
 constexpr int kSelfSlot = kSlots - 1;
+// Entries of a split depth-1 node's table: the 6^3 voxels around its 4^3.
+constexpr int kNodeEntries = 216;
 
 __device__ __forceinline__ uint32_t pack_iv(int a0, int a1, int b0, int b1, int c0, int c1) {
   return (uint32_t)(a0 | (a1 << 4) | (b0 << 8) | (b1 << 12) | (c0 << 16) | (c1 << 20));
@@ -369,14 +371,15 @@ __device__ __forceinline__ int depth2_splits(const Bits& b) {
 constexpr int kKinds = 4;
 
 // Per-tree counts: unit-voxel groups (split depth-2 nodes), each kind of
-// larger cell, and boundary-sum slots.  Edge-8 cells are unsplit trees,
+// larger cell, boundary-sum slots and split depth-1 nodes (node tables).  Edge-8 cells are unsplit trees,
 // edge-4 cells unsplit depth-1 nodes of a split root, edge-2 cells unsplit
 // depth-2 nodes of a split depth-1 node.  A split tree has one slot for
 // itself and one per split depth-1 node.
 __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees, int gd, int gh,
                              int gw, int32_t* __restrict__ n_grp, int32_t* __restrict__ n8t,
                              int32_t* __restrict__ n8n, int32_t* __restrict__ n4,
-                             int32_t* __restrict__ n2, int32_t* __restrict__ nslot) {
+                             int32_t* __restrict__ n2, int32_t* __restrict__ nslot,
+                             int32_t* __restrict__ nd1) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
   const Bits b = load_bits(trees, t);
@@ -402,6 +405,7 @@ __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees
   n4[t] = root ? 8 - p1 : 0;
   n2[t] = max(0, 8 * p1 - p2);
   nslot[t] = root ? 1 + p1 : 0;
+  nd1[t] = root ? p1 : 0;
 }
 
 // Leaf lists.  gkey: one key per unit-voxel group.  brow: the rows of every
@@ -412,9 +416,11 @@ __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees
 __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
                              const int64_t* __restrict__ gpre, const int64_t* __restrict__ p8t,
                              const int64_t* __restrict__ p8n, const int64_t* __restrict__ p4,
-                             const int64_t* __restrict__ p2, int64_t n_trees,
-                             int64_t* __restrict__ gkey, int32_t* __restrict__ brow, int64_t gcap,
-                             int64_t bcap, int32_t* __restrict__ stl, int64_t* __restrict__ meta) {
+                             const int64_t* __restrict__ p2, const int64_t* __restrict__ d1pre,
+                             int64_t n_trees, int64_t* __restrict__ gkey, int32_t* __restrict__ brow,
+                             int64_t gcap, int64_t bcap, int32_t* __restrict__ stl,
+                             int64_t* __restrict__ meta, int32_t* __restrict__ e2key, int64_t e2cap,
+                             int64_t* __restrict__ bkey, int64_t kcap) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= n_trees) return;
   const int64_t c8t = p8t[n_trees], c8n = p8n[n_trees], c4 = p4[n_trees], c2 = p2[n_trees];
@@ -432,12 +438,41 @@ __global__ void k_leaf_lists(const uint32_t* __restrict__ trees, const int64_t* 
   auto put = [&](int64_t k, int64_t row) {
     if (k >= 0 && k < bcap) brow[k] = (int32_t)row;
   };
-  if (p8t[t + 1] > p8t[t]) put(p8t[t], row0);
-  if (p8n[t + 1] > p8n[t]) put(c8t + p8n[t], row0);
+  // bkey: tree << 10 | bit index of the edge-8 and edge-4 cells' entries.
+  auto key = [&](int64_t k, int bi) {
+    if (k >= 0 && k < kcap) bkey[k] = (t << 10) | bi;
+  };
+  if (p8t[t + 1] > p8t[t]) {
+    put(p8t[t], row0);
+    key(p8t[t], 0);
+  }
+  if (p8n[t + 1] > p8n[t]) {
+    put(c8t + p8n[t], row0);
+    key(c8t + p8n[t], 0);
+  }
   if (b.lo & 1ull) stl[t - p8t[t] - p8n[t]] = (int32_t)t;
   const int64_t n4t = p4[t + 1] - p4[t];
   for (int64_t k = p4[t]; k < p4[t + 1]; ++k) put(c8t + c8n + k, row0 + (k - p4[t]));
+  if (b.lo & 1ull) {
+    int64_t k = c8t + c8n + p4[t];
+    for (int o1 = 0; o1 < 8; ++o1)
+      if (!bit(b, 1 + o1)) key(k++, 1 + o1);
+  }
   for (int64_t k = p2[t]; k < p2[t + 1]; ++k) put(c8t + c8n + c4 + k, row0 + n4t + (k - p2[t]));
+  // Edge-2 cells in the same order (ascending bit index): the split
+  // depth-1 node holding each (its index in the node tables) and its octant.
+  if (b.lo & 1ull) {
+    int64_t k2 = p2[t], node = d1pre[t];
+    for (int o1 = 0; o1 < 8; ++o1) {
+      if (!bit(b, 1 + o1)) continue;
+      for (int o2 = 0; o2 < 8; ++o2) {
+        if (bit(b, 9 + 8 * o1 + o2)) continue;
+        if (k2 >= 0 && k2 < e2cap && node < (1LL << 28)) e2key[k2] = (int32_t)((node << 3) | o2);
+        ++k2;
+      }
+      ++node;
+    }
+  }
   int64_t k = gpre[t];
   uint64_t m = b.lo >> 9;  // bits 9..63 -> positions 0..54
   while (m && k < gcap) {
@@ -497,39 +532,6 @@ __device__ __forceinline__ int32_t neighbour_row(const uint32_t* __restrict__ tr
   const int64_t tt = ((p.n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
   const Bits b = load_bits(trees, tt);
   return (int32_t)(prefix[tt] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7)));
-}
-
-// Neighbourhood table of the unit-voxel groups (structure only, built once
-// per structure): nbt[64 k + u] = neighbour_row(group k, u), -1 outside the
-// grid, for the G = min(n_groups, n_leaves / 8) groups.  One wave takes
-// kTableGroups groups, lane u entry u of each, so that the lookups of the
-// groups (tree bits, then prefix) are in flight together.
-constexpr int kTableGroups = 4;
-
-__global__ void k_unit_table(const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
-                             int gd, int gh, int gw, int64_t n_leaves,
-                             const int64_t* __restrict__ gkey, const int64_t* __restrict__ n_groups,
-                             int32_t* __restrict__ nbt) {
-  const int64_t wv = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int u = (int)(threadIdx.x & 63);
-  const int64_t G = min(*n_groups, n_leaves / 8);
-  const int64_t g0 = wv * kTableGroups;
-  if (g0 >= G) return;  // wave-uniform
-  // The keys are wave-uniform: tree positions are derived on the scalar unit.
-  int64_t key[kTableGroups];
-#pragma unroll
-  for (int q = 0; q < kTableGroups; ++q) {
-    const uint64_t k64 = (uint64_t)gkey[min(g0 + q, G - 1)];
-    const uint32_t klo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)k64);
-    const uint32_t khi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(k64 >> 32));
-    key[q] = (int64_t)(((uint64_t)khi << 32) | klo);
-  }
-  int32_t r[kTableGroups];
-#pragma unroll
-  for (int q = 0; q < kTableGroups; ++q) r[q] = neighbour_row(trees, prefix, gd, gh, gw, key[q], u);
-#pragma unroll
-  for (int q = 0; q < kTableGroups; ++q)
-    if (g0 + q < G) nbt[(g0 + q) * 64 + u] = r[q] < n_leaves ? r[q] : -1;  // only a non-canonical structure exceeds
 }
 
 // ---------------------------------------------------------------------------
@@ -1111,14 +1113,14 @@ __device__ __forceinline__ void contract_row_perm(const float (&S)[9][CIN / 4], 
 // pipeline serves together would read 16 different rows; in the gather
 // layout lane l holds chunk l % 4 of cell 4 (l / 16) + (l / 4) % 4, so
 // those 16 lanes read 4 rows, 64 contiguous bytes each.
+// The shell rows come from the parent depth-1 node's 6^3 table (e2key: node
+// << 3 | octant, one per cell of the list).
 template <int CIN, int NT>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
-    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
-    int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
-    const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__,
-    const float* __restrict__, int64_t, const float* __restrict__ in,
-    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
-    int relu, float* __restrict__ out, const int64_t* __restrict__, int64_t, int64_t) {
+    int64_t n_leaves, const int32_t* __restrict__ brow, const int32_t* __restrict__ e2key,
+    const int32_t* __restrict__ ntab, int64_t ncap, const int64_t* __restrict__ meta,
+    const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
+    const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
   // and its [n_leaves][cout] destination).
   wm += (int64_t)blockIdx.y * MfmaCfg<CIN, NT, 16>::WFLOATS;
@@ -1132,7 +1134,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
-  kind_range(meta, kind, n_leaves, lbeg, lcnt);
+  kind_range(meta, 3, n_leaves, lbeg, lcnt);
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
   // Gather layout: cell cl, chunk q.  MFMA lane (m, g) takes its operands
   // from lane 16 (m / 4) + 4 (m % 4) + g.
@@ -1147,26 +1149,21 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + cl;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
-    if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
-    int64_t n;
-    int o[3];
-    cell_origin(info, row, gd, gh, gw, n, o);
+    const int32_t key = row >= 0 ? e2key[idx] : 0;
+    const int64_t node = key >> 3;
+    if (row >= n_leaves || key < 0 || node >= ncap) row = -1;  // only a non-canonical structure
     // Shell rows as byte offsets, in the wave's LDS area: lane chunk q
-    // resolves shell voxels 4 j + q of its cell.
+    // takes shell voxels 4 j + q of its cell from the node's table (the
+    // cell's 4^3 neighbourhood is the sub-block at twice its octant).
     {
+      const int o2 = key & 7;
+      const int32_t* nt = ntab + (row >= 0 ? node : 0) * kNodeEntries + 2 * ((o2 >> 2) & 1) * 36 +
+                          2 * ((o2 >> 1) & 1) * 6 + 2 * (o2 & 1);
       int mine[14];
 #pragma unroll
       for (int j = 0; j < 14; ++j) {
         const int u = c_shell2.u[4 * j + q];
-        const int vd = o[0] - 1 + (u >> 4), vh = o[1] - 1 + ((u >> 2) & 3), vw = o[2] - 1 + (u & 3);
-        int r = -1;
-        if (row >= 0 && vd >= 0 && vh >= 0 && vw >= 0 && vd < 8 * gd && vh < 8 * gh && vw < 8 * gw) {
-          const int64_t tt = ((n * gd + (vd >> 3)) * gh + (vh >> 3)) * gw + (vw >> 3);
-          const Bits b = load_bits(trees, tt);
-          const int64_t rr = prefix[tt] + data_idx(b, leaf_at(b, vd & 7, vh & 7, vw & 7));
-          r = rr < n_leaves ? (int)rr : -1;
-        }
-        mine[j] = r;
+        mine[j] = row >= 0 ? nt[(u >> 4) * 36 + ((u >> 2) & 3) * 6 + (u & 3)] : -1;
       }
 #pragma unroll
       for (int j = 0; j < 14; ++j) offm[4 * j + q] = row_offset<CIN>(mine[j], 0);
@@ -1369,7 +1366,8 @@ __global__ void k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
 }
 
 // Region codes of the edge-4 and edge-8 cells (structure only, built once per
-// structure).  For list entry j (the first three kinds) and shell region r
+// structure; bkey gives each entry's tree and bit index).  For list entry j
+// (the first three kinds) and shell region r
 // (the 27 offsets dir without the centre, r = index of dir minus one past
 // the centre), codes[r ccap + j] = the row of the leaf that covers the
 // neighbouring block at offset dir (the tree for an edge-8 cell, the depth-1
@@ -1379,7 +1377,7 @@ __global__ void k_zero_u32(uint32_t* __restrict__ p, int64_t n) {
 // collects the boundary sets of slot s that some cell reads.
 __global__ void k_region_codes(const uint32_t* __restrict__ trees,
                                const int64_t* __restrict__ prefix, int gd, int gh, int gw,
-                               int64_t n_leaves, const uint64_t* __restrict__ info,
+                               int64_t n_leaves, const int64_t* __restrict__ bkey,
                                const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
                                const int64_t* __restrict__ sbase, int64_t cap, int64_t ccap,
                                int32_t* __restrict__ codes, uint32_t* __restrict__ smask) {
@@ -1391,9 +1389,17 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
   const int sz = j < n8 ? 8 : 4;
   int row = brow[j];
   if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
-  int64_t n;
-  int o[3];
-  cell_origin(info, row, gd, gh, gw, n, o);
+  int64_t n = 0;
+  int o[3] = {0, 0, 0};
+  if (row >= 0) {
+    const int64_t k = bkey[j];
+    const TreePos p = tree_pos(k >> 10, gd, gh, gw);
+    const Cell c = cell_of((int)(k & 1023));
+    n = p.n;
+    o[0] = 8 * p.d + c.d;
+    o[1] = 8 * p.h + c.h;
+    o[2] = 8 * p.w + c.w;
+  }
   const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
   // Grid row y takes regions y, y + gridDim.y, ... (indices without the
   // centre): on small structures one region per thread, so that a cell's
@@ -1444,6 +1450,146 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
       else code = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
     }
     codes[(int64_t)(r - (r > 13)) * ccap + j] = code;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Neighbourhood tables of a preparation (structure only), one wave per split
+// tree at a time (grid-stride over the split-tree list).  The 27 trees
+// around the wave's tree (bits, first row) are read once into LDS; every
+// table entry is then resolved from that copy (the voxel's leaf by the
+// tree's split bits, its row by Eq. 3), without branches and without
+// further global loads:
+//   - ntab: for every split depth-1 node (index d1pre[tree] + k for the
+//     tree's k-th), the rows of the 6^3 voxels [o - 1, o + 5) around its 4^3
+//     block, -1 outside the grid.  The 4^3 neighbourhood of each of its
+//     depth-2 octants (a unit-voxel group or an edge-2 cell) is the sub-block
+//     at twice the octant's offset.
+//   - nbt: those sub-blocks of the unit-voxel groups, 64 rows per group in
+//     group order, the layout the unit-voxel kernel stages.
+// ---------------------------------------------------------------------------
+struct NbTree {
+  uint32_t w0, w1, w2;  // split bits 0..31, 32..63, 64..72
+  int32_t inside;       // 0: outside the grid (zero padding)
+  int64_t row0;         // first row (prefix)
+  int64_t pad;
+};
+
+// Which of the 27 neighbour trees holds local coordinate x in [-1, 8]
+// (per axis: 0 below, 1 the wave's own tree, 2 above).
+__device__ __forceinline__ int nb_side(int x) { return x < 0 ? 0 : (x > 7 ? 2 : 1); }
+
+// Split bit i (0 <= i < 73) of words (w0, w1, w2), without branches.
+__device__ __forceinline__ uint32_t bit_bf(uint32_t w0, uint32_t w1, uint32_t w2, int i) {
+  const uint32_t w = i < 32 ? w0 : (i < 64 ? w1 : w2);
+  return (w >> (i & 31)) & 1u;
+}
+
+// Set bits among indices [0, n), 0 <= n <= 73, without branches.
+__device__ __forceinline__ int popc_bf(uint32_t w0, uint32_t w1, uint32_t w2, int n) {
+  const uint32_t m0 = n >= 32 ? 0xFFFFFFFFu : ((1u << (n & 31)) - 1u);
+  const uint32_t m1 = n >= 64 ? 0xFFFFFFFFu : (n <= 32 ? 0u : ((1u << (n - 32)) - 1u));
+  const uint32_t m2 = n <= 64 ? 0u : ((1u << (n - 64)) - 1u);
+  return __popc(w0 & m0) + __popc(w1 & m1) + __popc(w2 & m2 & 0x1FFu);
+}
+
+// Row of the leaf holding voxel (d, h, w), local coordinates of the wave's
+// tree in [-1, 8]; -1 outside the grid or past n_leaves (non-canonical).
+__device__ __forceinline__ int32_t nb_voxel_row(const NbTree* __restrict__ nt, int d, int h, int w,
+                                                int64_t n_leaves) {
+  const NbTree n = nt[nb_side(d) * 9 + nb_side(h) * 3 + nb_side(w)];
+  d &= 7;
+  h &= 7;
+  w &= 7;
+  // The leaf: descend while split (octant bits 2, 1, 0 of the coordinates).
+  const int n1 = 1 + (((d >> 2) & 1) << 2) + (((h >> 2) & 1) << 1) + ((w >> 2) & 1);
+  const int n2 = 8 * n1 + 1 + (((d >> 1) & 1) << 2) + (((h >> 1) & 1) << 1) + ((w >> 1) & 1);
+  const int n3 = 8 * n2 + 1 + ((d & 1) << 2) + ((h & 1) << 1) + (w & 1);
+  const uint32_t s0 = n.w0 & 1u, s1 = bit_bf(n.w0, n.w1, n.w2, n1), s2 = bit_bf(n.w0, n.w1, n.w2, n2);
+  const int i = s0 ? (s1 ? (s2 ? n3 : n2) : n1) : 0;
+  // Eq. 3 (an unsplit root is the only leaf: offset 0).
+  const int pa = (i - 1) >> 3;
+  const int di = i == 0 ? 0
+                        : 8 * popc_bf(n.w0, n.w1, n.w2, pa) + 1 - popc_bf(n.w0, n.w1, n.w2, min(i, 73)) +
+                              ((i - 1) & 7);
+  const int64_t r = n.row0 + di;
+  return (n.inside && r < n_leaves) ? (int32_t)r : -1;
+}
+
+constexpr int kTreeWaves = 4;
+
+__global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    int64_t n_trees, int64_t n_leaves, const int32_t* __restrict__ stl, const int64_t* __restrict__ meta,
+    const int64_t* __restrict__ gpre, const int64_t* __restrict__ d1pre, int32_t* __restrict__ nbt,
+    int64_t gcap, int32_t* __restrict__ ntab, int64_t ncap) {
+  __shared__ NbTree s_nb[kTreeWaves][27];
+  __shared__ int32_t s_node[kTreeWaves][kNodeEntries];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int64_t n_split = n_trees - meta[0] - meta[1];
+  n_split = n_split < 0 ? 0 : (n_split > n_trees ? n_trees : n_split);
+  NbTree* nb = s_nb[wave];
+  int32_t* sn = s_node[wave];
+  const int64_t nwaves = (int64_t)gridDim.x * kTreeWaves;
+  for (int64_t j = (int64_t)blockIdx.x * kTreeWaves + wave; j < n_split; j += nwaves) {
+    const int64_t t = stl[j];
+    if (lane < 27) {
+      const TreePos p = tree_pos(t, gd, gh, gw);
+      const int qd = p.d + lane / 9 - 1, qh = p.h + (lane / 3) % 3 - 1, qw = p.w + lane % 3 - 1;
+      NbTree n;
+      n.w0 = n.w1 = n.w2 = 0u;
+      n.inside = 0;
+      n.row0 = 0;
+      n.pad = 0;
+      if (qd >= 0 && qh >= 0 && qw >= 0 && qd < gd && qh < gh && qw < gw) {
+        const int64_t q = ((p.n * gd + qd) * gh + qh) * gw + qw;
+        const uint4 wv = reinterpret_cast<const uint4*>(trees)[q];
+        n.w0 = wv.x;
+        n.w1 = wv.y;
+        n.w2 = wv.z;
+        n.inside = 1;
+        n.row0 = prefix[q];
+      }
+      nb[lane] = n;
+    }
+    // The wave's own bits and counters, wave-uniform.
+    const uint4 ow = reinterpret_cast<const uint4*>(trees)[t];
+    const uint32_t b0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)ow.x);
+    const uint32_t b1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)ow.y);
+    const uint32_t b2 = (uint32_t)__builtin_amdgcn_readfirstlane((int)ow.z);
+    int64_t g = gpre[t], node = d1pre[t];
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+    for (int o1 = 0; o1 < 8; ++o1) {
+      if (!((b0 >> (1 + o1)) & 1u)) continue;
+      const int od = 4 * ((o1 >> 2) & 1) - 1, oh = 4 * ((o1 >> 1) & 1) - 1, ow1 = 4 * (o1 & 1) - 1;
+      int32_t v[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int u = lane + 64 * k;
+        v[k] = u < kNodeEntries ? nb_voxel_row(nb, od + u / 36, oh + (u / 6) % 6, ow1 + u % 6, n_leaves) : -1;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int u = lane + 64 * k;
+        if (u < kNodeEntries) {
+          sn[u] = v[k];
+          if (node < ncap) ntab[node * kNodeEntries + u] = v[k];
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+      for (int o2 = 0; o2 < 8; ++o2) {
+        if (!bit_bf(b0, b1, b2, 9 + 8 * o1 + o2)) continue;
+        const int idx = (2 * ((o2 >> 2) & 1) + (lane >> 4)) * 36 + (2 * ((o2 >> 1) & 1) + ((lane >> 2) & 3)) * 6 +
+                        2 * (o2 & 1) + (lane & 3);
+        if (g < gcap) nbt[g * 64 + lane] = sn[idx];
+        ++g;
+      }
+      ++node;
+      __builtin_amdgcn_wave_barrier();  // sn is rewritten for the next node
+    }
+    __builtin_amdgcn_wave_barrier();  // nb is rewritten for the next tree
   }
 }
 
@@ -1923,6 +2069,8 @@ typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, 
 typedef void (*WeightFn)(const float*, int, float*);
 typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*, int64_t,
                         const float*, const float*, uint32_t, const float*, int, int, float*);
+typedef void (*Cell2Fn)(int64_t, const int32_t*, const int32_t*, const int32_t*, int64_t, const int64_t*,
+                        const float*, const float*, uint32_t, const float*, int, int, float*);
 typedef void (*EffWeightFn)(const float*, int, int, float*);
 typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int64_t*,
                       const int64_t*, int64_t, int64_t, const float*, uint32_t, float*,
@@ -1934,7 +2082,8 @@ struct MfmaVariant {
   MfmaFn kernel;
   WeightFn weights;
   size_t cell_wfloats;  // cell kernels' weights (16-row tiles)
-  CellFn cell2, cell4, cell8;
+  Cell2Fn cell2;
+  CellFn cell4, cell8;
   WeightFn cell_weights;
   SumFn sums;
   Cell8Fn cell8g;          // edge-8 cells with unsplit face/edge neighbours
@@ -2114,7 +2263,7 @@ size_t smem_limit() {
 }
 
 // Workspace layout (each part 256-byte aligned):
-//   leaf_info  u64 [n_leaves]
+//   leaf_info  u64 [n_leaves]                written by execute, for the generic and GEMM paths
 //   wt         f32 [27 cin cout]            generic-kernel weights
 //   wm         f32 [variant wfloats]        unit-voxel kernel B operands (if a variant exists)
 //   wc         f32 [variant cell_wfloats]   cell kernels' B operands
@@ -2128,14 +2277,18 @@ size_t smem_limit() {
 //   meta       i64 [kKinds + 1]
 //   bsum       f32 [cap][26][cin]           boundary sums (if a variant exists)
 //   nbt        i32 [(n_leaves / 8 + 1) 64]  unit-group neighbourhood rows (if a variant exists)
+//   ntab       i32 [ncap][216]              6^3 rows around each split depth-1 node (if a variant exists)
+//   e2key      i32 [n_leaves]               edge-2 cells: node << 3 | octant (if a variant exists)
 //   codes      i32 [26][ccap]               region codes of edge-4/8 cells (if a variant exists)
+//   bkey       i64 [ccap]                   tree << 10 | bit of the edge-8/4 cells (if a variant exists)
 //   smask      u32 [cap]                    boundary sets read per slot
 // A slot belongs to a split node of depth 0 or 1 and every split node adds 7
 // leaves, so cap = (n_leaves - n_trees) / 7 slots hold every canonical
-// structure of that size; a tree holds at most 8 cells of edge 4 or 8, so
+// structure of that size (and ncap = cap node tables); a tree holds at most 8 cells of edge 4 or 8, so
 // ccap = min(8 n_trees, n_leaves).
-constexpr int kScans = 2 + kKinds;  // groups, the kinds, slots
+constexpr int kScans = 3 + kKinds;  // groups, the kinds, slots, split depth-1 nodes
 constexpr int kSlotScan = 1 + kKinds;
+constexpr int kNodeScan = 2 + kKinds;
 
 struct ConvWs {
   uint64_t* info;
@@ -2152,8 +2305,13 @@ struct ConvWs {
   float* bsum;
   int64_t cap;
   int32_t* nbt;
+  int32_t* ntab;   // 6^3 tables of the split depth-1 nodes
+  int64_t ncap;
+  int32_t* e2key;  // per edge-2 cell: node << 3 | octant
+  int64_t e2cap;
   int32_t* codes;
   int64_t ccap;
+  int64_t* bkey;   // per edge-8/4 cell entry: tree << 10 | bit index
   uint32_t* smask;
   float* sgemm;  // window sums of one row chunk (GEMM path)
   float* wblk;   // channel blocks: weight blocks, one input block, partial outputs
@@ -2199,8 +2357,13 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   // Also without a variant: the GEMM path gathers unit voxels' window sums
   // through it.
   w.nbt = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1)));
+  w.ncap = v ? w.cap : 0;
+  w.ntab = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kNodeEntries * (size_t)w.ncap));
+  w.e2cap = v ? n_leaves : 0;
+  w.e2key = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.e2cap));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
+  w.bkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)w.ccap));
   w.sgemm = reinterpret_cast<float*>(take(oci::conv_gemm_buffer(n_leaves, cin)));
   w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.wblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 27 * (size_t)cin * cout : 0));
@@ -2253,14 +2416,13 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
   if (e != hipSuccess) return e;
   auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
-    // The edge-2 kernel keeps the shell offsets of each wave's tile in LDS.
-    const size_t smem = wsmem + (k == 3 ? (size_t)(kMfmaThreads / 64) * kShell2Lds : 0);
+    const size_t smem = wsmem;
     if (smem > max_smem) return hipErrorInvalidConfiguration;
-    const CellFn f = k == 1 || k == 0 ? v->cell8 : (k == 2 ? v->cell4 : v->cell2);
+    const CellFn f = k == 1 || k == 0 ? v->cell8 : v->cell4;
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (r != hipSuccess) return r;
-    hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(k == 3 ? kMfmaThreads : kCellrThreads), smem, s, a.trees,
+    hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(kCellrThreads), smem, s, a.trees,
                        a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
                        (const float*)w.bsum, w.ccap, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out,
@@ -2277,9 +2439,20 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
                      o.w8, in_bytes, o.bias, o.cout, o.relu, o.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // Edge-2 cells (no boundary sums).
-  e = launch_cells(3, 0, a.n_trees);
-  if (e != hipSuccess) return e;
+  // Edge-2 cells (no boundary sums); the kernel keeps the shell offsets of
+  // each wave's tile in LDS.
+  {
+    const size_t smem = wsmem + (size_t)(kMfmaThreads / 64) * kShell2Lds;
+    if (smem > max_smem) return hipErrorInvalidConfiguration;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell2),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(v->cell2, dim3(nblk, nk), dim3(kMfmaThreads), smem, s, a.n_leaves,
+                       (const int32_t*)w.brow, (const int32_t*)w.e2key, (const int32_t*)w.ntab, w.ncap,
+                       (const int64_t*)w.meta, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   // Boundary sums and the cells that read them (other edge-8, edge-4), in
   // chunks of trees: the sums of the trees up to a chunk's end plus one tree
   // plane (every neighbour of its cells), then the chunk's cells, so that the
@@ -2343,8 +2516,7 @@ int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
 
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
-  hipError_t e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
-  if (e != hipSuccess) return e;
+  hipError_t e = hipSuccess;
   const int64_t nw = 27LL * a.cin * a.cout;
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
                      a.weight, a.cin, a.cout, w.wt);
@@ -2374,7 +2546,8 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   hipLaunchKernelGGL(k_leaf_kinds, dim3(tb), dim3(256), 0, s, a.trees, a.n_trees, a.gd, a.gh, a.gw,
                      scan_counts_buffer(w.scan[0]), scan_counts_buffer(w.scan[1]),
                      scan_counts_buffer(w.scan[2]), scan_counts_buffer(w.scan[3]),
-                     scan_counts_buffer(w.scan[4]), scan_counts_buffer(w.scan[kSlotScan]));
+                     scan_counts_buffer(w.scan[4]), scan_counts_buffer(w.scan[kSlotScan]),
+                     scan_counts_buffer(w.scan[kNodeScan]));
   {
     void* sws[kScans];
     int64_t* spre[kScans];
@@ -2386,21 +2559,26 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(k_leaf_lists, dim3(tb), dim3(256), 0, s, a.trees, a.prefix, w.pre[0], w.pre[1],
-                     w.pre[2], w.pre[3], w.pre[4], a.n_trees, w.gkey, w.brow, a.n_leaves / 8 + 1,
-                     a.n_leaves, w.stl, w.meta);
-  // Neighbourhood tables of the MFMA kernels.
-  const int64_t nt_threads = 64 * ((a.n_leaves / 8 + kTableGroups - 1) / kTableGroups);
-  if (nt_threads > 0)
-    hipLaunchKernelGGL(k_unit_table, dim3((unsigned)((nt_threads + 255) / 256)), dim3(256), 0, s,
-                       a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.gkey,
-                       (const int64_t*)(w.pre[0] + a.n_trees), w.nbt);
+                     w.pre[2], w.pre[3], w.pre[4], (const int64_t*)w.pre[kNodeScan], a.n_trees, w.gkey,
+                     w.brow, a.n_leaves / 8 + 1, a.n_leaves, w.stl, w.meta, w.e2key, w.e2cap, w.bkey,
+                     w.ccap);
   if (w.cap > 0)
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((w.cap + 255) / 256)), dim3(256), 0, s, w.smask,
                        w.cap);
+  // Neighbourhood tables of the unit-voxel groups and the split depth-1 nodes.
+  {
+    // Up to a wave per split tree (their count is on the device).
+    int64_t blocks = (a.n_trees + kTreeWaves - 1) / kTreeWaves;
+    if (blocks > (1LL << 30)) blocks = 1LL << 30;
+    hipLaunchKernelGGL(k_tree_tables, dim3((unsigned)blocks), dim3(64 * kTreeWaves), 0, s, a.trees, a.prefix,
+                       a.gd, a.gh, a.gw, a.n_trees, a.n_leaves, (const int32_t*)w.stl, (const int64_t*)w.meta,
+                       (const int64_t*)w.pre[0], (const int64_t*)w.pre[kNodeScan], w.nbt, a.n_leaves / 8,
+                       w.ntab, w.ncap);
+  }
   if (w.ccap > 0)
     hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256), w.ccap < 65536 ? kSets : 1),
                        dim3(256), 0, s,
-                       a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
+                       a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.bkey,
                        (const int32_t*)w.brow, (const int64_t*)w.meta,
                        (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes, w.smask);
   return hipGetLastError();
@@ -2429,6 +2607,12 @@ hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
   const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
+  if (impl != 2) {
+    // The generic kernel and the window sums of the GEMM path locate every
+    // leaf through the leaf index (the fused kernels need none).
+    hipError_t e = launch_leaf_index(a.trees, a.prefix, a.n_trees, w.info, s);
+    if (e != hipSuccess) return e;
+  }
   if (impl == 3)
     return launch_conv_gemm(a, w.info, w.wt, w.sgemm, w.nbt, w.pre[0], (const int64_t*)(w.pre[0] + a.n_trees),
                             s);
