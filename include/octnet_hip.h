@@ -182,6 +182,20 @@ size_t oc_structure_workspace(int64_t n_trees);
 int oc_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32_t* trees,
              int64_t* prefix, int64_t* n_leaves, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * oc_build without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid hipMalloc).  Same arguments and results as oc_build; the leaf
+ * counts and scan partials go to a static device array inside the library
+ * (16.1 MB per device, held until the process ends), so at most 4,194,304
+ * trees (e.g. a 512^3 grid in batches of 8); more give OC_EOVERFLOW before
+ * any launch.  Calls no allocating routine.  Every call on one device shares
+ * that array: calls that may overlap on one device (other streams, other
+ * threads) race and must be serialised by the caller.  Synchronizes.
+ */
+int oc_build_noalloc(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32_t* trees,
+                     int64_t* prefix, int64_t* n_leaves, void* stream);
+
 /* prefix from trees: leaves per tree = 1 + 7 * (set bits) (Eq. 3 counted to
  * the end of the tree), exclusive scan over trees.  *n_leaves [host] receives
  * the total.  Synchronizes. */

@@ -4,12 +4,51 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 
 #include "../../include/octnet_hip.h"
 #include "oc_internal.h"
 
 namespace {
+
+// Scratch of oc_build_noalloc: the per-tree leaf counts and the scan's chunk
+// sums for up to kNoAllocMaxTrees trees, in a file-scope device array (each
+// device the library runs on holds its own copy until the process ends).
+// In host code `scratch` only names the symbol; its device address comes
+// from hipGetSymbolAddress, once per device, and only that address is used.
+constexpr int64_t kNoAllocMaxTrees = 1LL << 22;
+constexpr size_t kNoAllocBytes = ((4 * (size_t)kNoAllocMaxTrees + 255) & ~(size_t)255) +
+                                 ((8 * ((size_t)kNoAllocMaxTrees / 256 + 2) + 255) & ~(size_t)255) + 1024;
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+constexpr int kMaxScratchDevices = 64;
+
+struct ScratchSlot {
+  std::once_flag once;
+  hipError_t err = hipSuccess;
+  void* ptr = nullptr;
+};
+
+ScratchSlot g_scratch[kMaxScratchDevices];
+
+// The current device's address of `scratch` (looked up on the first call on
+// each device, with that device current).
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  ScratchSlot& sl = g_scratch[dev];
+  std::call_once(sl.once, [&sl]() {
+    void* p = nullptr;
+    sl.err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    sl.ptr = p;
+  });
+  if (sl.err != hipSuccess) return sl.err;
+  *out = sl.ptr;
+  return hipSuccess;
+}
 
 thread_local std::string g_last_error;
 
@@ -96,6 +135,26 @@ int oc_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32
   OC_CHECK_HIP(oci::launch_build(occ, n, gd, gh, gw, rule, trees, oci::scan_counts_buffer(ws), s),
                "oc_build");
   return finish_prefix(nt, prefix, n_leaves, ws, s, "oc_build");
+}
+
+int oc_build_noalloc(const uint8_t* occ, int n, int gd, int gh, int gw, int rule, uint32_t* trees,
+                     int64_t* prefix, int64_t* n_leaves, void* stream) {
+  g_last_error.clear();
+  if (!occ || !trees || !prefix || !n_leaves) return fail(OC_EINVAL, "oc_build_noalloc: null pointer");
+  if (!dims_ok(n, gd, gh, gw)) return fail(OC_EINVAL, "oc_build_noalloc: non-positive dims");
+  if (!sizes_ok(n, gd, gh, gw)) return fail(OC_EOVERFLOW, "oc_build_noalloc: grid too large");
+  if (rule != OC_SPLIT_MIXED && rule != OC_SPLIT_ANY)
+    return fail(OC_EINVAL, "oc_build_noalloc: bad rule %d", rule);
+  const int64_t nt = n_trees_of(n, gd, gh, gw);
+  if (nt > kNoAllocMaxTrees || oci::scan_workspace(nt) > kNoAllocBytes)
+    return fail(OC_EOVERFLOW, "oc_build_noalloc: %lld trees exceed the static scratch (at most %lld trees)",
+                (long long)nt, (long long)kNoAllocMaxTrees);
+  void* ws = nullptr;
+  OC_CHECK_HIP(scratch_address(&ws), "oc_build_noalloc");
+  hipStream_t s = as_stream(stream);
+  OC_CHECK_HIP(oci::launch_build(occ, n, gd, gh, gw, rule, trees, oci::scan_counts_buffer(ws), s),
+               "oc_build_noalloc");
+  return finish_prefix(nt, prefix, n_leaves, ws, s, "oc_build_noalloc");
 }
 
 int oc_prefix(const uint32_t* trees, int64_t n_trees, int64_t* prefix, int64_t* n_leaves, void* ws,

@@ -38,6 +38,7 @@ SIGNATURES = {
     "oc_version": (_I, []),
     "oc_structure_workspace": (_S, [_L]),
     "oc_build": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _S, _P]),
+    "oc_build_noalloc": (_I, [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P]),
     "oc_prefix": (_I, [_P, _L, _P, _P, _P, _S, _P]),
     "oc_validate": (_I, [_P, _L, _P, _P, _S, _P]),
     "oc_leaf_index": (_I, [_P, _P, _L, _P, _P]),
@@ -165,6 +166,30 @@ def build(occ: torch.Tensor, rule: str = "mixed") -> Octree:
     _check(lib().oc_build(_ptr(occ), n, gd, gh, gw, OC_SPLIT_MIXED if rule == "mixed" else OC_SPLIT_ANY,
                           _ptr(trees), _ptr(prefix), ctypes.byref(nl), _ptr(ws), ws.numel(), _stream()),
            "oc_build")
+    return Octree(n, gd, gh, gw, trees, prefix, nl.value)
+
+
+def build_noalloc(occ: torch.Tensor, rule: str = "mixed", trees: torch.Tensor | None = None,
+                  prefix: torch.Tensor | None = None) -> Octree:
+    """build() through oc_build_noalloc: the library allocates nothing (its
+    scratch is a static device array); trees and prefix may be passed in."""
+    if occ.dtype != torch.uint8 or occ.dim() != 4:
+        raise OctNetError("occupancy must be uint8 [N, D, H, W]")
+    n, D, H, W = occ.shape
+    if D % 8 or H % 8 or W % 8:
+        raise OctNetError("voxel grid dims must be multiples of 8")
+    gd, gh, gw = D // 8, H // 8, W // 8
+    nt = n * gd * gh * gw
+    if trees is None:
+        trees = torch.empty((nt, 4), dtype=torch.int32, device=occ.device)
+    if prefix is None:
+        prefix = torch.empty(nt + 1, dtype=torch.int64, device=occ.device)
+    if tuple(trees.shape) != (nt, 4) or tuple(prefix.shape) != (nt + 1,):
+        raise OctNetError("trees must be [n_trees, 4] and prefix [n_trees + 1]")
+    nl = ctypes.c_int64(0)
+    _check(lib().oc_build_noalloc(_ptr(occ), n, gd, gh, gw, OC_SPLIT_MIXED if rule == "mixed" else OC_SPLIT_ANY,
+                                  _ptr(trees), _ptr(prefix), ctypes.byref(nl), _stream()),
+           "oc_build_noalloc")
     return Octree(n, gd, gh, gw, trees, prefix, nl.value)
 
 
