@@ -12,6 +12,7 @@
 // (Sec. 3.2 and the supplement's "Efficient Convolution"), turned into 27
 // window sums followed by one (27*Cin) x Cout contraction per leaf.
 #include <mutex>
+#include <type_traits>
 
 #include "oc_internal.h"
 
@@ -649,15 +650,69 @@ __device__ __forceinline__ uint32_t row_offset(int row, int ch) {
   return row < 0 ? kOutside : (uint32_t)row * (uint32_t)(CIN * 4) + (uint32_t)(ch * 4);
 }
 
+// The forward kernels gather rows by row index through one of two policies
+// (the host picks one per launch):
+//   RowsRaw:  one raw buffer resource over the input, 32-bit byte offsets
+//             row * 4 CIN + off; the row index kNoRow wraps to an offset
+//             past the end, which reads zero (the padding outside the grid).
+//             For inputs below 4 GiB.
+//   RowsWide: 64-bit addresses per lane; kNoRow reads zero through a masked
+//             load.  For inputs of 4 GiB and more (up to 2^31 rows).
+constexpr uint32_t kNoRow = 0xFFFFFFFFu;
+
+// A gathered row is named by addr(row) (-1: outside the grid), which the
+// kernels stage, then loaded at byte off of the row by load(a, off).
+template <int CIN>
+struct RowsRaw {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ __forceinline__ static RowsRaw make(const float* in, uint32_t n_rows) {
+    RowsRaw g;
+    g.r = input_rsrc(in, n_rows * (uint32_t)(4 * CIN));
+    return g;
+  }
+  __device__ __forceinline__ static uint32_t addr(int row) {
+    return row < 0 ? kOutside : (uint32_t)row * (uint32_t)(4 * CIN);
+  }
+  template <int V>
+  __device__ __forceinline__ typename VecT<V>::type load(uint32_t a, uint32_t off) const {
+    return gather<V>(r, a + off);
+  }
+};
+
+template <int CIN>
+struct RowsWide {
+  const float* base;
+  __device__ __forceinline__ static RowsWide make(const float* in, uint32_t) {
+    RowsWide g;
+    g.base = in;
+    return g;
+  }
+  __device__ __forceinline__ static uint32_t addr(int row) { return row < 0 ? kNoRow : (uint32_t)row; }
+  template <int V>
+  __device__ __forceinline__ typename VecT<V>::type load(uint32_t row, uint32_t off) const {
+    typename VecT<V>::type v;
+    if constexpr (V == 1) v = 0.f;
+    else v = typename VecT<V>::type(0.f);
+    if (row != kNoRow)
+      v = *reinterpret_cast<const typename VecT<V>::type*>(base + (uint64_t)row * CIN + (off >> 2));
+    return v;
+  }
+};
+
+template <int V, class G>
+__device__ __forceinline__ typename VecT<V>::type gather_at(const G& g, uint32_t a, uint32_t off) {
+  return g.template load<V>(a, off);
+}
+
 #ifndef OC_UNIT_THREADS
 #define OC_UNIT_THREADS 512
 #endif
 constexpr int kUnitThreads = OC_UNIT_THREADS;
 
-template <int CIN, int NT, int MS>
+template <int CIN, int NT, int MS, class GP>
 __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
     int64_t n_leaves, const int32_t* __restrict__ nbt, const int64_t* __restrict__ n_groups,
-    const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
+    const float* __restrict__ in, const float* __restrict__ wm, uint32_t n_rows,
     const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
   // and its [n_leaves][cout] destination).
@@ -665,7 +720,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
   out += (int64_t)blockIdx.y * n_leaves * cout;
   if (bias != nullptr) bias += (int64_t)blockIdx.y * cout;
   using C = MfmaCfg<CIN, NT, MS>;
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const GP rin = GP::make(in, n_rows);
   using Vec = typename VecT<C::VEC>::type;
   using Acc = typename AccT<MS>::type;
   extern __shared__ float smem[];
@@ -742,16 +797,16 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
   constexpr int PD = OC_UNIT_PREFETCH;  // deltas of gathers in flight
   static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
   Vec abuf[PD + 1][C::NV];
-  auto gather_row = [&](uint32_t off, Vec* a) {
+  const uint32_t coff = 4u * C::VEC * g;  // the lane's first channel, in bytes
+  auto gather_row = [&](uint32_t row, Vec* a) {
 #pragma unroll
-    for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
+    for (int v = 0; v < C::NV; ++v) a[v] = gather_at<C::VEC>(rin, row, coff + 4 * C::VSTRIDE * v);
   };
-  // Byte offsets of the lane's A rows for the first PD deltas of a table.
+  // The lane's A rows for the first PD deltas of a table.
   uint32_t noff[PD];
   auto first_offsets = [&](const int32_t* t) {
 #pragma unroll
-    for (int k = 0; k < PD; ++k)
-      noff[k] = row_offset<CIN>(t[ubase + (k / 9) * 16 + ((k / 3) % 3) * 4 + k % 3], C::VEC * g);
+    for (int k = 0; k < PD; ++k) noff[k] = GP::addr(t[ubase + (k / 9) * 16 + ((k / 3) % 3) * 4 + k % 3]);
   };
   // A finished tile is stored during the next tile's fifth delta: its stores
   // then queue behind gathers that are already consumed, and the gathers
@@ -781,12 +836,11 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
 #pragma unroll
         for (int r = 0; r < (MS == 32 ? 16 : 4); ++r) acc2[a2][nt][r] = 0.f;
     Vec bbuf[2][NT][C::NV];
-    // The 27 A-row offsets of this lane, read from the table up front so that
-    // no LDS round trip sits between a delta's MFMAs and its gathers.
+    // The 27 A rows of this lane, read from the table up front so that no
+    // LDS round trip sits between a delta's MFMAs and its gathers.
     uint32_t aoff[27];
 #pragma unroll
-    for (int dl = 0; dl < 27; ++dl)
-      aoff[dl] = row_offset<CIN>(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3], C::VEC * g);
+    for (int dl = 0; dl < 27; ++dl) aoff[dl] = GP::addr(nb[ubase + (dl / 9) * 16 + ((dl / 3) % 3) * 4 + dl % 3]);
     auto load_b = [&](int dl, Vec (*b)[C::NV]) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
@@ -910,6 +964,19 @@ __device__ __forceinline__ void contract_layer(const float (&S)[9][CIN / 4],
   }
 }
 
+// The lane's CH channels of row `row`, starting at byte off of the row.
+template <int CIN, class G>
+__device__ __forceinline__ void gather_channels_at(const G& rin, uint32_t row, uint32_t off,
+                                                   float (&x)[CIN / 4]) {
+  using K = CellCfg<CIN, 1>;
+#pragma unroll
+  for (int jv = 0; jv < K::NV; ++jv) {
+    const typename K::Vec v = gather_at<K::VEC>(rin, row, off + 4u * K::VSTRIDE * jv);
+#pragma unroll
+    for (int e = 0; e < K::VEC; ++e) x[K::VEC * jv + e] = vget<K::VEC>(v, e);
+  }
+}
+
 // The lane's CH channels of the row at byte offset off.
 template <int CIN>
 __device__ __forceinline__ void gather_channels(__amdgpu_buffer_rsrc_t rin, uint32_t off,
@@ -1007,23 +1074,24 @@ constexpr bool shell2_inner(int u) {
 
 template <int JD, int UH, int K, int CIN>
 struct Shell2RowLoad {
-  __device__ __forceinline__ static void run(float (&X)[8][CIN / 4], const uint32_t* offs,
-                                             __amdgpu_buffer_rsrc_t rin, uint32_t choff) {
+  template <class G>
+  __device__ __forceinline__ static void run(float (&X)[8][CIN / 4], const uint32_t* rows, const G& rin,
+                                             uint32_t choff) {
     constexpr int u = (JD + K / 4) * 16 + UH * 4 + (K % 4);
     if constexpr (!shell2_inner(u)) {
       constexpr int q = shell2_q(u);
-      gather_channels<CIN>(rin, offs[q] + choff, X[K]);
+      gather_channels_at<CIN>(rin, rows[q], choff, X[K]);
     }
-    Shell2RowLoad<JD, UH, K + 1, CIN>::run(X, offs, rin, choff);
+    Shell2RowLoad<JD, UH, K + 1, CIN>::run(X, rows, rin, choff);
   }
 };
 template <int JD, int UH, int CIN>
 struct Shell2RowLoad<JD, UH, 8, CIN> {
-  __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t*,
-                                             __amdgpu_buffer_rsrc_t, uint32_t) {}
+  template <class G>
+  __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t*, const G&, uint32_t) {}
 };
 
-// LDS bytes per wave for the shell offsets of a 16-cell tile.
+// LDS bytes per wave for the shell rows of a 16-cell tile.
 constexpr int kShell2Lds = 16 * 56 * 4;
 
 // The box sums are separable: the two planes of the row are summed first,
@@ -1115,11 +1183,11 @@ __device__ __forceinline__ void contract_row_perm(const float (&S)[9][CIN / 4], 
 // those 16 lanes read 4 rows, 64 contiguous bytes each.
 // The shell rows come from the parent depth-1 node's 6^3 table (e2key: node
 // << 3 | octant, one per cell of the list).
-template <int CIN, int NT>
+template <int CIN, int NT, class GP>
 __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     int64_t n_leaves, const int32_t* __restrict__ brow, const int32_t* __restrict__ e2key,
     const int32_t* __restrict__ ntab, int64_t ncap, const int64_t* __restrict__ meta,
-    const float* __restrict__ in, const float* __restrict__ wm, uint32_t in_bytes,
+    const float* __restrict__ in, const float* __restrict__ wm, uint32_t n_rows,
     const float* __restrict__ bias, int cout, int relu, float* __restrict__ out) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
   // and its [n_leaves][cout] destination).
@@ -1131,7 +1199,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const GP rin = GP::make(in, n_rows);
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, 3, n_leaves, lbeg, lcnt);
@@ -1152,7 +1220,7 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
     const int32_t key = row >= 0 ? e2key[idx] : 0;
     const int64_t node = key >> 3;
     if (row >= n_leaves || key < 0 || node >= ncap) row = -1;  // only a non-canonical structure
-    // Shell rows as byte offsets, in the wave's LDS area: lane chunk q
+    // Shell rows, in the wave's LDS area: lane chunk q
     // takes shell voxels 4 j + q of its cell from the node's table (the
     // cell's 4^3 neighbourhood is the sub-block at twice its octant).
     {
@@ -1166,12 +1234,12 @@ __global__ void __launch_bounds__(512) k_conv_cell2_mfma(
         mine[j] = row >= 0 ? nt[(u >> 4) * 36 + ((u >> 2) & 3) * 6 + (u & 3)] : -1;
       }
 #pragma unroll
-      for (int j = 0; j < 14; ++j) offm[4 * j + q] = row_offset<CIN>(mine[j], 0);
+      for (int j = 0; j < 14; ++j) offm[4 * j + q] = GP::addr(mine[j]);
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     }
     float xs[CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(row, 0) + choff, xs);
+    gather_channels_at<CIN>(rin, GP::addr(row), choff, xs);
     typename K::Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -1252,15 +1320,15 @@ struct BoundaryVoxels {
   static constexpr int x0 = V >> 4, x1 = (V >> 2) & 3, x2 = V & 3;
   static constexpr bool skip = interior4(V);
   static constexpr int NK = skip ? K : K + 1;
-  template <int CIN>
-  __device__ __forceinline__ static void load(float (&xv)[56], const int (&r2)[8], int sp,
-                                              __amdgpu_buffer_rsrc_t rin, int c) {
+  template <int CIN, class G>
+  __device__ __forceinline__ static void load(float (&xv)[56], const int (&r2)[8], int sp, const G& rin,
+                                              int c) {
     if constexpr (!skip) {
       constexpr int o2 = 4 * (x0 >> 1) + 2 * (x1 >> 1) + (x2 >> 1);
       constexpr int u = 4 * (x0 & 1) + 2 * (x1 & 1) + (x2 & 1);
-      xv[K] = gather<1>(rin, row_offset<CIN>(r2[o2] + (((sp >> o2) & 1) ? u : 0), c));
+      xv[K] = gather_at<1>(rin, G::addr(r2[o2] + (((sp >> o2) & 1) ? u : 0)), 4u * c);
     }
-    BoundaryVoxels<V + 1, NK>::template load<CIN>(xv, r2, sp, rin, c);
+    BoundaryVoxels<V + 1, NK>::template load<CIN, G>(xv, r2, sp, rin, c);
   }
   __device__ __forceinline__ static void add(float (&cs)[kSets], const float (&xv)[56]) {
     if constexpr (!skip) {
@@ -1276,9 +1344,8 @@ struct BoundaryVoxels {
 };
 template <int K>
 struct BoundaryVoxels<64, K> {
-  template <int CIN>
-  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int,
-                                              __amdgpu_buffer_rsrc_t, int) {}
+  template <int CIN, class G>
+  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int, const G&, int) {}
   __device__ __forceinline__ static void add(float (&)[kSets], const float (&)[56]) {}
 };
 
@@ -1287,12 +1354,12 @@ struct BoundaryVoxels<64, K> {
 // unsplit child reads its one row 56 times, from cache), all 56 loads in
 // flight before the sums; a tree set is the sum of the same set over the
 // children on that side.
-template <int CIN>
+template <int CIN, class GP>
 __global__ void __launch_bounds__(256) k_boundary_sums(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
     const int32_t* __restrict__ stl, const int64_t* __restrict__ meta,
     const int64_t* __restrict__ sbase, int64_t n_trees, int64_t cap, const float* __restrict__ in,
-    uint32_t in_bytes, float* __restrict__ bsum, const int64_t* __restrict__ p8t,
+    uint32_t n_rows, float* __restrict__ bsum, const int64_t* __restrict__ p8t,
     const int64_t* __restrict__ p8n, int64_t t0, int64_t t1, const uint32_t* __restrict__ smask) {
   constexpr int TPW = 64 / CIN;
   const int lane = threadIdx.x & 63, c = lane % CIN, sub = lane / CIN;
@@ -1301,7 +1368,7 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
   // The split trees among trees [t0, t1): list entries [j0, j1).
   const int64_t j0 = min(n_split, max((int64_t)0, t0 - p8t[t0] - p8n[t0]));
   const int64_t j1 = min(n_split, max(j0, t1 - p8t[t1] - p8n[t1]));
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const GP rin = GP::make(in, n_rows);
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int64_t nwaves = ((int64_t)gridDim.x * blockDim.x) >> 6;
   for (int64_t j = j0 + wave * TPW + sub; j < j1; j += nwaves * TPW) {
@@ -1326,7 +1393,7 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
         r2[o2] = split1 ? rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2) : r1;
       }
       float xv[56];
-      BoundaryVoxels<0, 0>::load<CIN>(xv, r2, sp, rin, c);
+      BoundaryVoxels<0, 0>::load<CIN, GP>(xv, r2, sp, rin, c);
       __builtin_amdgcn_sched_barrier(0);
       float cs[kSets];
 #pragma unroll
@@ -1670,32 +1737,32 @@ __device__ __forceinline__ void summary_add(float (&S)[9][PV * cell_vec<CIN>()],
 // all its codes are rows, as corner codes always are; then the row gather is
 // issued whatever the code (a code that is not a row reads zeros), so that
 // it need not wait behind a branch.
-// The lane's channel vectors P PV .. P PV + PV - 1 of the row at byte offset off.
-template <int CIN, int PV, int P>
-__device__ __forceinline__ void gather_pass(__amdgpu_buffer_rsrc_t rin, uint32_t off,
+// The lane's channel vectors P PV .. P PV + PV - 1 of row `row` (off: the
+// byte offset of the lane's first channel).
+template <int CIN, int PV, int P, class G>
+__device__ __forceinline__ void gather_pass(const G& rin, uint32_t row, uint32_t off,
                                             float (&x)[PV * cell_vec<CIN>()]) {
   using K = CellCfg<CIN, 1>;
 #pragma unroll
   for (int i = 0; i < PV; ++i) {
-    const typename K::Vec v = gather<K::VEC>(rin, off + 4u * K::VSTRIDE * (P * PV + i));
+    const typename K::Vec v = gather_at<K::VEC>(rin, row, off + 4u * K::VSTRIDE * (P * PV + i));
 #pragma unroll
     for (int e = 0; e < K::VEC; ++e) x[K::VEC * i + e] = vget<K::VEC>(v, e);
   }
 }
 
-template <int R, int JD, int SZ, int CIN, bool TRIV, int PV, int P>
-__device__ __forceinline__ void region_sum(float (&S)[9][PV * cell_vec<CIN>()], int32_t code,
-                                           __amdgpu_buffer_rsrc_t rin, const float* __restrict__ bsum,
-                                           int choff) {
+template <int R, int JD, int SZ, int CIN, bool TRIV, int PV, int P, class G>
+__device__ __forceinline__ void region_sum(float (&S)[9][PV * cell_vec<CIN>()], int32_t code, const G& rin,
+                                           const float* __restrict__ bsum, int choff) {
   constexpr int CH = PV * cell_vec<CIN>();
   constexpr int nz = (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1);
   if constexpr (TRIV || nz == 3) {  // codes are rows (or outside)
     float x[CH];
-    gather_pass<CIN, PV, P>(rin, code >= 0 ? row_offset<CIN>(code, choff) : kOutside, x);
+    gather_pass<CIN, PV, P>(rin, G::addr(code), 4u * choff, x);
     region_add<R, JD, SZ, CH>(S, x);
   } else if (code >= 0) {
     float x[CH];
-    gather_pass<CIN, PV, P>(rin, row_offset<CIN>(code, choff), x);
+    gather_pass<CIN, PV, P>(rin, G::addr(code), 4u * choff, x);
     region_add<R, JD, SZ, CH>(S, x);
   } else if (code <= -2) {
     summary_add<R, JD, CIN, PV, P>(S, bsum + (int64_t)(-2 - code) * (kSets * CIN) + choff, true);
@@ -1717,9 +1784,9 @@ struct RegionLayer {
     if constexpr (in_layer<JD>(R)) c[R] = col[(int64_t)(R - (R > 13)) * ccap];
     RegionLayer<R + 1, JD, SZ, CIN, TRIV, PV, P>::codes(c, col, ccap);
   }
-  __device__ __forceinline__ static void run(float (&S)[9][W], const int32_t (&c)[27],
-                                             __amdgpu_buffer_rsrc_t rin, const float* bsum,
-                                             int choff) {
+  template <class G>
+  __device__ __forceinline__ static void run(float (&S)[9][W], const int32_t (&c)[27], const G& rin,
+                                             const float* bsum, int choff) {
     if constexpr (in_layer<JD>(R)) {
       region_sum<R, JD, SZ, CIN, TRIV, PV, P>(S, c[R], rin, bsum, choff);
       // A few regions' loads in flight at a time (more would spill).
@@ -1732,8 +1799,9 @@ template <int JD, int SZ, int CIN, bool TRIV, int PV, int P>
 struct RegionLayer<27, JD, SZ, CIN, TRIV, PV, P> {
   static constexpr int W = PV * cell_vec<CIN>();
   __device__ __forceinline__ static void codes(int32_t (&)[27], const int32_t*, int64_t) {}
-  __device__ __forceinline__ static void run(float (&)[9][W], const int32_t (&)[27],
-                                             __amdgpu_buffer_rsrc_t, const float*, int) {}
+  template <class G>
+  __device__ __forceinline__ static void run(float (&)[9][W], const int32_t (&)[27], const G&, const float*,
+                                             int) {}
 };
 
 // Contract pass P (vectors P PV .. + PV - 1) of layer JD into acc.
@@ -1764,8 +1832,9 @@ __device__ __forceinline__ void contract_pass(const float (&S)[9][PV * cell_vec<
 // vectors (fewer registers per pass; the codes are loaded once per layer).
 template <int CIN, int NT, int SZ, bool TRIV, int JD, int PV, int P>
 struct LayerPasses {
+  template <class G>
   __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
-                                             bool live, __amdgpu_buffer_rsrc_t rin,
+                                             bool live, const G& rin,
                                              const float* bsum, int choff, const float* wl,
                                              int lane, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
     using K = CellCfg<CIN, NT>;
@@ -1793,13 +1862,13 @@ struct LayerPasses {
 #endif
 constexpr int kCellrThreads = OC_CELLR_THREADS;
 
-template <int CIN, int NT, int SZ, bool TRIV>
+template <int CIN, int NT, int SZ, bool TRIV, class GP>
 __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
     const float* __restrict__ bsum, int64_t ccap, const float* __restrict__ in,
-    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
+    const float* __restrict__ wm, uint32_t n_rows, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out, const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
   // and its [n_leaves][cout] destination).
@@ -1813,7 +1882,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const GP rin = GP::make(in, n_rows);
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
@@ -1835,7 +1904,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     if (row >= n_leaves || lbeg + idx >= ccap) row = -1;  // only a non-canonical structure
     const int32_t* col = codes + (lbeg + idx);  // the cell's column of region codes
     float xs[CH];
-    gather_channels<CIN>(rin, row_offset<CIN>(row, choff), xs);
+    gather_channels_at<CIN>(rin, GP::addr(row), 4u * choff, xs);
     typename K::Acc acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
@@ -1868,11 +1937,11 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
 // weight set.  That is the unit voxels' gather-GEMM (K = 27 cin): MS cells
 // per tile, term r's rows gathered into the A operand two terms ahead, the
 // next tile's term rows loaded during this one.
-template <int CIN, int NT, int MS>
+template <int CIN, int NT, int MS, class GP>
 __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
     int64_t n_leaves, const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
     const int32_t* __restrict__ codes, int64_t ccap, const float* __restrict__ in,
-    const float* __restrict__ wm, uint32_t in_bytes, const float* __restrict__ bias, int cout,
+    const float* __restrict__ wm, uint32_t n_rows, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
   // and its [n_leaves][cout] destination).
@@ -1882,7 +1951,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
   using C = MfmaCfg<CIN, NT, MS>;
   using Vec = typename VecT<C::VEC>::type;
   using Acc = typename AccT<MS>::type;
-  const __amdgpu_buffer_rsrc_t rin = input_rsrc(in, in_bytes);
+  const GP rin = GP::make(in, n_rows);
   extern __shared__ float smem[];
   float* wl = smem;
   weights_to_lds<CIN, NT, MS>(wm, wl);
@@ -1928,14 +1997,15 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
   constexpr int PD = OC_UNIT_PREFETCH;
   static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
   Vec abuf[PD + 1][C::NV];
-  auto gather_row = [&](uint32_t off, Vec* a) {
+  const uint32_t coff = 4u * C::VEC * g;  // the lane's first channel, in bytes
+  auto gather_row = [&](uint32_t row, Vec* a) {
 #pragma unroll
-    for (int v = 0; v < C::NV; ++v) a[v] = gather<C::VEC>(rin, off + 4 * C::VSTRIDE * v);
+    for (int v = 0; v < C::NV; ++v) a[v] = gather_at<C::VEC>(rin, row, coff + 4 * C::VSTRIDE * v);
   };
   uint32_t aoff[27];
   auto offsets = [&]() {
 #pragma unroll
-    for (int r = 0; r < 27; ++r) aoff[r] = row_offset<CIN>(trow[r], C::VEC * g);
+    for (int r = 0; r < 27; ++r) aoff[r] = GP::addr(trow[r]);
   };
   Acc pacc[NT];
   int psrow = -1;
@@ -1973,7 +2043,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
         // The next tile's offsets (this tile's are no longer needed past
         // the gathers already issued).
 #pragma unroll
-        for (int k = 0; k < PD; ++k) aoff[k] = row_offset<CIN>(trow[k], C::VEC * g);
+        for (int k = 0; k < PD; ++k) aoff[k] = GP::addr(trow[k]);
       }
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -2079,16 +2149,31 @@ typedef void (*SumFn)(const uint32_t*, const int64_t*, const int32_t*, const int
 struct MfmaVariant {
   int cin, cout_max, cout_min, ms, nt;
   size_t wfloats;       // unit-voxel kernel weights (MS-row tiles)
-  MfmaFn kernel;
   WeightFn weights;
   size_t cell_wfloats;  // cell kernels' weights (16-row tiles)
-  Cell2Fn cell2;
-  CellFn cell4, cell8;
   WeightFn cell_weights;
-  SumFn sums;
-  Cell8Fn cell8g;          // edge-8 cells with unsplit face/edge neighbours
-  EffWeightFn eff_weights; // their effective weights (unit-kernel layout)
+  EffWeightFn eff_weights; // edge-8 effective weights (unit-kernel layout)
+  // The kernels, [0] gathering through RowsRaw (input below 4 GiB), [1]
+  // through RowsWide.
+  MfmaFn kernel[2];
+  Cell2Fn cell2[2];
+  CellFn cell4[2], cell8[2];
+  SumFn sums[2];
+  Cell8Fn cell8g[2];    // edge-8 cells with unsplit face/edge neighbours
 };
+
+template <int CIN, int NT, int MS, int WIDE>
+void set_kernels(MfmaVariant& v) {
+  using C = MfmaCfg<CIN, NT, MS>;
+  constexpr int CNT = (C::NCOL + 15) / 16;
+  using G = typename std::conditional<WIDE != 0, RowsWide<CIN>, RowsRaw<CIN>>::type;
+  v.kernel[WIDE] = &k_conv_unit_mfma<CIN, NT, MS, G>;
+  v.cell2[WIDE] = &k_conv_cell2_mfma<CIN, CNT, G>;
+  v.cell4[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 4, false, G>;
+  v.cell8[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 8, false, G>;
+  v.sums[WIDE] = &k_boundary_sums<CIN, G>;
+  v.cell8g[WIDE] = &k_conv_cell8t_gemm<CIN, NT, MS, G>;
+}
 
 template <int CIN, int NT, int MS>
 MfmaVariant make_variant(int cout_min) {
@@ -2100,17 +2185,13 @@ MfmaVariant make_variant(int cout_min) {
   v.ms = MS;
   v.nt = NT;
   v.wfloats = C::WFLOATS;
-  v.kernel = &k_conv_unit_mfma<CIN, NT, MS>;
   v.weights = &k_mfma_weights<CIN, NT, MS>;
   constexpr int CNT = (C::NCOL + 15) / 16;
   v.cell_wfloats = MfmaCfg<CIN, CNT, 16>::WFLOATS;
-  v.cell2 = &k_conv_cell2_mfma<CIN, CNT>;
-  v.cell4 = &k_conv_cellr_mfma<CIN, CNT, 4, false>;
-  v.cell8 = &k_conv_cellr_mfma<CIN, CNT, 8, false>;
   v.cell_weights = &k_mfma_weights<CIN, CNT, 16>;
-  v.sums = &k_boundary_sums<CIN>;
-  v.cell8g = &k_conv_cell8t_gemm<CIN, NT, MS>;
   v.eff_weights = &k_eff_weights<CIN, NT, MS>;
+  set_kernels<CIN, NT, MS, 0>(v);
+  set_kernels<CIN, NT, MS, 1>(v);
   return v;
 }
 
@@ -2392,51 +2473,53 @@ constexpr int kMaxOutBlocks = 8;
 #endif
 constexpr int64_t kBlockedMinLeaves = OC_BLOCKED_MIN_LEAVES;
 
-// The fused kernels of variant v on input `in` (v->cin channels; in_bytes its
-// size) for nk output blocks (grid rows; block k's weight layouts and
+// The fused kernels of variant v on input `in` (v->cin channels, n_rows
+// rows) for nk output blocks (grid rows; block k's weight layouts and
 // destination follow block k - 1's, as the kernels expect): unit voxels,
 // edge-8 cells with unsplit neighbours and edge-2 cells, then the boundary
 // sums of split nodes (once, they depend on the input only) and the edge-8
 // and edge-4 cells that read them.
 hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant* v, const float* in,
-                      uint32_t in_bytes, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
+                      uint32_t n_rows, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
   const int num_cus = L.num_cus;
   const size_t max_smem = L.max_smem;
+  // Raw buffer gathers below 4 GiB of input, 64-bit ones from there.
+  const int wide = (uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ? 1 : 0;
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > max_smem) return hipErrorInvalidConfiguration;
   const int nblk = ((num_cus + 7) / 8) * 8;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel),
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->kernel[wide]),
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)msmem);
   if (e != hipSuccess) return e;
   // Edge-8 cells with unsplit face and edge neighbours: the gather-GEMM with
   // effective weights (same LDS footprint as the unit kernel, no tables).
   const size_t gsm = sizeof(float) * v->wfloats;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g),
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell8g[wide]),
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)gsm);
   if (e != hipSuccess) return e;
   auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     const size_t smem = wsmem;
     if (smem > max_smem) return hipErrorInvalidConfiguration;
-    const CellFn f = k == 1 || k == 0 ? v->cell8 : v->cell4;
+    const CellFn f = k == 1 || k == 0 ? v->cell8[wide] : v->cell4[wide];
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (r != hipSuccess) return r;
     hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(kCellrThreads), smem, s, a.trees,
                        a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
-                       (const float*)w.bsum, w.ccap, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out,
+                       (const float*)w.bsum, w.ccap, in, o.wc, n_rows, o.bias, o.cout, o.relu, o.out,
                        (const int64_t*)w.pre[1 + k], t0, t1);
     return hipGetLastError();
   };
-  hipLaunchKernelGGL(v->kernel, dim3(nblk, nk), dim3(kUnitThreads), msmem, s, a.n_leaves,
-                     (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), in, o.wm, in_bytes,
+  hipLaunchKernelGGL(v->kernel[wide], dim3(nblk, nk), dim3(kUnitThreads), msmem, s, a.n_leaves,
+                     (const int32_t*)w.nbt, (const int64_t*)(w.pre[0] + a.n_trees), in, o.wm, n_rows,
                      o.bias, o.cout, o.relu, o.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(v->cell8g, dim3(nblk, nk), dim3(kUnitThreads), gsm, s, a.n_leaves,
+  hipLaunchKernelGGL(v->cell8g[wide], dim3(nblk, nk), dim3(kUnitThreads), gsm, s, a.n_leaves,
                      (const int32_t*)w.brow, (const int64_t*)w.meta, (const int32_t*)w.codes, w.ccap, in,
-                     o.w8, in_bytes, o.bias, o.cout, o.relu, o.out);
+                     o.w8, n_rows, o.bias, o.cout, o.relu, o.out);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // Edge-2 cells (no boundary sums); the kernel keeps the shell offsets of
@@ -2444,12 +2527,12 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   {
     const size_t smem = wsmem + (size_t)(kMfmaThreads / 64) * kShell2Lds;
     if (smem > max_smem) return hipErrorInvalidConfiguration;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell2),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(v->cell2[wide]),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(v->cell2, dim3(nblk, nk), dim3(kMfmaThreads), smem, s, a.n_leaves,
+    hipLaunchKernelGGL(v->cell2[wide], dim3(nblk, nk), dim3(kMfmaThreads), smem, s, a.n_leaves,
                        (const int32_t*)w.brow, (const int32_t*)w.e2key, (const int32_t*)w.ntab, w.ncap,
-                       (const int64_t*)w.meta, in, o.wc, in_bytes, o.bias, o.cout, o.relu, o.out);
+                       (const int64_t*)w.meta, in, o.wc, n_rows, o.bias, o.cout, o.relu, o.out);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2466,9 +2549,9 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
     if (need > done) {
       int64_t blocks = (need - done + per_block - 1) / per_block;
       if (blocks > 8LL * num_cus) blocks = 8LL * num_cus;
-      hipLaunchKernelGGL(v->sums, dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
+      hipLaunchKernelGGL(v->sums[wide], dim3((unsigned)blocks), dim3(256), 0, s, a.trees, a.prefix,
                          (const int32_t*)w.stl, (const int64_t*)w.meta,
-                         (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, in, in_bytes, w.bsum,
+                         (const int64_t*)w.pre[kSlotScan], a.n_trees, w.cap, in, n_rows, w.bsum,
                          (const int64_t*)w.pre[1], (const int64_t*)w.pre[2], done, need,
                          (const uint32_t*)w.smask);
       e = hipGetLastError();
@@ -2588,10 +2671,9 @@ bool conv_runs_fused(const ConvArgs& a, int impl) {
   if (impl != 2) return false;
   const MfmaVariant* v = find_variant(a.cin, a.cout);
   if (v == nullptr && conv_blocks(a.cin, a.cout).v == nullptr) return false;
-  // The MFMA kernels gather input rows with 16-byte buffer loads at 32-bit
-  // offsets below kOutside.
-  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)(v ? a.cin : 32) * 4u;
-  return (reinterpret_cast<uintptr_t>(a.in) & 15) == 0 && in_bytes64 < kOutside;
+  // The MFMA kernels gather input rows by a 32-bit row index (every
+  // n_leaves < 2^31 the convolution accepts) with 16-byte loads.
+  return (reinterpret_cast<uintptr_t>(a.in) & 15) == 0 && a.n_leaves < (int64_t)kNoRow;
 }
 
 hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_t s) {
@@ -2599,11 +2681,10 @@ hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_
   // Where the MFMA kernels cannot gather the input, the generic kernel (or,
   // for channel blocks, the GEMM path) runs.
   const MfmaVariant* v = find_variant(a.cin, a.cout);
-  const uint64_t in_bytes64 = (uint64_t)a.n_leaves * (uint64_t)(v ? a.cin : 32) * 4u;
   if (impl == 2 && !conv_runs_fused(a, impl)) impl = v ? 1 : 3;
   // Cell sums come from the fused kernels' epilogues only.
   if (a.sum_cells && impl != 2) return hipErrorInvalidValue;
-  const uint32_t in_bytes = (uint32_t)(in_bytes64 < kOutside ? in_bytes64 : 0);
+  const uint32_t n_rows = (uint32_t)a.n_leaves;
   const int tm = generic_tile(a.cin);
   const size_t gsmem = generic_smem(a.cin, tm);
   const int64_t all_tiles = (a.n_leaves + tm - 1) / tm;
@@ -2629,7 +2710,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_
   const int num_cus = L.num_cus;
   if (v != nullptr) {
     const FusedOut o{w.wm, w.wc, w.w8, a.bias, a.cout, a.relu | (a.sum_cells ? 2 : 0), a.out};
-    return fused_pass(a, w, v, a.in, in_bytes, o, 1, L, s);
+    return fused_pass(a, w, v, a.in, n_rows, o, 1, L, s);
   }
   // Channel blocks: per input block j (copied to a dense [n_leaves][32]
   // array unless it is the whole input), the boundary sums once, the K
@@ -2649,7 +2730,7 @@ hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_
     const size_t b = (size_t)j * bl.K;
     const FusedOut o{w.wm + b * bl.v->wfloats, w.wc + b * bl.v->cell_wfloats, w.w8 + b * bl.v->wfloats,
                      nullptr, bl.cb, a.sum_cells ? 2 : 0, w.part};
-    e = fused_pass(a, w, bl.v, xin, in_bytes, o, bl.K, L, s);
+    e = fused_pass(a, w, bl.v, xin, n_rows, o, bl.K, L, s);
     if (e != hipSuccess) return e;
     int64_t rb = (n * a.cout + 255) / 256;
     if (rb > 8LL * num_cus * 8) rb = 8LL * num_cus * 8;
