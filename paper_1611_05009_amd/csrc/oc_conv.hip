@@ -1183,8 +1183,13 @@ __device__ __forceinline__ void contract_row_perm(const float (&S)[9][CIN / 4], 
 // those 16 lanes read 4 rows, 64 contiguous bytes each.
 // The shell rows come from the parent depth-1 node's 6^3 table (e2key: node
 // << 3 | octant, one per cell of the list).
+#ifndef OC_CELL2_THREADS
+#define OC_CELL2_THREADS 512
+#endif
+constexpr int kMfmaThreads = OC_CELL2_THREADS;
+
 template <int CIN, int NT, class GP>
-__global__ void __launch_bounds__(512) k_conv_cell2_mfma(
+__global__ void __launch_bounds__(kMfmaThreads) k_conv_cell2_mfma(
     int64_t n_leaves, const int32_t* __restrict__ brow, const int32_t* __restrict__ e2key,
     const int32_t* __restrict__ ntab, int64_t ncap, const int64_t* __restrict__ meta,
     const float* __restrict__ in, const float* __restrict__ wm, uint32_t n_rows,
@@ -1349,11 +1354,50 @@ struct BoundaryVoxels<64, K> {
   __device__ __forceinline__ static void add(float (&)[kSets], const float (&)[56]) {}
 };
 
-// CIN lanes per split tree (lane = channel).  Each depth-1 child is summed
-// from its 56 boundary voxels, each read from the leaf that holds it (an
-// unsplit child reads its one row 56 times, from cache), all 56 loads in
-// flight before the sums; a tree set is the sum of the same set over the
-// children on that side.
+// The boundary sets of a tree that its depth-1 child o1 touches (26-bit mask
+// over the set index): along each axis a set with e_a = -1 holds the children
+// with coordinate bit 0, e_a = +1 those with bit 1, e_a = 0 all of them.
+template <int A, int E>
+__host__ __device__ constexpr uint32_t sets_with_dir() {
+  uint32_t m = 0;
+  for (int r = 0; r < 27; ++r) {
+    const int e = A == 0 ? r / 9 - 1 : (A == 1 ? (r / 3) % 3 - 1 : r % 3 - 1);
+    if (r != 13 && e == E) m |= 1u << (r - (r > 13));
+  }
+  return m;
+}
+
+__device__ __forceinline__ uint32_t child_sides(int o1) {
+  const uint32_t miss_d = (o1 & 4) ? sets_with_dir<0, -1>() : sets_with_dir<0, 1>();
+  const uint32_t miss_h = (o1 & 2) ? sets_with_dir<1, -1>() : sets_with_dir<1, 1>();
+  const uint32_t miss_w = (o1 & 1) ? sets_with_dir<2, -1>() : sets_with_dir<2, 1>();
+  return ((1u << kSets) - 1u) & ~(miss_d | miss_h | miss_w);
+}
+
+// Voxels of an unsplit depth-1 child (4^3) in a tree set that it touches:
+// 4 per axis along which the set spans the tree, 1 across it.
+__host__ __device__ constexpr float child_set_voxels(int s) {
+  const int r = s + (s >= 13);
+  return (float)((r / 9 == 1 ? 4 : 1) * ((r / 3) % 3 == 1 ? 4 : 1) * (r % 3 == 1 ? 4 : 1));
+}
+
+// Position of the k-th set bit of m (k < popcount(m)).
+__device__ __forceinline__ int nth_bit(uint32_t m, int k) {
+  for (int i = 0; i < k; ++i) m &= m - 1u;
+  return __ffs(m) - 1;
+}
+
+// Split trees per wave of the boundary sums.
+constexpr int sum_trees_per_wave(int cin) { return 64 / cin > 8 ? 64 / cin / 8 : 1; }
+
+// One split tree per wave (two per wave for CIN = 4), split into lane
+// groups of CIN lanes (lane = channel).  The groups take the tree's split
+// depth-1 children in turn: each is summed from its 56 boundary voxels, each
+// read from the leaf that holds it, all 56 loads in flight before the sums.
+// An unsplit child is one leaf, so its share of a tree set is its row times
+// its voxels in the set.  A tree set is the sum of the same set over the
+// children on that side: each group sums its children, then the groups of
+// the tree add theirs (a fixed butterfly, so the result is deterministic).
 template <int CIN, class GP>
 __global__ void __launch_bounds__(256) k_boundary_sums(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix,
@@ -1361,8 +1405,11 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
     const int64_t* __restrict__ sbase, int64_t n_trees, int64_t cap, const float* __restrict__ in,
     uint32_t n_rows, float* __restrict__ bsum, const int64_t* __restrict__ p8t,
     const int64_t* __restrict__ p8n, int64_t t0, int64_t t1, const uint32_t* __restrict__ smask) {
-  constexpr int TPW = 64 / CIN;
-  const int lane = threadIdx.x & 63, c = lane % CIN, sub = lane / CIN;
+  constexpr int NG = 64 / CIN;              // lane groups per wave
+  constexpr int TPW = sum_trees_per_wave(CIN);
+  constexpr int GPT = NG / TPW;             // lane groups per tree
+  const int lane = threadIdx.x & 63, c = lane % CIN, grp = lane / CIN;
+  const int sub = grp / GPT, gi = grp % GPT;
   int64_t n_split = n_trees - meta[0] - meta[1];
   n_split = n_split < 0 ? 0 : (n_split > n_trees ? n_trees : n_split);
   // The split trees among trees [t0, t1): list entries [j0, j1).
@@ -1376,13 +1423,13 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
     const Bits b = load_bits(trees, t);
     const int rbase = (int)prefix[t];
     const int64_t s0 = sbase[t];
+    const uint32_t m1 = (uint32_t)(b.lo >> 1) & 0xFFu;  // split depth-1 children
+    const int p1 = __popc(m1);
     float ts[kSets];
 #pragma unroll
     for (int s = 0; s < kSets; ++s) ts[s] = 0.f;
-#pragma unroll
-    for (int o1 = 0; o1 < 8; ++o1) {
-      const bool split1 = bit(b, 1 + o1);
-      const int r1 = rbase + data_idx(b, 1 + o1);
+    for (int k = gi; k < p1; k += GPT) {
+      const int o1 = nth_bit(m1, k);
       int r2[8];
       int sp = 0;
 #pragma unroll
@@ -1390,7 +1437,7 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
         const int n2 = 9 + 8 * o1 + o2;
         const int s2 = bit(b, n2);
         sp |= s2 << o2;
-        r2[o2] = split1 ? rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2) : r1;
+        r2[o2] = rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2);
       }
       float xv[56];
       BoundaryVoxels<0, 0>::load<CIN, GP>(xv, r2, sp, rin, c);
@@ -1399,25 +1446,33 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
 #pragma unroll
       for (int s = 0; s < kSets; ++s) cs[s] = 0.f;
       BoundaryVoxels<0, 0>::add(cs, xv);
-      if (split1) {
-        const int64_t slot = s0 + 1 + __popc((uint32_t)(b.lo >> 1) & ((1u << o1) - 1u));
-        if (slot < cap) {
-          const uint32_t mk = smask[slot];  // only the sets some cell reads
-          float* dst = bsum + slot * (kSets * CIN) + c;
+      const int64_t slot = s0 + 1 + k;
+      if (slot < cap) {
+        const uint32_t mk = smask[slot];  // only the sets some cell reads
+        float* dst = bsum + slot * (kSets * CIN) + c;
 #pragma unroll
-          for (int s = 0; s < kSets; ++s)
-            if ((mk >> s) & 1u) dst[s * CIN] = cs[s];
-        }
+        for (int s = 0; s < kSets; ++s)
+          if ((mk >> s) & 1u) dst[s * CIN] = cs[s];
       }
+      const uint32_t side = child_sides(o1);
 #pragma unroll
-      for (int r = 0; r < 27; ++r) {
-        if (r == 13) continue;
-        if (in_set(r / 9 - 1, (o1 >> 2) & 1, 2) && in_set((r / 3) % 3 - 1, (o1 >> 1) & 1, 2) &&
-            in_set(r % 3 - 1, o1 & 1, 2))
-          ts[r - (r > 13)] += cs[r - (r > 13)];
-      }
+      for (int s = 0; s < kSets; ++s)
+        if ((side >> s) & 1u) ts[s] += cs[s];
     }
-    if (s0 < cap) {
+    const uint32_t u1 = ~m1 & 0xFFu;  // unsplit depth-1 children (leaves)
+    for (int k = gi; k < 8 - p1; k += GPT) {
+      const int o1 = nth_bit(u1, k);
+      const float x = gather_at<1>(rin, GP::addr(rbase + data_idx(b, 1 + o1)), 4u * c);
+      const uint32_t side = child_sides(o1);
+#pragma unroll
+      for (int s = 0; s < kSets; ++s)
+        if ((side >> s) & 1u) ts[s] = fmaf(child_set_voxels(s), x, ts[s]);
+    }
+#pragma unroll
+    for (int off = CIN; off < CIN * GPT; off <<= 1)
+#pragma unroll
+      for (int s = 0; s < kSets; ++s) ts[s] += __shfl_xor(ts[s], off, 64);
+    if (gi == 0 && s0 < cap) {
       const uint32_t mk = smask[s0];
       float* dst = bsum + s0 * (kSets * CIN) + c;
 #pragma unroll
@@ -2286,7 +2341,6 @@ __global__ void k_block_accum(const float* __restrict__ part, int K, int cb, int
   }
 }
 
-constexpr int kMfmaThreads = 512;
 
 // Chunks of trees for the boundary sums and the cells that read them (one:
 // more chunks keep the sums in cache for their readers, but each chunk's
@@ -2541,7 +2595,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   // plane (every neighbour of its cells), then the chunk's cells, so that the
   // sums they read were written moments before and are still cached.
   const int64_t plane = (int64_t)a.gh * a.gw + a.gw + 1;
-  const int64_t per_block = 4 * (64 / v->cin);  // trees per pass of a 256-thread block
+  const int64_t per_block = 4 * sum_trees_per_wave(v->cin);  // trees per pass of a 256-thread block
   int64_t done = 0;
   for (int c = 0; c < kSumChunks; ++c) {
     const int64_t t0 = a.n_trees * c / kSumChunks, t1 = a.n_trees * (c + 1) / kSumChunks;
