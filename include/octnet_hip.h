@@ -230,10 +230,39 @@ int oc_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int g
  * n_leaves leaves.  *bytes [host].  The size is a bound that holds for every
  * canonical structure of that size and covers every implementation; on the
  * fused MFMA path it is dominated by the per-call boundary sums of split
- * nodes, 26*cin*4*(n_leaves - n_trees)/7 bytes, in channel blocks by the
- * partial outputs of one input block, n_leaves*cout*4 bytes, and on the GEMM path by
- * one chunk of window sums (about 256 MB). */
+ * nodes, whose slots it bounds by (n_leaves - n_trees)/7 (every split node
+ * adds 7 leaves) at 26*cin*4 + 868 bytes each, in channel blocks by the
+ * partial outputs of one input block, n_leaves*cout*4 bytes, and on the GEMM
+ * path by one chunk of window sums (about 256 MB). */
 int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t* bytes);
+
+/* Bytes of workspace for oc_conv3x3x3 on this structure: as
+ * oc_conv3x3x3_workspace with the boundary-sum slots the structure has (its
+ * split trees plus split depth-1 nodes, Sec. 3.1, at least 1) in place of
+ * the bound.  The slots are counted on the device: scratch is 256 bytes of
+ * device memory (its contents are overwritten), the count runs on stream,
+ * and the call synchronizes with it.  *bytes [host].  A workspace of this
+ * size serves this structure (and any other with no more slots); the
+ * convolution calls take their slot capacity from ws_bytes, so a workspace
+ * below the structure's exact size gives wrong results, not an error (one
+ * below the one-slot size gives OC_EWORKSPACE). */
+int oc_conv3x3x3_workspace_exact(const uint32_t* trees, int n, int gd, int gh, int gw, int64_t n_leaves,
+                                 int cin, int cout, size_t* bytes, void* scratch, void* stream);
+
+/* Bytes of workspace for oc_conv3x3x3 on a structure of this size with
+ * `slots` boundary-sum slots (split trees plus split depth-1 nodes; values
+ * below 1 count as 1, values above the bound as the bound): what
+ * oc_conv3x3x3_workspace_exact returns for a structure with that count.
+ * Host only.  *bytes [host]. */
+int oc_conv3x3x3_workspace_slots(int64_t n_trees, int64_t n_leaves, int cin, int cout, int64_t slots,
+                                 size_t* bytes);
+
+/* The boundary-sum slots a workspace of ws_bytes holds for a structure of
+ * this size: the convolution calls work with this capacity (the bound at
+ * most; 0 where the layer has no fused kernels).  *slots [host]; a
+ * workspace below the one-slot size gives OC_EWORKSPACE.  Host only. */
+int oc_conv3x3x3_workspace_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t ws_bytes,
+                                    int64_t* slots);
 
 /*
  * Grid-octree 3x3x3 convolution, Eq. 8 with average pooling: for every leaf,
@@ -245,7 +274,8 @@ int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout,
  *           multiplies input voxel (i-l+1, j-m+1, k-n+1) for output (i,j,k).
  *   bias:   float [cout] or NULL.
  *   out:    float [n_leaves][cout].
- * Requires n_leaves < 2^31.  ws: at least oc_conv3x3x3_workspace bytes.
+ * Requires n_leaves < 2^31.  ws: at least oc_conv3x3x3_workspace bytes, or
+ * the oc_conv3x3x3_workspace_exact bytes of this structure.
  */
 int oc_conv3x3x3(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh, int gw,
                  int64_t n_leaves, const float* in, int cin, const float* weight,

@@ -251,6 +251,46 @@ int oc_conv3x3x3_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout,
   return OC_OK;
 }
 
+int oc_conv3x3x3_workspace_exact(const uint32_t* trees, int n, int gd, int gh, int gw, int64_t n_leaves,
+                                 int cin, int cout, size_t* bytes, void* scratch, void* stream) {
+  g_last_error.clear();
+  if (!trees || !bytes || !scratch) return fail(OC_EINVAL, "oc_conv3x3x3_workspace_exact: null pointer");
+  if (!dims_ok(n, gd, gh, gw) || n_leaves <= 0 || cin <= 0 || cout <= 0)
+    return fail(OC_EINVAL, "oc_conv3x3x3_workspace_exact: non-positive size");
+  const int64_t nt = n_trees_of(n, gd, gh, gw);
+  hipStream_t s = as_stream(stream);
+  unsigned long long* count = static_cast<unsigned long long*>(scratch);
+  OC_CHECK_HIP(oci::launch_count_slots(trees, nt, count, s), "oc_conv3x3x3_workspace_exact");
+  unsigned long long slots = 0;
+  OC_CHECK_HIP(hipMemcpyAsync(&slots, count, sizeof(slots), hipMemcpyDeviceToHost, s),
+               "oc_conv3x3x3_workspace_exact");
+  OC_CHECK_HIP(hipStreamSynchronize(s), "oc_conv3x3x3_workspace_exact");
+  *bytes = oci::conv_workspace_slots(nt, n_leaves, cin, cout, (int64_t)slots);
+  return OC_OK;
+}
+
+int oc_conv3x3x3_workspace_slots(int64_t n_trees, int64_t n_leaves, int cin, int cout, int64_t slots,
+                                 size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(OC_EINVAL, "oc_conv3x3x3_workspace_slots: null pointer");
+  if (n_trees <= 0 || n_leaves <= 0 || cin <= 0 || cout <= 0)
+    return fail(OC_EINVAL, "oc_conv3x3x3_workspace_slots: non-positive size");
+  *bytes = oci::conv_workspace_slots(n_trees, n_leaves, cin, cout, slots);
+  return OC_OK;
+}
+
+int oc_conv3x3x3_workspace_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t ws_bytes,
+                                    int64_t* slots) {
+  g_last_error.clear();
+  if (!slots) return fail(OC_EINVAL, "oc_conv3x3x3_workspace_capacity: null pointer");
+  if (n_trees <= 0 || n_leaves <= 0 || cin <= 0 || cout <= 0)
+    return fail(OC_EINVAL, "oc_conv3x3x3_workspace_capacity: non-positive size");
+  const int64_t cap = oci::conv_slot_capacity(n_trees, n_leaves, cin, cout, ws_bytes);
+  if (cap < 0) return fail(OC_EWORKSPACE, "oc_conv3x3x3_workspace_capacity: below the one-slot size");
+  *slots = cap;
+  return OC_OK;
+}
+
 int oc_conv3x3x3_mfma_supported(int cin, int cout) { return oci::conv_mfma_supported(cin, cout) ? 1 : 0; }
 
 namespace {
@@ -267,9 +307,12 @@ int conv_args(const char* who, const uint32_t* trees, const int64_t* prefix, int
   if (n_leaves >= (1LL << 31)) return fail(OC_EOVERFLOW, "%s: n_leaves >= 2^31", who);
   const int64_t nt = n_trees_of(n, gd, gh, gw);
   if (n_leaves > 512 * nt) return fail(OC_EINVAL, "%s: n_leaves > 512 * n_trees", who);
-  const size_t need = oci::conv_workspace(nt, n_leaves, cin, cout);
-  if (ws_bytes < need) return fail(OC_EWORKSPACE, "%s: workspace %zu < %zu", who, ws_bytes, need);
+  const int64_t cap = oci::conv_slot_capacity(nt, n_leaves, cin, cout, ws_bytes);
+  if (cap < 0)
+    return fail(OC_EWORKSPACE, "%s: workspace %zu < %zu", who, ws_bytes,
+                oci::conv_workspace_slots(nt, n_leaves, cin, cout, 1));
   *a = oci::ConvArgs();
+  a->slot_cap = cap;
   a->trees = trees; a->prefix = prefix;
   a->n = n; a->gd = gd; a->gh = gh; a->gw = gw;
   a->n_trees = nt; a->n_leaves = n_leaves;

@@ -2410,17 +2410,23 @@ size_t smem_limit() {
 //   brow       i32 [n_leaves]
 //   stl        i32 [n_trees]                split trees
 //   meta       i64 [kKinds + 1]
-//   bsum       f32 [cap][26][cin]           boundary sums (if a variant exists)
 //   nbt        i32 [(n_leaves / 8 + 1) 64]  unit-group neighbourhood rows (if a variant exists)
-//   ntab       i32 [ncap][216]              6^3 rows around each split depth-1 node (if a variant exists)
 //   e2key      i32 [n_leaves]               edge-2 cells: node << 3 | octant (if a variant exists)
 //   codes      i32 [26][ccap]               region codes of edge-4/8 cells (if a variant exists)
 //   bkey       i64 [ccap]                   tree << 10 | bit of the edge-8/4 cells (if a variant exists)
+//   sgemm, wblk, xblk, part                 GEMM window sums, channel blocks
+// and last, the parts sized by the slot capacity cap (if a variant exists):
+//   bsum       f32 [cap][26][cin]           boundary sums
+//   ntab       i32 [cap][216]               6^3 rows around each split depth-1 node
 //   smask      u32 [cap]                    boundary sets read per slot
-// A slot belongs to a split node of depth 0 or 1 and every split node adds 7
-// leaves, so cap = (n_leaves - n_trees) / 7 slots hold every canonical
-// structure of that size (and ncap = cap node tables); a tree holds at most 8 cells of edge 4 or 8, so
-// ccap = min(8 n_trees, n_leaves).
+// A slot belongs to a split tree or a split depth-1 node (a node table to
+// the latter).  Every split node adds 7 leaves, so (n_leaves - n_trees) / 7
+// slots hold every canonical structure of that size: the bound the size-only
+// workspace query assumes.  A structure needs only its own count (split
+// trees plus split depth-1 nodes, at least 1), which the exact query counts
+// on the device; the capacity a call works with is what its workspace holds
+// past the fixed parts (at most the bound).  A tree holds at most 8 cells of
+// edge 4 or 8, so ccap = min(8 n_trees, n_leaves).
 constexpr int kScans = 3 + kKinds;  // groups, the kinds, slots, split depth-1 nodes
 constexpr int kSlotScan = 1 + kKinds;
 constexpr int kNodeScan = 2 + kKinds;
@@ -2455,7 +2461,18 @@ struct ConvWs {
   size_t total;
 };
 
-ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
+// Slot bound of a structure size (see the layout above).
+int64_t slot_bound(int64_t n_trees, int64_t n_leaves) {
+  return n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1;
+}
+
+// Bytes per slot of the slot-sized parts (each part's alignment aside).
+size_t slot_bytes(int kcin) {
+  return sizeof(float) * kSets * (size_t)kcin + sizeof(int32_t) * kNodeEntries + sizeof(uint32_t);
+}
+
+// slot_cap < 0: the bound.
+ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout, int64_t slot_cap = -1) {
   using oci::align256;
   char* p = static_cast<char*>(base);
   size_t off = 0;
@@ -2485,28 +2502,66 @@ ConvWs carve(void* base, int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   w.brow = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_leaves));
   w.stl = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)n_trees));
   w.meta = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (1 + kKinds)));
-  // At least one slot where a variant exists: the cell kernels may read slot
-  // 0 (and discard it) when no cell of a wave needs boundary sums.
-  w.cap = v ? (n_leaves > n_trees + 7 ? (n_leaves - n_trees) / 7 : 1) : 0;
-  w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)kcin * (size_t)w.cap));
   // Also without a variant: the GEMM path gathers unit voxels' window sums
   // through it.
   w.nbt = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * 64 * (size_t)(n_leaves / 8 + 1)));
-  w.ncap = v ? w.cap : 0;
-  w.ntab = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kNodeEntries * (size_t)w.ncap));
   w.e2cap = v ? n_leaves : 0;
   w.e2key = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * (size_t)w.e2cap));
   w.ccap = v ? (8 * n_trees < n_leaves ? 8 * n_trees : n_leaves) : 0;
   w.codes = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kSets * (size_t)w.ccap));
   w.bkey = reinterpret_cast<int64_t*>(take(sizeof(int64_t) * (size_t)w.ccap));
   w.sgemm = reinterpret_cast<float*>(take(oci::conv_gemm_buffer(n_leaves, cin)));
-  w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.wblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 27 * (size_t)cin * cout : 0));
   w.xblk = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * 32 * (size_t)n_leaves : 0));
   w.part = reinterpret_cast<float*>(take(bl.v ? sizeof(float) * (size_t)n_leaves * cout : 0));
+  // The slot-sized parts.  At least one slot where a variant exists: the
+  // cell kernels may read slot 0 (and discard it) when no cell of a wave
+  // needs boundary sums.
+  const int64_t bound = slot_bound(n_trees, n_leaves);
+  w.cap = v ? (slot_cap < 1 ? bound : (slot_cap < bound ? slot_cap : bound)) : 0;
+  w.bsum = reinterpret_cast<float*>(take(sizeof(float) * kSets * (size_t)kcin * (size_t)w.cap));
+  w.ncap = w.cap;
+  w.ntab = reinterpret_cast<int32_t*>(take(sizeof(int32_t) * kNodeEntries * (size_t)w.ncap));
+  w.smask = reinterpret_cast<uint32_t*>(take(sizeof(uint32_t) * (size_t)w.cap));
   w.total = off + 256;
   return w;
 }
+
+// The slot capacity a workspace of ws_bytes holds (the bound at most), 0
+// where no variant exists; -1 if it holds less than one slot.
+int64_t slot_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t ws_bytes) {
+  const ConvWs one = carve(nullptr, n_trees, n_leaves, cin, cout, 1);
+  if (one.cap == 0) return ws_bytes >= one.total ? 0 : -1;
+  if (ws_bytes < one.total) return -1;
+  const int kcin = find_variant(cin, cout) ? cin : 32;
+  // Each added slot adds slot_bytes over the three parts, whose alignment
+  // padding may shrink by up to 3 x 255 bytes: start from that upper
+  // estimate and step down to the largest capacity that fits.
+  const size_t spare = ws_bytes - one.total;
+  int64_t cap = 1 + (int64_t)((spare + 3 * 255) / slot_bytes(kcin));
+  const int64_t bound = slot_bound(n_trees, n_leaves);
+  if (cap > bound) cap = bound;
+  while (cap > 1 && carve(nullptr, n_trees, n_leaves, cin, cout, cap).total > ws_bytes) --cap;
+  return cap;
+}
+
+// Split trees plus split depth-1 nodes, added into *count.
+__global__ void k_count_slots(const uint32_t* __restrict__ trees, int64_t n_trees,
+                              unsigned long long* __restrict__ count) {
+  __shared__ unsigned long long part[4];
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  unsigned long long k = 0;
+  if (t < n_trees) {
+    const uint32_t w0 = trees[4 * t];
+    if (w0 & 1u) k = 1 + __popc((w0 >> 1) & 0xFFu);
+  }
+  for (int o = 32; o > 0; o >>= 1) k += __shfl_xor(k, o, 64);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = k;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicAdd(count, part[0] + part[1] + part[2] + part[3]);
+}
+
+__global__ void k_zero_u64(unsigned long long* p) { *p = 0ull; }
 
 // Output side of one fused pass: weight layouts, bias, width, epilogue mode
 // and the [n_leaves][cout] destination.  relu: bit 0 applies max(0, .),
@@ -2630,6 +2685,22 @@ size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout) {
   return carve(nullptr, n_trees, n_leaves, cin, cout).total;
 }
 
+size_t conv_workspace_slots(int64_t n_trees, int64_t n_leaves, int cin, int cout, int64_t slots) {
+  return carve(nullptr, n_trees, n_leaves, cin, cout, slots < 1 ? 1 : slots).total;
+}
+
+int64_t conv_slot_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t ws_bytes) {
+  return slot_capacity(n_trees, n_leaves, cin, cout, ws_bytes);
+}
+
+hipError_t launch_count_slots(const uint32_t* trees, int64_t n_trees, unsigned long long* count,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, count);
+  hipLaunchKernelGGL(k_count_slots, dim3((unsigned)((n_trees + 255) / 256)), dim3(256), 0, s, trees, n_trees,
+                     count);
+  return hipGetLastError();
+}
+
 bool conv_mfma_supported(int cin, int cout) {
   const MfmaVariant* v = find_variant(cin, cout);
   if (!v) v = conv_blocks(cin, cout).v;
@@ -2652,7 +2723,7 @@ int conv_auto_impl(int64_t n_leaves, int cin, int cout) {
 }
 
 hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
-  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
+  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout, a.slot_cap);
   hipError_t e = hipSuccess;
   const int64_t nw = 27LL * a.cin * a.cout;
   hipLaunchKernelGGL(k_transpose_weights, dim3((unsigned)((nw + 255) / 256)), dim3(256), 0, s,
@@ -2731,7 +2802,7 @@ bool conv_runs_fused(const ConvArgs& a, int impl) {
 }
 
 hipError_t launch_conv_execute(const ConvArgs& a, void* ws, int impl, hipStream_t s) {
-  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout);
+  const ConvWs w = carve(ws, a.n_trees, a.n_leaves, a.cin, a.cout, a.slot_cap);
   // Where the MFMA kernels cannot gather the input, the generic kernel (or,
   // for channel blocks, the GEMM path) runs.
   const MfmaVariant* v = find_variant(a.cin, a.cout);

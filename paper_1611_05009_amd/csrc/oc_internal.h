@@ -93,8 +93,21 @@ struct ConvArgs {
   // Internal: the fused kernels write each cell's sum (|l| times Eq. 8's
   // mean) instead of its mean; only where conv_runs_fused holds.
   int sum_cells = 0;
+  // Boundary-sum slots the workspace holds (conv_slot_capacity); -1: the
+  // size-only bound.
+  int64_t slot_cap = -1;
 };
+// Workspace bound for every canonical structure of this size.
 size_t conv_workspace(int64_t n_trees, int64_t n_leaves, int cin, int cout);
+// Workspace for a structure with `slots` split trees plus split depth-1
+// nodes (at least 1).
+size_t conv_workspace_slots(int64_t n_trees, int64_t n_leaves, int cin, int cout, int64_t slots);
+// Slots a workspace of ws_bytes holds (at most the bound; 0 where the
+// layer has no fused variant); -1 below the one-slot size.
+int64_t conv_slot_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size_t ws_bytes);
+// *count = split trees plus split depth-1 nodes (asynchronous on s).
+hipError_t launch_count_slots(const uint32_t* trees, int64_t n_trees, unsigned long long* count,
+                              hipStream_t s);
 bool conv_mfma_supported(int cin, int cout);
 // The implementation OC_CONV_AUTO runs: 2 (fused MFMA kernels, in channel
 // blocks for wide layers on large structures) or 3 (window-sum GEMM).

@@ -46,6 +46,9 @@ SIGNATURES = {
     "oc_oc2ten": (_I, [_P, _P, _I, _I, _I, _I, _P, _I, _P, _P]),
     "oc_ten2oc": (_I, [_P, _P, _I, _I, _I, _I, _P, _I, _I, _P, _P]),
     "oc_conv3x3x3_workspace": (_I, [_L, _L, _I, _I, _P]),
+    "oc_conv3x3x3_workspace_exact": (_I, [_P, _I, _I, _I, _I, _L, _I, _I, _P, _P, _P]),
+    "oc_conv3x3x3_workspace_slots": (_I, [_L, _L, _I, _I, _L, _P]),
+    "oc_conv3x3x3_workspace_capacity": (_I, [_L, _L, _I, _I, ctypes.c_size_t, _P]),
     "oc_conv3x3x3": (_I, [_P, _P, _I, _I, _I, _I, _L, _P, _I, _P, _P, _I, _I, _P, _P, _S, _P]),
     "oc_conv3x3x3_ex": (_I, [_P, _P, _I, _I, _I, _I, _L, _P, _I, _P, _P, _I, _I, _P, _P, _S, _I, _P]),
     "oc_conv3x3x3_prepare": (_I, [_P, _P, _I, _I, _I, _I, _L, _P, _I, _I, _P, _S, _P]),
@@ -249,10 +252,19 @@ def ten2oc(g: Octree, dense: torch.Tensor, pool: str = "avg") -> torch.Tensor:
     return out
 
 
-def conv_workspace_bytes(g: Octree, cin: int, cout: int) -> int:
+def conv_workspace_bytes(g: Octree, cin: int, cout: int, exact: bool = True) -> int:
+    """Workspace of a convolution on g: sized for g's own boundary-sum slots
+    (counted on the device, one synchronization) or, exact=False, the bound
+    for every structure of g's size."""
     nb = ctypes.c_size_t(0)
-    _check(lib().oc_conv3x3x3_workspace(g.n_trees, g.n_leaves, cin, cout, ctypes.byref(nb)),
-           "oc_conv3x3x3_workspace")
+    if exact:
+        scratch = torch.empty(256, dtype=torch.uint8, device=g.trees.device)
+        _check(lib().oc_conv3x3x3_workspace_exact(_ptr(g.trees), *g.dims(), g.n_leaves, cin, cout,
+                                                  ctypes.byref(nb), _ptr(scratch), _stream()),
+               "oc_conv3x3x3_workspace_exact")
+    else:
+        _check(lib().oc_conv3x3x3_workspace(g.n_trees, g.n_leaves, cin, cout, ctypes.byref(nb)),
+               "oc_conv3x3x3_workspace")
     return nb.value
 
 

@@ -83,6 +83,50 @@ def test_null_pointers_and_bad_sizes_are_rejected_on_the_host(L):
     assert L.oc_relu(fake, -1, None) == -1
 
 
+def test_workspace_by_slot_count(L):
+    """The exact-size query adds the slot-sized parts (boundary sums, 6^3
+    node tables, set masks) per slot to the fixed parts; the size-only query
+    is the one for the bound (n_leaves - n_trees) / 7 slots."""
+    fake = ctypes.c_void_p(0x1000)
+    for nt, nl, cin, cout in [(8, 100, 32, 32), (4096, 300000, 16, 32), (64, 4000, 8, 16), (64, 4000, 1, 8),
+                              (512, 60000, 64, 64)]:
+        nb, one, two, big = (ctypes.c_size_t(0) for _ in range(4))
+        assert L.oc_conv3x3x3_workspace(nt, nl, cin, cout, ctypes.byref(nb)) == 0
+        bound = max(1, (nl - nt) // 7) if nl > nt + 7 else 1
+        assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, bound, ctypes.byref(big)) == 0
+        assert big.value == nb.value, (nt, nl, cin, cout)
+        assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, 10 * bound, ctypes.byref(big)) == 0
+        assert big.value == nb.value
+        assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, 0, ctypes.byref(one)) == 0
+        assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, 1, ctypes.byref(two)) == 0
+        assert one.value == two.value <= nb.value
+        fused = L.oc_conv3x3x3_mfma_supported(cin, cout) == 1 and (cin <= 32)
+        if fused and bound > 3000:
+            # 26 cin floats + a 216-entry table + a mask word per slot
+            assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, 3001, ctypes.byref(big)) == 0
+            per = (big.value - one.value) / 3000
+            assert abs(per - (26 * cin * 4 + 216 * 4 + 4)) < 1, per
+        # the capacity a workspace holds round-trips the size by slot count
+        cap = ctypes.c_int64(-7)
+        for k in sorted({1, 2, 3, 5, 17, 255, 256, 257, bound // 3, bound - 1, bound}):
+            if k < 1:
+                continue
+            assert L.oc_conv3x3x3_workspace_slots(nt, nl, cin, cout, k, ctypes.byref(big)) == 0
+            assert L.oc_conv3x3x3_workspace_capacity(nt, nl, cin, cout, big.value, ctypes.byref(cap)) == 0
+            want = min(k, bound) if fused or L.oc_conv3x3x3_mfma_supported(cin, cout) == 1 else 0
+            assert cap.value == want, (nt, nl, cin, cout, k, cap.value)
+            if want > 1:  # one byte less holds one slot less
+                assert L.oc_conv3x3x3_workspace_capacity(nt, nl, cin, cout, big.value - 1,
+                                                          ctypes.byref(cap)) == 0
+                assert cap.value == want - 1, (nt, nl, cin, cout, k, cap.value)
+        assert L.oc_conv3x3x3_workspace_capacity(nt, nl, cin, cout, one.value - 1, ctypes.byref(cap)) == -3
+        # below the one-slot size the convolution refuses the workspace
+        args = [fake, fake, 1, 2, 2, 2] if nt == 8 else None
+        if args:
+            assert L.oc_conv3x3x3(*args, nl, fake, cin, fake, None, cout, 0, fake, fake, one.value - 1,
+                                  None) == -3
+
+
 def test_mfma_support_query(L):
     # the query is pure host logic
     for cin, cout in [(1, 8), (32, 32), (16, 32), (70, 3)]:
