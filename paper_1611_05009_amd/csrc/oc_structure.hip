@@ -1,6 +1,8 @@
 // Structure kernels: octree build, leaf counts and prefix scan, leaf index,
 // voxel->row map, canonical-form check, and the structure side of 2x2x2
 // pooling / unpooling (OctNet Sec. 3.1, Eq. 1-3, Eq. 10, Eq. 12).
+#include <type_traits>
+
 #include "oc_internal.h"
 
 using namespace ocd;
@@ -12,63 +14,157 @@ constexpr int kScanItems = 16;
 constexpr int kScanChunk = kScanThreads * kScanItems;
 
 // ---------------------------------------------------------------------------
-// Build: one wave per tree.  Lane q = 8*o1 + o2 owns the 2x2x2 block of the
-// depth-2 node (o1, o2) (bit 9 + q).  Two ballots (any occupied / all
-// occupied per block) give every split decision of the tree.
+// Build.  A workgroup takes up to kBuildTrees consecutive trees along w (one
+// row of the same n, d, h): their 64 voxel rows of 8 bytes each are
+// contiguous per row (256 bytes for 32 trees), so the rows are read as whole
+// cache lines into LDS, 16 bytes per lane where the grid width is even.
+// The any-occupied / all-occupied flags of the 64 depth-2 blocks (2x2x2
+// voxels, node q = 8 o1 + o2 at bit 9 + q) of a tree then give every split
+// decision of the tree.
 // ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(256) k_build(const uint8_t* __restrict__ occ, int64_t n_trees,
-                                               int gd, int gh, int gw, int rule,
-                                               uint32_t* __restrict__ trees,
-                                               int32_t* __restrict__ counts) {
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= n_trees) return;  // whole wave exits together
-  const int q = lane_id();
-  const TreePos p = tree_pos(t, gd, gh, gw);
-  const int o1 = q >> 3, o2 = q & 7;
-  const int d0 = 4 * ((o1 >> 2) & 1) + 2 * ((o2 >> 2) & 1);
-  const int h0 = 4 * ((o1 >> 1) & 1) + 2 * ((o2 >> 1) & 1);
-  const int w0 = 4 * (o1 & 1) + 2 * (o2 & 1);
+constexpr int kBuildTrees = 32;
+#ifndef OC_BUILD_THREADS
+#define OC_BUILD_THREADS 256
+#endif
+#ifndef OC_BUILD_SEGS
+#define OC_BUILD_SEGS 1
+#endif
+constexpr int kBuildThreads = OC_BUILD_THREADS;
+constexpr int kBuildSegs = OC_BUILD_SEGS;       // segments of up to 32 trees per workgroup
+constexpr int kBuildStride = kBuildTrees + 1;  // uint2 per LDS row (padding against bank conflicts)
+
+// Segment seg of the grid: trees [tw0, tw0 + count) of line (n, tree d, tree h).
+struct BuildSeg {
+  int64_t line;
+  int tw0, count;
+};
+
+__device__ __forceinline__ BuildSeg build_seg(int64_t seg, int64_t n_lines, int gw) {
+  const int wblocks = (gw + kBuildTrees - 1) / kBuildTrees;
+  BuildSeg b;
+  b.line = seg / wblocks;
+  b.tw0 = kBuildTrees * (int)(seg % wblocks);
+  b.count = b.line < n_lines ? min(kBuildTrees, gw - b.tw0) : 0;
+  return b;
+}
+
+template <bool PAIRS>
+__global__ void __launch_bounds__(kBuildThreads) k_build(const uint8_t* __restrict__ occ, int64_t n_trees,
+                                                        int gd, int gh, int gw, int rule,
+                                                        uint32_t* __restrict__ trees,
+                                                        int32_t* __restrict__ counts) {
+  __shared__ uint2 rows[kBuildSegs][64 * kBuildStride];  // [seg][voxel row 8 d + h][tree] 8 voxels along w
+  const int64_t n_lines = n_trees / gw;
   const int64_t H = 8LL * gh, W = 8LL * gw, D = 8LL * gd;
-  const int64_t vd = 8LL * p.d + d0, vh = 8LL * p.h + h0, vw = 8LL * p.w + w0;
-  const uint8_t* base = occ + ((p.n * D + vd) * H + vh) * W + vw;
-  int any = 0, all = 1;
+  // Every segment's row pieces are loaded before any is stored.
+  constexpr int PER = PAIRS ? kBuildTrees / 2 : kBuildTrees;  // loads per voxel row
+  constexpr int NL = 64 * PER / kBuildThreads;
+  using V = typename std::conditional<PAIRS, uint4, uint2>::type;
+  V v[kBuildSegs][NL];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int sg = 0; sg < kBuildSegs; ++sg) {
+    const BuildSeg b = build_seg((int64_t)blockIdx.x * kBuildSegs + sg, n_lines, gw);
+    const int th = (int)(b.line % gh);
+    const int td = (int)((b.line / gh) % gd);
+    const int64_t n = b.line / ((int64_t)gh * gd);
+    const uint8_t* base = occ + ((n * D + 8LL * td) * H + 8LL * th) * W + 8LL * b.tw0;
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const uint16_t v = *reinterpret_cast<const uint16_t*>(base + (a * H + b) * W);
-      const int v0 = (v & 0xFF) != 0, v1 = (v >> 8) != 0;
-      any |= v0 | v1;
-      all &= v0 & v1;
-    }
-  const uint64_t A = __ballot(any);
-  const uint64_t L = __ballot(all);
-  const uint64_t split2_ok = rule == 0 ? (A & ~L) : A;
-  int split0 = rule == 0 ? (A != 0ull && L != ~0ull) : (A != 0ull);
-  uint32_t s1 = 0;
-  uint64_t s2 = 0;
-  if (split0) {
-#pragma unroll
-    for (int o = 0; o < 8; ++o) {
-      const uint32_t ga = (uint32_t)((A >> (8 * o)) & 0xFFull);
-      const uint32_t gl = (uint32_t)((L >> (8 * o)) & 0xFFull);
-      const int sp = rule == 0 ? (ga != 0u && gl != 0xFFu) : (ga != 0u);
-      if (sp) {
-        s1 |= 1u << o;
-        s2 |= split2_ok & (0xFFull << (8 * o));
-      }
+    for (int i = 0; i < NL; ++i) {
+      const int k = threadIdx.x + kBuildThreads * i;
+      const int r = k / PER, tl = (PAIRS ? 2 : 1) * (k % PER);  // r = 8 d + h
+      if constexpr (PAIRS) v[sg][i] = make_uint4(0u, 0u, 0u, 0u);
+      else v[sg][i] = make_uint2(0u, 0u);
+      // PAIRS: count is even (gw and kBuildTrees are)
+      if (tl < b.count) v[sg][i] = *reinterpret_cast<const V*>(base + ((r >> 3) * H + (r & 7)) * W + 8 * tl);
     }
   }
-  if (q == 0) {
-    const uint64_t lo = (uint64_t)split0 | ((uint64_t)s1 << 1) | (s2 << 9);
-    const uint32_t hi = (uint32_t)(s2 >> 55);
-    uint4 w;
-    w.x = (uint32_t)lo;
-    w.y = (uint32_t)(lo >> 32);
-    w.z = hi;
-    w.w = 0u;
-    reinterpret_cast<uint4*>(trees)[t] = w;
-    counts[t] = 1 + 7 * (split0 + __popc(s1) + __popcll(s2));
+#pragma unroll
+  for (int sg = 0; sg < kBuildSegs; ++sg)
+#pragma unroll
+    for (int i = 0; i < NL; ++i) {
+      const int k = threadIdx.x + kBuildThreads * i;
+      const int r = k / PER, tl = (PAIRS ? 2 : 1) * (k % PER);
+      if constexpr (PAIRS) {
+        rows[sg][r * kBuildStride + tl] = make_uint2(v[sg][i].x, v[sg][i].y);
+        rows[sg][r * kBuildStride + tl + 1] = make_uint2(v[sg][i].z, v[sg][i].w);
+      } else {
+        rows[sg][r * kBuildStride + tl] = v[sg][i];
+      }
+    }
+  __syncthreads();
+  // Then 16 lanes per tree, 4 trees per wave: lane (dp, hp) takes the voxel
+  // rows d = 2 dp + {0, 1}, h = 2 hp + {0, 1} of its tree, i.e. the four
+  // depth-2 blocks w = 2j + {0, 1} (j = 0..3) there, and finds for each
+  // whether any / all of its 8 voxels are occupied; OR over the tree's 16
+  // lanes gives the 64-bit any / all masks by depth-2 node q = 8 o1 + o2.
+  const int lane = lane_id();
+  const int grp = lane >> 4, dp = (lane >> 2) & 3, hp = lane & 3;
+  constexpr uint64_t kLow = 0x0101010101010101ull;
+  for (int sg = 0; sg < kBuildSegs; ++sg) {
+    const BuildSeg b = build_seg((int64_t)blockIdx.x * kBuildSegs + sg, n_lines, gw);
+    for (int tl0 = (threadIdx.x >> 6) * 4; tl0 < b.count; tl0 += kBuildThreads / 16) {
+      const int tl = tl0 + grp;
+      uint64_t any8 = 0, all8 = kLow;  // per voxel column: some / every row occupied
+      if (tl < b.count) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const uint2 r2 = rows[sg][((2 * dp + a) * 8 + 2 * hp + c) * kBuildStride + tl];
+            uint64_t t = (uint64_t)r2.x | ((uint64_t)r2.y << 32);
+            t |= (t >> 4) & 0x0F0F0F0F0F0F0F0Full;
+            t |= (t >> 2) & 0x3333333333333333ull;
+            t |= (t >> 1) & 0x5555555555555555ull;
+            t &= kLow;  // bit 8k: voxel k of the row is occupied
+            any8 |= t;
+            all8 &= t;
+          }
+      }
+      uint64_t A = 0, L = 0;
+#pragma unroll
+      for (int jb = 0; jb < 4; ++jb) {
+        const uint32_t an = (uint32_t)(any8 >> (16 * jb)) & 0x0101u;
+        const uint32_t al = (uint32_t)(all8 >> (16 * jb)) & 0x0101u;
+        const int o1 = 4 * (dp >> 1) + 2 * (hp >> 1) + (jb >> 1);
+        const int o2 = 4 * (dp & 1) + 2 * (hp & 1) + (jb & 1);
+        const int qb = 8 * o1 + o2;
+        A |= (uint64_t)(an != 0u) << qb;
+        L |= (uint64_t)(al == 0x0101u) << qb;
+      }
+#pragma unroll
+      for (int off = 1; off < 16; off <<= 1) {
+        A |= __shfl_xor(A, off, 64);
+        L |= __shfl_xor(L, off, 64);
+      }
+      const uint64_t split2_ok = rule == 0 ? (A & ~L) : A;
+      const int split0 = rule == 0 ? (A != 0ull && L != ~0ull) : (A != 0ull);
+      uint32_t s1 = 0;
+      uint64_t s2 = 0;
+      if (split0) {
+#pragma unroll
+        for (int o = 0; o < 8; ++o) {
+          const uint32_t ga = (uint32_t)((A >> (8 * o)) & 0xFFull);
+          const uint32_t gl = (uint32_t)((L >> (8 * o)) & 0xFFull);
+          const int sp = rule == 0 ? (ga != 0u && gl != 0xFFu) : (ga != 0u);
+          if (sp) {
+            s1 |= 1u << o;
+            s2 |= split2_ok & (0xFFull << (8 * o));
+          }
+        }
+      }
+      if ((lane & 15) == 0 && tl < b.count) {
+        const int64_t t = b.line * gw + b.tw0 + tl;
+        const uint64_t lo = (uint64_t)split0 | ((uint64_t)s1 << 1) | (s2 << 9);
+        const uint32_t hi = (uint32_t)(s2 >> 55);
+        uint4 w;
+        w.x = (uint32_t)lo;
+        w.y = (uint32_t)(lo >> 32);
+        w.z = hi;
+        w.w = 0u;
+        reinterpret_cast<uint4*>(trees)[t] = w;
+        counts[t] = 1 + 7 * (split0 + __popc(s1) + __popcll(s2));
+      }
+    }
   }
 }
 
@@ -410,8 +506,16 @@ int32_t* scan_counts_buffer(void* ws) { return static_cast<int32_t*>(ws); }
 hipError_t launch_build(const uint8_t* occ, int n, int gd, int gh, int gw, int rule,
                         uint32_t* trees, int32_t* counts, hipStream_t s) {
   const int64_t nt = (int64_t)n * gd * gh * gw;
-  hipLaunchKernelGGL(k_build, dim3(blocks_for(nt, 4)), dim3(256), 0, s, occ, nt, gd, gh, gw, rule,
-                     trees, counts);
+  const int64_t segs = (nt / gw) * ((gw + kBuildTrees - 1) / kBuildTrees);
+  const int64_t blocks = (segs + kBuildSegs - 1) / kBuildSegs;
+  // 16-byte loads need an even grid width (rows of 8 gw bytes on 16-byte
+  // boundaries; the input itself is 16-byte aligned).
+  if (gw % 2 == 0 && (reinterpret_cast<uintptr_t>(occ) & 15) == 0)
+    hipLaunchKernelGGL(k_build<true>, dim3((unsigned)blocks), dim3(kBuildThreads), 0, s, occ, nt, gd, gh, gw,
+                       rule, trees, counts);
+  else
+    hipLaunchKernelGGL(k_build<false>, dim3((unsigned)blocks), dim3(kBuildThreads), 0, s, occ, nt, gd, gh, gw,
+                       rule, trees, counts);
   return hipGetLastError();
 }
 

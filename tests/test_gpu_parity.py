@@ -75,6 +75,17 @@ def test_build_index_rowmap_bitexact(case, rule):
     assert np.array_equal(host(g2.prefix), ref.prefix)
 
 
+@pytest.mark.parametrize("case", [(6, 1, 1, 1, 37), (7, 2, 1, 2, 70), (8, 1, 2, 1, 64)])
+def test_build_wide_grids(case):
+    """Grid widths past one build workgroup's 32 trees: odd (8-byte row
+    pieces), even with a partial last workgroup, and whole workgroups."""
+    occ = small_occ(*case)
+    for rule in ("mixed", "any"):
+        ref = O.build(occ, rule)
+        g = oc.build(dev(occ), rule)
+        check_structure(g, ref)
+
+
 @pytest.mark.parametrize("fill", ["empty", "full", "checker"])
 def test_build_degenerate_grids(fill):
     occ = np.zeros((2, 16, 8, 24), dtype=np.uint8)
