@@ -1639,6 +1639,9 @@ __device__ __forceinline__ int32_t nb_voxel_row(const NbTree* __restrict__ nt, i
 }
 
 constexpr int kTreeWaves = 4;
+#ifndef OC_TREE_TABLE_BLOCKS
+#define OC_TREE_TABLE_BLOCKS 16
+#endif
 
 __global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
@@ -2775,8 +2778,15 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                        w.cap);
   // Neighbourhood tables of the unit-voxel groups and the split depth-1 nodes.
   {
-    // Up to a wave per split tree (their count is on the device).
+    // Up to a wave per split tree (their count is on the device), at most
+    // OC_TREE_TABLE_BLOCKS workgroups per CU (the waves then take several
+    // trees each instead of most of them exiting at once).
     int64_t blocks = (a.n_trees + kTreeWaves - 1) / kTreeWaves;
+    DevLimits L;
+    e = device_limits(&L);
+    if (e != hipSuccess) return e;
+    const int64_t most = (int64_t)OC_TREE_TABLE_BLOCKS * L.num_cus;
+    if (OC_TREE_TABLE_BLOCKS > 0 && blocks > most) blocks = most;
     if (blocks > (1LL << 30)) blocks = 1LL << 30;
     hipLaunchKernelGGL(k_tree_tables, dim3((unsigned)blocks), dim3(64 * kTreeWaves), 0, s, a.trees, a.prefix,
                        a.gd, a.gh, a.gw, a.n_trees, a.n_leaves, (const int32_t*)w.stl, (const int64_t*)w.meta,
