@@ -1503,11 +1503,12 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
                                const int32_t* __restrict__ brow, const int64_t* __restrict__ meta,
                                const int64_t* __restrict__ sbase, int64_t cap, int64_t ccap,
                                int32_t* __restrict__ codes, uint32_t* __restrict__ smask) {
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t n8 = meta[0] + meta[1], nbig = n8 + meta[2];
   if (nbig > ccap) nbig = ccap;
   if (nbig > n_leaves) nbig = n_leaves;
-  if (j >= nbig) return;
+  // Grid-stride over the cells (their count is on the device).
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < nbig;
+       j += (int64_t)gridDim.x * blockDim.x) {
   const int sz = j < n8 ? 8 : 4;
   int row = brow[j];
   if (row >= n_leaves) row = -1;  // only a non-canonical structure gets here
@@ -1572,6 +1573,7 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
       else code = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
     }
     codes[(int64_t)(r - (r > 13)) * ccap + j] = code;
+  }
   }
 }
 
@@ -2776,15 +2778,15 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
   if (w.cap > 0)
     hipLaunchKernelGGL(k_zero_u32, dim3((unsigned)((w.cap + 255) / 256)), dim3(256), 0, s, w.smask,
                        w.cap);
+  DevLimits L;
+  e = device_limits(&L);
+  if (e != hipSuccess) return e;
   // Neighbourhood tables of the unit-voxel groups and the split depth-1 nodes.
   {
     // Up to a wave per split tree (their count is on the device), at most
     // OC_TREE_TABLE_BLOCKS workgroups per CU (the waves then take several
     // trees each instead of most of them exiting at once).
     int64_t blocks = (a.n_trees + kTreeWaves - 1) / kTreeWaves;
-    DevLimits L;
-    e = device_limits(&L);
-    if (e != hipSuccess) return e;
     const int64_t most = (int64_t)OC_TREE_TABLE_BLOCKS * L.num_cus;
     if (OC_TREE_TABLE_BLOCKS > 0 && blocks > most) blocks = most;
     if (blocks > (1LL << 30)) blocks = 1LL << 30;
@@ -2793,12 +2795,16 @@ hipError_t launch_conv_prepare(const ConvArgs& a, void* ws, hipStream_t s) {
                        (const int64_t*)w.pre[0], (const int64_t*)w.pre[kNodeScan], w.nbt, a.n_leaves / 8,
                        w.ntab, w.ncap);
   }
-  if (w.ccap > 0)
-    hipLaunchKernelGGL(k_region_codes, dim3((unsigned)((w.ccap + 255) / 256), w.ccap < 65536 ? kSets : 1),
+  if (w.ccap > 0) {
+    int64_t rblocks = (w.ccap + 255) / 256;
+    if (OC_TREE_TABLE_BLOCKS > 0 && rblocks > (int64_t)OC_TREE_TABLE_BLOCKS * L.num_cus)
+      rblocks = (int64_t)OC_TREE_TABLE_BLOCKS * L.num_cus;
+    hipLaunchKernelGGL(k_region_codes, dim3((unsigned)rblocks, w.ccap < 65536 ? kSets : 1),
                        dim3(256), 0, s,
                        a.trees, a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const int64_t*)w.bkey,
                        (const int32_t*)w.brow, (const int64_t*)w.meta,
                        (const int64_t*)w.pre[kSlotScan], w.cap, w.ccap, w.codes, w.smask);
+  }
   return hipGetLastError();
 }
 
