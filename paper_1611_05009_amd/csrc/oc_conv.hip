@@ -2550,15 +2550,16 @@ int64_t slot_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout, size
   return cap;
 }
 
-// Split trees plus split depth-1 nodes, added into *count.
+// Split trees plus split depth-1 nodes, added into *count (grid-stride, one
+// atomic per workgroup).
 __global__ void k_count_slots(const uint32_t* __restrict__ trees, int64_t n_trees,
                               unsigned long long* __restrict__ count) {
   __shared__ unsigned long long part[4];
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   unsigned long long k = 0;
-  if (t < n_trees) {
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n_trees;
+       t += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t w0 = trees[4 * t];
-    if (w0 & 1u) k = 1 + __popc((w0 >> 1) & 0xFFu);
+    if (w0 & 1u) k += 1 + __popc((w0 >> 1) & 0xFFu);
   }
   for (int o = 32; o > 0; o >>= 1) k += __shfl_xor(k, o, 64);
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = k;
@@ -2701,8 +2702,9 @@ int64_t conv_slot_capacity(int64_t n_trees, int64_t n_leaves, int cin, int cout,
 hipError_t launch_count_slots(const uint32_t* trees, int64_t n_trees, unsigned long long* count,
                               hipStream_t s) {
   hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, count);
-  hipLaunchKernelGGL(k_count_slots, dim3((unsigned)((n_trees + 255) / 256)), dim3(256), 0, s, trees, n_trees,
-                     count);
+  int64_t blocks = (n_trees + 255) / 256;
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_count_slots, dim3((unsigned)blocks), dim3(256), 0, s, trees, n_trees, count);
   return hipGetLastError();
 }
 
