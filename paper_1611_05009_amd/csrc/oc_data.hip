@@ -31,46 +31,94 @@ __global__ void k_oc2ten(const uint32_t* __restrict__ trees, const int64_t* __re
   for (int k = 0; k < c; ++k) dst[k] = src[k];
 }
 
-// Eq. 5: one wave per tree, one lane per leaf; sums in double.
+// Eq. 5: one wave per tree.  Lane l = 8 h + w takes the voxel column (h, w)
+// of the tree and reads its 8 voxels along d, c channels each: 8 lanes read
+// 8 consecutive voxels of a grid row, so a load instruction covers 8 rows
+// (16-byte loads where c % 4 == 0).  The cell values at every level come
+// from that one read: the 2^3 blocks by adding d pairs in the lane, then
+// lanes w ^ 1 and h ^ 1; the 4^3 blocks from pairs of those, lanes w ^ 2
+// and h ^ 2; the tree from lanes w ^ 4 and h ^ 4 -- sums in double for the
+// average, maxima for max pooling, in a fixed order.  The leaf holding each
+// voxel comes from the split bits; the lane holding the leaf's first voxel
+// writes its row (Eq. 3 gives the row).
+template <bool VEC4>
 __global__ void __launch_bounds__(256) k_ten2oc(const uint32_t* __restrict__ trees,
                                                 const int64_t* __restrict__ prefix, int64_t n_trees,
                                                 int gd, int gh, int gw,
                                                 const float* __restrict__ dense, int c, int pool,
                                                 float* __restrict__ data) {
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= n_trees) return;
+  if (t >= n_trees) return;  // whole wave exits together
   const Bits b = load_bits(trees, t);
   const TreePos p = tree_pos(t, gd, gh, gw);
   const int64_t W = 8LL * gw, H = 8LL * gh, D = 8LL * gd;
   const int64_t row0 = prefix[t];
-  int base = 0;
-  // No split depth-2 node: no leaf past position 72.
-  const int nend = (((b.lo >> 9) != 0ull) || b.hi) ? kNodes : 73;
-  for (int c0 = 0; c0 < nend; c0 += 64) {
-    const int i = c0 + lane_id();
-    const bool leaf = i < kNodes && is_leaf(b, i);
-    const uint64_t m = __ballot(leaf);
-    if (leaf) {
-      const int64_t row = row0 + base + __popcll(m & lanemask_lt());
-      const Cell cl = cell_of(i);
-      const int64_t vd0 = 8LL * p.d + cl.d, vh0 = 8LL * p.h + cl.h, vw0 = 8LL * p.w + cl.w;
-      for (int k = 0; k < c; ++k) {
-        double acc = 0.0;
-        float mx = -INFINITY;
-        for (int a = 0; a < cl.size; ++a)
-          for (int bb = 0; bb < cl.size; ++bb) {
-            const float* src = dense + (((p.n * D + vd0 + a) * H + vh0 + bb) * W + vw0) * c + k;
-            for (int e = 0; e < cl.size; ++e) {
-              const float x = src[(int64_t)e * c];
-              acc += (double)x;
-              mx = fmaxf(mx, x);
-            }
-          }
-        data[row * c + k] =
-            pool == 0 ? (float)(acc / (double)(cl.size * cl.size * cl.size)) : mx;
+  const int lane = lane_id(), lh = lane >> 3, lw = lane & 7;
+  const float* src = dense + (((p.n * D + 8LL * p.d) * H + 8LL * p.h + lh) * W + 8LL * p.w + lw) * c;
+  const int64_t dstep = H * W * c;  // floats from one d plane to the next
+  // The leaf of each voxel of the column.
+  int leaf[8], dep[8];
+#pragma unroll
+  for (int d = 0; d < 8; ++d) {
+    const int i = leaf_at(b, d, lh, lw);
+    leaf[d] = i;
+    dep[d] = i == 0 ? 0 : (i < 9 ? 1 : (i < 73 ? 2 : 3));
+  }
+  const bool avg = pool == 0;
+  for (int k0 = 0; k0 < c; k0 += 4) {
+    const int kc = min(4, c - k0);
+    // v[d][e]: channel k0 + e of voxel d (0 past c).
+    double v[8][4];
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      if constexpr (VEC4) {
+        const float4 x = *reinterpret_cast<const float4*>(src + d * dstep + k0);
+        v[d][0] = x.x; v[d][1] = x.y; v[d][2] = x.z; v[d][3] = x.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[d][e] = e < kc ? (double)src[d * dstep + k0 + e] : 0.0;
       }
     }
-    base += __popcll(m);
+    auto comb = [&](double a, double x) { return avg ? a + x : fmax(a, x); };
+    // 2^3 blocks: d pairs, then lanes w ^ 1, h ^ 1 (every lane of the block
+    // ends up with the block's value); then 4^3 and 8^3 alike.
+    double s2[4][4], s4[2][4], s8[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        double x = comb(v[2 * q][e], v[2 * q + 1][e]);
+        x = comb(x, __shfl_xor(x, 1, 64));
+        x = comb(x, __shfl_xor(x, 8, 64));
+        s2[q][e] = x;
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        double x = comb(s2[2 * q][e], s2[2 * q + 1][e]);
+        x = comb(x, __shfl_xor(x, 2, 64));
+        x = comb(x, __shfl_xor(x, 16, 64));
+        s4[q][e] = x;
+      }
+      double x = comb(s4[0][e], s4[1][e]);
+      x = comb(x, __shfl_xor(x, 4, 64));
+      x = comb(x, __shfl_xor(x, 32, 64));
+      s8[e] = x;
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const int dp = dep[d];
+      // Cell edge 8 >> depth; this lane writes if the voxel is the cell's first.
+      const int msk = (8 >> dp) - 1;
+      if ((d & msk) || (lh & msk) || (lw & msk)) continue;
+      const int64_t row = row0 + data_idx(b, leaf[d]);
+      const double scale = avg ? 1.0 / (double)((8 >> dp) * (8 >> dp) * (8 >> dp)) : 1.0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e >= kc) continue;
+        const double x = dp == 3 ? v[d][e] : (dp == 2 ? s2[d >> 1][e] : (dp == 1 ? s4[d >> 2][e] : s8[e]));
+        data[row * c + k0 + e] = (float)(avg ? x * scale : x);
+      }
+    }
   }
 }
 
@@ -582,8 +630,12 @@ hipError_t launch_oc2ten(const uint32_t* trees, const int64_t* prefix, int n, in
 hipError_t launch_ten2oc(const uint32_t* trees, const int64_t* prefix, int n, int gd, int gh,
                          int gw, const float* dense, int c, int pool, float* data, hipStream_t s) {
   const int64_t nt = (int64_t)n * gd * gh * gw;
-  hipLaunchKernelGGL(k_ten2oc, dim3(blocks_for(nt, 4)), dim3(256), 0, s, trees, prefix, nt, gd, gh,
-                     gw, dense, c, pool, data);
+  if (c % 4 == 0 && (reinterpret_cast<uintptr_t>(dense) & 15) == 0)
+    hipLaunchKernelGGL(k_ten2oc<true>, dim3(blocks_for(nt, 4)), dim3(256), 0, s, trees, prefix, nt, gd, gh,
+                       gw, dense, c, pool, data);
+  else
+    hipLaunchKernelGGL(k_ten2oc<false>, dim3(blocks_for(nt, 4)), dim3(256), 0, s, trees, prefix, nt, gd, gh,
+                       gw, dense, c, pool, data);
   return hipGetLastError();
 }
 

@@ -148,6 +148,20 @@ def test_oc2ten_ten2oc(case):
     assert np.array_equal(host(oc.ten2oc(g, dev(x), "max")), O.ten2oc(ref, x, "max").astype(np.float32))
 
 
+@pytest.mark.parametrize("c", [1, 4, 8, 6])
+def test_ten2oc_channel_widths(c):
+    """ten2oc over 4-channel chunks: whole 16-byte chunks (c = 4, 8), a
+    partial last chunk (6) and one channel; both split rules' structures."""
+    rng = np.random.default_rng(100 + c)
+    occ = synth.random_occupancy(rng, 2, 2, 3, 2)
+    for rule in ("mixed", "any"):
+        ref = O.build(occ, rule)
+        g = oc.build(dev(occ), rule)
+        x = rng.standard_normal(ref.dense_shape + (c,)).astype(np.float32)
+        assert_close(host(oc.ten2oc(g, dev(x), "avg")), O.ten2oc(ref, x, "avg"), "ten2oc avg c=%d" % c)
+        assert np.array_equal(host(oc.ten2oc(g, dev(x), "max")), O.ten2oc(ref, x, "max").astype(np.float32))
+
+
 # ----------------------------------------------------------------------------
 # Convolution
 # ----------------------------------------------------------------------------
