@@ -25,6 +25,20 @@
 #ifndef OC_UNIT_PREFETCH
 #define OC_UNIT_PREFETCH 2
 #endif
+// Deltas of gathers in flight where a lane's row piece is small (at most
+// OC_UNIT_SMALL_CH floats per lane per delta, so more deltas fit in
+// registers): the narrow layers are bound by the gathers, not by the
+// matrix unit.
+#ifndef OC_UNIT_PREFETCH_SMALL
+#define OC_UNIT_PREFETCH_SMALL 8
+#endif
+#ifndef OC_UNIT_SMALL_CH
+#define OC_UNIT_SMALL_CH 2
+#endif
+template <int CIN, int MS>
+constexpr int unit_prefetch() {
+  return CIN / (MS == 32 ? 2 : 4) <= OC_UNIT_SMALL_CH ? OC_UNIT_PREFETCH_SMALL : OC_UNIT_PREFETCH;
+}
 using namespace ocd;
 
 namespace {
@@ -794,7 +808,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_unit_mfma(
   // tile's last ones (PD + 1 divides 27, so the buffer ring lines up).  The
   // scheduling barriers keep the compiler from sinking the loads back to
   // their use.
-  constexpr int PD = OC_UNIT_PREFETCH;  // deltas of gathers in flight
+  constexpr int PD = unit_prefetch<CIN, MS>();  // deltas of gathers in flight
   static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
   Vec abuf[PD + 1][C::NV];
   const uint32_t coff = 4u * C::VEC * g;  // the lane's first channel, in bytes
@@ -2054,7 +2068,7 @@ __global__ void __launch_bounds__(kUnitThreads) k_conv_cell8t_gemm(
       }
     }
   };
-  constexpr int PD = OC_UNIT_PREFETCH;
+  constexpr int PD = unit_prefetch<CIN, MS>();
   static_assert(27 % (PD + 1) == 0, "the gather ring must line up across tiles");
   Vec abuf[PD + 1][C::NV];
   const uint32_t coff = 4u * C::VEC * g;  // the lane's first channel, in bytes
