@@ -1189,6 +1189,54 @@ __device__ __forceinline__ void contract_row_perm(const float (&S)[9][CIN / 4], 
   }
 }
 
+// Row steps of the edge-2 window sums, D deep: step K (layer JD = K / 4,
+// h-row UH = K % 4) adds its rows, issues the gathers of step K + D, and
+// contracts delta-row UH - 1 of the layer once its rows are in; the last
+// row of a layer is followed by the next layer's own-voxel terms.
+#ifndef OC_CELL2_DEPTH_SMALL
+#define OC_CELL2_DEPTH_SMALL 6
+#endif
+template <int CIN>
+constexpr int cell2_depth() {
+  return CIN / 4 <= 2 ? OC_CELL2_DEPTH_SMALL : 2;
+}
+
+template <int K, int D, int CIN, int NT, class G>
+struct Cell2Steps {
+  __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], float (&X)[D][8][CIN / 4],
+                                             const uint32_t* offm, const G& rin, uint32_t choff,
+                                             const float (&xs)[CIN / 4], const float* wl, int lane,
+                                             int perm, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+    if constexpr (K < 12) {
+      constexpr int JD = K / 4, UH = K % 4;
+      __builtin_amdgcn_sched_barrier(0);
+      shell2_row_add<JD, UH, CIN>(S, X[K % D]);
+      if constexpr (K + D < 12) {
+        Shell2RowLoad<(K + D) / 4, (K + D) % 4, 0, CIN>::run(X[(K + D) % D], offm, rin, choff);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if constexpr (UH >= 1) contract_row_perm<CIN, NT, JD, UH - 1>(S, wl, lane, perm, acc);
+      if constexpr (UH == 3 && JD < 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        init_layer<2, JD + 1>(S, xs);
+      }
+      Cell2Steps<K + 1, D, CIN, NT, G>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
+    }
+  }
+};
+
+template <int K, int D, int CIN, class G>
+struct Cell2Prologue {
+  __device__ __forceinline__ static void run(float (&X)[D][8][CIN / 4], const uint32_t* offm, const G& rin,
+                                             uint32_t choff) {
+    if constexpr (K < D) {
+      Shell2RowLoad<K / 4, K % 4, 0, CIN>::run(X[K], offm, rin, choff);
+      __builtin_amdgcn_sched_barrier(0);
+      Cell2Prologue<K + 1, D, CIN, G>::run(X, offm, rin, choff);
+    }
+  }
+};
+
 // Edge-2 cells.  The window sums are built in a gather layout and moved to
 // the MFMA layout before each contraction: in the MFMA layout lane
 // m + 16 g holds channel chunk g of cell m, so the 16 lanes that the memory
@@ -1264,39 +1312,15 @@ __global__ void __launch_bounds__(kMfmaThreads) k_conv_cell2_mfma(
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) acc[nt][r] = 0.f;
-    // The 12 row steps (layer JD, h-row UH) run two deep: the gathers of
-    // step k + 2 are issued once step k's rows are added.
+    // The 12 row steps (layer JD, h-row UH) run D deep: the gathers of step
+    // k + D are issued once step k's rows are added (D = 2, or 6 where a
+    // lane's row piece is at most 2 floats).
+    constexpr int D = cell2_depth<CIN>();
     float S[9][CH];
-    float X[2][8][CH];
-#define OC_LOAD(JD, UH, B) \
-  Shell2RowLoad<JD, UH, 0, CIN>::run(X[B], offm, rin, choff); \
-  __builtin_amdgcn_sched_barrier(0)
-#define OC_ADD(JD, UH, B) \
-  __builtin_amdgcn_sched_barrier(0); \
-  shell2_row_add<JD, UH, CIN>(S, X[B])
-#define OC_MMA(JD, JH) contract_row_perm<CIN, NT, JD, JH>(S, wl, lane, perm, acc)
-#define OC_INIT(JD) \
-  __builtin_amdgcn_sched_barrier(0); \
-  init_layer<2, JD>(S, xs)
+    float X[D][8][CH];
     init_layer<2, 0>(S, xs);
-    OC_LOAD(0, 0, 0); OC_LOAD(0, 1, 1);
-    OC_ADD(0, 0, 0); OC_LOAD(0, 2, 0);
-    OC_ADD(0, 1, 1); OC_LOAD(0, 3, 1);
-    OC_MMA(0, 0); OC_ADD(0, 2, 0); OC_LOAD(1, 0, 0);
-    OC_MMA(0, 1); OC_ADD(0, 3, 1); OC_LOAD(1, 1, 1);
-    OC_MMA(0, 2); OC_INIT(1); OC_ADD(1, 0, 0); OC_LOAD(1, 2, 0);
-    OC_ADD(1, 1, 1); OC_LOAD(1, 3, 1);
-    OC_MMA(1, 0); OC_ADD(1, 2, 0); OC_LOAD(2, 0, 0);
-    OC_MMA(1, 1); OC_ADD(1, 3, 1); OC_LOAD(2, 1, 1);
-    OC_MMA(1, 2); OC_INIT(2); OC_ADD(2, 0, 0); OC_LOAD(2, 2, 0);
-    OC_ADD(2, 1, 1); OC_LOAD(2, 3, 1);
-    OC_MMA(2, 0); OC_ADD(2, 2, 0);
-    OC_MMA(2, 1); OC_ADD(2, 3, 1);
-    OC_MMA(2, 2);
-#undef OC_LOAD
-#undef OC_ADD
-#undef OC_MMA
-#undef OC_INIT
+    Cell2Prologue<0, D, CIN, GP>::run(X, offm, rin, choff);
+    Cell2Steps<0, D, CIN, NT, GP>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
     __builtin_amdgcn_wave_barrier();  // offm is rewritten by the next tile
     // The row of cell m, for the store's MFMA layout.
     const int row_m = __builtin_amdgcn_ds_bpermute(perm, row);
