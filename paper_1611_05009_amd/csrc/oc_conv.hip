@@ -1902,6 +1902,224 @@ struct RegionLayer<27, JD, SZ, CIN, TRIV, PV, P> {
                                              int) {}
 };
 
+// Batched form of a layer's regions (the default): the regions' loads are
+// issued in groups and added once the whole group is in, instead of one
+// region at a time behind a branch on its code.
+//   - Rows: every region of the layer, the gather made whatever the code (a
+//     code that is not a row reads zeros), RG regions per group.
+//   - Boundary sums: regions that can be split (faces and edges), only when
+//     some lane of the wave has that region split (a wave-uniform branch);
+//     lanes whose region is a row read zeros.  Groups hold up to SB sets.
+// A lane's region is either a row or split, so each adds exactly what the
+// one-region form adds.
+#ifndef OC_CELLR_BATCH
+#define OC_CELLR_BATCH 1
+#endif
+#ifndef OC_CELLR_ROW_GROUP
+#define OC_CELLR_ROW_GROUP 17
+#endif
+#ifndef OC_CELLR_SET_GROUP
+#define OC_CELLR_SET_GROUP 18
+#endif
+
+struct RegionList {
+  int n;
+  int r[26];
+};
+
+constexpr int region_nz(int R) { return (R / 9 != 1) + ((R / 3) % 3 != 1) + (R % 3 != 1); }
+
+// The regions of layer JD (all of them, or those that can be split).
+constexpr RegionList layer_list(int JD, bool splittable) {
+  RegionList l{0, {}};
+  for (int R = 0; R < 27; ++R) {
+    const int nz = region_nz(R);
+    if (R == 13 || !(R / 9 - 1 == 0 || R / 9 - 1 == JD - 1)) continue;
+    if (splittable && nz == 3) continue;  // corners are always one leaf
+    l.r[l.n++] = R;
+  }
+  return l;
+}
+
+// Boundary sets that layer JD reads of split region R (as summary_add).
+constexpr int layer_sets(int R, int JD) {
+  const int d0 = R / 9 - 1, d1 = (R / 3) % 3 - 1, d2 = R % 3 - 1;
+  return (d0 != 0 ? 1 : (JD == 1 ? 1 : 2)) * (d1 != 0 ? 1 : 3) * (d2 != 0 ? 1 : 3);
+}
+
+// End of the set group (at most SB sets) that starts at list entry k0.
+constexpr int set_group_end(int JD, int k0, int SB) {
+  const RegionList l = layer_list(JD, true);
+  int k = k0, n = 0;
+  while (k < l.n && (k == k0 || n + layer_sets(l.r[k], JD) <= SB)) n += layer_sets(l.r[k++], JD);
+  return k;
+}
+constexpr int set_group_offset(int JD, int k0, int k) {
+  int n = 0;
+  for (int i = k0; i < k; ++i) n += layer_sets(layer_list(JD, true).r[i], JD);
+  return n;
+}
+
+// Loads of the sets of split region R that layer JD reads, in summary_add's
+// order, into y[O ..]; a = the slot's first set row (or no row), rs: the
+// boundary sums as rows of CIN floats.
+template <int R, int JD, int CIN, int PV, int P, int O, int NB, class G>
+__device__ __forceinline__ void summary_load(float (&y)[NB][PV * cell_vec<CIN>()], const G& rs, uint32_t a,
+                                             int choff) {
+  using K = CellCfg<CIN, 1>;
+  constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
+  int j = O;
+#pragma unroll
+  for (int ed = -1; ed <= 1; ++ed) {
+    if (dir0 != 0 ? ed != -dir0 : (ed != 0 && ed != 1 - JD)) continue;
+#pragma unroll
+    for (int eh = -1; eh <= 1; ++eh) {
+      if (dir1 != 0 && eh != -dir1) continue;
+#pragma unroll
+      for (int ew = -1; ew <= 1; ++ew) {
+        if (dir2 != 0 && ew != -dir2) continue;
+#pragma unroll
+        for (int i = 0; i < PV; ++i) {
+          const typename K::Vec q = gather_at<K::VEC>(
+              rs, a, 4u * (uint32_t)(bset(ed, eh, ew) * CIN + choff + K::VSTRIDE * (P * PV + i)));
+#pragma unroll
+          for (int e = 0; e < K::VEC; ++e) y[j][K::VEC * i + e] = vget<K::VEC>(q, e);
+        }
+        ++j;
+      }
+    }
+  }
+}
+
+// summary_add over sets already loaded (y[O ..], the order of summary_load).
+template <int R, int JD, int CIN, int PV, int O, int NB>
+__device__ __forceinline__ void summary_add_loaded(float (&S)[9][PV * cell_vec<CIN>()],
+                                                   const float (&y)[NB][PV * cell_vec<CIN>()]) {
+  constexpr int CH = PV * cell_vec<CIN>();
+  constexpr int dir0 = R / 9 - 1, dir1 = (R / 3) % 3 - 1, dir2 = R % 3 - 1;
+  int j = O;
+#pragma unroll
+  for (int ed = -1; ed <= 1; ++ed) {
+    if (dir0 != 0 ? ed != -dir0 : (ed != 0 && ed != 1 - JD)) continue;
+#pragma unroll
+    for (int eh = -1; eh <= 1; ++eh) {
+      if (dir1 != 0 && eh != -dir1) continue;
+#pragma unroll
+      for (int ew = -1; ew <= 1; ++ew) {
+        if (dir2 != 0 && ew != -dir2) continue;
+        const bool n0 = dir0 == 0 && ed != 0;
+#pragma unroll
+        for (int j1 = 0; j1 < 3; ++j1) {
+          if (dir1 != 0 ? j1 != dir1 + 1 : (eh != 0 && j1 != 1 - eh)) continue;
+          const bool n1 = n0 != (dir1 == 0 && eh != 0);
+#pragma unroll
+          for (int j2 = 0; j2 < 3; ++j2) {
+            if (dir2 != 0 ? j2 != dir2 + 1 : (ew != 0 && j2 != 1 - ew)) continue;
+            const bool neg = n1 != (dir2 == 0 && ew != 0);
+#pragma unroll
+            for (int e = 0; e < CH; ++e) S[j1 * 3 + j2][e] += neg ? -y[j][e] : y[j][e];
+          }
+        }
+        ++j;
+      }
+    }
+  }
+}
+
+// Row groups: list entries [K, K1) (at most RG) loaded, then added; then the
+// next group.
+template <int JD, int K, int SZ, int CIN, int PV, int P, int RG = OC_CELLR_ROW_GROUP>
+struct RowGroups {
+  static constexpr int W = PV * cell_vec<CIN>();
+  static constexpr int N = layer_list(JD, false).n;
+  template <int I, int K1, class G>
+  __device__ __forceinline__ static void load(float (&x)[RG][W], const int32_t (&c)[27],
+                                              const G& rin, int choff) {
+    if constexpr (I < K1) {
+      constexpr int R = layer_list(JD, false).r[I];
+      const int32_t code = c[R];
+      gather_pass<CIN, PV, P>(rin, G::addr(code >= 0 ? code : -1), 4u * choff, x[I - K]);
+      load<I + 1, K1>(x, c, rin, choff);
+    }
+  }
+  template <int I, int K1>
+  __device__ __forceinline__ static void add(float (&S)[9][W], const float (&x)[RG][W]) {
+    if constexpr (I < K1) {
+      constexpr int R = layer_list(JD, false).r[I];
+      region_add<R, JD, SZ, W>(S, x[I - K]);
+      add<I + 1, K1>(S, x);
+    }
+  }
+  template <class G>
+  __device__ __forceinline__ static void run(float (&S)[9][W], const int32_t (&c)[27], const G& rin, int choff) {
+    if constexpr (K < N) {
+      constexpr int K1 = K + RG < N ? K + RG : N;
+      float x[RG][W];
+      load<K, K1>(x, c, rin, choff);
+      __builtin_amdgcn_sched_barrier(0);
+      add<K, K1>(S, x);
+      __builtin_amdgcn_sched_barrier(0);
+      RowGroups<JD, K1, SZ, CIN, PV, P, RG>::run(S, c, rin, choff);
+    }
+  }
+};
+
+// Set groups of the splittable regions: list entries [K, K1) (at most SB
+// sets, or one region) whose region some lane has split, loaded, then
+// added; then the next group.
+template <int JD, int K, int CIN, int PV, int P, int SB = OC_CELLR_SET_GROUP>
+struct SetGroups {
+  static constexpr int W = PV * cell_vec<CIN>();
+  static constexpr int N = layer_list(JD, true).n;
+  static constexpr int NB = SB > 9 ? SB : 9;
+  template <int I, int K1, class G>
+  __device__ __forceinline__ static void load(float (&y)[NB][W], const int32_t (&c)[27], uint32_t need,
+                                              const G& rs, int choff) {
+    if constexpr (I < K1) {
+      constexpr int R = layer_list(JD, true).r[I];
+      if (need & (1u << (I - K))) {
+        const int32_t code = c[R];
+        summary_load<R, JD, CIN, PV, P, set_group_offset(JD, K, I), NB>(
+            y, rs, G::addr(code <= -2 ? kSets * (-2 - code) : -1), choff);
+      }
+      load<I + 1, K1>(y, c, need, rs, choff);
+    }
+  }
+  template <int I, int K1>
+  __device__ __forceinline__ static void add(float (&S)[9][W], const float (&y)[NB][W], uint32_t need) {
+    if constexpr (I < K1) {
+      constexpr int R = layer_list(JD, true).r[I];
+      if (need & (1u << (I - K))) summary_add_loaded<R, JD, CIN, PV, set_group_offset(JD, K, I), NB>(S, y);
+      add<I + 1, K1>(S, y, need);
+    }
+  }
+  template <int I, int K1>
+  __device__ __forceinline__ static uint32_t needed(const int32_t (&c)[27]) {
+    if constexpr (I < K1) {
+      constexpr int R = layer_list(JD, true).r[I];
+      const uint32_t any = __ballot(c[R] <= -2) != 0ull ? 1u : 0u;
+      return (any << (I - K)) | needed<I + 1, K1>(c);
+    } else {
+      return 0u;
+    }
+  }
+  template <class G>
+  __device__ __forceinline__ static void run(float (&S)[9][W], const int32_t (&c)[27], const G& rs, int choff) {
+    if constexpr (K < N) {
+      constexpr int K1 = set_group_end(JD, K, SB);
+      const uint32_t need = __builtin_amdgcn_readfirstlane(needed<K, K1>(c));
+      if (need != 0u) {
+        float y[NB][W];
+        load<K, K1>(y, c, need, rs, choff);
+        __builtin_amdgcn_sched_barrier(0);
+        add<K, K1>(S, y, need);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      SetGroups<JD, K1, CIN, PV, P, SB>::run(S, c, rs, choff);
+    }
+  }
+};
+
 // Contract pass P (vectors P PV .. + PV - 1) of layer JD into acc.
 template <int CIN, int NT, int JD, int PV, int P>
 __device__ __forceinline__ void contract_pass(const float (&S)[9][PV * cell_vec<CIN>()],
@@ -1932,7 +2150,7 @@ template <int CIN, int NT, int SZ, bool TRIV, int JD, int PV, int P>
 struct LayerPasses {
   template <class G>
   __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
-                                             bool live, const G& rin,
+                                             bool live, const G& rin, const G& rs,
                                              const float* bsum, int choff, const float* wl,
                                              int lane, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
     using K = CellCfg<CIN, NT>;
@@ -1943,10 +2161,16 @@ struct LayerPasses {
       for (int e = 0; e < W; ++e) xp[e] = xs[P * W + e];
       float S[9][W];
       init_layer<SZ, JD>(S, xp);
-      if (live) RegionLayer<0, JD, SZ, CIN, TRIV, PV, P>::run(S, c, rin, bsum, choff);
+      if constexpr (OC_CELLR_BATCH && !TRIV) {
+        // c holds -1 (outside: nothing) for lanes without a cell.
+        RowGroups<JD, 0, SZ, CIN, PV, P>::run(S, c, rin, choff);
+        SetGroups<JD, 0, CIN, PV, P>::run(S, c, rs, choff);
+      } else {
+        if (live) RegionLayer<0, JD, SZ, CIN, TRIV, PV, P>::run(S, c, rin, bsum, choff);
+      }
       contract_pass<CIN, NT, JD, PV, P>(S, wl, lane, acc);
       __builtin_amdgcn_sched_barrier(0);
-      LayerPasses<CIN, NT, SZ, TRIV, JD, PV, P + 1>::run(c, xs, live, rin, bsum, choff, wl, lane,
+      LayerPasses<CIN, NT, SZ, TRIV, JD, PV, P + 1>::run(c, xs, live, rin, rs, bsum, choff, wl, lane,
                                                         acc);
     }
   }
@@ -1956,7 +2180,7 @@ struct LayerPasses {
 #define OC_CELLR_THREADS 512
 #endif
 #ifndef OC_CELLR_PV
-#define OC_CELLR_PV 2
+#define OC_CELLR_PV 1
 #endif
 constexpr int kCellrThreads = OC_CELLR_THREADS;
 
@@ -1965,7 +2189,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
-    const float* __restrict__ bsum, int64_t ccap, const float* __restrict__ in,
+    const float* __restrict__ bsum, uint32_t n_sum_rows, int64_t ccap, const float* __restrict__ in,
     const float* __restrict__ wm, uint32_t n_rows, const float* __restrict__ bias, int cout,
     int relu, float* __restrict__ out, const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
   // Channel blocks: blockIdx.y selects an output block (its weight layout
@@ -1981,6 +2205,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
   const GP rin = GP::make(in, n_rows);
+  const GP rs = GP::make(bsum, n_sum_rows);  // the boundary sums, as rows of CIN floats
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
@@ -2011,14 +2236,16 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
 #pragma unroll
     for (int jd = 0; jd < 3; ++jd) {
       int32_t c[27];
+#pragma unroll
+      for (int r = 0; r < 27; ++r) c[r] = -1;
       if (row >= 0) {
         if (jd == 0) RegionLayer<0, 0, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
         if (jd == 1) RegionLayer<0, 1, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
         if (jd == 2) RegionLayer<0, 2, SZ, CIN, TRIV, 1, 0>::codes(c, col, ccap);
       }
-      if (jd == 0) LayerPasses<CIN, NT, SZ, TRIV, 0, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
-      if (jd == 1) LayerPasses<CIN, NT, SZ, TRIV, 1, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
-      if (jd == 2) LayerPasses<CIN, NT, SZ, TRIV, 2, PV, 0>::run(c, xs, row >= 0, rin, bsum, choff, wl, lane, acc);
+      if (jd == 0) LayerPasses<CIN, NT, SZ, TRIV, 0, PV, 0>::run(c, xs, row >= 0, rin, rs, bsum, choff, wl, lane, acc);
+      if (jd == 1) LayerPasses<CIN, NT, SZ, TRIV, 1, PV, 0>::run(c, xs, row >= 0, rin, rs, bsum, choff, wl, lane, acc);
+      if (jd == 2) LayerPasses<CIN, NT, SZ, TRIV, 2, PV, 0>::run(c, xs, row >= 0, rin, rs, bsum, choff, wl, lane, acc);
       __builtin_amdgcn_sched_barrier(0);  // keeps the next layer's loads out of this one
     }
     store_tile16<NT>(acc, row, (relu & 2) ? 1.f : 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu,
@@ -2231,8 +2458,8 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, const float*,
                        uint32_t, const float*, int, int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
-                       const int32_t*, const int64_t*, int, const int32_t*, const float*, int64_t,
-                       const float*, const float*, uint32_t, const float*, int, int, float*,
+                       const int32_t*, const int64_t*, int, const int32_t*, const float*, uint32_t,
+                       int64_t, const float*, const float*, uint32_t, const float*, int, int, float*,
                        const int64_t*, int64_t, int64_t);
 typedef void (*WeightFn)(const float*, int, float*);
 typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*, int64_t,
@@ -2636,8 +2863,12 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
                       uint32_t n_rows, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
   const int num_cus = L.num_cus;
   const size_t max_smem = L.max_smem;
-  // Raw buffer gathers below 4 GiB of input, 64-bit ones from there.
-  const int wide = (uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ? 1 : 0;
+  // Raw buffer gathers below 4 GiB of input and of boundary sums, 64-bit
+  // ones from there.
+  const uint64_t sum_rows = (uint64_t)(w.cap > 0 ? w.cap : 0) * kSets;
+  const int wide = ((uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ||
+                    sum_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside) ? 1 : 0;
+  const uint32_t n_sum_rows = wide ? 0u : (uint32_t)sum_rows;
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > max_smem) return hipErrorInvalidConfiguration;
@@ -2661,7 +2892,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
     hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(kCellrThreads), smem, s, a.trees,
                        a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
-                       (const float*)w.bsum, w.ccap, in, o.wc, n_rows, o.bias, o.cout, o.relu, o.out,
+                       (const float*)w.bsum, n_sum_rows, w.ccap, in, o.wc, n_rows, o.bias, o.cout, o.relu, o.out,
                        (const int64_t*)w.pre[1 + k], t0, t1);
     return hipGetLastError();
   };
