@@ -2144,6 +2144,45 @@ __device__ __forceinline__ void contract_pass(const float (&S)[9][PV * cell_vec<
   }
 }
 
+// As contract_pass, for window sums held in the gather layout: the A
+// operand of MFMA lane L comes from lane perm / 4.
+template <int CIN, int NT, int JD, int PV, int P>
+__device__ __forceinline__ void contract_pass_perm(const float (&S)[9][PV * cell_vec<CIN>()],
+                                                   const float* wl, int lane, int perm,
+                                                   typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
+  constexpr int W = PV * cell_vec<CIN>();
+  float T[9][W];
+#pragma unroll
+  for (int k = 0; k < 9; ++k)
+#pragma unroll
+    for (int e = 0; e < W; ++e)
+      T[k][e] = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(perm, __builtin_bit_cast(int, S[k][e])));
+  contract_pass<CIN, NT, JD, PV, P>(T, wl, lane, acc);
+}
+
+// Lane layout of the edge-4/8 kernels' window sums.  The MFMA layout (lane
+// m + 16 g: channel chunk g of cell m) has the 16 lanes that the memory
+// pipeline serves together read 16 rows; the gather layout (lane l: chunk
+// l % 4 of cell 4 (l / 16) + (l / 4) % 4) has them read 4 rows, 64
+// contiguous bytes each, and the sums move to the MFMA layout by
+// ds_bpermute before each contraction.
+#ifndef OC_CELLR_GATHER_LAYOUT
+#define OC_CELLR_GATHER_LAYOUT 1
+#endif
+// The cell and channel chunk of a lane, and the ds_bpermute address that
+// fetches the MFMA lane's operand.
+__device__ __forceinline__ int cellr_cell(int lane) {
+  return OC_CELLR_GATHER_LAYOUT ? 4 * (lane >> 4) + ((lane >> 2) & 3) : lane % 16;
+}
+__device__ __forceinline__ int cellr_chunk(int lane) { return OC_CELLR_GATHER_LAYOUT ? lane & 3 : lane / 16; }
+__device__ __forceinline__ int cellr_perm(int lane) {
+  return 4 * (16 * ((lane & 15) >> 2) + 4 * (lane & 3) + (lane >> 4));
+}
+// The lane that holds cell i (i < 16) in the kernels' layout.
+__device__ __forceinline__ int cellr_lane(int i) {
+  return OC_CELLR_GATHER_LAYOUT ? 16 * (i >> 2) + 4 * (i & 3) : i;
+}
+
 // One layer of the window sums, in NV / PV passes over the lane's channel
 // vectors (fewer registers per pass; the codes are loaded once per layer).
 template <int CIN, int NT, int SZ, bool TRIV, int JD, int PV, int P>
@@ -2168,7 +2207,10 @@ struct LayerPasses {
       } else {
         if (live) RegionLayer<0, JD, SZ, CIN, TRIV, PV, P>::run(S, c, rin, bsum, choff);
       }
-      contract_pass<CIN, NT, JD, PV, P>(S, wl, lane, acc);
+      if constexpr (OC_CELLR_GATHER_LAYOUT)
+        contract_pass_perm<CIN, NT, JD, PV, P>(S, wl, lane, cellr_perm(lane), acc);
+      else
+        contract_pass<CIN, NT, JD, PV, P>(S, wl, lane, acc);
       __builtin_amdgcn_sched_barrier(0);
       LayerPasses<CIN, NT, SZ, TRIV, JD, PV, P + 1>::run(c, xs, live, rin, rs, bsum, choff, wl, lane,
                                                         acc);
@@ -2217,7 +2259,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     lcnt = b - a;
   }
   const WaveTiles wt = wave_tiles((lcnt + 15) / 16);
-  const int m = lane % 16, g = lane / 16;
+  const int m = cellr_cell(lane), g = cellr_chunk(lane);
   const int choff = K::VEC * g;  // the lane's first channel
   float bvals[NT];
   bias16<NT>(bias, cout, lane, bvals);
@@ -2248,7 +2290,9 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
       if (jd == 2) LayerPasses<CIN, NT, SZ, TRIV, 2, PV, 0>::run(c, xs, row >= 0, rin, rs, bsum, choff, wl, lane, acc);
       __builtin_amdgcn_sched_barrier(0);  // keeps the next layer's loads out of this one
     }
-    store_tile16<NT>(acc, row, (relu & 2) ? 1.f : 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu,
+    // The row of cell m, for the store's MFMA layout.
+    const int row_m = OC_CELLR_GATHER_LAYOUT ? __builtin_amdgcn_ds_bpermute(cellr_perm(lane), row) : row;
+    store_tile16<NT>(acc, row_m, (relu & 2) ? 1.f : 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu,
                      out);
   }
 }
