@@ -1358,20 +1358,34 @@ constexpr bool interior4(int v) {
   return (v >> 4) % 3 != 0 && ((v >> 2) & 3) % 3 != 0 && (v & 3) % 3 != 0;
 }
 
+// The boundary sets (26-bit mask over the set index) that hold voxel V of a
+// 4^3 block.
+constexpr uint32_t voxel_sets(int V) {
+  uint32_t m = 0;
+  for (int r = 0; r < 27; ++r)
+    if (r != 13 && in_set(r / 9 - 1, V >> 4, 4) && in_set((r / 3) % 3 - 1, (V >> 2) & 3, 4) &&
+        in_set(r % 3 - 1, V & 3, 4))
+      m |= 1u << (r - (r > 13));
+  return m;
+}
+
 template <int V, int K>
 struct BoundaryVoxels {
   static constexpr int x0 = V >> 4, x1 = (V >> 2) & 3, x2 = V & 3;
   static constexpr bool skip = interior4(V);
   static constexpr int NK = skip ? K : K + 1;
+  // need: the sets that are read; a voxel in none of them reads zero (no
+  // memory traffic) and the sets it would change are not written.
   template <int CIN, class G>
   __device__ __forceinline__ static void load(float (&xv)[56], const int (&r2)[8], int sp, const G& rin,
-                                              int c) {
+                                              int c, uint32_t need) {
     if constexpr (!skip) {
       constexpr int o2 = 4 * (x0 >> 1) + 2 * (x1 >> 1) + (x2 >> 1);
       constexpr int u = 4 * (x0 & 1) + 2 * (x1 & 1) + (x2 & 1);
-      xv[K] = gather_at<1>(rin, G::addr(r2[o2] + (((sp >> o2) & 1) ? u : 0)), 4u * c);
+      const int row = (need & voxel_sets(V)) != 0u ? r2[o2] + (((sp >> o2) & 1) ? u : 0) : -1;
+      xv[K] = gather_at<1>(rin, G::addr(row), 4u * c);
     }
-    BoundaryVoxels<V + 1, NK>::template load<CIN, G>(xv, r2, sp, rin, c);
+    BoundaryVoxels<V + 1, NK>::template load<CIN, G>(xv, r2, sp, rin, c, need);
   }
   __device__ __forceinline__ static void add(float (&cs)[kSets], const float (&xv)[56]) {
     if constexpr (!skip) {
@@ -1388,7 +1402,7 @@ struct BoundaryVoxels {
 template <int K>
 struct BoundaryVoxels<64, K> {
   template <int CIN, class G>
-  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int, const G&, int) {}
+  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int, const G&, int, uint32_t) {}
   __device__ __forceinline__ static void add(float (&)[kSets], const float (&)[56]) {}
 };
 
@@ -1477,16 +1491,19 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
         sp |= s2 << o2;
         r2[o2] = rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2);
       }
+      // The child's sets that are read: its own, and those of the tree's
+      // sets on its side.
+      const int64_t slot = s0 + 1 + k;
+      const uint32_t mk = slot < cap ? smask[slot] : 0u;
+      const uint32_t need = mk | (s0 < cap ? smask[s0] & child_sides(o1) : 0u);
       float xv[56];
-      BoundaryVoxels<0, 0>::load<CIN, GP>(xv, r2, sp, rin, c);
+      BoundaryVoxels<0, 0>::load<CIN, GP>(xv, r2, sp, rin, c, need);
       __builtin_amdgcn_sched_barrier(0);
       float cs[kSets];
 #pragma unroll
       for (int s = 0; s < kSets; ++s) cs[s] = 0.f;
       BoundaryVoxels<0, 0>::add(cs, xv);
-      const int64_t slot = s0 + 1 + k;
       if (slot < cap) {
-        const uint32_t mk = smask[slot];  // only the sets some cell reads
         float* dst = bsum + slot * (kSets * CIN) + c;
 #pragma unroll
         for (int s = 0; s < kSets; ++s)
@@ -2187,9 +2204,9 @@ __device__ __forceinline__ int cellr_lane(int i) {
 // vectors (fewer registers per pass; the codes are loaded once per layer).
 template <int CIN, int NT, int SZ, bool TRIV, int JD, int PV, int P>
 struct LayerPasses {
-  template <class G>
+  template <class G, class GS>
   __device__ __forceinline__ static void run(const int32_t (&c)[27], const float (&xs)[CIN / 4],
-                                             bool live, const G& rin, const G& rs,
+                                             bool live, const G& rin, const GS& rs,
                                              const float* bsum, int choff, const float* wl,
                                              int lane, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
     using K = CellCfg<CIN, NT>;
@@ -2226,7 +2243,8 @@ struct LayerPasses {
 #endif
 constexpr int kCellrThreads = OC_CELLR_THREADS;
 
-template <int CIN, int NT, int SZ, bool TRIV, class GP>
+// GP gathers the input rows, GS the boundary sums (as rows of CIN floats).
+template <int CIN, int NT, int SZ, bool TRIV, class GP, class GS = GP>
 __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
@@ -2247,7 +2265,7 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
   float* wl = smem;
   weights_to_lds<CIN, NT, 16>(wm, wl);
   const GP rin = GP::make(in, n_rows);
-  const GP rs = GP::make(bsum, n_sum_rows);  // the boundary sums, as rows of CIN floats
+  const GS rs = GS::make(bsum, n_sum_rows);  // the boundary sums, as rows of CIN floats
   const int lane = threadIdx.x & 63;
   int64_t lbeg, lcnt;
   kind_range(meta, kind, n_leaves, lbeg, lcnt);
@@ -2526,7 +2544,7 @@ struct MfmaVariant {
   // through RowsWide.
   MfmaFn kernel[2];
   Cell2Fn cell2[2];
-  CellFn cell4[2], cell8[2];
+  CellFn cell4[2][2], cell8[2][2];  // [input gathers][boundary-sum gathers]
   SumFn sums[2];
   Cell8Fn cell8g[2];    // edge-8 cells with unsplit face/edge neighbours
 };
@@ -2538,8 +2556,12 @@ void set_kernels(MfmaVariant& v) {
   using G = typename std::conditional<WIDE != 0, RowsWide<CIN>, RowsRaw<CIN>>::type;
   v.kernel[WIDE] = &k_conv_unit_mfma<CIN, NT, MS, G>;
   v.cell2[WIDE] = &k_conv_cell2_mfma<CIN, CNT, G>;
-  v.cell4[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 4, false, G>;
-  v.cell8[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 8, false, G>;
+  // Boundary sums of 4 GiB or more are gathered through RowsWide whatever
+  // the input's size (the bound-sized workspace of a large structure).
+  v.cell4[WIDE][1] = &k_conv_cellr_mfma<CIN, CNT, 4, false, G, RowsWide<CIN>>;
+  v.cell8[WIDE][1] = &k_conv_cellr_mfma<CIN, CNT, 8, false, G, RowsWide<CIN>>;
+  v.cell4[WIDE][0] = WIDE ? v.cell4[WIDE][1] : &k_conv_cellr_mfma<CIN, CNT, 4, false, G, RowsRaw<CIN>>;
+  v.cell8[WIDE][0] = WIDE ? v.cell8[WIDE][1] : &k_conv_cellr_mfma<CIN, CNT, 8, false, G, RowsRaw<CIN>>;
   v.sums[WIDE] = &k_boundary_sums<CIN, G>;
   v.cell8g[WIDE] = &k_conv_cell8t_gemm<CIN, NT, MS, G>;
 }
@@ -2907,12 +2929,12 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
                       uint32_t n_rows, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
   const int num_cus = L.num_cus;
   const size_t max_smem = L.max_smem;
-  // Raw buffer gathers below 4 GiB of input and of boundary sums, 64-bit
-  // ones from there.
+  // Raw buffer gathers below 4 GiB of input (and of boundary sums, for the
+  // kernels that read them), 64-bit ones from there.
+  const int wide = (uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ? 1 : 0;
   const uint64_t sum_rows = (uint64_t)(w.cap > 0 ? w.cap : 0) * kSets;
-  const int wide = ((uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ||
-                    sum_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside) ? 1 : 0;
-  const uint32_t n_sum_rows = wide ? 0u : (uint32_t)sum_rows;
+  const int wide_sums = (wide || sum_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside) ? 1 : 0;
+  const uint32_t n_sum_rows = wide_sums ? 0u : (uint32_t)sum_rows;
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > max_smem) return hipErrorInvalidConfiguration;
@@ -2929,7 +2951,7 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     const size_t smem = wsmem;
     if (smem > max_smem) return hipErrorInvalidConfiguration;
-    const CellFn f = k == 1 || k == 0 ? v->cell8[wide] : v->cell4[wide];
+    const CellFn f = k == 1 || k == 0 ? v->cell8[wide][wide_sums] : v->cell4[wide][wide_sums];
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (r != hipSuccess) return r;
