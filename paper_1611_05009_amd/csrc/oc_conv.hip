@@ -2167,14 +2167,29 @@ template <int CIN, int NT, int JD, int PV, int P>
 __device__ __forceinline__ void contract_pass_perm(const float (&S)[9][PV * cell_vec<CIN>()],
                                                    const float* wl, int lane, int perm,
                                                    typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
-  constexpr int W = PV * cell_vec<CIN>();
-  float T[9][W];
+  using K = CellCfg<CIN, NT>;
+  constexpr int W = PV * K::VEC;
 #pragma unroll
-  for (int k = 0; k < 9; ++k)
+  for (int k = 0; k < 9; ++k) {
+    // One window sum at a time, so that few moved values are live.
+    float T[W];
 #pragma unroll
     for (int e = 0; e < W; ++e)
-      T[k][e] = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(perm, __builtin_bit_cast(int, S[k][e])));
-  contract_pass<CIN, NT, JD, PV, P>(T, wl, lane, acc);
+      T[e] = __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute(perm, __builtin_bit_cast(int, S[k][e])));
+    const int dl = 9 * JD + k;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int i = 0; i < PV; ++i) {
+        const int jv = P * PV + i;
+        const typename K::Vec bv =
+            reinterpret_cast<const typename K::Vec*>(wl)[((dl * NT + nt) * K::NV + jv) * 64 + lane];
+#pragma unroll
+        for (int e = 0; e < K::VEC; ++e)
+          acc[nt] = mfma<16>(T[K::VEC * i + e], vget<K::VEC>(bv, e), acc[nt]);
+      }
+    if (k % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bounds the B loads in flight
+  }
 }
 
 // Lane layout of the edge-4/8 kernels' window sums.  The MFMA layout (lane
@@ -2587,7 +2602,11 @@ MfmaVariant make_variant(int cout_min) {
 }
 
 // cout in [cout_min, cout_max]; 32-wide tiles for cout 17..32, 16-wide ones
-// for cout 5..16 (narrower outputs use the generic kernel).
+// for cout 1..16 (a tile column past cout holds zero weights and is not
+// stored).
+#ifndef OC_NARROW_COUT_MIN
+#define OC_NARROW_COUT_MIN 1
+#endif
 const MfmaVariant* find_variant(int cin, int cout) {
   static const MfmaVariant table[] = {
 #ifdef OC_UNIT_MS16
@@ -2597,8 +2616,8 @@ const MfmaVariant* find_variant(int cin, int cout) {
       make_variant<32, 1, 32>(17), make_variant<16, 1, 32>(17), make_variant<8, 1, 32>(17),
       make_variant<4, 1, 32>(17),
 #endif
-      make_variant<32, 1, 16>(5),  make_variant<16, 1, 16>(5),
-      make_variant<8, 1, 16>(5),   make_variant<4, 1, 16>(5),
+      make_variant<32, 1, 16>(OC_NARROW_COUT_MIN),  make_variant<16, 1, 16>(OC_NARROW_COUT_MIN),
+      make_variant<8, 1, 16>(OC_NARROW_COUT_MIN),   make_variant<4, 1, 16>(OC_NARROW_COUT_MIN),
   };
   for (const MfmaVariant& v : table)
     if (v.cin == cin && cout >= v.cout_min && cout <= v.cout_max) return &v;

@@ -57,7 +57,7 @@ def structure(case):
 
 
 @pytest.mark.parametrize("cin,cout", [(32, 32), (16, 32), (8, 16), (4, 16), (32, 8), (3, 5), (64, 64),
-                                      (128, 64)])
+                                      (128, 64), (4, 8), (2, 16), (16, 4)])
 @pytest.mark.parametrize("case", CASES)
 def test_conv_backward(case, cin, cout):
     rng, ref, g = structure(case)

@@ -38,7 +38,7 @@ def dev(a):
 from test_conv_paths_cpu import CASES  # noqa: E402
 
 
-@pytest.mark.parametrize("cin,cout", [(32, 32), (16, 32), (8, 16), (4, 16), (32, 8)])
+@pytest.mark.parametrize("cin,cout", [(32, 32), (16, 32), (8, 16), (4, 16), (32, 8), (16, 4), (32, 2)])
 @pytest.mark.parametrize("case", CASES)
 def test_conv_random_split_strings(case, cin, cout):
     seed, n, gd, gh, gw, p0, p1, p2 = case

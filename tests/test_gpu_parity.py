@@ -166,7 +166,7 @@ def test_ten2oc_channel_widths(c):
 # Convolution
 # ----------------------------------------------------------------------------
 
-CHANNELS = [(1, 8), (3, 5), (4, 16), (8, 16), (16, 32), (32, 32), (32, 8), (70, 3)]
+CHANNELS = [(1, 8), (3, 5), (4, 16), (8, 16), (16, 32), (32, 32), (32, 8), (70, 3), (16, 4), (32, 1), (8, 2), (4, 3)]
 
 
 def conv_case(seed, cin, cout, shape=(2, 3, 2, 3)):
