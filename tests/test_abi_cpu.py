@@ -133,7 +133,7 @@ def test_mfma_support_query(L):
         assert L.oc_conv3x3x3_mfma_supported(cin, cout) in (0, 1)
     # Widths that run in 32-channel blocks: cin a multiple of 32, cout a
     # multiple of 32 up to 256 or a fused width below 32.
-    for cin, cout in [(64, 64), (128, 64), (256, 128), (32, 64), (64, 8), (96, 16)]:
+    for cin, cout in [(64, 64), (128, 64), (256, 128), (32, 64), (64, 8), (96, 16), (64, 3)]:
         assert L.oc_conv3x3x3_mfma_supported(cin, cout) == 1, (cin, cout)
-    for cin, cout in [(64, 130), (48, 32), (64, 3), (32, 288)]:
+    for cin, cout in [(64, 130), (48, 32), (32, 288), (64, 40)]:
         assert L.oc_conv3x3x3_mfma_supported(cin, cout) == 0, (cin, cout)

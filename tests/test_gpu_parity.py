@@ -224,7 +224,7 @@ def test_conv_degenerate_structures(impl):
 
 @pytest.mark.parametrize("impl", ["auto", "mfma", "gemm"])
 @pytest.mark.parametrize("cin,cout", [(64, 64), (128, 64), (256, 128), (64, 130), (32, 64), (64, 8),
-                                      (96, 16), (64, 32)])
+                                      (96, 16), (64, 32), (64, 3)])
 def test_conv_wide_channels(cin, cout, impl):
     """Widths of the encoder-decoder's coarse levels, which have no fused
     variant: the window-sum GEMM path, and the fused kernels run in 32-channel
