@@ -1579,35 +1579,37 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
     o[2] = 8 * p.w + c.w;
   }
   const int lim[3] = {8 * gd, 8 * gh, 8 * gw};
-  // Grid row y takes regions y, y + gridDim.y, ... (indices without the
-  // centre): on small structures one region per thread, so that a cell's
-  // lookups run side by side; on large ones one thread per cell.
-  for (int rs = (int)blockIdx.y; rs < kSets; rs += (int)gridDim.y) {
-    const int r = rs + (rs >= 13 ? 1 : 0);
+  // Region r's block: its tree tt (-1 outside the grid) and its corner lo.
+  auto locate = [&](int r, int (&lo)[3]) -> int64_t {
     const int dir[3] = {r / 9 - 1, (r / 3) % 3 - 1, r % 3 - 1};
-    int lo[3];
     bool inside = row >= 0;
     for (int a = 0; a < 3; ++a) {
       lo[a] = dir[a] < 0 ? o[a] - 1 : (dir[a] == 0 ? o[a] : o[a] + sz);
       const int hi = dir[a] < 0 ? o[a] : (dir[a] == 0 ? o[a] + sz : o[a] + sz + 1);
       inside = inside && lo[a] >= 0 && hi <= lim[a];
     }
+    return inside ? ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3) : -1;
+  };
+  // Region r's code from its tree's words, first row and slot base.
+  auto resolve = [&](int r, const int (&lo)[3], int64_t tt, const uint4 tw, int64_t rr, int64_t sb) {
+    const int dir[3] = {r / 9 - 1, (r / 3) % 3 - 1, r % 3 - 1};
     int32_t code = -1;
-    if (inside) {
-      const int64_t tt = ((n * gd + (lo[0] >> 3)) * gh + (lo[1] >> 3)) * gw + (lo[2] >> 3);
-      const uint32_t w0 = trees[4 * tt];  // split bits 0..31
-      int64_t rr = prefix[tt], slot = -1;
+    if (tt >= 0) {
+      const uint32_t w0 = tw.x;  // split bits 0..31
+      int64_t slot = -1;
       const bool corner = dir[0] != 0 && dir[1] != 0 && dir[2] != 0;
       if (corner) {
-        const Bits b = load_bits(trees, tt);
+        Bits b;
+        b.lo = (uint64_t)tw.x | ((uint64_t)tw.y << 32);
+        b.hi = tw.z & 0x1FFu;
         rr += data_idx(b, leaf_at(b, lo[0] & 7, lo[1] & 7, lo[2] & 7));
       } else if (w0 & 1u) {
         if (sz == 8) {
-          slot = sbase[tt];
+          slot = sb;
         } else {
           const int o1 = 4 * ((lo[0] >> 2) & 1) + 2 * ((lo[1] >> 2) & 1) + ((lo[2] >> 2) & 1);
           const int m = __popc((w0 >> 1) & ((1u << o1) - 1u));  // split depth-1 nodes before it
-          if ((w0 >> (1 + o1)) & 1u) slot = sbase[tt] + 1 + m;
+          if ((w0 >> (1 + o1)) & 1u) slot = sb + 1 + m;
           else rr += o1 - m;  // Eq. 3 for a depth-1 leaf
         }
       }
@@ -1628,6 +1630,42 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
       else code = rr < n_leaves ? (int32_t)rr : -1;  // only a non-canonical structure exceeds
     }
     codes[(int64_t)(r - (r > 13)) * ccap + j] = code;
+  };
+  if (gridDim.y == 1) {
+    // One thread per cell: the regions in two groups of 13, each group's
+    // tree words, first rows and slot bases loaded together (a region
+    // outside the grid reads tree 0's), then resolved.
+#pragma unroll
+    for (int g0 = 0; g0 < kSets; g0 += 13) {
+      int lo[13][3];
+      int64_t tt[13], rr[13], sb[13];
+      uint4 tw[13];
+#pragma unroll
+      for (int i = 0; i < 13; ++i) {
+        const int rs = g0 + i, r = rs + (rs >= 13 ? 1 : 0);
+        tt[i] = locate(r, lo[i]);
+        const int64_t q = tt[i] >= 0 ? tt[i] : 0;
+        tw[i] = reinterpret_cast<const uint4*>(trees)[q];
+        rr[i] = prefix[q];
+        sb[i] = sbase[q];
+      }
+#pragma unroll
+      for (int i = 0; i < 13; ++i) {
+        const int rs = g0 + i, r = rs + (rs >= 13 ? 1 : 0);
+        resolve(r, lo[i], tt[i], tw[i], rr[i], sb[i]);
+      }
+    }
+  } else {
+    // Grid row y takes regions y, y + gridDim.y, ... (indices without the
+    // centre): on small structures one region per thread, so that a cell's
+    // lookups run side by side.
+    for (int rs = (int)blockIdx.y; rs < kSets; rs += (int)gridDim.y) {
+      const int r = rs + (rs >= 13 ? 1 : 0);
+      int lo[3];
+      const int64_t t = locate(r, lo);
+      const int64_t q = t >= 0 ? t : 0;
+      resolve(r, lo, t, reinterpret_cast<const uint4*>(trees)[q], prefix[q], sbase[q]);
+    }
   }
   }
 }
