@@ -1105,8 +1105,11 @@ struct Shell2RowLoad<JD, UH, 8, CIN> {
   __device__ __forceinline__ static void run(float (&)[8][CIN / 4], const uint32_t*, const G&, uint32_t) {}
 };
 
-// LDS bytes per wave for the shell rows of a 16-cell tile.
-constexpr int kShell2Lds = 16 * 56 * 4;
+// LDS bytes per wave for the shell rows of a 16-cell tile: 57 words per cell
+// (56 and a pad, an odd stride, so that the 16 cells' words at one shell
+// position fall in different banks).
+constexpr int kShell2Stride = 57;
+constexpr int kShell2Lds = 16 * kShell2Stride * 4;
 
 // The box sums are separable: the two planes of the row are summed first,
 // then neighbouring pairs along w, and each pair sum goes to the two
@@ -1280,7 +1283,7 @@ __global__ void __launch_bounds__(kMfmaThreads) k_conv_cell2_mfma(
   bias16<NT>(bias, cout, lane, bvals);
   // The wave's shell offsets: 56 per cell, after the weights.
   uint32_t* offm = reinterpret_cast<uint32_t*>(smem + MfmaCfg<CIN, NT, 16>::WFLOATS) +
-                   (threadIdx.x >> 6) * (kShell2Lds / 4) + cl * 56;
+                   (threadIdx.x >> 6) * (kShell2Lds / 4) + cl * kShell2Stride;
   for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
     const int64_t idx = tile * 16 + cl;
     int row = idx < lcnt ? brow[lbeg + idx] : -1;
