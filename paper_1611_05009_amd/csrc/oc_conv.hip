@@ -1204,13 +1204,13 @@ constexpr int cell2_depth() {
   return CIN / 4 <= 2 ? OC_CELL2_DEPTH_SMALL : 2;
 }
 
-template <int K, int D, int CIN, int NT, class G>
+template <int K, int D, int CIN, int NT, class G, int E = 12>
 struct Cell2Steps {
   __device__ __forceinline__ static void run(float (&S)[9][CIN / 4], float (&X)[D][8][CIN / 4],
                                              const uint32_t* offm, const G& rin, uint32_t choff,
                                              const float (&xs)[CIN / 4], const float* wl, int lane,
                                              int perm, typename CellCfg<CIN, NT>::Acc (&acc)[NT]) {
-    if constexpr (K < 12) {
+    if constexpr (K < E) {
       constexpr int JD = K / 4, UH = K % 4;
       __builtin_amdgcn_sched_barrier(0);
       shell2_row_add<JD, UH, CIN>(S, X[K % D]);
@@ -1223,7 +1223,7 @@ struct Cell2Steps {
         __builtin_amdgcn_sched_barrier(0);
         init_layer<2, JD + 1>(S, xs);
       }
-      Cell2Steps<K + 1, D, CIN, NT, G>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
+      Cell2Steps<K + 1, D, CIN, NT, G, E>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
     }
   }
 };
@@ -1284,30 +1284,47 @@ __global__ void __launch_bounds__(kMfmaThreads) k_conv_cell2_mfma(
   // The wave's shell offsets: 56 per cell, after the weights.
   uint32_t* offm = reinterpret_cast<uint32_t*>(smem + MfmaCfg<CIN, NT, 16>::WFLOATS) +
                    (threadIdx.x >> 6) * (kShell2Lds / 4) + cl * kShell2Stride;
-  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+  // Tiles are pipelined: a tile's row and key are loaded at the start of
+  // the tile before it, and its shell table entries halfway through that
+  // tile's row steps, so that a tile starts with its shell rows at hand.
+  // Row and key of the lane's cell of `tile` (row -1: no cell).
+  auto cell_of_tile = [&](int64_t tile, int& row, int32_t& key) {
     const int64_t idx = tile * 16 + cl;
-    int row = idx < lcnt ? brow[lbeg + idx] : -1;
-    const int32_t key = row >= 0 ? e2key[idx] : 0;
+    const bool in = tile < wt.end && idx < lcnt;
+    row = in ? brow[lbeg + idx] : -1;
+    key = in ? e2key[idx] : 0;
+  };
+  // The lane's 14 shell table entries (chunk q takes shell voxels 4 j + q of
+  // its cell; the cell's 4^3 neighbourhood is the sub-block of its node's
+  // table at twice its octant).
+  auto shell_entries = [&](int& row, int32_t key, int (&mine)[14]) {
     const int64_t node = key >> 3;
     if (row >= n_leaves || key < 0 || node >= ncap) row = -1;  // only a non-canonical structure
-    // Shell rows, in the wave's LDS area: lane chunk q
-    // takes shell voxels 4 j + q of its cell from the node's table (the
-    // cell's 4^3 neighbourhood is the sub-block at twice its octant).
-    {
-      const int o2 = key & 7;
-      const int32_t* nt = ntab + (row >= 0 ? node : 0) * kNodeEntries + 2 * ((o2 >> 2) & 1) * 36 +
-                          2 * ((o2 >> 1) & 1) * 6 + 2 * (o2 & 1);
-      int mine[14];
+    const int o2 = key & 7;
+    // Read whatever the cell (node 0's entries when there is none, taken by
+    // no one), so that the loads need no branch; with no node at all there
+    // are no edge-2 cells and nothing is read.
+    const int32_t* nt = ntab + (row >= 0 ? node : 0) * kNodeEntries + 2 * ((o2 >> 2) & 1) * 36 +
+                        2 * ((o2 >> 1) & 1) * 6 + 2 * (o2 & 1);
 #pragma unroll
-      for (int j = 0; j < 14; ++j) {
-        const int u = c_shell2.u[4 * j + q];
-        mine[j] = row >= 0 ? nt[(u >> 4) * 36 + ((u >> 2) & 3) * 6 + (u & 3)] : -1;
-      }
-#pragma unroll
-      for (int j = 0; j < 14; ++j) offm[4 * j + q] = GP::addr(mine[j]);
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    for (int j = 0; j < 14; ++j) {
+      const int u = c_shell2.u[4 * j + q];
+      mine[j] = ncap > 0 ? nt[(u >> 4) * 36 + ((u >> 2) & 3) * 6 + (u & 3)] : -1;
     }
+  };
+  int row_n;
+  int32_t key_n;
+  int mine_n[14];
+  cell_of_tile(wt.first, row_n, key_n);
+  shell_entries(row_n, key_n, mine_n);
+  for (int64_t tile = wt.first; tile < wt.end; tile += wt.stride) {
+    int row = row_n;
+    // Shell rows of this tile, in the wave's LDS area.
+#pragma unroll
+    for (int j = 0; j < 14; ++j) offm[4 * j + q] = GP::addr(row >= 0 ? mine_n[j] : -1);
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    cell_of_tile(tile + wt.stride, row_n, key_n);
     float xs[CH];
     gather_channels_at<CIN>(rin, GP::addr(row), choff, xs);
     typename K::Acc acc[NT];
@@ -1323,7 +1340,9 @@ __global__ void __launch_bounds__(kMfmaThreads) k_conv_cell2_mfma(
     float X[D][8][CH];
     init_layer<2, 0>(S, xs);
     Cell2Prologue<0, D, CIN, GP>::run(X, offm, rin, choff);
-    Cell2Steps<0, D, CIN, NT, GP>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
+    Cell2Steps<0, D, CIN, NT, GP, 6>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
+    shell_entries(row_n, key_n, mine_n);  // the next tile's
+    Cell2Steps<6, D, CIN, NT, GP>::run(S, X, offm, rin, choff, xs, wl, lane, perm, acc);
     __builtin_amdgcn_wave_barrier();  // offm is rewritten by the next tile
     // The row of cell m, for the store's MFMA layout.
     const int row_m = __builtin_amdgcn_ds_bpermute(perm, row);
