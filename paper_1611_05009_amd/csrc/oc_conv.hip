@@ -2319,8 +2319,8 @@ struct LayerPasses {
 constexpr int kCellrThreads = OC_CELLR_THREADS;
 
 // GP gathers the input rows, GS the boundary sums (as rows of CIN floats).
-template <int CIN, int NT, int SZ, bool TRIV, class GP, class GS = GP>
-__global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
+template <int CIN, int NT, int SZ, bool TRIV, class GP, class GS>
+__device__ __forceinline__ void cellr_tiles(
     const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
     int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
     const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
@@ -2388,6 +2388,33 @@ __global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
     store_tile16<NT>(acc, row_m, (relu & 2) ? 1.f : 1.f / (float)(SZ * SZ * SZ), lane, bvals, cout, relu,
                      out);
   }
+}
+
+// The boundary sums are gathered through 32-bit offsets (RowsRaw) when the
+// structure's slots (their count read on the device, *slot_total: a
+// workspace sized by the bound may hold far more) span less than 4 GiB of
+// sums and the input does too, else through 64-bit addresses.
+template <int CIN, int NT, int SZ, bool TRIV, class GP>
+__global__ void __launch_bounds__(kCellrThreads) k_conv_cellr_mfma(
+    const uint32_t* __restrict__ trees, const int64_t* __restrict__ prefix, int gd, int gh, int gw,
+    int64_t n_leaves, const uint64_t* __restrict__ info, const int32_t* __restrict__ brow,
+    const int64_t* __restrict__ meta, int kind, const int32_t* __restrict__ codes,
+    const float* __restrict__ bsum, const int64_t* __restrict__ slot_total, int64_t cap, int64_t ccap,
+    const float* __restrict__ in, const float* __restrict__ wm, uint32_t n_rows,
+    const float* __restrict__ bias, int cout, int relu, float* __restrict__ out,
+    const int64_t* __restrict__ kpre, int64_t t0, int64_t t1) {
+  int64_t ns = slot_total[0];
+  ns = ns < 0 ? 0 : (ns > cap ? cap : ns);
+  const bool raw = std::is_same<GP, RowsRaw<CIN>>::value &&
+                   (uint64_t)ns * kSets * (uint64_t)CIN * 4u < (uint64_t)kOutside;
+  if (raw)
+    cellr_tiles<CIN, NT, SZ, TRIV, GP, RowsRaw<CIN>>(trees, prefix, gd, gh, gw, n_leaves, info, brow, meta, kind,
+                                                     codes, bsum, (uint32_t)(ns * kSets), ccap, in, wm, n_rows,
+                                                     bias, cout, relu, out, kpre, t0, t1);
+  else
+    cellr_tiles<CIN, NT, SZ, TRIV, GP, RowsWide<CIN>>(trees, prefix, gd, gh, gw, n_leaves, info, brow, meta, kind,
+                                                      codes, bsum, 0u, ccap, in, wm, n_rows, bias, cout, relu, out,
+                                                      kpre, t0, t1);
 }
 
 // Edge-8 cells whose face and edge neighbour trees are unsplit.  Every shell
@@ -2595,8 +2622,8 @@ __global__ void k_mfma_weights(const float* __restrict__ w, int cout, float* __r
 typedef void (*MfmaFn)(int64_t, const int32_t*, const int64_t*, const float*, const float*,
                        uint32_t, const float*, int, int, float*);
 typedef void (*CellFn)(const uint32_t*, const int64_t*, int, int, int, int64_t, const uint64_t*,
-                       const int32_t*, const int64_t*, int, const int32_t*, const float*, uint32_t,
-                       int64_t, const float*, const float*, uint32_t, const float*, int, int, float*,
+                       const int32_t*, const int64_t*, int, const int32_t*, const float*, const int64_t*,
+                       int64_t, int64_t, const float*, const float*, uint32_t, const float*, int, int, float*,
                        const int64_t*, int64_t, int64_t);
 typedef void (*WeightFn)(const float*, int, float*);
 typedef void (*Cell8Fn)(int64_t, const int32_t*, const int64_t*, const int32_t*, int64_t,
@@ -2619,7 +2646,7 @@ struct MfmaVariant {
   // through RowsWide.
   MfmaFn kernel[2];
   Cell2Fn cell2[2];
-  CellFn cell4[2][2], cell8[2][2];  // [input gathers][boundary-sum gathers]
+  CellFn cell4[2], cell8[2];
   SumFn sums[2];
   Cell8Fn cell8g[2];    // edge-8 cells with unsplit face/edge neighbours
 };
@@ -2631,12 +2658,8 @@ void set_kernels(MfmaVariant& v) {
   using G = typename std::conditional<WIDE != 0, RowsWide<CIN>, RowsRaw<CIN>>::type;
   v.kernel[WIDE] = &k_conv_unit_mfma<CIN, NT, MS, G>;
   v.cell2[WIDE] = &k_conv_cell2_mfma<CIN, CNT, G>;
-  // Boundary sums of 4 GiB or more are gathered through RowsWide whatever
-  // the input's size (the bound-sized workspace of a large structure).
-  v.cell4[WIDE][1] = &k_conv_cellr_mfma<CIN, CNT, 4, false, G, RowsWide<CIN>>;
-  v.cell8[WIDE][1] = &k_conv_cellr_mfma<CIN, CNT, 8, false, G, RowsWide<CIN>>;
-  v.cell4[WIDE][0] = WIDE ? v.cell4[WIDE][1] : &k_conv_cellr_mfma<CIN, CNT, 4, false, G, RowsRaw<CIN>>;
-  v.cell8[WIDE][0] = WIDE ? v.cell8[WIDE][1] : &k_conv_cellr_mfma<CIN, CNT, 8, false, G, RowsRaw<CIN>>;
+  v.cell4[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 4, false, G>;
+  v.cell8[WIDE] = &k_conv_cellr_mfma<CIN, CNT, 8, false, G>;
   v.sums[WIDE] = &k_boundary_sums<CIN, G>;
   v.cell8g[WIDE] = &k_conv_cell8t_gemm<CIN, NT, MS, G>;
 }
@@ -3008,12 +3031,9 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
                       uint32_t n_rows, const FusedOut& o, int nk, const DevLimits& L, hipStream_t s) {
   const int num_cus = L.num_cus;
   const size_t max_smem = L.max_smem;
-  // Raw buffer gathers below 4 GiB of input (and of boundary sums, for the
-  // kernels that read them), 64-bit ones from there.
+  // Raw buffer gathers below 4 GiB of input, 64-bit ones from there (the
+  // edge-4/8 kernels pick their boundary sums' policy on the device).
   const int wide = (uint64_t)n_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside ? 1 : 0;
-  const uint64_t sum_rows = (uint64_t)(w.cap > 0 ? w.cap : 0) * kSets;
-  const int wide_sums = (wide || sum_rows * (uint64_t)v->cin * 4u >= (uint64_t)kOutside) ? 1 : 0;
-  const uint32_t n_sum_rows = wide_sums ? 0u : (uint32_t)sum_rows;
   const size_t wsmem = sizeof(float) * v->cell_wfloats;
   const size_t msmem = mfma_smem(*v);
   if (msmem > max_smem) return hipErrorInvalidConfiguration;
@@ -3030,14 +3050,15 @@ hipError_t fused_pass(const oci::ConvArgs& a, const ConvWs& w, const MfmaVariant
   auto launch_cells = [&](int k, int64_t t0, int64_t t1) -> hipError_t {
     const size_t smem = wsmem;
     if (smem > max_smem) return hipErrorInvalidConfiguration;
-    const CellFn f = k == 1 || k == 0 ? v->cell8[wide][wide_sums] : v->cell4[wide][wide_sums];
+    const CellFn f = k == 1 || k == 0 ? v->cell8[wide] : v->cell4[wide];
     hipError_t r = hipFuncSetAttribute(reinterpret_cast<const void*>(f),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem);
     if (r != hipSuccess) return r;
     hipLaunchKernelGGL(f, dim3(nblk, nk), dim3(kCellrThreads), smem, s, a.trees,
                        a.prefix, a.gd, a.gh, a.gw, a.n_leaves, (const uint64_t*)w.info,
                        (const int32_t*)w.brow, (const int64_t*)w.meta, k, (const int32_t*)w.codes,
-                       (const float*)w.bsum, n_sum_rows, w.ccap, in, o.wc, n_rows, o.bias, o.cout, o.relu, o.out,
+                       (const float*)w.bsum, (const int64_t*)w.pre[kSlotScan] + a.n_trees, w.cap, w.ccap, in,
+                       o.wc, n_rows, o.bias, o.cout, o.relu, o.out,
                        (const int64_t*)w.pre[1 + k], t0, t1);
     return hipGetLastError();
   };
