@@ -1373,9 +1373,10 @@ __host__ __device__ constexpr bool in_set(int e, int x, int B) {
 }
 
 // The 56 boundary voxels V (= 16 x0 + 4 x1 + x2) of a 4^3 block, K-th in
-// ascending order: load reads each from its leaf (r2: row of each 2^3
-// octant's leaf or first unit voxel, sp: which octants are split), add puts
-// each into the sets that hold it.
+// ascending order: load reads each from its leaf (a2: gather address of each
+// 2^3 octant's leaf or first unit voxel, st2: the address step from one unit
+// voxel of the octant to the next, 0 for an unsplit octant), add puts each
+// into the sets that hold it.
 constexpr bool interior4(int v) {
   return (v >> 4) % 3 != 0 && ((v >> 2) & 3) % 3 != 0 && (v & 3) % 3 != 0;
 }
@@ -1399,15 +1400,15 @@ struct BoundaryVoxels {
   // need: the sets that are read; a voxel in none of them reads zero (no
   // memory traffic) and the sets it would change are not written.
   template <int CIN, class G>
-  __device__ __forceinline__ static void load(float (&xv)[56], const int (&r2)[8], int sp, const G& rin,
-                                              int c, uint32_t need) {
+  __device__ __forceinline__ static void load(float (&xv)[56], const uint32_t (&a2)[8], const uint32_t (&st2)[8],
+                                              const G& rin, uint32_t off, uint32_t need) {
     if constexpr (!skip) {
       constexpr int o2 = 4 * (x0 >> 1) + 2 * (x1 >> 1) + (x2 >> 1);
-      constexpr int u = 4 * (x0 & 1) + 2 * (x1 & 1) + (x2 & 1);
-      const int row = (need & voxel_sets(V)) != 0u ? r2[o2] + (((sp >> o2) & 1) ? u : 0) : -1;
-      xv[K] = gather_at<1>(rin, G::addr(row), 4u * c);
+      constexpr uint32_t u = 4 * (x0 & 1) + 2 * (x1 & 1) + (x2 & 1);
+      const uint32_t a = (need & voxel_sets(V)) != 0u ? a2[o2] + u * st2[o2] : G::addr(-1);
+      xv[K] = gather_at<1>(rin, a, off);
     }
-    BoundaryVoxels<V + 1, NK>::template load<CIN, G>(xv, r2, sp, rin, c, need);
+    BoundaryVoxels<V + 1, NK>::template load<CIN, G>(xv, a2, st2, rin, off, need);
   }
   __device__ __forceinline__ static void add(float (&cs)[kSets], const float (&xv)[56]) {
     if constexpr (!skip) {
@@ -1424,7 +1425,8 @@ struct BoundaryVoxels {
 template <int K>
 struct BoundaryVoxels<64, K> {
   template <int CIN, class G>
-  __device__ __forceinline__ static void load(float (&)[56], const int (&)[8], int, const G&, int, uint32_t) {}
+  __device__ __forceinline__ static void load(float (&)[56], const uint32_t (&)[8], const uint32_t (&)[8], const G&,
+                                              uint32_t, uint32_t) {}
   __device__ __forceinline__ static void add(float (&)[kSets], const float (&)[56]) {}
 };
 
@@ -1499,19 +1501,33 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
     const int64_t s0 = sbase[t];
     const uint32_t m1 = (uint32_t)(b.lo >> 1) & 0xFFu;  // split depth-1 children
     const int p1 = __popc(m1);
+    // Eq. 3 for the depth-2 nodes below a split child o1 and for the first
+    // unit voxel of each split one, from the set-bit counts below bit 1 + o1,
+    // below bit 9 + 8 o1 + o2 and of the whole string.  Bit j of dbits is
+    // split bit 9 + j (the depth-2 nodes).
+    const uint64_t dbits = (b.lo >> 9) | ((uint64_t)b.hi << 55);
+    const int pall = popc_all(b), p9 = __popcll(b.lo & 0x1FFull);
+    // The gather address of a row: a2 holds the channel offset for the raw
+    // policy, the wide one takes it at the load.
+    constexpr bool RAW = std::is_same<GP, RowsRaw<CIN>>::value;
+    const uint32_t coff = RAW ? 4u * c : 0u, loff = RAW ? 0u : 4u * c;
+    const uint32_t step = RAW ? 4u * CIN : 1u;  // address step of one row
     float ts[kSets];
 #pragma unroll
     for (int s = 0; s < kSets; ++s) ts[s] = 0.f;
     for (int k = gi; k < p1; k += GPT) {
       const int o1 = nth_bit(m1, k);
-      int r2[8];
-      int sp = 0;
+      const uint32_t sp = (uint32_t)(dbits >> (8 * o1)) & 0xFFu;  // split octants
+      const int pd1 = __popcll(b.lo & ((2ull << o1) - 1ull));
+      const int pd2 = p9 + __popcll(dbits & ((1ull << (8 * o1)) - 1ull));
+      uint32_t a2[8], st2[8];
 #pragma unroll
       for (int o2 = 0; o2 < 8; ++o2) {
-        const int n2 = 9 + 8 * o1 + o2;
-        const int s2 = bit(b, n2);
-        sp |= s2 << o2;
-        r2[o2] = rbase + data_idx(b, s2 ? 8 * n2 + 1 : n2);
+        const int p2 = pd2 + __popc(sp & ((1u << o2) - 1u));
+        const bool s2 = (sp >> o2) & 1u;
+        const int row = rbase + (s2 ? 8 * p2 + 1 - pall : 8 * pd1 + 1 - p2 + o2);
+        a2[o2] = GP::addr(row) + coff;
+        st2[o2] = s2 && row >= 0 ? step : 0u;
       }
       // The child's sets that are read: its own, and those of the tree's
       // sets on its side.
@@ -1519,7 +1535,7 @@ __global__ void __launch_bounds__(256) k_boundary_sums(
       const uint32_t mk = slot < cap ? smask[slot] : 0u;
       const uint32_t need = mk | (s0 < cap ? smask[s0] & child_sides(o1) : 0u);
       float xv[56];
-      BoundaryVoxels<0, 0>::load<CIN, GP>(xv, r2, sp, rin, c, need);
+      BoundaryVoxels<0, 0>::load<CIN, GP>(xv, a2, st2, rin, loff, need);
       __builtin_amdgcn_sched_barrier(0);
       float cs[kSets];
 #pragma unroll
@@ -1708,51 +1724,37 @@ __global__ void k_region_codes(const uint32_t* __restrict__ trees,
 //     group order, the layout the unit-voxel kernel stages.
 // ---------------------------------------------------------------------------
 struct NbTree {
-  uint32_t w0, w1, w2;  // split bits 0..31, 32..63, 64..72
-  int32_t inside;       // 0: outside the grid (zero padding)
-  int64_t row0;         // first row (prefix)
-  int64_t pad;
+  uint32_t w0;      // split bits 0..31 (the root's and the depth-1 nodes' are 0..8)
+  uint32_t d0, d1;  // depth-2 split bits: bit j of (d1, d0) is bit 9 + j
+  int32_t p9;       // set bits among 0..8
+  int32_t pd0;      // p9 + set bits of d0
+  int32_t pall;     // set bits among 0..72
+  uint32_t row0;    // first row (prefix), modulo 2^32
+  int32_t lim;      // n_leaves - first row, clamped to int32 (INT32_MIN outside the grid)
 };
-
-// Which of the 27 neighbour trees holds local coordinate x in [-1, 8]
-// (per axis: 0 below, 1 the wave's own tree, 2 above).
-__device__ __forceinline__ int nb_side(int x) { return x < 0 ? 0 : (x > 7 ? 2 : 1); }
-
-// Split bit i (0 <= i < 73) of words (w0, w1, w2), without branches.
-__device__ __forceinline__ uint32_t bit_bf(uint32_t w0, uint32_t w1, uint32_t w2, int i) {
-  const uint32_t w = i < 32 ? w0 : (i < 64 ? w1 : w2);
-  return (w >> (i & 31)) & 1u;
-}
-
-// Set bits among indices [0, n), 0 <= n <= 73, without branches.
-__device__ __forceinline__ int popc_bf(uint32_t w0, uint32_t w1, uint32_t w2, int n) {
-  const uint32_t m0 = n >= 32 ? 0xFFFFFFFFu : ((1u << (n & 31)) - 1u);
-  const uint32_t m1 = n >= 64 ? 0xFFFFFFFFu : (n <= 32 ? 0u : ((1u << (n - 32)) - 1u));
-  const uint32_t m2 = n <= 64 ? 0u : ((1u << (n - 64)) - 1u);
-  return __popc(w0 & m0) + __popc(w1 & m1) + __popc(w2 & m2 & 0x1FFu);
-}
 
 // Row of the leaf holding voxel (d, h, w), local coordinates of the wave's
 // tree in [-1, 8]; -1 outside the grid or past n_leaves (non-canonical).
-__device__ __forceinline__ int32_t nb_voxel_row(const NbTree* __restrict__ nt, int d, int h, int w,
-                                                int64_t n_leaves) {
-  const NbTree n = nt[nb_side(d) * 9 + nb_side(h) * 3 + nb_side(w)];
-  d &= 7;
-  h &= 7;
-  w &= 7;
-  // The leaf: descend while split (octant bits 2, 1, 0 of the coordinates).
-  const int n1 = 1 + (((d >> 2) & 1) << 2) + (((h >> 2) & 1) << 1) + ((w >> 2) & 1);
-  const int n2 = 8 * n1 + 1 + (((d >> 1) & 1) << 2) + (((h >> 1) & 1) << 1) + ((w >> 1) & 1);
-  const int n3 = 8 * n2 + 1 + ((d & 1) << 2) + ((h & 1) << 1) + (w & 1);
-  const uint32_t s0 = n.w0 & 1u, s1 = bit_bf(n.w0, n.w1, n.w2, n1), s2 = bit_bf(n.w0, n.w1, n.w2, n2);
-  const int i = s0 ? (s1 ? (s2 ? n3 : n2) : n1) : 0;
-  // Eq. 3 (an unsplit root is the only leaf: offset 0).
-  const int pa = (i - 1) >> 3;
-  const int di = i == 0 ? 0
-                        : 8 * popc_bf(n.w0, n.w1, n.w2, pa) + 1 - popc_bf(n.w0, n.w1, n.w2, min(i, 73)) +
-                              ((i - 1) & 7);
-  const int64_t r = n.row0 + di;
-  return (n.inside && r < n_leaves) ? (int32_t)r : -1;
+// The neighbour tree along an axis is (x + 8) >> 3 (0 below, 1 the wave's
+// own, 2 above), and the octant bits of x & 7 are those of x itself.  The
+// leaf's offset is Eq. 3 at the depth where the descent stops, from the
+// set-bit counts below bits 1 + o1 and 9 + 8 o1 + o2 (the depth-1 and
+// depth-2 node bits) and of the whole string; an unsplit root is the only
+// leaf (offset 0).
+__device__ __forceinline__ int32_t nb_voxel_row(const NbTree* __restrict__ nt, int d, int h, int w) {
+  const NbTree n = nt[((d + 8) >> 3) * 9 + ((h + 8) >> 3) * 3 + ((w + 8) >> 3)];
+  const int o1 = (((d >> 2) & 1) << 2) | (((h >> 2) & 1) << 1) | ((w >> 2) & 1);
+  const int o2 = (((d >> 1) & 1) << 2) | (((h >> 1) & 1) << 1) | ((w >> 1) & 1);
+  const int o3 = ((d & 1) << 2) | ((h & 1) << 1) | (w & 1);
+  const int p1 = __popc(n.w0 & ((2u << o1) - 1u));  // bits 0 .. o1
+  const uint32_t s1 = (n.w0 >> (1 + o1)) & 1u;
+  const int jj = ((o1 & 3) << 3) | o2;  // bit 9 + 8 o1 + o2, within d0 or d1
+  const uint32_t dw = o1 < 4 ? n.d0 : n.d1;
+  const int p2 = (o1 < 4 ? n.p9 : n.pd0) + __popc(dw & ((1u << jj) - 1u));
+  const uint32_t s2 = (dw >> jj) & 1u;
+  const int di1 = 1 - p1 + o1, di2 = 8 * p1 + 1 - p2 + o2, di3 = 8 * p2 + 1 - n.pall + o3;
+  const int di = (n.w0 & 1u) ? (s1 ? (s2 ? di3 : di2) : di1) : 0;
+  return di < n.lim ? (int32_t)(n.row0 + (uint32_t)di) : -1;
 }
 
 constexpr int kTreeWaves = 4;
@@ -1772,26 +1774,42 @@ __global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
   n_split = n_split < 0 ? 0 : (n_split > n_trees ? n_trees : n_split);
   NbTree* nb = s_nb[wave];
   int32_t* sn = s_node[wave];
+  // The 6^3 block coordinates of the lane's entries lane + 64 k.
+  int ud[4], uh[4], uw[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int u = lane + 64 * k;
+    ud[k] = u / 36;
+    uh[k] = (u / 6) % 6;
+    uw[k] = u % 6;
+  }
   const int64_t nwaves = (int64_t)gridDim.x * kTreeWaves;
   for (int64_t j = (int64_t)blockIdx.x * kTreeWaves + wave; j < n_split; j += nwaves) {
     const int64_t t = stl[j];
     if (lane < 27) {
       const TreePos p = tree_pos(t, gd, gh, gw);
       const int qd = p.d + lane / 9 - 1, qh = p.h + (lane / 3) % 3 - 1, qw = p.w + lane % 3 - 1;
-      NbTree n;
-      n.w0 = n.w1 = n.w2 = 0u;
-      n.inside = 0;
-      n.row0 = 0;
-      n.pad = 0;
+      uint32_t w0 = 0u, w1 = 0u, w2 = 0u;
+      int64_t r0 = 0, lim = INT32_MIN;
       if (qd >= 0 && qh >= 0 && qw >= 0 && qd < gd && qh < gh && qw < gw) {
         const int64_t q = ((p.n * gd + qd) * gh + qh) * gw + qw;
         const uint4 wv = reinterpret_cast<const uint4*>(trees)[q];
-        n.w0 = wv.x;
-        n.w1 = wv.y;
-        n.w2 = wv.z;
-        n.inside = 1;
-        n.row0 = prefix[q];
+        w0 = wv.x;
+        w1 = wv.y;
+        w2 = wv.z & 0x1FFu;
+        r0 = prefix[q];
+        lim = n_leaves - r0;
+        lim = lim < INT32_MIN ? INT32_MIN : (lim > INT32_MAX ? INT32_MAX : lim);
       }
+      NbTree n;
+      n.w0 = w0;
+      n.d0 = (w0 >> 9) | (w1 << 23);
+      n.d1 = (w1 >> 9) | (w2 << 23);
+      n.p9 = __popc(w0 & 0x1FFu);
+      n.pd0 = n.p9 + __popc(n.d0);
+      n.pall = __popc(w0) + __popc(w1) + __popc(w2);
+      n.row0 = (uint32_t)r0;
+      n.lim = (int32_t)lim;
       nb[lane] = n;
     }
     // The wave's own bits and counters, wave-uniform.
@@ -1807,10 +1825,8 @@ __global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
       const int od = 4 * ((o1 >> 2) & 1) - 1, oh = 4 * ((o1 >> 1) & 1) - 1, ow1 = 4 * (o1 & 1) - 1;
       int32_t v[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int u = lane + 64 * k;
-        v[k] = u < kNodeEntries ? nb_voxel_row(nb, od + u / 36, oh + (u / 6) % 6, ow1 + u % 6, n_leaves) : -1;
-      }
+      for (int k = 0; k < 4; ++k)
+        v[k] = lane + 64 * k < kNodeEntries ? nb_voxel_row(nb, od + ud[k], oh + uh[k], ow1 + uw[k]) : -1;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int u = lane + 64 * k;
@@ -1822,7 +1838,8 @@ __global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
       for (int o2 = 0; o2 < 8; ++o2) {
-        if (!bit_bf(b0, b1, b2, 9 + 8 * o1 + o2)) continue;
+        const int n2 = 9 + 8 * o1 + o2;
+        if (!(((n2 < 32 ? b0 : (n2 < 64 ? b1 : b2)) >> (n2 & 31)) & 1u)) continue;
         const int idx = (2 * ((o2 >> 2) & 1) + (lane >> 4)) * 36 + (2 * ((o2 >> 1) & 1) + ((lane >> 2) & 3)) * 6 +
                         2 * (o2 & 1) + (lane & 3);
         if (g < gcap) nbt[g * 64 + lane] = sn[idx];
