@@ -1820,6 +1820,7 @@ __global__ void __launch_bounds__(64 * kTreeWaves) k_tree_tables(
     int64_t g = gpre[t], node = d1pre[t];
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+#pragma unroll 1  // rolled: fewer registers, more waves in flight
     for (int o1 = 0; o1 < 8; ++o1) {
       if (!((b0 >> (1 + o1)) & 1u)) continue;
       const int od = 4 * ((o1 >> 2) & 1) - 1, oh = 4 * ((o1 >> 1) & 1) - 1, ow1 = 4 * (o1 & 1) - 1;
