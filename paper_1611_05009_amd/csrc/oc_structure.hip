@@ -217,6 +217,48 @@ __device__ __forceinline__ int64_t block_excl_scan(int64_t v, int64_t* sh_waves,
   return off + incl - v;
 }
 
+// A thread's kScanItems consecutive counts from base (zero past n): 16-byte
+// loads when all are in range and the array is 16-byte aligned.
+__device__ __forceinline__ void load_items(const int32_t* __restrict__ counts, int64_t base, int64_t n,
+                                           int32_t (&v)[kScanItems]) {
+  if (base + kScanItems <= n && (reinterpret_cast<uintptr_t>(counts) & 15) == 0) {
+    const int4* q = reinterpret_cast<const int4*>(counts + base);
+#pragma unroll
+    for (int i = 0; i < kScanItems / 4; ++i) {
+      const int4 x = q[i];
+      v[4 * i] = x.x;
+      v[4 * i + 1] = x.y;
+      v[4 * i + 2] = x.z;
+      v[4 * i + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) v[k] = base + k < n ? counts[base + k] : 0;
+  }
+}
+
+// Writes the exclusive prefix run + v[0] + ... + v[k - 1] to prefix[base + k]
+// (k < kScanItems, base + k < n): 16-byte stores when all are in range and
+// the array is 16-byte aligned.
+__device__ __forceinline__ void store_items(int64_t* __restrict__ prefix, int64_t base, int64_t n, int64_t run,
+                                            const int32_t (&v)[kScanItems]) {
+  int64_t r[kScanItems];
+#pragma unroll
+  for (int k = 0; k < kScanItems; ++k) {
+    r[k] = run;
+    run += v[k];
+  }
+  if (base + kScanItems <= n && (reinterpret_cast<uintptr_t>(prefix) & 15) == 0) {
+    longlong2* q = reinterpret_cast<longlong2*>(prefix + base);
+#pragma unroll
+    for (int i = 0; i < kScanItems / 2; ++i) q[i] = make_longlong2(r[2 * i], r[2 * i + 1]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k)
+      if (base + k < n) prefix[base + k] = r[k];
+  }
+}
+
 // Several scans of the same length at once (blockIdx.y selects the array).
 struct ScanSet {
   const int32_t* counts[oci::kMaxScans];
@@ -228,10 +270,11 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_reduce(const int32_t* __r
                                                               int64_t n, int64_t* __restrict__ sums) {
   __shared__ int64_t sh[kScanThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  load_items(counts, base, n, v);
   int64_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k)
-    if (base + k < n) s += counts[base + k];
+  for (int k = 0; k < kScanItems; ++k) s += v[k];
   int64_t tot;
   block_excl_scan(s, sh, &tot);
   if (threadIdx.x == 0) sums[blockIdx.x] = tot;
@@ -241,10 +284,11 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_reduce_set(ScanSet set, i
   __shared__ int64_t sh[kScanThreads / 64];
   const int32_t* __restrict__ counts = set.counts[blockIdx.y];
   const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
+  int32_t v[kScanItems];
+  load_items(counts, base, n, v);
   int64_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k)
-    if (base + k < n) s += counts[base + k];
+  for (int k = 0; k < kScanItems; ++k) s += v[k];
   int64_t tot;
   block_excl_scan(s, sh, &tot);
   if (threadIdx.x == 0) set.sums[blockIdx.y][blockIdx.x] = tot;
@@ -287,19 +331,12 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply_set(ScanSet set, in
   int64_t* __restrict__ prefix = set.prefix[blockIdx.y];
   const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
   int32_t v[kScanItems];
+  load_items(counts, base, n, v);
   int64_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k) {
-    v[k] = base + k < n ? counts[base + k] : 0;
-    s += v[k];
-  }
+  for (int k = 0; k < kScanItems; ++k) s += v[k];
   int64_t tot;
-  int64_t run = block_excl_scan(s, sh, &tot) + set.sums[blockIdx.y][blockIdx.x];
-#pragma unroll
-  for (int k = 0; k < kScanItems; ++k) {
-    if (base + k < n) prefix[base + k] = run;
-    run += v[k];
-  }
+  store_items(prefix, base, n, block_excl_scan(s, sh, &tot) + set.sums[blockIdx.y][blockIdx.x], v);
 }
 
 __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const int32_t* __restrict__ counts,
@@ -308,19 +345,12 @@ __global__ void __launch_bounds__(kScanThreads) k_scan_apply(const int32_t* __re
   __shared__ int64_t sh[kScanThreads / 64];
   const int64_t base = (int64_t)blockIdx.x * kScanChunk + (int64_t)threadIdx.x * kScanItems;
   int32_t v[kScanItems];
+  load_items(counts, base, n, v);
   int64_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kScanItems; ++k) {
-    v[k] = base + k < n ? counts[base + k] : 0;
-    s += v[k];
-  }
+  for (int k = 0; k < kScanItems; ++k) s += v[k];
   int64_t tot;
-  int64_t run = block_excl_scan(s, sh, &tot) + sums[blockIdx.x];
-#pragma unroll
-  for (int k = 0; k < kScanItems; ++k) {
-    if (base + k < n) prefix[base + k] = run;
-    run += v[k];
-  }
+  store_items(prefix, base, n, block_excl_scan(s, sh, &tot) + sums[blockIdx.x], v);
 }
 
 // ---------------------------------------------------------------------------
