@@ -403,16 +403,22 @@ __global__ void k_leaf_kinds(const uint32_t* __restrict__ trees, int64_t n_trees
   const int p2 = depth2_splits(b);
   int trivial = 0;
   if (!root) {
+    // Trivial: no face or edge neighbour tree is split.  All 18 root bits
+    // are read at once (a neighbour outside the grid reads the tree's own,
+    // unsplit, root bit).
     const TreePos p = tree_pos(t, gd, gh, gw);
-    trivial = 1;
-    for (int r = 0; r < 27 && trivial; ++r) {
+    uint32_t split = 0u;
+#pragma unroll
+    for (int r = 0; r < 27; ++r) {
       const int dd = r / 9 - 1, dh = (r / 3) % 3 - 1, dw = r % 3 - 1;
-      if ((dd != 0) + (dh != 0) + (dw != 0) != 1 && (dd != 0) + (dh != 0) + (dw != 0) != 2) continue;
+      const int nz = (dd != 0) + (dh != 0) + (dw != 0);
+      if (nz != 1 && nz != 2) continue;
       const int qd = p.d + dd, qh = p.h + dh, qw = p.w + dw;
-      if (qd < 0 || qh < 0 || qw < 0 || qd >= gd || qh >= gh || qw >= gw) continue;
-      const int64_t q = ((p.n * gd + qd) * gh + qh) * gw + qw;
-      if (trees[4 * q] & 1u) trivial = 0;
+      const bool in = qd >= 0 && qh >= 0 && qw >= 0 && qd < gd && qh < gh && qw < gw;
+      const int64_t q = in ? ((p.n * gd + qd) * gh + qh) * gw + qw : t;
+      split |= trees[4 * q];
     }
+    trivial = (split & 1u) ? 0 : 1;
   }
   n_grp[t] = p2;
   n8t[t] = (!root && trivial) ? 1 : 0;
