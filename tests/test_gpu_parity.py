@@ -100,6 +100,29 @@ def test_build_degenerate_grids(fill):
         assert np.array_equal(host(oc.leaf_index(g)).view(np.uint64), O.leaf_info(ref))
 
 
+@pytest.mark.parametrize("nt", [1, 15, 16, 17, 4095, 4096, 4097, 65537, (1 << 20) + 3])
+def test_prefix_across_scan_chunks(nt):
+    """oc_prefix (Eq. 3's per-tree offsets: an exclusive scan of 1 + 7 x set
+    bits) for tree counts around the scan's per-thread (16 trees) and
+    per-block (4096 trees) chunks, into an aligned and a misaligned output
+    (the scan's vector and element paths), against the oracle's prefix."""
+    import ctypes
+    words = synth.random_trees(np.random.default_rng(nt), nt, 1, 1, 1)
+    ref = O.prefix_of(words)
+    log("prefix nt=%d" % nt)
+    g = oc.from_trees(dev(words.view(np.int32)), nt, 1, 1, 1)
+    assert g.n_leaves == ref[-1]
+    assert np.array_equal(host(g.prefix), ref)
+    buf = torch.empty(nt + 2, dtype=torch.int64, device="cuda")
+    out = buf[1:]  # 8-byte aligned, not 16
+    ws = oc.structure_workspace(nt)
+    nl = ctypes.c_int64(0)
+    rc = oc.lib().oc_prefix(oc._ptr(g.trees), nt, oc._ptr(out), ctypes.byref(nl), oc._ptr(ws), ws.numel(),
+                            oc._stream())
+    assert rc == 0 and nl.value == ref[-1]
+    assert np.array_equal(host(out), ref)
+
+
 def test_validate_flags_noncanonical_trees():
     occ = small_occ(5, 1, 2, 2, 2)
     g = oc.build(dev(occ))
